@@ -1,0 +1,156 @@
+"""CPU oracle for decode attention over a block-wise low-rank KV cache.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or
+execute this package: only the tests, the package smoke check and the
+benchmark's CPU-baseline leg use it.  It shares no code with the GPU library
+and imports nothing from it; it takes plain float64 arrays.
+
+What it computes (the method's result, written out plainly in fp64):
+
+* Each context block b is stored as factors of its keys and values
+  (Sec. 4.2, Eq. 3), with the diagonal of singular values already multiplied
+  into the left factor:  K_b = P^K_b R^K_b,  V_b = P^V_b R^V_b.
+  P^*_b is T_b x r_b, R^*_b is r_b x (H_kv*d); the columns of R are head-major,
+  so KV head g owns columns g*d .. g*d+d-1.
+* At inference the selected blocks (Alg. 1 inference stage; the caller's block
+  table stands in for the retriever) and the request's own uncompressed KV are
+  attended together with scaled dot-product attention (Sec. 4.1, Eq. 1).
+* Query head h reads KV head g = floor(h / G), G = H_q / H_kv.
+
+`attend_dense` is that definition: rebuild K and V, then softmax attention.
+`attend_latent` reaches the same numbers by exact reassociation,
+q.(P R)_t = P_t.(R q) and sum_t w_t (P R)_t = (sum_t w_t P_t) R, which is the
+order the GPU path follows: project the query per block, score against P^K
+rows, softmax over all keys, accumulate weights times P^V rows in rank space,
+up-project through R^V, add the dense tail, normalise.  Both use one global
+maximum per column (two-pass softmax) and sum blocks in table order, tokens
+ascending, then the tail.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = ["attend_dense", "attend_latent", "reconstruct"]
+
+
+def reconstruct(p: np.ndarray, r: np.ndarray) -> np.ndarray:
+    """Eq. 3 with the singular values folded into P: the dense block P R."""
+    return p @ r
+
+
+def _shapes(q, rk_list, tail_k):
+    n_q, n_q_heads, d = q.shape
+    n_kv = tail_k.shape[2]
+    if n_q_heads % n_kv:
+        raise ValueError("query heads must be a multiple of KV heads")
+    for r in rk_list:
+        if r.shape[1] != n_kv * d:
+            raise ValueError("R must have H_kv*d columns")
+    return n_q, n_q_heads, d, n_kv, n_q_heads // n_kv
+
+
+def attend_dense(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale):
+    """Definition: Eq. 1 over the keys/values that the factors of the selected
+    blocks define (Eq. 3), concatenated in table order, followed by request i's
+    first tail_len[i] uncompressed tail tokens.
+
+    pk, rk, pv, rv: lists (indexed by block id) of float64 arrays
+        P^K_b [T_b, rk_b], R^K_b [rk_b, H_kv*d], P^V_b [T_b, rv_b], R^V_b [rv_b, H_kv*d]
+    table: selected block ids, in order
+    q: [n_q, H_q, d]; tail_k, tail_v: [n_q, tail_cap, H_kv, d]; tail_len: [n_q]
+    returns o: [n_q, H_q, d] float64
+    """
+    n_q, n_q_heads, d, n_kv, G = _shapes(q, [rk[b] for b in table], tail_k)
+    D = n_kv * d
+    keys = [reconstruct(pk[b], rk[b]) for b in table]
+    vals = [reconstruct(pv[b], rv[b]) for b in table]
+    k_ctx = np.concatenate(keys) if keys else np.zeros((0, D))
+    v_ctx = np.concatenate(vals) if vals else np.zeros((0, D))
+    out = np.empty((n_q, n_q_heads, d))
+    for i in range(n_q):
+        n_t = int(tail_len[i])
+        for h in range(n_q_heads):
+            g = h // G
+            k_all = np.concatenate([k_ctx[:, g * d:(g + 1) * d], tail_k[i, :n_t, g, :]])
+            v_all = np.concatenate([v_ctx[:, g * d:(g + 1) * d], tail_v[i, :n_t, g, :]])
+            if k_all.shape[0] == 0:
+                raise ValueError("no keys to attend to")
+            s = scale * (k_all @ q[i, h])
+            w = np.exp(s - s.max())
+            out[i, h] = (w / w.sum()) @ v_all
+    return out
+
+
+def attend_latent(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale,
+                  columns=None, return_weights=False):
+    """Same result as attend_dense, computed in each block's rank space.
+
+    For query column (i, h) with KV head g and selected block b:
+      (projection)    qt_b = R^K_b[:, g*d:(g+1)*d] q_ih          (length rk_b)
+      (scores)        s_bt = scale * P^K_b[t] . qt_b
+      (tail scores)   s_tau = scale * tail_k[i, tau, g] . q_ih
+      (softmax)       M = max of every score, w = exp(s - M), l = sum of all w
+      (latent V)      ot_b = sum_t w_bt P^V_b[t]                (length rv_b)
+      (up-projection) u_b = R^V_b[:, g*d:(g+1)*d]^T ot_b
+      (tail values)   u_tail = sum_tau w_tau tail_v[i, tau, g]
+      (output)        o = (sum_b u_b + u_tail) / l
+
+    columns: optional list of (i, h) pairs to evaluate (default: all).
+    Returns o [len(columns), d] when columns is given, else [n_q, H_q, d].
+    With return_weights, also returns the normalised weights of every column
+    (blocks in table order, tokens ascending, then the tail).
+    """
+    n_q, n_q_heads, d, n_kv, G = _shapes(q, [rk[b] for b in table], tail_k)
+    all_cols = columns is None
+    if all_cols:
+        columns = [(i, h) for i in range(n_q) for h in range(n_q_heads)]
+    columns = [(int(i), int(h)) for i, h in columns]
+    out = np.empty((len(columns), d))
+    weights = [None] * len(columns)
+
+    by_group = {}
+    for c, (i, h) in enumerate(columns):
+        by_group.setdefault(h // G, []).append(c)
+
+    for g, cidx in by_group.items():
+        gs = slice(g * d, (g + 1) * d)
+        qg = np.stack([q[columns[c][0], columns[c][1]] for c in cidx], axis=1)  # [d, n]
+        # scores of every selected block: [T_b, n]
+        s_blk = [scale * (pk[b] @ (rk[b][:, gs] @ qg)) for b in table]
+        # tail scores per column (each request has its own tail)
+        s_tail = []
+        for c in cidx:
+            i, h = columns[c]
+            n_t = int(tail_len[i])
+            s_tail.append(scale * (tail_k[i, :n_t, g, :] @ q[i, h]))
+        m = np.full(len(cidx), -np.inf)
+        for s in s_blk:
+            if s.shape[0]:
+                m = np.maximum(m, s.max(axis=0))
+        for k, s in enumerate(s_tail):
+            if s.shape[0]:
+                m[k] = max(m[k], s.max())
+        if not np.all(np.isfinite(m)):
+            raise ValueError("no keys to attend to")
+        w_blk = [np.exp(s - m) for s in s_blk]
+        w_tail = [np.exp(s - m[k]) for k, s in enumerate(s_tail)]
+        l = np.zeros(len(cidx))
+        for w in w_blk:
+            l += w.sum(axis=0)
+        for k, w in enumerate(w_tail):
+            l[k] += w.sum()
+        u = np.zeros((d, len(cidx)))
+        for b, w in zip(table, w_blk):
+            ot = pv[b].T @ w                      # [rv_b, n]
+            u += rv[b][:, gs].T @ ot              # [d, n]
+        for k, c in enumerate(cidx):
+            i, h = columns[c]
+            n_t = int(tail_len[i])
+            u_tail = w_tail[k] @ tail_v[i, :n_t, g, :]
+            out[c] = (u[:, k] + u_tail) / l[k]
+            if return_weights:
+                weights[c] = np.concatenate([w[:, k] for w in w_blk] + [w_tail[k]]) / l[k]
+
+    if all_cols:
+        out = out.reshape(n_q, n_q_heads, d)
+    return (out, weights) if return_weights else out
