@@ -1,0 +1,147 @@
+/*
+ * milo.h - decode attention over a block-wise low-rank KV cache (C ABI).
+ *
+ * The operation (MILO, Sec. 4.2 Eq. 3, Sec. 4.4 Alg. 1 inference stage, Sec. 4.1
+ * Eq. 1): a many-shot context is split into blocks; block b of T_b tokens keeps
+ * its keys and values as factors
+ *        K_b ~ P^K_b R^K_b,      V_b ~ P^V_b R^V_b,
+ * where P is T_b x r and R is r x (H_kv*d), with the diagonal of singular values
+ * already multiplied into P (or split between P and R in any way).  Ranks may
+ * differ per block and between K and V (Sec. 4.3, Sec. 4.4).  The columns of R
+ * are head-major: KV head g owns columns g*d .. g*d+d-1.  A decode step attends
+ * every query token to the selected blocks (the retriever's output, Alg. 1) and
+ * to that request's own uncompressed KV (the "dense tail"):
+ *        o_{i,h} = softmax(scale * [K_sel; K_tail,i] q_{i,h}) [V_sel; V_tail,i]
+ * with query head h reading KV head g = h / (H_q / H_kv).  The library computes
+ * this in each block's rank space (project the query through R^K, score against
+ * P^K rows, accumulate weights times P^V rows, up-project through R^V) and merges
+ * blocks and tail with a log-sum-exp reduction; it never rebuilds K or V.
+ *
+ * Conventions
+ *  - bf16 values are passed as uint16_t bit patterns; all buffers row-major and
+ *    C-contiguous.  Output is fp32.  Accumulation is fp32.
+ *  - "host" pointers are ordinary CPU memory; "device" pointers are HIP device
+ *    memory of the current device (e.g. torch tensors on cuda:N).
+ *  - Every function returns a status code (MILO_OK = 0, negative on error) and
+ *    never throws.  On error, milo_last_error() holds a message for the calling
+ *    thread.  Argument checks happen on the host before any GPU work is queued.
+ *  - milo_attend_decode is asynchronous: it only enqueues kernels on hip_stream
+ *    (NULL = the default stream).  Errors inside kernels surface at the next
+ *    synchronisation.
+ */
+#ifndef MILO_H
+#define MILO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MILO_OK 0
+#define MILO_ERR_INVALID_ARG (-1)   /* bad pointer, shape, rank, id or length   */
+#define MILO_ERR_OUT_OF_MEMORY (-2) /* device allocation failed or over the cap */
+#define MILO_ERR_HIP (-3)           /* a HIP runtime call failed                */
+#define MILO_ERR_UNSUPPORTED (-4)   /* valid input this build does not handle   */
+
+/* Opaque cache handle: owns one device buffer with every block's factors in the
+ * library's packed layout, plus per-call workspace. */
+typedef struct milo_cache milo_cache;
+
+/* Shape of a low-rank cache (Sec. 4.2: per-block factors, Sec. 4.3: per-block
+ * ranks).  All arrays are host memory, read during milo_cache_create only.
+ *   n_blocks      number of blocks N >= 1
+ *   n_kv_heads    H_kv >= 1
+ *   head_dim      d, 64 or 128 (others return MILO_ERR_UNSUPPORTED)
+ *   block_tokens  [n_blocks] T_b >= 1
+ *   rank_k/v      [n_blocks] 1 <= r <= min(T_b, H_kv*d); this build supports
+ *                 r <= 960 (larger ranks return MILO_ERR_UNSUPPORTED). */
+typedef struct milo_cache_desc {
+  int32_t n_blocks;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  const int32_t* block_tokens;
+  const int32_t* rank_k;
+  const int32_t* rank_v;
+} milo_cache_desc;
+
+/* Build a cache from per-block factors (LC.Store of Alg. 1, encoding stage, with
+ * the singular values folded into P).
+ *   pk, pv        [n_blocks] pointers to bf16 P^K_b [T_b][rank_k_b], P^V_b [T_b][rank_v_b]
+ *   rk, rv        [n_blocks] pointers to bf16 R^K_b [rank_k_b][H_kv*d], R^V_b [rank_v_b][H_kv*d]
+ *   src_on_device 0: the factor pointers are host memory; 1: device memory.
+ *                 The pointer arrays themselves are always host memory.
+ *   hip_stream    stream used for the copies and packing kernels.
+ *   out           receives the handle (set to NULL on failure).
+ * Synchronous: when it returns the caller may free or reuse its factor buffers.
+ * Errors: INVALID_ARG (null pointer, bad shape or rank), UNSUPPORTED (head_dim,
+ * rank above the supported maximum), OUT_OF_MEMORY (hipMalloc failed, or the
+ * total exceeds the byte cap in the MILO_MAX_DEVICE_BYTES environment variable),
+ * HIP_ERROR. */
+int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk,
+                      const uint16_t* const* rk, const uint16_t* const* pv,
+                      const uint16_t* const* rv, int src_on_device, void* hip_stream,
+                      milo_cache** out);
+
+/* One decode step of attention over the selected blocks plus each request's
+ * dense tail (Alg. 1 inference stage; Eq. 1).
+ *   cache         from milo_cache_create, on the current device.
+ *   block_table   host [n_sel] distinct block ids in [0, n_blocks) (the retriever's
+ *                 selection; any order gives the same result up to rounding).
+ *                 May be NULL when n_sel == 0 (tail-only attention).
+ *   n_q           decode batch: independent query tokens sharing the context, >= 1.
+ *   n_q_heads     H_q, a multiple of H_kv with H_q / H_kv <= 16.
+ *   q             device bf16 [n_q][H_q][d].
+ *   tail_k/v      device bf16 [n_q][tail_cap][H_kv][d]; request i uses its first
+ *                 tail_len[i] rows.  May be NULL when tail_cap == 0.
+ *   tail_len      host [n_q], 0 <= tail_len[i] <= tail_cap; may be NULL when
+ *                 tail_cap == 0.  Every request must see at least one key
+ *                 (n_sel > 0 or tail_len[i] > 0).
+ *   scale         softmax temperature, usually 1/sqrt(d) (Eq. 1); finite.
+ *   out           device fp32 [n_q][H_q][d], fully overwritten.
+ *   hip_stream    stream the work is queued on.
+ * q, tail_k, tail_v and out are borrowed until the queued work completes.  The
+ * cache's workspace is shared by its calls: calls on one cache must be ordered on
+ * one stream (calls on different streams race).  Workspace growth and a change of
+ * (block_table, n_q, H_q, tail_len, tail_cap) since the previous call allocate or
+ * upload synchronously; repeated calls with the same arguments do neither.
+ * Errors: INVALID_ARG, UNSUPPORTED, OUT_OF_MEMORY, HIP_ERROR. */
+int milo_attend_decode(milo_cache* cache, const int32_t* block_table, int32_t n_sel,
+                       int32_t n_q, int32_t n_q_heads, const uint16_t* q,
+                       const uint16_t* tail_k, const uint16_t* tail_v,
+                       const int32_t* tail_len, int32_t tail_cap, float scale, float* out,
+                       void* hip_stream);
+
+/* Release the cache and its device memory (synchronises the device first).
+ * NULL is accepted and ignored. */
+void milo_cache_free(milo_cache* cache);
+
+/* Message describing the last error on the calling thread ("" if none). The
+ * pointer stays valid until the thread's next library call. */
+const char* milo_last_error(void);
+
+/* Bytes of device memory the cache holds for its packed factors. Returns
+ * INVALID_ARG for NULL arguments. */
+int milo_cache_device_bytes(const milo_cache* cache, int64_t* bytes);
+
+/* Copy one stored factor of one block back to host memory in the caller's
+ * row-major layout (for checking the packed layout).  which: 0 = P^K, 1 = R^K,
+ * 2 = P^V, 3 = R^V.  dst: host buffer of the factor's size in uint16_t.
+ * Synchronous.  Errors: INVALID_ARG, HIP_ERROR. */
+int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which,
+                           uint16_t* dst);
+
+/* Kernel timing for measurement.  While enabled, every milo_attend_decode
+ * records HIP events on its stream around its attention kernel (the fused
+ * projection / score / latent-V / up-projection / tail kernel) and around its
+ * merge kernel.  milo_timing_read synchronises on those events, returns the
+ * summed durations in milliseconds and the number of calls, and clears them.
+ * Any argument of milo_timing_read may be NULL. */
+int milo_timing_enable(int enable);
+int milo_timing_read(double* attend_kernel_ms, double* merge_kernel_ms, int64_t* n_calls);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MILO_H */

@@ -1,0 +1,507 @@
+// Host side of the C ABI in include/milo.h: argument validation, the packed
+// cache (Sec. 4.2 factors stored per block with per-block ranks, Sec. 4.3),
+// the per-call work plan and the kernel launches of one decode step
+// (Alg. 1 inference stage: attention over the selected blocks plus the
+// request's own KV).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "milo.h"
+#include "milo_internal.h"
+
+using namespace milo;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  const int code = (e == hipErrorOutOfMemory) ? MILO_ERR_OUT_OF_MEMORY : MILO_ERR_HIP;
+  return fail(code, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define MILO_HIP(call)                                    \
+  do {                                                    \
+    hipError_t e_ = (call);                               \
+    if (e_ != hipSuccess) return hip_fail(e_, #call);     \
+  } while (0)
+
+constexpr int kXcds = 8;          // gfx950: 8 accelerator dies, workgroups dealt round-robin
+constexpr int kTailChunk = 128;   // dense-tail tokens per work item
+constexpr int64_t kAlignElems = 128;  // 256-byte alignment of every packed factor
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+int64_t env_byte_cap() {
+  const char* s = std::getenv("MILO_MAX_DEVICE_BYTES");
+  if (!s || !*s) return -1;
+  return std::strtoll(s, nullptr, 10);
+}
+
+// Timing hooks (measurement only).
+struct TimingState {
+  std::mutex mu;
+  bool enabled = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<hipEvent_t> recorded;  // groups of 3: start, after attend kernel, after merge
+};
+TimingState g_timing;
+
+}  // namespace
+
+struct milo_cache {
+  int device = -1;
+  int n_blocks = 0, n_kv = 0, d = 0;
+  std::vector<int32_t> T, rk, rv;
+  std::vector<BlockMeta> meta;
+  uint16_t* data = nullptr;
+  int64_t data_elems = 0;
+  BlockMeta* meta_d = nullptr;
+  // per-call workspace
+  float* part_o = nullptr;
+  float2* part_ml = nullptr;
+  int64_t part_cols_slots = 0;  // capacity in (column, slot) pairs
+  int4* tasks_d = nullptr;
+  int64_t tasks_cap = 0;
+  int32_t* tail_len_d = nullptr;
+  int64_t tail_len_cap = 0;
+  int4* tasks_pinned = nullptr;
+  int32_t* tail_len_pinned = nullptr;
+  int64_t pinned_tasks_cap = 0, pinned_tl_cap = 0;
+  // the plan of the previous call
+  std::vector<int32_t> plan_key;
+  int grid = 0, n_slots = 0, max_rt = 0, rk_pad_max = 0;
+  size_t lds = 0;
+};
+
+namespace {
+
+FactorGeom geom_of(const milo_cache& c, int b, int which) {
+  FactorGeom f{};
+  f.kind = which;
+  f.n_kv = c.n_kv;
+  f.d = c.d;
+  const int D = c.n_kv * c.d;
+  f.T_pad = (int)round_up(c.T[b], 32);
+  switch (which) {
+    case kPK: f.rows = c.T[b]; f.cols = c.rk[b]; f.r_pad = (int)round_up(c.rk[b], 32); break;
+    case kRK: f.rows = c.rk[b]; f.cols = D; f.r_pad = (int)round_up(c.rk[b], 32); break;
+    case kPV: f.rows = c.T[b]; f.cols = c.rv[b]; f.r_pad = (int)round_up(c.rv[b], 32); break;
+    default:  f.rows = c.rv[b]; f.cols = D; f.r_pad = (int)round_up(c.rv[b], 32); break;
+  }
+  return f;
+}
+
+int64_t factor_offset(const BlockMeta& m, int which) {
+  switch (which) {
+    case kPK: return m.off_pk;
+    case kRK: return m.off_rk;
+    case kPV: return m.off_pv;
+    default:  return m.off_rv;
+  }
+}
+
+void destroy(milo_cache* c) {
+  if (!c) return;
+  if (c->device >= 0) {
+    int cur = -1;
+    if (hipGetDevice(&cur) == hipSuccess && cur != c->device) (void)hipSetDevice(c->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(c->data);
+    (void)hipFree(c->meta_d);
+    (void)hipFree(c->part_o);
+    (void)hipFree(c->part_ml);
+    (void)hipFree(c->tasks_d);
+    (void)hipFree(c->tail_len_d);
+    (void)hipHostFree(c->tasks_pinned);
+    (void)hipHostFree(c->tail_len_pinned);
+    if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
+  }
+  delete c;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* milo_last_error(void) { return g_err.c_str(); }
+
+int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, const uint16_t* const* rk,
+                      const uint16_t* const* pv, const uint16_t* const* rv, int src_on_device,
+                      void* hip_stream, milo_cache** out) {
+  g_err.clear();
+  if (!out) return fail(MILO_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!desc) return fail(MILO_ERR_INVALID_ARG, "desc is NULL");
+  if (desc->n_blocks < 1) return fail(MILO_ERR_INVALID_ARG, "n_blocks must be >= 1 (got %d)", desc->n_blocks);
+  if (desc->n_kv_heads < 1) return fail(MILO_ERR_INVALID_ARG, "n_kv_heads must be >= 1");
+  if (desc->head_dim != 64 && desc->head_dim != 128)
+    return fail(MILO_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", desc->head_dim);
+  if (!desc->block_tokens || !desc->rank_k || !desc->rank_v)
+    return fail(MILO_ERR_INVALID_ARG, "block_tokens / rank_k / rank_v must be non-NULL");
+  if (!pk || !rk || !pv || !rv) return fail(MILO_ERR_INVALID_ARG, "factor pointer arrays must be non-NULL");
+  if (src_on_device != 0 && src_on_device != 1) return fail(MILO_ERR_INVALID_ARG, "src_on_device must be 0 or 1");
+  const int64_t D = (int64_t)desc->n_kv_heads * desc->head_dim;
+  for (int b = 0; b < desc->n_blocks; ++b) {
+    const int T = desc->block_tokens[b], a = desc->rank_k[b], v = desc->rank_v[b];
+    if (T < 1) return fail(MILO_ERR_INVALID_ARG, "block %d: T_b must be >= 1 (got %d)", b, T);
+    if (a < 1 || a > T || a > D || v < 1 || v > T || v > D)
+      return fail(MILO_ERR_INVALID_ARG, "block %d: ranks (%d, %d) must lie in [1, min(T_b=%d, H_kv*d=%lld)]",
+                  b, a, v, T, (long long)D);
+    if (a > kMaxRank || v > kMaxRank)
+      return fail(MILO_ERR_UNSUPPORTED, "block %d: rank above the supported maximum %d", b, kMaxRank);
+    if (!pk[b] || !rk[b] || !pv[b] || !rv[b]) return fail(MILO_ERR_INVALID_ARG, "block %d: NULL factor", b);
+  }
+
+  milo_cache* c = new milo_cache();
+  c->n_blocks = desc->n_blocks;
+  c->n_kv = desc->n_kv_heads;
+  c->d = desc->head_dim;
+  c->T.assign(desc->block_tokens, desc->block_tokens + c->n_blocks);
+  c->rk.assign(desc->rank_k, desc->rank_k + c->n_blocks);
+  c->rv.assign(desc->rank_v, desc->rank_v + c->n_blocks);
+  c->meta.resize(c->n_blocks);
+  int64_t off = 0, max_src = 0;
+  for (int b = 0; b < c->n_blocks; ++b) {
+    BlockMeta& m = c->meta[b];
+    m.T = c->T[b];
+    m.T_pad = (int)round_up(c->T[b], 32);
+    m.rk_pad = (int)round_up(c->rk[b], 32);
+    m.rv_pad = (int)round_up(c->rv[b], 32);
+    int64_t* offs[4] = {&m.off_pk, &m.off_rk, &m.off_pv, &m.off_rv};
+    for (int w = 0; w < 4; ++w) {
+      const FactorGeom f = geom_of(*c, b, w);
+      *offs[w] = off;
+      off = round_up(off + frag_count(f) * kFragElems, kAlignElems);
+      max_src = std::max<int64_t>(max_src, (int64_t)f.rows * f.cols);
+    }
+  }
+  c->data_elems = off;
+  const int64_t need = off * 2 + (int64_t)sizeof(BlockMeta) * c->n_blocks +
+                       (src_on_device ? 0 : max_src * 2);
+  const int64_t cap = env_byte_cap();
+  if (cap >= 0 && need > cap) {
+    delete c;
+    return fail(MILO_ERR_OUT_OF_MEMORY, "cache needs %lld device bytes, above MILO_MAX_DEVICE_BYTES=%lld",
+                (long long)need, (long long)cap);
+  }
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  uint16_t* staging = nullptr;
+  auto cleanup_fail = [&](int code) {
+    if (staging) (void)hipFree(staging);
+    destroy(c);
+    return code;
+  };
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) { c->device = -1; return cleanup_fail(hip_fail(e, "hipGetDevice")); }
+  if ((e = hipMalloc(&c->data, (size_t)c->data_elems * 2)) != hipSuccess)
+    return cleanup_fail(hip_fail(e, "hipMalloc(packed factors)"));
+  if ((e = hipMalloc(&c->meta_d, sizeof(BlockMeta) * c->n_blocks)) != hipSuccess)
+    return cleanup_fail(hip_fail(e, "hipMalloc(block metadata)"));
+  if (!src_on_device && (e = hipMalloc(&staging, (size_t)max_src * 2)) != hipSuccess)
+    return cleanup_fail(hip_fail(e, "hipMalloc(staging)"));
+  const uint16_t* const* srcs[4] = {pk, rk, pv, rv};
+  for (int b = 0; b < c->n_blocks; ++b) {
+    for (int w = 0; w < 4; ++w) {
+      const FactorGeom f = geom_of(*c, b, w);
+      const uint16_t* src = srcs[w][b];
+      if (!src_on_device) {
+        if ((e = hipMemcpyAsync(staging, src, (size_t)f.rows * f.cols * 2, hipMemcpyHostToDevice, s)) != hipSuccess)
+          return cleanup_fail(hip_fail(e, "hipMemcpyAsync(factor)"));
+        src = staging;
+      }
+      PackArgs pa{src, c->data + factor_offset(c->meta[b], w), f, frag_count(f)};
+      if ((e = launch_pack(pa, s)) != hipSuccess) return cleanup_fail(hip_fail(e, "pack kernel"));
+    }
+  }
+  if ((e = hipMemcpyAsync(c->meta_d, c->meta.data(), sizeof(BlockMeta) * c->n_blocks, hipMemcpyHostToDevice, s)) !=
+      hipSuccess)
+    return cleanup_fail(hip_fail(e, "hipMemcpyAsync(metadata)"));
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return cleanup_fail(hip_fail(e, "hipStreamSynchronize"));
+  if (staging) (void)hipFree(staging);
+  staging = nullptr;
+  *out = c;
+  return MILO_OK;
+}
+
+void milo_cache_free(milo_cache* cache) { destroy(cache); }
+
+int milo_cache_device_bytes(const milo_cache* cache, int64_t* bytes) {
+  g_err.clear();
+  if (!cache || !bytes) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
+  *bytes = cache->data_elems * 2;
+  return MILO_OK;
+}
+
+int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which, uint16_t* dst) {
+  g_err.clear();
+  if (!cache || !dst) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
+  if (block < 0 || block >= cache->n_blocks) return fail(MILO_ERR_INVALID_ARG, "block %d out of range", block);
+  if (which < 0 || which > 3) return fail(MILO_ERR_INVALID_ARG, "which must be 0..3");
+  const FactorGeom f = geom_of(*cache, block, which);
+  const int64_t n = frag_count(f) * kFragElems;
+  std::vector<uint16_t> packed((size_t)n);
+  MILO_HIP(hipMemcpy(packed.data(), cache->data + factor_offset(cache->meta[block], which), (size_t)n * 2,
+                     hipMemcpyDeviceToHost));
+  for (int64_t fr = 0; fr < frag_count(f); ++fr)
+    for (int lane = 0; lane < 64; ++lane)
+      for (int e = 0; e < 8; ++e) {
+        int row, col;
+        frag_source(f, fr, lane, e, &row, &col);
+        if (row < f.rows && col < f.cols) dst[(int64_t)row * f.cols + col] = packed[(size_t)(fr * kFragElems + lane * 8 + e)];
+      }
+  return MILO_OK;
+}
+
+int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_q, int32_t n_q_heads,
+                       const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
+                       int32_t tail_cap, float scale, float* out, void* hip_stream) {
+  g_err.clear();
+  // ---- validation (host only, nothing queued yet) ----
+  if (!c) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
+  if (n_sel < 0) return fail(MILO_ERR_INVALID_ARG, "n_sel must be >= 0");
+  if (n_sel > 0 && !block_table) return fail(MILO_ERR_INVALID_ARG, "block_table is NULL");
+  if (n_q < 1) return fail(MILO_ERR_INVALID_ARG, "n_q must be >= 1");
+  if (n_q_heads < 1 || n_q_heads % c->n_kv != 0)
+    return fail(MILO_ERR_INVALID_ARG, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)", n_q_heads,
+                c->n_kv);
+  const int G = n_q_heads / c->n_kv;
+  if (G > kMaxGroup) return fail(MILO_ERR_UNSUPPORTED, "more than %d query heads per KV head", kMaxGroup);
+  if (!q || !out) return fail(MILO_ERR_INVALID_ARG, "q / out must be non-NULL");
+  if (tail_cap < 0) return fail(MILO_ERR_INVALID_ARG, "tail_cap must be >= 0");
+  if (tail_cap > 0 && (!tail_k || !tail_v || !tail_len))
+    return fail(MILO_ERR_INVALID_ARG, "tail_k / tail_v / tail_len must be non-NULL when tail_cap > 0");
+  if (!std::isfinite(scale)) return fail(MILO_ERR_INVALID_ARG, "scale must be finite");
+  if ((int64_t)n_q * n_q_heads > (int64_t)1 << 24) return fail(MILO_ERR_UNSUPPORTED, "too many query columns");
+  std::vector<int32_t> tl(n_q, 0);
+  for (int i = 0; i < n_q; ++i) {
+    if (tail_cap > 0) tl[i] = tail_len[i];
+    if (tl[i] < 0 || tl[i] > tail_cap)
+      return fail(MILO_ERR_INVALID_ARG, "tail_len[%d]=%d outside [0, tail_cap=%d]", i, tl[i], tail_cap);
+    if (n_sel == 0 && tl[i] == 0) return fail(MILO_ERR_INVALID_ARG, "request %d has no keys to attend to", i);
+  }
+  if (n_sel > 0) {
+    std::vector<char> seen(c->n_blocks, 0);
+    for (int j = 0; j < n_sel; ++j) {
+      const int b = block_table[j];
+      if (b < 0 || b >= c->n_blocks)
+        return fail(MILO_ERR_INVALID_ARG, "block_table[%d]=%d outside [0, %d)", j, b, c->n_blocks);
+      if (seen[b]) return fail(MILO_ERR_INVALID_ARG, "block id %d selected twice", b);
+      seen[b] = 1;
+    }
+  }
+  int dev = -1;
+  MILO_HIP(hipGetDevice(&dev));
+  if (dev != c->device) return fail(MILO_ERR_INVALID_ARG, "cache lives on device %d, current device is %d", c->device, dev);
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+
+  // ---- plan (rebuilt only when the call's shape changes) ----
+  std::vector<int32_t> key;
+  key.reserve(6 + n_sel + n_q);
+  key.push_back(n_sel);
+  key.push_back(n_q);
+  key.push_back(n_q_heads);
+  key.push_back(tail_cap);
+  key.insert(key.end(), block_table, block_table + n_sel);
+  key.insert(key.end(), tl.begin(), tl.end());
+  const int n_cols = n_q * n_q_heads;
+  int max_chunks = 0;
+  for (int i = 0; i < n_q; ++i) max_chunks = std::max(max_chunks, (tl[i] + kTailChunk - 1) / kTailChunk);
+  const int n_slots = n_sel + max_chunks;
+  if (key != c->plan_key) {
+    const int ncg = n_q * G;
+    const int n_ct = (ncg + kCols - 1) / kCols;
+    // block items: a block's items (all KV heads and column tiles) stay on one XCD so
+    // its P factors are fetched from HBM once and re-read from that XCD's L2.
+    std::vector<int> order(n_sel);
+    std::iota(order.begin(), order.end(), 0);
+    auto cost = [&](int j) {
+      const int b = block_table[j];
+      const BlockMeta& m = c->meta[b];
+      return (int64_t)(m.T_pad + c->d) * (m.rk_pad + m.rv_pad);
+    };
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return cost(x) > cost(y); });
+    std::vector<std::vector<int4>> per_xcd(kXcds);
+    std::vector<int64_t> load(kXcds, 0);
+    int rk_pad_max = 32, rv_pad_max = 32;
+    for (int j : order) {
+      const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+      load[x] += cost(j);
+      const int b = block_table[j];
+      rk_pad_max = std::max(rk_pad_max, c->meta[b].rk_pad);
+      rv_pad_max = std::max(rv_pad_max, c->meta[b].rv_pad);
+      for (int g = 0; g < c->n_kv; ++g)
+        for (int ct = 0; ct < n_ct; ++ct) per_xcd[x].push_back(make_int4(b, j, g, ct));
+    }
+    size_t per = 0;
+    for (auto& v : per_xcd) per = std::max(per, v.size());
+    std::vector<int4> tasks;
+    tasks.reserve(per * kXcds + (size_t)n_q * c->n_kv * max_chunks);
+    for (size_t k = 0; k < per; ++k)
+      for (int x = 0; x < kXcds; ++x)
+        tasks.push_back(k < per_xcd[x].size() ? per_xcd[x][k] : make_int4(kEmptyTask, 0, 0, 0));
+    for (int i = 0; i < n_q; ++i)
+      for (int ch = 0; ch * kTailChunk < tl[i]; ++ch)
+        for (int g = 0; g < c->n_kv; ++g) tasks.push_back(make_int4(-1 - i, n_sel + ch, g, ch));
+    const int rt_need = (rv_pad_max / 32 + kWaves - 1) / kWaves;
+    int max_rt = 1;
+    for (int cand : {1, 2, 4, 6, 8})
+      if (cand >= rt_need) { max_rt = cand; break; }
+    // device buffers
+    const int64_t ntask = (int64_t)tasks.size();
+    if (ntask > c->tasks_cap) {
+      MILO_HIP(hipStreamSynchronize(s));
+      (void)hipFree(c->tasks_d);
+      (void)hipHostFree(c->tasks_pinned);
+      c->tasks_d = nullptr;
+      c->tasks_pinned = nullptr;
+      c->tasks_cap = 0;
+      MILO_HIP(hipMalloc(&c->tasks_d, sizeof(int4) * ntask));
+      MILO_HIP(hipHostMalloc(&c->tasks_pinned, sizeof(int4) * ntask, hipHostMallocDefault));
+      c->tasks_cap = ntask;
+    }
+    if (n_q > c->tail_len_cap) {
+      MILO_HIP(hipStreamSynchronize(s));
+      (void)hipFree(c->tail_len_d);
+      (void)hipHostFree(c->tail_len_pinned);
+      c->tail_len_d = nullptr;
+      c->tail_len_pinned = nullptr;
+      c->tail_len_cap = 0;
+      MILO_HIP(hipMalloc(&c->tail_len_d, sizeof(int32_t) * n_q));
+      MILO_HIP(hipHostMalloc(&c->tail_len_pinned, sizeof(int32_t) * n_q, hipHostMallocDefault));
+      c->tail_len_cap = n_q;
+    }
+    // the pinned staging buffers may still feed an earlier upload
+    MILO_HIP(hipStreamSynchronize(s));
+    std::memcpy(c->tasks_pinned, tasks.data(), sizeof(int4) * ntask);
+    std::memcpy(c->tail_len_pinned, tl.data(), sizeof(int32_t) * n_q);
+    if (ntask) MILO_HIP(hipMemcpyAsync(c->tasks_d, c->tasks_pinned, sizeof(int4) * ntask, hipMemcpyHostToDevice, s));
+    MILO_HIP(hipMemcpyAsync(c->tail_len_d, c->tail_len_pinned, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
+    c->grid = (int)ntask;
+    c->n_slots = n_slots;
+    c->max_rt = max_rt;
+    c->rk_pad_max = rk_pad_max;
+    c->lds = attend_lds_bytes(c->d, rk_pad_max, G, kTailChunk);
+    c->plan_key.swap(key);
+  }
+  const int64_t need = (int64_t)n_cols * c->n_slots;
+  if (need > c->part_cols_slots) {
+    MILO_HIP(hipStreamSynchronize(s));
+    (void)hipFree(c->part_o);
+    (void)hipFree(c->part_ml);
+    c->part_o = nullptr;
+    c->part_ml = nullptr;
+    c->part_cols_slots = 0;
+    const int64_t cap = env_byte_cap();
+    const int64_t bytes = need * ((int64_t)c->d * 4 + 8);
+    if (cap >= 0 && c->data_elems * 2 + bytes > cap)
+      return fail(MILO_ERR_OUT_OF_MEMORY, "workspace of %lld bytes exceeds MILO_MAX_DEVICE_BYTES", (long long)bytes);
+    MILO_HIP(hipMalloc(&c->part_o, (size_t)need * c->d * 4));
+    MILO_HIP(hipMalloc(&c->part_ml, (size_t)need * sizeof(float2)));
+    c->part_cols_slots = need;
+  }
+
+  // ---- launches ----
+  AttendArgs aa{};
+  aa.data = c->data;
+  aa.meta = c->meta_d;
+  aa.tasks = c->tasks_d;
+  aa.q = q;
+  aa.tail_k = tail_k;
+  aa.tail_v = tail_v;
+  aa.tail_len = c->tail_len_d;
+  aa.part_o = c->part_o;
+  aa.part_ml = c->part_ml;
+  aa.qscale = scale * 1.4426950408889634f;
+  aa.n_q = n_q;
+  aa.H_q = n_q_heads;
+  aa.H_kv = c->n_kv;
+  aa.G = G;
+  aa.tail_cap = tail_cap;
+  aa.tail_chunk = kTailChunk;
+  aa.n_slots = c->n_slots;
+  aa.qt_stride = c->rk_pad_max + 8;
+  MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out, n_q_heads, n_sel, c->n_slots, kTailChunk};
+
+  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+  bool timed = false;
+  {
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    if (g_timing.enabled) {
+      for (int k = 0; k < 3; ++k) {
+        if (g_timing.pool.empty()) {
+          hipEvent_t e;
+          MILO_HIP(hipEventCreate(&e));
+          g_timing.pool.push_back(e);
+        }
+        ev[k] = g_timing.pool.back();
+        g_timing.pool.pop_back();
+      }
+      timed = true;
+    }
+  }
+  if (timed) MILO_HIP(hipEventRecord(ev[0], s));
+  hipError_t e = launch_attend(aa, c->d, c->max_rt, c->grid, c->lds, s);
+  if (e != hipSuccess) return hip_fail(e, "attend kernel launch");
+  if (timed) MILO_HIP(hipEventRecord(ev[1], s));
+  e = launch_merge(ma, c->d, n_cols, s);
+  if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+  if (timed) {
+    MILO_HIP(hipEventRecord(ev[2], s));
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    g_timing.recorded.insert(g_timing.recorded.end(), ev, ev + 3);
+  }
+  return MILO_OK;
+}
+
+int milo_timing_enable(int enable) {
+  g_err.clear();
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.enabled = enable != 0;
+  return MILO_OK;
+}
+
+int milo_timing_read(double* attend_kernel_ms, double* merge_kernel_ms, int64_t* n_calls) {
+  g_err.clear();
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  double ta = 0.0, tm = 0.0;
+  const size_t n = g_timing.recorded.size() / 3;
+  for (size_t k = 0; k < n; ++k) {
+    hipEvent_t* e = &g_timing.recorded[3 * k];
+    MILO_HIP(hipEventSynchronize(e[2]));
+    float a = 0.f, m = 0.f;
+    MILO_HIP(hipEventElapsedTime(&a, e[0], e[1]));
+    MILO_HIP(hipEventElapsedTime(&m, e[1], e[2]));
+    ta += a;
+    tm += m;
+  }
+  g_timing.pool.insert(g_timing.pool.end(), g_timing.recorded.begin(), g_timing.recorded.end());
+  g_timing.recorded.clear();
+  if (attend_kernel_ms) *attend_kernel_ms = ta;
+  if (merge_kernel_ms) *merge_kernel_ms = tm;
+  if (n_calls) *n_calls = (int64_t)n;
+  return MILO_OK;
+}
+
+}  // extern "C"

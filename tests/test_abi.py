@@ -1,0 +1,99 @@
+"""The C ABI without a GPU: the library loads, exports every entry point that
+include/milo.h declares, and rejects bad arguments on the host before any HIP
+call (no compute is launched here)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2609_29913_amd import milo
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "milo.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(milo_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("milo_cache_create", "milo_attend_decode", "milo_cache_free", "milo_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = milo.lib()
+    out = subprocess.run(["nm", "-D", "--defined-only", milo.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (milo_\w+)", out))
+    for n in declared_functions():
+        assert n in exported, n
+        assert hasattr(L, n)
+
+
+def _desc(nb=1, nkv=1, d=64, T=(64,), rk=(8,), rv=(8,)):
+    bt, a, b = (ctypes.c_int32 * nb)(*T), (ctypes.c_int32 * nb)(*rk), (ctypes.c_int32 * nb)(*rv)
+    return milo.milo_cache_desc(nb, nkv, d, bt, a, b), (bt, a, b)
+
+
+def _create(desc, nb=1, null_factor=False):
+    buf = np.zeros(1 << 16, dtype=np.uint16)
+    ptrs = [(ctypes.c_void_p * nb)(*([None if null_factor else buf.ctypes.data] * nb)) for _ in range(4)]
+    out = ctypes.c_void_p(123)
+    rc = milo.lib().milo_cache_create(ctypes.byref(desc), *ptrs, 0, None, ctypes.byref(out))
+    return rc, out
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(nb=1, T=(0,), rk=(1,), rv=(1,)), milo.MILO_ERR_INVALID_ARG),        # empty block
+    (dict(nb=1, T=(4,), rk=(5,), rv=(1,)), milo.MILO_ERR_INVALID_ARG),        # rank > T_b
+    (dict(nb=1, T=(300,), rk=(65,), rv=(8,)), milo.MILO_ERR_INVALID_ARG),     # rank > H_kv*d
+    (dict(nb=1, T=(64,), rk=(8,), rv=(0,)), milo.MILO_ERR_INVALID_ARG),       # rank 0
+    (dict(nb=1, d=96, T=(64,), rk=(8,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # head_dim
+    (dict(nb=1, nkv=8, d=128, T=(2048,), rk=(992,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # rank cap
+    (dict(nb=1, nkv=0, T=(64,), rk=(8,), rv=(8,)), milo.MILO_ERR_INVALID_ARG),
+])
+def test_create_rejects(kw, code):
+    desc, keep = _desc(**kw)
+    rc, out = _create(desc)
+    assert rc == code, milo.milo_last_error()
+    assert out.value is None
+    assert milo.milo_last_error() != ""
+
+
+def test_create_rejects_null_pointers():
+    desc, keep = _desc()
+    rc, _ = _create(desc, null_factor=True)
+    assert rc == milo.MILO_ERR_INVALID_ARG
+    out = ctypes.c_void_p()
+    assert milo.lib().milo_cache_create(None, None, None, None, None, 0, None, ctypes.byref(out)) == \
+        milo.MILO_ERR_INVALID_ARG
+    desc0, keep0 = _desc(nb=1)
+    desc0.n_blocks = 0
+    assert _create(desc0)[0] == milo.MILO_ERR_INVALID_ARG
+
+
+def test_create_byte_cap_is_out_of_memory(monkeypatch):
+    monkeypatch.setenv("MILO_MAX_DEVICE_BYTES", "1000")
+    desc, keep = _desc()
+    rc, _ = _create(desc)
+    assert rc == milo.MILO_ERR_OUT_OF_MEMORY
+    assert "MILO_MAX_DEVICE_BYTES" in milo.milo_last_error()
+
+
+def test_attend_null_cache_and_free_null():
+    rc = milo.lib().milo_attend_decode(None, None, 0, 1, 1, None, None, None, None, 0, 1.0, None, None)
+    assert rc == milo.MILO_ERR_INVALID_ARG
+    milo.milo_cache_free(None)
+    v = ctypes.c_int64()
+    assert milo.lib().milo_cache_device_bytes(None, ctypes.byref(v)) == milo.MILO_ERR_INVALID_ARG
+    assert milo.lib().milo_cache_read_factor(None, 0, 0, None) == milo.MILO_ERR_INVALID_ARG
+
+
+def test_timing_read_without_calls():
+    milo.milo_timing_enable(False)
+    assert milo.milo_timing_read() == (0.0, 0.0, 0)
