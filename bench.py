@@ -1,0 +1,254 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark: low-rank (block-wise factorised) KV-cache attention on one GPU.
+
+One step = one milo_attend_decode per layer of the workload: latent query
+projection, scores + online softmax + latent V, up-projection, dense tail and
+the log-sum-exp merge, for every query column of the decode batch.  Inputs are
+seeded synthetic tensors with the workload's shapes, resident in HBM before the
+timed region.  The default workload is a Qwen2.5-7B-shaped layer (28 query /
+4 KV heads, d=128, 64 blocks x 1024 tokens, ranks 64..512, 256-token dense tail
+per request, 8 decode queries).  A single-layer working set (~117 MB) fits in
+the 256 MB Infinity Cache, so steps rotate over independent copies of the layer
+(each with its own cache, queries and tails) until the rotation exceeds 512 MB.
+
+Prints one JSON line (see the fields below).  --gpus above 1 is rejected: this
+path runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+METRIC = "effective context tokens/s per decode step (1 GPU) + % of HBM roofline"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, AMD published
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_29913_amd", "csrc", f)
+                  for f in ("milo_kernels.hip", "milo_internal.h", "milo_api.cpp")]
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "attend_kernel_q7b_1l_counters.md")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(workload: str):
+    """HBM bytes per attention-kernel launch from the committed rocprofv3 counter
+    summary, or None when absent or taken on different kernel sources."""
+    if workload != "q7b_1l" or not os.path.exists(COUNTER_SUMMARY):
+        return None
+    txt = open(COUNTER_SUMMARY).read()
+    m = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    hsh = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", txt)
+    if not m or not hsh or hsh.group(1) != kernel_source_hash():
+        return None
+    return float(m.group(1))
+
+
+def to_device(a, dev):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
+
+
+class Layer:
+    def __init__(self, inp: synth.LayerInputs, dev):
+        import torch
+        from paper_2609_29913_amd import milo
+        self.inp = inp
+        self.cache = milo.milo_cache_create(inp.block_tokens, inp.rank_k, inp.rank_v, inp.n_kv_heads,
+                                            inp.head_dim, inp.pk, inp.rk, inp.pv, inp.rv)
+        self.q = to_device(inp.q, dev)
+        self.tk = to_device(inp.tail_k, dev)
+        self.tv = to_device(inp.tail_v, dev)
+        self.out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
+        self.table = list(range(inp.n_blocks))
+
+    def step(self, stream):
+        from paper_2609_29913_amd import milo
+        inp = self.inp
+        milo.milo_attend_decode(self.cache, self.table, self.q, self.tk, self.tv, inp.tail_len, inp.scale,
+                                self.out, stream=stream)
+
+
+def cpu_baseline(inp: synth.LayerInputs, n_layers: int, budget_s: float):
+    """The CPU oracle (fp64 numpy, latent order) timed on this host on the same
+    workload: whole layer steps repeated until ~budget_s of CPU work."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    f64 = synth.bf16_to_f64
+    args = dict(pk=[f64(x) for x in inp.pk], rk=[f64(x) for x in inp.rk], pv=[f64(x) for x in inp.pv],
+                rv=[f64(x) for x in inp.rv], table=list(range(inp.n_blocks)), q=f64(inp.q),
+                tail_k=f64(inp.tail_k), tail_v=f64(inp.tail_v), tail_len=inp.tail_len, scale=inp.scale)
+    times = []
+    t_start = time.perf_counter()
+    while not times or (time.perf_counter() - t_start < budget_s and len(times) < 50):
+        t0 = time.perf_counter()
+        oracle.attend_latent(**args)
+        times.append(time.perf_counter() - t0)
+    t_layer = float(np.median(times))
+    tokens = inp.n_q * (int(inp.block_tokens.sum()) + int(inp.tail_len.max()))
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    return {"value": tokens / (t_layer * n_layers), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"full layer step of the workload (fp64 numpy oracle, latent order), {len(times)} "
+                      f"repetitions, median {t_layer * 1e3:.1f} ms per layer"
+                      + (f", x{n_layers} layers" if n_layers > 1 else "")}
+
+
+def calibrate_copy(dev, n_bytes=1 << 30, reps=5):
+    """Plain device copy of known size (for scaling HBM byte counters)."""
+    import torch
+    a = torch.empty(n_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration_copy_bytes_read": n_bytes, "bytes_written": n_bytes, "reps": reps}))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="q7b_1l", choices=sorted(synth.CONFIGS))
+    ap.add_argument("--rotate-bytes", type=float, default=512e6,
+                    help="minimum bytes of distinct layer copies rotated over (defeats the Infinity Cache)")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true", help="only run a 1 GiB device copy (counter scaling)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this decode-attention path runs on one GPU; --gpus {args.gpus} is not supported "
+              "(multi-GPU sharding by blocks is described in DESIGN.md, not built).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.calibrate_copy:
+        calibrate_copy(dev)
+        return
+    from paper_2609_29913_amd import milo
+    milo.lib()
+
+    cfg = synth.CONFIGS[args.config]
+    layers_inp = [synth.gen_layer(cfg, l) for l in range(cfg.n_layers)]
+    per_step = sum(synth.algorithmic_bytes(x) for x in layers_inp)
+    copies = max(1, int(np.ceil(args.rotate_bytes / per_step)))
+    groups = [[Layer(x, dev) for x in layers_inp] for _ in range(copies)]
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def run_step(k):
+        for layer in groups[k % copies]:
+            layer.step(stream)
+
+    for k in range(args.warmup):
+        run_step(k)
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` decode steps, host wall clock between synchronisations
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        run_step(k)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    # second pass with HIP events around the attention kernel on the launch stream
+    milo.milo_timing_enable(True)
+    for k in range(args.steps):
+        run_step(k)
+    torch.cuda.synchronize()
+    att_ms, merge_ms, n_calls = milo.milo_timing_read()
+    milo.milo_timing_enable(False)
+    att_avg_s = att_ms / n_calls * 1e-3
+    merge_avg_s = merge_ms / n_calls * 1e-3
+
+    # the attention kernel reads every factor once, the tails and the queries
+    out_bytes = sum(4 * x.n_q * x.n_q_heads * x.head_dim for x in layers_inp)
+    kern_bytes = (per_step - out_bytes) / cfg.n_layers
+    flops = sum(synth.latent_flops(x) for x in layers_inp) / cfg.n_layers
+    achieved = kern_bytes / att_avg_s / 1e9
+    traffic = counter_traffic(args.config)
+
+    x0 = layers_inp[0]
+    ctx_tokens = int(x0.block_tokens.sum()) + int(x0.tail_len.max())
+    value = x0.n_q * ctx_tokens / (ms_per_step * 1e-3)
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) factors / N(0,1/r) R, bf16)",
+        "config": {
+            "workload": cfg.name,
+            "description": cfg.description,
+            "layers": cfg.n_layers,
+            "decode_batch": x0.n_q,
+            "context_tokens": int(x0.block_tokens.sum()),
+            "tail_tokens": int(x0.tail_len.max()),
+            "blocks": x0.n_blocks,
+            "q_heads": x0.n_q_heads,
+            "kv_heads": x0.n_kv_heads,
+            "head_dim": x0.head_dim,
+            "mean_rank": float(np.mean([x.rank_k.mean() for x in layers_inp])),
+            "accumulation": "fp32",
+            "rotated_copies": copies,
+            "step_bytes_algorithmic": per_step,
+            "hbm_frac_of_step": per_step / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "kernel": "attend_kernel",
+            "kernel_avg_us": att_avg_s * 1e6,
+            "merge_kernel_avg_us": merge_avg_s * 1e6,
+            "algorithmic_bytes_per_launch": kern_bytes,
+            "mfma_tflops": flops / att_avg_s / 1e12,
+            "mfma_frac": flops / att_avg_s / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+            "kernel_source_sha256_16": kernel_source_hash(),
+        },
+        "cpu_baseline": None,
+    }
+    for grp in groups:
+        for layer in grp:
+            milo.milo_cache_free(layer.cache)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(x0, cfg.n_layers, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -47,7 +47,7 @@ int hip_fail(hipError_t e, const char* what) {
   } while (0)
 
 constexpr int kXcds = 8;          // gfx950: 8 accelerator dies, workgroups dealt round-robin
-constexpr int kTailChunk = 128;   // dense-tail tokens per work item
+constexpr int kCUs = 256;         // compute units of an MI355X
 constexpr int64_t kAlignElems = 128;  // 256-byte alignment of every packed factor
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -76,21 +76,20 @@ struct milo_cache {
   std::vector<BlockMeta> meta;
   uint16_t* data = nullptr;
   int64_t data_elems = 0;
-  BlockMeta* meta_d = nullptr;
   // per-call workspace
   float* part_o = nullptr;
   float2* part_ml = nullptr;
   int64_t part_cols_slots = 0;  // capacity in (column, slot) pairs
-  int4* tasks_d = nullptr;
+  WorkItem* tasks_d = nullptr;
   int64_t tasks_cap = 0;
   int32_t* tail_len_d = nullptr;
   int64_t tail_len_cap = 0;
-  int4* tasks_pinned = nullptr;
+  WorkItem* tasks_pinned = nullptr;
   int32_t* tail_len_pinned = nullptr;
   int64_t pinned_tasks_cap = 0, pinned_tl_cap = 0;
   // the plan of the previous call
   std::vector<int32_t> plan_key;
-  int grid = 0, n_slots = 0, max_rt = 0, rk_pad_max = 0;
+  int grid = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0, ring_offset = 0;
   size_t lds = 0;
 };
 
@@ -102,7 +101,7 @@ FactorGeom geom_of(const milo_cache& c, int b, int which) {
   f.n_kv = c.n_kv;
   f.d = c.d;
   const int D = c.n_kv * c.d;
-  f.T_pad = (int)round_up(c.T[b], 32);
+  f.T_pad = (int)round_up(c.T[b], kTile);
   switch (which) {
     case kPK: f.rows = c.T[b]; f.cols = c.rk[b]; f.r_pad = (int)round_up(c.rk[b], 32); break;
     case kRK: f.rows = c.rk[b]; f.cols = D; f.r_pad = (int)round_up(c.rk[b], 32); break;
@@ -128,7 +127,6 @@ void destroy(milo_cache* c) {
     if (hipGetDevice(&cur) == hipSuccess && cur != c->device) (void)hipSetDevice(c->device);
     (void)hipDeviceSynchronize();
     (void)hipFree(c->data);
-    (void)hipFree(c->meta_d);
     (void)hipFree(c->part_o);
     (void)hipFree(c->part_ml);
     (void)hipFree(c->tasks_d);
@@ -185,7 +183,7 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
   for (int b = 0; b < c->n_blocks; ++b) {
     BlockMeta& m = c->meta[b];
     m.T = c->T[b];
-    m.T_pad = (int)round_up(c->T[b], 32);
+    m.T_pad = (int)round_up(c->T[b], kTile);
     m.rk_pad = (int)round_up(c->rk[b], 32);
     m.rv_pad = (int)round_up(c->rv[b], 32);
     int64_t* offs[4] = {&m.off_pk, &m.off_rk, &m.off_pv, &m.off_rv};
@@ -197,8 +195,7 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     }
   }
   c->data_elems = off;
-  const int64_t need = off * 2 + (int64_t)sizeof(BlockMeta) * c->n_blocks +
-                       (src_on_device ? 0 : max_src * 2);
+  const int64_t need = off * 2 + (src_on_device ? 0 : max_src * 2);
   const int64_t cap = env_byte_cap();
   if (cap >= 0 && need > cap) {
     delete c;
@@ -217,8 +214,6 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
   if (e != hipSuccess) { c->device = -1; return cleanup_fail(hip_fail(e, "hipGetDevice")); }
   if ((e = hipMalloc(&c->data, (size_t)c->data_elems * 2)) != hipSuccess)
     return cleanup_fail(hip_fail(e, "hipMalloc(packed factors)"));
-  if ((e = hipMalloc(&c->meta_d, sizeof(BlockMeta) * c->n_blocks)) != hipSuccess)
-    return cleanup_fail(hip_fail(e, "hipMalloc(block metadata)"));
   if (!src_on_device && (e = hipMalloc(&staging, (size_t)max_src * 2)) != hipSuccess)
     return cleanup_fail(hip_fail(e, "hipMalloc(staging)"));
   const uint16_t* const* srcs[4] = {pk, rk, pv, rv};
@@ -235,9 +230,6 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
       if ((e = launch_pack(pa, s)) != hipSuccess) return cleanup_fail(hip_fail(e, "pack kernel"));
     }
   }
-  if ((e = hipMemcpyAsync(c->meta_d, c->meta.data(), sizeof(BlockMeta) * c->n_blocks, hipMemcpyHostToDevice, s)) !=
-      hipSuccess)
-    return cleanup_fail(hip_fail(e, "hipMemcpyAsync(metadata)"));
   if ((e = hipStreamSynchronize(s)) != hipSuccess) return cleanup_fail(hip_fail(e, "hipStreamSynchronize"));
   if (staging) (void)hipFree(staging);
   staging = nullptr;
@@ -328,46 +320,97 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   const int n_cols = n_q * n_q_heads;
   int max_chunks = 0;
   for (int i = 0; i < n_q; ++i) max_chunks = std::max(max_chunks, (tl[i] + kTailChunk - 1) / kTailChunk);
-  const int n_slots = n_sel + max_chunks;
   if (key != c->plan_key) {
     const int ncg = n_q * G;
     const int n_ct = (ncg + kCols - 1) / kCols;
-    // block items: a block's items (all KV heads and column tiles) stay on one XCD so
-    // its P factors are fetched from HBM once and re-read from that XCD's L2.
-    std::vector<int> order(n_sel);
-    std::iota(order.begin(), order.end(), 0);
-    auto cost = [&](int j) {
+    // Cost of one work item (one KV head, one column tile) over `nt` tiles of a
+    // block: the streamed factor bytes plus the projection / up-projection work.
+    auto item_cost = [&](const BlockMeta& m, int nt) {
+      return (int64_t)(nt * kTile + 2 * c->d) * (m.rk_pad + m.rv_pad);
+    };
+    int64_t total = 0;
+    for (int j = 0; j < n_sel; ++j) {
+      const BlockMeta& m = c->meta[block_table[j]];
+      total += item_cost(m, m.T_pad / kTile) * c->n_kv * n_ct;
+    }
+    const int64_t share = std::max<int64_t>(1, total / kCUs);
+    // A block whose items would exceed the per-CU share is split into parts of
+    // whole tiles; every part writes its own partial slot.
+    struct Part { int b, tile0, ntile; int64_t cost; };
+    std::vector<Part> parts;
+    for (int j = 0; j < n_sel; ++j) {
       const int b = block_table[j];
       const BlockMeta& m = c->meta[b];
-      return (int64_t)(m.T_pad + c->d) * (m.rk_pad + m.rv_pad);
-    };
-    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return cost(x) > cost(y); });
-    std::vector<std::vector<int4>> per_xcd(kXcds);
+      const int nt = m.T_pad / kTile;
+      const int np = (int)std::min<int64_t>(nt, std::max<int64_t>(1, (item_cost(m, nt) + share - 1) / share));
+      for (int p = 0; p < np; ++p) {
+        const int t_a = (int)((int64_t)nt * p / np), t_b = (int)((int64_t)nt * (p + 1) / np);
+        parts.push_back({b, t_a, t_b - t_a, item_cost(m, t_b - t_a)});
+      }
+    }
+    const int n_parts = (int)parts.size();
+    const int n_slots = n_parts + max_chunks;
+    // Parts are dealt to the XCDs largest first (each XCD takes the next part
+    // while it has the least work); a part's items (all KV heads and column
+    // tiles) stay on one XCD, so its P factors are fetched from HBM once and
+    // re-read from that XCD's L2.
+    std::vector<int> order(n_parts);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return parts[x].cost > parts[y].cost; });
+    std::vector<std::vector<WorkItem>> per_xcd(kXcds);
     std::vector<int64_t> load(kXcds, 0);
     int rk_pad_max = 32, rv_pad_max = 32;
-    for (int j : order) {
+    WorkItem w{};
+    for (int pi : order) {
+      const Part& pt = parts[pi];
       const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-      load[x] += cost(j);
-      const int b = block_table[j];
-      rk_pad_max = std::max(rk_pad_max, c->meta[b].rk_pad);
-      rv_pad_max = std::max(rv_pad_max, c->meta[b].rv_pad);
+      load[x] += pt.cost * c->n_kv * n_ct;
+      rk_pad_max = std::max(rk_pad_max, c->meta[pt.b].rk_pad);
+      rv_pad_max = std::max(rv_pad_max, c->meta[pt.b].rv_pad);
+      w.blk = c->meta[pt.b];
+      w.kind = kItemBlock;
+      w.slot = pi;
+      w.tile0 = pt.tile0;
+      w.ntile = pt.ntile;
       for (int g = 0; g < c->n_kv; ++g)
-        for (int ct = 0; ct < n_ct; ++ct) per_xcd[x].push_back(make_int4(b, j, g, ct));
+        for (int ct = 0; ct < n_ct; ++ct) {
+          w.g = g;
+          w.sub = ct;
+          per_xcd[x].push_back(w);
+        }
     }
     size_t per = 0;
     for (auto& v : per_xcd) per = std::max(per, v.size());
-    std::vector<int4> tasks;
-    tasks.reserve(per * kXcds + (size_t)n_q * c->n_kv * max_chunks);
-    for (size_t k = 0; k < per; ++k)
-      for (int x = 0; x < kXcds; ++x)
-        tasks.push_back(k < per_xcd[x].size() ? per_xcd[x][k] : make_int4(kEmptyTask, 0, 0, 0));
+    WorkItem empty{};
+    empty.kind = kItemEmpty;
+    // Dense-tail items go first (a whole number of rounds over the XCDs, padded
+    // with empty items) so they run while the memory system is still quiet;
+    // the block items follow, round-robin over the XCDs.
+    std::vector<WorkItem> tasks;
+    WorkItem tw{};
+    tw.kind = kItemTail;
     for (int i = 0; i < n_q; ++i)
       for (int ch = 0; ch * kTailChunk < tl[i]; ++ch)
-        for (int g = 0; g < c->n_kv; ++g) tasks.push_back(make_int4(-1 - i, n_sel + ch, g, ch));
+        for (int g = 0; g < c->n_kv; ++g) {
+          tw.req = i;
+          tw.slot = n_parts + ch;
+          tw.g = g;
+          tw.sub = ch;
+          tasks.push_back(tw);
+        }
+    while (tasks.size() % kXcds) tasks.push_back(empty);
+    tasks.reserve(tasks.size() + per * kXcds);
+    for (size_t k = 0; k < per; ++k)
+      for (int x = 0; x < kXcds; ++x) tasks.push_back(k < per_xcd[x].size() ? per_xcd[x][k] : empty);
     const int rt_need = (rv_pad_max / 32 + kWaves - 1) / kWaves;
-    int max_rt = 1;
-    for (int cand : {1, 2, 4, 6, 8})
+    int max_rt = 8;
+    for (int cand : {2, 4, 6, 8})
       if (cand >= rt_need) { max_rt = cand; break; }
+    // deepest fragment ring that fits next to the projected query and weight tile
+    const size_t base = attend_lds_base_bytes(c->d, rk_pad_max);
+    int nslot = 0;
+    for (int cand : {12, 6})
+      if (base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
     // device buffers
     const int64_t ntask = (int64_t)tasks.size();
     if (ntask > c->tasks_cap) {
@@ -377,8 +420,8 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
       c->tasks_d = nullptr;
       c->tasks_pinned = nullptr;
       c->tasks_cap = 0;
-      MILO_HIP(hipMalloc(&c->tasks_d, sizeof(int4) * ntask));
-      MILO_HIP(hipHostMalloc(&c->tasks_pinned, sizeof(int4) * ntask, hipHostMallocDefault));
+      MILO_HIP(hipMalloc(&c->tasks_d, sizeof(WorkItem) * ntask));
+      MILO_HIP(hipHostMalloc(&c->tasks_pinned, sizeof(WorkItem) * ntask, hipHostMallocDefault));
       c->tasks_cap = ntask;
     }
     if (n_q > c->tail_len_cap) {
@@ -394,15 +437,18 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     }
     // the pinned staging buffers may still feed an earlier upload
     MILO_HIP(hipStreamSynchronize(s));
-    std::memcpy(c->tasks_pinned, tasks.data(), sizeof(int4) * ntask);
+    std::memcpy(c->tasks_pinned, tasks.data(), sizeof(WorkItem) * ntask);
     std::memcpy(c->tail_len_pinned, tl.data(), sizeof(int32_t) * n_q);
-    if (ntask) MILO_HIP(hipMemcpyAsync(c->tasks_d, c->tasks_pinned, sizeof(int4) * ntask, hipMemcpyHostToDevice, s));
+    if (ntask) MILO_HIP(hipMemcpyAsync(c->tasks_d, c->tasks_pinned, sizeof(WorkItem) * ntask, hipMemcpyHostToDevice, s));
     MILO_HIP(hipMemcpyAsync(c->tail_len_d, c->tail_len_pinned, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
     c->grid = (int)ntask;
     c->n_slots = n_slots;
+    c->n_block_slots = n_parts;
     c->max_rt = max_rt;
+    c->nslot = nslot;
     c->rk_pad_max = rk_pad_max;
-    c->lds = attend_lds_bytes(c->d, rk_pad_max, G, kTailChunk);
+    c->ring_offset = (int)base;
+    c->lds = base + attend_ring_bytes(nslot);
     c->plan_key.swap(key);
   }
   const int64_t need = (int64_t)n_cols * c->n_slots;
@@ -425,8 +471,7 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   // ---- launches ----
   AttendArgs aa{};
   aa.data = c->data;
-  aa.meta = c->meta_d;
-  aa.tasks = c->tasks_d;
+  aa.items = c->tasks_d;
   aa.q = q;
   aa.tail_k = tail_k;
   aa.tail_v = tail_v;
@@ -439,10 +484,10 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   aa.H_kv = c->n_kv;
   aa.G = G;
   aa.tail_cap = tail_cap;
-  aa.tail_chunk = kTailChunk;
   aa.n_slots = c->n_slots;
   aa.qt_stride = c->rk_pad_max + 8;
-  MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out, n_q_heads, n_sel, c->n_slots, kTailChunk};
+  aa.ring_offset = c->ring_offset;
+  MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out, n_q_heads, c->n_block_slots, c->n_slots};
 
   hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
   bool timed = false;
@@ -462,7 +507,7 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     }
   }
   if (timed) MILO_HIP(hipEventRecord(ev[0], s));
-  hipError_t e = launch_attend(aa, c->d, c->max_rt, c->grid, c->lds, s);
+  hipError_t e = launch_attend(aa, c->d, c->max_rt, c->nslot, c->grid, c->lds, s);
   if (e != hipSuccess) return hip_fail(e, "attend kernel launch");
   if (timed) MILO_HIP(hipEventRecord(ev[1], s));
   e = launch_merge(ma, c->d, n_cols, s);

@@ -14,21 +14,46 @@ namespace milo {
 // 64 lanes x 8 bf16, exactly the per-lane operand of one
 // v_mfma_f32_32x32x16_bf16, so one wave loads one fragment with one fully
 // coalesced 16-byte load per lane.  Rows beyond T_b and ranks beyond r are
-// stored as zeros (token count padded to 32, ranks padded to 32).
+// stored as zeros (tokens padded to whole 256-token tiles, ranks to 32).
 //
 // Lane l = 32*c + m (c = lane group 0/1, m = 0..31), element e = 0..7.
-//   P^K frag (tau, kap):   P^K[32*tau + m][16*kap + 8*c + e]        (A: tokens x rank)
-//   P^V frag (sig, rho):   P^V[16*sig + 8*c + e][32*rho + m]        (A: rank x tokens)
-//   R^K frag (g, rho, kap): R^K[32*rho + m][g*d + 16*kap + 8*c + e] (A: rank x d)
-//   R^V frag (g, dlt, kap): R^V[16*kap + 8*(e/4) + 4*c + e%4][g*d + 32*dlt + m]
-//                                                                   (A: d x rank)
+//   P^K fragment (token sub-tile tau, rank step kap):
+//       P^K[32*tau + m][16*kap + 8*c + e]                         (A: tokens x rank)
+//   P^V fragment (token step sig, rank tile rho):
+//       P^V[16*sig + 8*c + e][32*rho + m]                         (A: rank x tokens)
+//   R^K fragment (KV head g, rank tile rho, d step kap):
+//       R^K[32*rho + m][g*d + 16*kap + 8*c + e]                   (A: rank x d)
+//   R^V fragment (KV head g, d tile dl, rank step kap):
+//       R^V[16*kap + 8*(e/4) + 4*c + e%4][g*d + 32*dl + m]        (A: d x rank)
 // The R^V rank order inside a 16-rank step matches the rows that one lane holds
 // in the fp32 accumulator of a 32x32 MFMA (rows 8*(v/4) + 4*c + v%4), so the
 // latent accumulator feeds the up-projection straight from registers.
-// Fragment order: P^K [tau][kap], P^V [sig][rho], R^K [g][rho][kap], R^V [g][dlt][kap].
+//
+// Fragment order follows the attention kernel's work split, so that every wave
+// of a workgroup reads each factor as one contiguous run in the order it
+// consumes it.  A 256-token tile t is split over the kWaves waves: wave w owns
+// token sub-tiles tau = 8t + 2w + {0,1}; rank tiles are dealt round-robin, wave
+// w owning rho = w + kWaves*j.
+//   P^K: [w][t][kap][tau%2]
+//   P^V: [w][sig][j]                (wave w's run has owned_tiles(nrt_v, w) per sig)
+//   R^K: [g][w][j][kap]
+//   R^V: [g][w][pass][j][half][dt]  (kap = 2*rho + half, dl = 2*pass + dt, 64-row passes)
 // ---------------------------------------------------------------------------
 constexpr int kFragElems = 512;  // 64 lanes x 8 bf16
+constexpr int kWaves = 4;        // waves per attention workgroup
+constexpr int kTile = 256;       // tokens per attention tile
 enum FactorKind : int { kPK = 0, kRK = 1, kPV = 2, kRV = 3 };
+
+// rank tiles dealt round-robin over the waves: how many wave w owns, and how
+// many the waves before it own
+__host__ __device__ inline int owned_tiles(int nrt, int w) {
+  return nrt > w ? (nrt - w + kWaves - 1) / kWaves : 0;
+}
+__host__ __device__ inline int owned_before(int nrt, int w) {
+  int s = 0;
+  for (int v = 0; v < w; ++v) s += owned_tiles(nrt, v);
+  return s;
+}
 
 struct FactorGeom {
   int kind;
@@ -46,41 +71,72 @@ __host__ __device__ inline int64_t frag_count(const FactorGeom& f) {
   }
 }
 
+// the wave whose run holds unit u, when wave w's run has per*owned_tiles(nrt, w)
+// units and the runs are stored in wave order; *first = start of that run
+__host__ __device__ inline int run_owner(int nrt, int64_t u, int64_t per, int64_t* first) {
+  int w = 0;
+  int64_t start = 0;
+  while (w + 1 < kWaves && u >= start + per * owned_tiles(nrt, w)) {
+    start += per * owned_tiles(nrt, w);
+    ++w;
+  }
+  *first = start;
+  return w;
+}
+
 // Source (row, col) of element e of lane `lane` in fragment `frag`.
 __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, int lane, int e,
                                             int* row, int* col) {
   const int m = lane & 31, c = lane >> 5;
   switch (f.kind) {
     case kPK: {
-      const int nk = f.r_pad / 16;
-      const int tau = (int)(frag / nk), kap = (int)(frag % nk);
+      const int nks = f.r_pad / 16, ntiles = f.T_pad / kTile;
+      const int mt = (int)(frag % 2);
+      const int kap = (int)((frag / 2) % nks);
+      const int t = (int)((frag / (2 * nks)) % ntiles);
+      const int w = (int)(frag / ((int64_t)2 * nks * ntiles));
+      const int tau = 8 * t + 2 * w + mt;
       *row = 32 * tau + m;
       *col = 16 * kap + 8 * c + e;
       return;
     }
     case kPV: {
-      const int nr = f.r_pad / 32;
-      const int sig = (int)(frag / nr), rho = (int)(frag % nr);
+      const int nrt = f.r_pad / 32, T16 = f.T_pad / 16;
+      int64_t first;
+      const int w = run_owner(nrt, frag, T16, &first);
+      const int own = owned_tiles(nrt, w);
+      const int64_t local = frag - first;
+      const int sig = (int)(local / own), j = (int)(local % own);
       *row = 16 * sig + 8 * c + e;
-      *col = 32 * rho + m;
+      *col = 32 * (w + kWaves * j) + m;
       return;
     }
     case kRK: {
-      const int nk = f.d / 16, nr = f.r_pad / 32;
-      const int kap = (int)(frag % nk);
-      const int rho = (int)((frag / nk) % nr);
-      const int g = (int)(frag / ((int64_t)nk * nr));
-      *row = 32 * rho + m;
+      const int nk = f.d / 16, nrt = f.r_pad / 32;
+      const int g = (int)(frag / ((int64_t)nrt * nk));
+      const int64_t in_g = frag % ((int64_t)nrt * nk);
+      int64_t first;
+      const int w = run_owner(nrt, in_g, nk, &first);
+      const int64_t local = in_g - first;
+      const int j = (int)(local / nk), kap = (int)(local % nk);
+      *row = 32 * (w + kWaves * j) + m;
       *col = g * f.d + 16 * kap + 8 * c + e;
       return;
     }
     default: {
-      const int nk = f.r_pad / 16, nd = f.d / 32;
-      const int kap = (int)(frag % nk);
-      const int dlt = (int)((frag / nk) % nd);
-      const int g = (int)(frag / ((int64_t)nk * nd));
+      const int nrt = f.r_pad / 32, npass = f.d / 64;
+      const int64_t per_g = (int64_t)(f.d / 32) * (f.r_pad / 16);
+      const int g = (int)(frag / per_g);
+      const int64_t in_g = frag % per_g;
+      int64_t first;
+      const int w = run_owner(nrt, in_g, (int64_t)npass * 4, &first);
+      const int own = owned_tiles(nrt, w);
+      const int64_t local = in_g - first;
+      const int dt = (int)(local % 2), half = (int)((local / 2) % 2);
+      const int j = (int)((local / 4) % own), pass = (int)(local / (4 * own));
+      const int kap = 2 * (w + kWaves * j) + half;
       *row = 16 * kap + 8 * (e >> 2) + 4 * c + (e & 3);
-      *col = g * f.d + 32 * dlt + m;
+      *col = g * f.d + 32 * (2 * pass + dt) + m;
       return;
     }
   }
@@ -93,27 +149,36 @@ struct BlockMeta {
   int32_t T, T_pad, rk_pad, rv_pad;
 };
 
-// Work item of the attention kernel (one workgroup each), as int4:
-//   block task: {block id >= 0, partial slot, kv group g, column tile}
-//   tail task:  {-1 - request i, partial slot, kv group g, tail chunk}
-//   empty:      {kEmptyTask, 0, 0, 0}
-constexpr int kEmptyTask = -0x7fffffff;
+// Work item of the attention kernel (one workgroup each).  Block items carry
+// their block's metadata inline so a workgroup starts with a single load.
+enum ItemKind : int32_t { kItemBlock = 0, kItemTail = 1, kItemEmpty = 2 };
+struct WorkItem {
+  BlockMeta blk;      // block items: the block's packed offsets and padded sizes
+  int32_t kind;       // ItemKind
+  int32_t slot;       // partial slot written for every column of the item
+  int32_t g;          // KV head
+  int32_t sub;        // block items: 64-column tile; tail items: 128-token chunk
+  int32_t req;        // tail items: request index
+  int32_t tile0;      // block items: first 256-token tile of the block covered
+  int32_t ntile;      // block items: number of tiles covered
+  int32_t pad;
+};
+static_assert(sizeof(WorkItem) == 80, "work item layout");
 
 // Attention kernel geometry.
-constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCols = 64;                      // query columns per workgroup
-constexpr int kTokWave = 64;                   // tokens per wave per tile
-constexpr int kTile = kWaves * kTokWave;       // tokens per tile
+constexpr int kTokWave = kTile / kWaves;       // tokens per wave per tile
 constexpr int kWStride = kTile + 8;            // bf16 row stride of the weight tile in LDS
 constexpr int kORow = 68;                      // fp32 row stride of the up-projection reduction
 constexpr int kMaxGroup = 16;                  // max query heads per KV head
 constexpr int kMaxRank = 960;                  // largest supported rank (LDS bound)
+constexpr int kLdsBytes = 160 * 1024;          // LDS per workgroup on gfx950
+constexpr int kTailChunk = 128;                // dense-tail tokens per work item
 
 struct AttendArgs {
   const uint16_t* data;      // packed factors
-  const BlockMeta* meta;     // [n_blocks]
-  const int4* tasks;         // [grid]
+  const WorkItem* items;     // [grid]
   const uint16_t* q;         // [n_q][H_q][d]
   const uint16_t* tail_k;    // [n_q][tail_cap][H_kv][d]
   const uint16_t* tail_v;
@@ -122,9 +187,10 @@ struct AttendArgs {
   float2* part_ml;           // [n_q*H_q][n_slots] (max in log2 units, sum)
   float qscale;              // scale * log2(e)
   int n_q, H_q, H_kv, G;
-  int tail_cap, tail_chunk;
+  int tail_cap;
   int n_slots;
   int qt_stride;             // bf16 row stride of the projected query in LDS
+  int ring_offset;           // byte offset of the per-wave fragment rings in LDS
 };
 
 struct MergeArgs {
@@ -132,7 +198,7 @@ struct MergeArgs {
   const float2* part_ml;
   const int32_t* tail_len;   // device [n_q]
   float* out;                // [n_q][H_q][d]
-  int H_q, n_sel, n_slots, tail_chunk;
+  int H_q, n_block_slots, n_slots;
 };
 
 struct PackArgs {
@@ -144,9 +210,12 @@ struct PackArgs {
 
 // Launchers (defined in milo_kernels.hip).
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
-hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int grid, size_t lds_bytes,
+hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, int grid, size_t lds_bytes,
                          hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s);
-size_t attend_lds_bytes(int head_dim, int rk_pad_max, int G, int tail_chunk);
+// LDS of the attention kernel: a base region (projected query, weight tile and
+// reductions, or the tail item's buffers) followed by kWaves rings of nslot fragments.
+size_t attend_lds_base_bytes(int head_dim, int rk_pad_max);
+size_t attend_ring_bytes(int nslot);
 
 }  // namespace milo

@@ -1,0 +1,31 @@
+"""Packed factor layout (host logic, no GPU): the fragment order the kernels
+stream must be a bijection onto the padded source block for every factor."""
+import os
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GEOMS = [
+    (1, 1, 1, 64), (45, 33, 3, 64), (256, 64, 2, 128), (300, 100, 4, 128), (1024, 288, 4, 128),
+    (700, 96, 2, 64), (1000, 960, 8, 128), (2048, 512, 8, 128), (513, 160, 1, 64), (100, 40, 4, 128),
+]
+
+
+@pytest.fixture(scope="module")
+def checker(tmp_path_factory):
+    exe = str(tmp_path_factory.mktemp("layout") / "layout_check")
+    cmd = ["g++", "-O2", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+           "-I", os.path.join(ROOT, "paper_2609_29913_amd", "csrc"),
+           os.path.join(ROOT, "tests", "layout_check.cpp"), "-o", exe]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        pytest.fail("could not build the layout checker:\n" + res.stderr[-3000:])
+    return exe
+
+
+def test_fragment_layout_is_a_bijection(checker):
+    args = [str(x) for g in GEOMS for x in g]
+    res = subprocess.run([checker, *args], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert res.stdout.startswith("OK")
