@@ -136,7 +136,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py: this decode-attention path runs on one GPU; --gpus {args.gpus} is not supported "
-              "(multi-GPU sharding by blocks is described in DESIGN.md, not built).", file=sys.stderr)
+              "(sharding by blocks across GPUs is not built).", file=sys.stderr)
         sys.exit(2)
 
     import torch

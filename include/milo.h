@@ -42,7 +42,7 @@ extern "C" {
 #define MILO_ERR_INVALID_ARG (-1)   /* bad pointer, shape, rank, id or length   */
 #define MILO_ERR_OUT_OF_MEMORY (-2) /* device allocation failed or over the cap */
 #define MILO_ERR_HIP (-3)           /* a HIP runtime call failed                */
-#define MILO_ERR_UNSUPPORTED (-4)   /* valid input this build does not handle   */
+#define MILO_ERR_UNSUPPORTED (-4)   /* valid input this library does not handle */
 
 /* Opaque cache handle: owns one device buffer with every block's factors in the
  * library's packed layout, plus per-call workspace. */
@@ -54,7 +54,7 @@ typedef struct milo_cache milo_cache;
  *   n_kv_heads    H_kv >= 1
  *   head_dim      d, 64 or 128 (others return MILO_ERR_UNSUPPORTED)
  *   block_tokens  [n_blocks] T_b >= 1
- *   rank_k/v      [n_blocks] 1 <= r <= min(T_b, H_kv*d); this build supports
+ *   rank_k/v      [n_blocks] 1 <= r <= min(T_b, H_kv*d); this library supports
  *                 r <= 960 (larger ranks return MILO_ERR_UNSUPPORTED). */
 typedef struct milo_cache_desc {
   int32_t n_blocks;
