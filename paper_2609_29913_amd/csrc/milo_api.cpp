@@ -46,9 +46,7 @@ int hip_fail(hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail(e_, #call);     \
   } while (0)
 
-constexpr int kXcds = 8;          // gfx950: 8 accelerator dies, workgroups dealt round-robin
-constexpr int kCUs = 256;         // compute units of an MI355X
-constexpr int64_t kAlignElems = 128;  // 256-byte alignment of every packed factor
+constexpr int64_t kAlignElems = kFragElems;  // every packed factor starts on a whole fragment
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -80,16 +78,16 @@ struct milo_cache {
   float* part_o = nullptr;
   float2* part_ml = nullptr;
   int64_t part_cols_slots = 0;  // capacity in (column, slot) pairs
-  WorkItem* tasks_d = nullptr;
-  int64_t tasks_cap = 0;
+  unsigned char* plan_d = nullptr;       // program table + programs of the attention launches
+  unsigned char* plan_pinned = nullptr;  // staging copy for the upload
+  int64_t plan_cap = 0;
   int32_t* tail_len_d = nullptr;
   int64_t tail_len_cap = 0;
-  WorkItem* tasks_pinned = nullptr;
   int32_t* tail_len_pinned = nullptr;
-  int64_t pinned_tasks_cap = 0, pinned_tl_cap = 0;
   // the plan of the previous call
   std::vector<int32_t> plan_key;
-  int grid = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0, ring_offset = 0;
+  int n_launch = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0;
+  int prog_bytes = 0, ring_offset = 0;
   size_t lds = 0;
 };
 
@@ -120,6 +118,187 @@ int64_t factor_offset(const BlockMeta& m, int which) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Work schedule of one attention call.
+//
+// Work is cut into jobs: a block job is one part of a selected block (a range
+// of whole 256-token tiles; large blocks are split so the work evens out) for
+// one 64-column tile of query columns, and a tail job is one 128-token chunk of
+// one request's dense KV.  Each job covers S KV heads at once: the S work items
+// of a job run on a "gang" of S workgroups of one XCD (S = KV heads rounded up
+// to a power of two, at most 32), so a block's P factors are fetched from HBM
+// once and re-read by the other heads from that XCD's L2.  Jobs are dealt to
+// the gangs longest first (each to the gang with the least estimated work);
+// within a gang, tail jobs run first so their latency overlaps the start of the
+// fragment streams.  Workgroup b runs on XCD b % 8 (round-robin dispatch), so
+// gang k on XCD k % 8 uses workgroups (k % 8) + 8 * ((k / 8) * S + j), j < S.
+// ---------------------------------------------------------------------------
+// Cost model (microseconds on an MI355X, fitted to kernel timings): one
+// fragment of the slowest wave's stream, the per-tile softmax and barriers, the
+// per-item set-up, and one dense-tail chunk.
+constexpr double kCostFrag = 0.09, kCostTile = 3.0, kCostItem = 5.0, kCostTail = 7.0;
+constexpr int kMaxPartTiles = 8;  // keeps every item's run list short
+
+struct Schedule {
+  std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs
+  int n_launch = 0, n_parts = 0, prog_bytes = 0, rk_pad_max = 32, rv_pad_max = 32;
+};
+
+// The fragment runs wave w of a block item consumes, in the kernel's order:
+// its R^K rank tiles (projection), then per tile its P^K sub-tiles and its P^V
+// rank tiles, then its R^V rank tiles (up-projection).  Offsets follow the
+// packed layout of each factor.
+void append_runs(const WorkItem& it, int w, int d, std::vector<int2>& out) {
+  const BlockMeta& bm = it.blk;
+  const int NK = d / 16;
+  const int nrt_k = bm.rk_pad / 32, nks = bm.rk_pad / 16, nrt_v = bm.rv_pad / 32, nkv = bm.rv_pad / 16;
+  const int my_k = owned_tiles(nrt_k, w), my_v = owned_tiles(nrt_v, w);
+  const int tiles_all = bm.T_pad / kTile;
+  auto add = [&](int64_t elem_off, int64_t n) {
+    if (n > 0) out.push_back(make_int2((int)(elem_off / kFragElems), (int)n));
+  };
+  add(bm.off_rk + ((int64_t)it.g * nrt_k * NK + (int64_t)NK * owned_before(nrt_k, w)) * kFragElems,
+      (int64_t)NK * my_k);
+  for (int t = it.tile0; t < it.tile0 + it.ntile; ++t) {
+    add(bm.off_pk + ((int64_t)w * tiles_all + t) * 2 * nks * kFragElems, 2 * nks);
+    add(bm.off_pv + ((int64_t)(bm.T_pad / 16) * owned_before(nrt_v, w) + (int64_t)t * 16 * my_v) * kFragElems,
+        16 * my_v);
+  }
+  add(bm.off_rv + ((int64_t)it.g * (d / 32) * nkv + (int64_t)(d / 64) * 4 * owned_before(nrt_v, w)) * kFragElems,
+      (int64_t)(d / 64) * 4 * my_v);
+}
+
+int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const std::vector<int32_t>& tl, int n_ct,
+                   Schedule* out) {
+  const int NK = c.d / 16;
+  auto item_cost = [&](const BlockMeta& m, int nt) {
+    const int nrt_k = m.rk_pad / 32, nks = m.rk_pad / 16, nrt_v = m.rv_pad / 32;
+    const int mk = (nrt_k + kWaves - 1) / kWaves, mv = (nrt_v + kWaves - 1) / kWaves;
+    const double frags = (double)NK * mk + nt * (2.0 * nks + 16.0 * mv) + (c.d / 64) * 4.0 * mv;
+    return kCostFrag * frags + kCostTile * nt + kCostItem;
+  };
+  int S = 1;
+  while (S < c.n_kv && S < 32) S *= 2;
+  const int n_hc = (c.n_kv + S - 1) / S;
+  const int n_gangs = kCUs / S;
+  double total = 0.0;
+  for (int j = 0; j < n_sel; ++j) {
+    const BlockMeta& m = c.meta[table[j]];
+    total += item_cost(m, m.T_pad / kTile) * n_ct * n_hc;
+  }
+  for (int32_t len : tl) total += kCostTail * ((len + kTailChunk - 1) / kTailChunk) * n_hc;
+  // parts of at most 2/3 of a gang's average work (and at most kMaxPartTiles tiles)
+  const double target = std::max(1e-9, total / n_gangs / 1.5);
+  struct Part { int b, tile0, ntile; double cost; };
+  std::vector<Part> parts;
+  for (int j = 0; j < n_sel; ++j) {
+    const int b = table[j];
+    const BlockMeta& m = c.meta[b];
+    const int nt = m.T_pad / kTile;
+    const int np_cost = (int)std::min<double>(nt, std::max(1.0, std::ceil(item_cost(m, nt) / target)));
+    const int np = std::max(np_cost, (nt + kMaxPartTiles - 1) / kMaxPartTiles);
+    for (int p = 0; p < np; ++p) {
+      const int t_a = (int)((int64_t)nt * p / np), t_b = (int)((int64_t)nt * (p + 1) / np);
+      parts.push_back({b, t_a, t_b - t_a, item_cost(m, t_b - t_a)});
+    }
+    out->rk_pad_max = std::max(out->rk_pad_max, m.rk_pad);
+    out->rv_pad_max = std::max(out->rv_pad_max, m.rv_pad);
+  }
+  const int n_parts = (int)parts.size();
+  out->n_parts = n_parts;
+  struct Job { int part, req, ch, ct, hc; double cost; };
+  std::vector<Job> jobs;
+  for (int p = 0; p < n_parts; ++p)
+    for (int ct = 0; ct < n_ct; ++ct)
+      for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({p, -1, -1, ct, hc, parts[p].cost});
+  for (int i = 0; i < (int)tl.size(); ++i)
+    for (int ch = 0; ch * kTailChunk < tl[i]; ++ch)
+      for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({-1, i, ch, 0, hc, kCostTail});
+  std::stable_sort(jobs.begin(), jobs.end(), [](const Job& x, const Job& y) { return x.cost > y.cost; });
+
+  const size_t base = attend_lds_base_bytes(c.d, out->rk_pad_max);
+  const size_t cap = std::min<size_t>(kProgCap, base < (size_t)kLdsBytes ? kLdsBytes - base : 0);
+  for (int L = 1; L <= (1 << 20); L *= 2) {
+    std::vector<std::vector<unsigned char>> progs((size_t)L * kCUs);
+    std::vector<WgProgram> entries((size_t)L * kCUs);
+    size_t max_prog = 0;
+    for (int l = 0; l < L; ++l) {
+      std::vector<std::vector<int>> lists(n_gangs);
+      std::vector<double> load(n_gangs, 0.0);
+      for (size_t k = l; k < jobs.size(); k += L) {
+        const int best = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+        load[best] += jobs[k].cost;
+        lists[best].push_back((int)k);
+      }
+      for (int gang = 0; gang < n_gangs; ++gang) {
+        std::stable_partition(lists[gang].begin(), lists[gang].end(), [&](int k) { return jobs[k].part < 0; });
+        for (int j = 0; j < S; ++j) {
+          const int wg = (gang % kXcds) + kXcds * ((gang / kXcds) * S + j);
+          std::vector<WorkItem> items;
+          std::vector<int2> runs[kWaves];
+          for (int k : lists[gang]) {
+            const Job& jb = jobs[k];
+            const int g = jb.hc * S + j;
+            if (g >= c.n_kv) continue;
+            WorkItem w{};
+            w.g = g;
+            if (jb.part >= 0) {
+              const Part& pt = parts[jb.part];
+              w.blk = c.meta[pt.b];
+              w.kind = kItemBlock;
+              w.slot = jb.part;
+              w.sub = jb.ct;
+              w.tile0 = pt.tile0;
+              w.ntile = pt.ntile;
+              for (int v = 0; v < kWaves; ++v) append_runs(w, v, c.d, runs[v]);
+            } else {
+              w.kind = kItemTail;
+              w.blk.T = std::min(kTailChunk, tl[jb.req] - jb.ch * kTailChunk);  // tokens of the chunk
+              w.req = jb.req;
+              w.slot = n_parts + jb.ch;
+              w.sub = jb.ch;
+            }
+            items.push_back(w);
+          }
+          WgProgram& e = entries[(size_t)l * kCUs + wg];
+          e = WgProgram{};
+          if (items.empty()) continue;
+          std::vector<unsigned char>& pb = progs[(size_t)l * kCUs + wg];
+          pb.resize(items.size() * sizeof(WorkItem));
+          std::memcpy(pb.data(), items.data(), pb.size());
+          for (int v = 0; v < kWaves; ++v) {
+            runs[v].push_back(make_int2(0, kSentinelRun));
+            e.run_off[v] = (int32_t)pb.size();
+            const size_t at = pb.size();
+            pb.resize(at + runs[v].size() * sizeof(int2));
+            std::memcpy(pb.data() + at, runs[v].data(), runs[v].size() * sizeof(int2));
+          }
+          pb.resize(round_up((int64_t)pb.size(), 16), 0);
+          e.n_items = (int32_t)items.size();
+          e.words = (int32_t)(pb.size() / 4);
+          max_prog = std::max(max_prog, pb.size());
+        }
+      }
+    }
+    const size_t prog_bytes = (size_t)round_up((int64_t)max_prog, 256);
+    if (prog_bytes > cap) continue;
+    // assemble: the entry table, then every program at a 16-byte aligned offset
+    size_t off = entries.size() * sizeof(WgProgram);
+    for (size_t k = 0; k < progs.size(); ++k) {
+      entries[k].off = (int64_t)off;
+      off += progs[k].size();
+    }
+    out->bytes.assign(std::max<size_t>(off, 16), 0);
+    std::memcpy(out->bytes.data(), entries.data(), entries.size() * sizeof(WgProgram));
+    for (size_t k = 0; k < progs.size(); ++k)
+      if (!progs[k].empty()) std::memcpy(out->bytes.data() + entries[k].off, progs[k].data(), progs[k].size());
+    out->n_launch = L;
+    out->prog_bytes = (int)prog_bytes;
+    return MILO_OK;
+  }
+  return fail(MILO_ERR_UNSUPPORTED, "work schedule does not fit in LDS");
+}
+
 void destroy(milo_cache* c) {
   if (!c) return;
   if (c->device >= 0) {
@@ -129,9 +308,9 @@ void destroy(milo_cache* c) {
     (void)hipFree(c->data);
     (void)hipFree(c->part_o);
     (void)hipFree(c->part_ml);
-    (void)hipFree(c->tasks_d);
+    (void)hipFree(c->plan_d);
     (void)hipFree(c->tail_len_d);
-    (void)hipHostFree(c->tasks_pinned);
+    (void)hipHostFree(c->plan_pinned);
     (void)hipHostFree(c->tail_len_pinned);
     if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
   }
@@ -195,6 +374,10 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     }
   }
   c->data_elems = off;
+  if (off / kFragElems >= ((int64_t)1 << 31)) {
+    delete c;
+    return fail(MILO_ERR_UNSUPPORTED, "cache of %lld elements exceeds the 2^31-fragment index range", (long long)off);
+  }
   const int64_t need = off * 2 + (src_on_device ? 0 : max_src * 2);
   const int64_t cap = env_byte_cap();
   if (cap >= 0 && need > cap) {
@@ -323,106 +506,31 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   if (key != c->plan_key) {
     const int ncg = n_q * G;
     const int n_ct = (ncg + kCols - 1) / kCols;
-    // Cost of one work item (one KV head, one column tile) over `nt` tiles of a
-    // block: the streamed factor bytes plus the projection / up-projection work.
-    auto item_cost = [&](const BlockMeta& m, int nt) {
-      return (int64_t)(nt * kTile + 2 * c->d) * (m.rk_pad + m.rv_pad);
-    };
-    int64_t total = 0;
-    for (int j = 0; j < n_sel; ++j) {
-      const BlockMeta& m = c->meta[block_table[j]];
-      total += item_cost(m, m.T_pad / kTile) * c->n_kv * n_ct;
-    }
-    const int64_t share = std::max<int64_t>(1, total / kCUs);
-    // A block whose items would exceed the per-CU share is split into parts of
-    // whole tiles; every part writes its own partial slot.
-    struct Part { int b, tile0, ntile; int64_t cost; };
-    std::vector<Part> parts;
-    for (int j = 0; j < n_sel; ++j) {
-      const int b = block_table[j];
-      const BlockMeta& m = c->meta[b];
-      const int nt = m.T_pad / kTile;
-      const int np = (int)std::min<int64_t>(nt, std::max<int64_t>(1, (item_cost(m, nt) + share - 1) / share));
-      for (int p = 0; p < np; ++p) {
-        const int t_a = (int)((int64_t)nt * p / np), t_b = (int)((int64_t)nt * (p + 1) / np);
-        parts.push_back({b, t_a, t_b - t_a, item_cost(m, t_b - t_a)});
-      }
-    }
-    const int n_parts = (int)parts.size();
-    const int n_slots = n_parts + max_chunks;
-    // Parts are dealt to the XCDs largest first (each XCD takes the next part
-    // while it has the least work); a part's items (all KV heads and column
-    // tiles) stay on one XCD, so its P factors are fetched from HBM once and
-    // re-read from that XCD's L2.
-    std::vector<int> order(n_parts);
-    std::iota(order.begin(), order.end(), 0);
-    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return parts[x].cost > parts[y].cost; });
-    std::vector<std::vector<WorkItem>> per_xcd(kXcds);
-    std::vector<int64_t> load(kXcds, 0);
-    int rk_pad_max = 32, rv_pad_max = 32;
-    WorkItem w{};
-    for (int pi : order) {
-      const Part& pt = parts[pi];
-      const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-      load[x] += pt.cost * c->n_kv * n_ct;
-      rk_pad_max = std::max(rk_pad_max, c->meta[pt.b].rk_pad);
-      rv_pad_max = std::max(rv_pad_max, c->meta[pt.b].rv_pad);
-      w.blk = c->meta[pt.b];
-      w.kind = kItemBlock;
-      w.slot = pi;
-      w.tile0 = pt.tile0;
-      w.ntile = pt.ntile;
-      for (int g = 0; g < c->n_kv; ++g)
-        for (int ct = 0; ct < n_ct; ++ct) {
-          w.g = g;
-          w.sub = ct;
-          per_xcd[x].push_back(w);
-        }
-    }
-    size_t per = 0;
-    for (auto& v : per_xcd) per = std::max(per, v.size());
-    WorkItem empty{};
-    empty.kind = kItemEmpty;
-    // Dense-tail items go first (a whole number of rounds over the XCDs, padded
-    // with empty items) so they run while the memory system is still quiet;
-    // the block items follow, round-robin over the XCDs.
-    std::vector<WorkItem> tasks;
-    WorkItem tw{};
-    tw.kind = kItemTail;
-    for (int i = 0; i < n_q; ++i)
-      for (int ch = 0; ch * kTailChunk < tl[i]; ++ch)
-        for (int g = 0; g < c->n_kv; ++g) {
-          tw.req = i;
-          tw.slot = n_parts + ch;
-          tw.g = g;
-          tw.sub = ch;
-          tasks.push_back(tw);
-        }
-    while (tasks.size() % kXcds) tasks.push_back(empty);
-    tasks.reserve(tasks.size() + per * kXcds);
-    for (size_t k = 0; k < per; ++k)
-      for (int x = 0; x < kXcds; ++x) tasks.push_back(k < per_xcd[x].size() ? per_xcd[x][k] : empty);
-    const int rt_need = (rv_pad_max / 32 + kWaves - 1) / kWaves;
+    Schedule sch;
+    const int err = build_schedule(*c, block_table, n_sel, tl, n_ct, &sch);
+    if (err != MILO_OK) return err;
+    const int rt_need = (sch.rv_pad_max / 32 + kWaves - 1) / kWaves;
     int max_rt = 8;
     for (int cand : {2, 4, 6, 8})
       if (cand >= rt_need) { max_rt = cand; break; }
-    // deepest fragment ring that fits next to the projected query and weight tile
-    const size_t base = attend_lds_base_bytes(c->d, rk_pad_max);
+    // deepest fragment ring that fits next to the program, projected query and weight tile
+    const size_t base = attend_lds_base_bytes(c->d, sch.rk_pad_max);
+    const size_t prog = (size_t)sch.prog_bytes;
     int nslot = 0;
-    for (int cand : {12, 6})
-      if (base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
+    for (int cand : {14, 12, 6})
+      if (prog + base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
     // device buffers
-    const int64_t ntask = (int64_t)tasks.size();
-    if (ntask > c->tasks_cap) {
+    const int64_t plan_bytes = (int64_t)sch.bytes.size();
+    if (plan_bytes > c->plan_cap) {
       MILO_HIP(hipStreamSynchronize(s));
-      (void)hipFree(c->tasks_d);
-      (void)hipHostFree(c->tasks_pinned);
-      c->tasks_d = nullptr;
-      c->tasks_pinned = nullptr;
-      c->tasks_cap = 0;
-      MILO_HIP(hipMalloc(&c->tasks_d, sizeof(WorkItem) * ntask));
-      MILO_HIP(hipHostMalloc(&c->tasks_pinned, sizeof(WorkItem) * ntask, hipHostMallocDefault));
-      c->tasks_cap = ntask;
+      (void)hipFree(c->plan_d);
+      (void)hipHostFree(c->plan_pinned);
+      c->plan_d = nullptr;
+      c->plan_pinned = nullptr;
+      c->plan_cap = 0;
+      MILO_HIP(hipMalloc(&c->plan_d, (size_t)plan_bytes));
+      MILO_HIP(hipHostMalloc(&c->plan_pinned, (size_t)plan_bytes, hipHostMallocDefault));
+      c->plan_cap = plan_bytes;
     }
     if (n_q > c->tail_len_cap) {
       MILO_HIP(hipStreamSynchronize(s));
@@ -437,18 +545,19 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     }
     // the pinned staging buffers may still feed an earlier upload
     MILO_HIP(hipStreamSynchronize(s));
-    std::memcpy(c->tasks_pinned, tasks.data(), sizeof(WorkItem) * ntask);
+    std::memcpy(c->plan_pinned, sch.bytes.data(), (size_t)plan_bytes);
     std::memcpy(c->tail_len_pinned, tl.data(), sizeof(int32_t) * n_q);
-    if (ntask) MILO_HIP(hipMemcpyAsync(c->tasks_d, c->tasks_pinned, sizeof(WorkItem) * ntask, hipMemcpyHostToDevice, s));
+    MILO_HIP(hipMemcpyAsync(c->plan_d, c->plan_pinned, (size_t)plan_bytes, hipMemcpyHostToDevice, s));
     MILO_HIP(hipMemcpyAsync(c->tail_len_d, c->tail_len_pinned, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
-    c->grid = (int)ntask;
-    c->n_slots = n_slots;
-    c->n_block_slots = n_parts;
+    c->n_launch = sch.n_launch;
+    c->n_slots = sch.n_parts + max_chunks;
+    c->n_block_slots = sch.n_parts;
     c->max_rt = max_rt;
     c->nslot = nslot;
-    c->rk_pad_max = rk_pad_max;
+    c->rk_pad_max = sch.rk_pad_max;
+    c->prog_bytes = sch.prog_bytes;
     c->ring_offset = (int)base;
-    c->lds = base + attend_ring_bytes(nslot);
+    c->lds = prog + base + attend_ring_bytes(nslot);
     c->plan_key.swap(key);
   }
   const int64_t need = (int64_t)n_cols * c->n_slots;
@@ -471,7 +580,7 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   // ---- launches ----
   AttendArgs aa{};
   aa.data = c->data;
-  aa.items = c->tasks_d;
+  aa.prog = c->plan_d;
   aa.q = q;
   aa.tail_k = tail_k;
   aa.tail_v = tail_v;
@@ -486,6 +595,7 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   aa.tail_cap = tail_cap;
   aa.n_slots = c->n_slots;
   aa.qt_stride = c->rk_pad_max + 8;
+  aa.prog_bytes = c->prog_bytes;
   aa.ring_offset = c->ring_offset;
   MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out, n_q_heads, c->n_block_slots, c->n_slots};
 
@@ -507,8 +617,12 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     }
   }
   if (timed) MILO_HIP(hipEventRecord(ev[0], s));
-  hipError_t e = launch_attend(aa, c->d, c->max_rt, c->nslot, c->grid, c->lds, s);
-  if (e != hipSuccess) return hip_fail(e, "attend kernel launch");
+  hipError_t e = hipSuccess;
+  for (int l = 0; l < c->n_launch; ++l) {
+    aa.wg = reinterpret_cast<const WgProgram*>(c->plan_d) + (size_t)l * kCUs;
+    e = launch_attend(aa, c->d, c->max_rt, c->nslot, kCUs, c->lds, s);
+    if (e != hipSuccess) return hip_fail(e, "attend kernel launch");
+  }
   if (timed) MILO_HIP(hipEventRecord(ev[1], s));
   e = launch_merge(ma, c->d, n_cols, s);
   if (e != hipSuccess) return hip_fail(e, "merge kernel launch");

@@ -149,11 +149,12 @@ struct BlockMeta {
   int32_t T, T_pad, rk_pad, rv_pad;
 };
 
-// Work item of the attention kernel (one workgroup each).  Block items carry
-// their block's metadata inline so a workgroup starts with a single load.
-enum ItemKind : int32_t { kItemBlock = 0, kItemTail = 1, kItemEmpty = 2 };
+// Work item of the attention kernel.  Block items carry their block's metadata
+// inline, so an item is self-contained.
+enum ItemKind : int32_t { kItemBlock = 0, kItemTail = 1 };
 struct WorkItem {
-  BlockMeta blk;      // block items: the block's packed offsets and padded sizes
+  BlockMeta blk;      // block items: the block's packed offsets and padded sizes;
+                      // tail items: blk.T = tokens of the chunk
   int32_t kind;       // ItemKind
   int32_t slot;       // partial slot written for every column of the item
   int32_t g;          // KV head
@@ -165,6 +166,22 @@ struct WorkItem {
 };
 static_assert(sizeof(WorkItem) == 80, "work item layout");
 
+// The attention kernel is persistent: workgroup b runs the program of entry b,
+// a byte range of the program buffer holding its work items in order, followed
+// by one fragment-run list per wave.  A run is (first fragment index, count):
+// the fragments the wave consumes, in consumption order, over all of the
+// workgroup's block items (tail items consume none).  Each list ends with a
+// sentinel run (fragment 0, 2^30) that feeds the look-ahead loads issued past
+// the last real fragment.  The program is copied into LDS at kernel start.
+struct WgProgram {
+  int64_t off;                // byte offset in the program buffer (16-byte aligned)
+  int32_t words;              // program size in 4-byte words
+  int32_t n_items;            // work items (they start the program)
+  int32_t run_off[4];         // byte offset of wave w's run list within the program
+};
+static_assert(sizeof(WgProgram) == 32, "program entry layout");
+constexpr int kSentinelRun = 1 << 30;
+
 // Attention kernel geometry.
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCols = 64;                      // query columns per workgroup
@@ -175,10 +192,14 @@ constexpr int kMaxGroup = 16;                  // max query heads per KV head
 constexpr int kMaxRank = 960;                  // largest supported rank (LDS bound)
 constexpr int kLdsBytes = 160 * 1024;          // LDS per workgroup on gfx950
 constexpr int kTailChunk = 128;                // dense-tail tokens per work item
+constexpr int kXcds = 8;                       // XCDs of an MI355X (workgroup b runs on XCD b % 8)
+constexpr int kCUs = 256;                      // compute units; one persistent workgroup each
+constexpr int kProgCap = 8192;                 // largest per-workgroup program (bytes of LDS)
 
 struct AttendArgs {
   const uint16_t* data;      // packed factors
-  const WorkItem* items;     // [grid]
+  const unsigned char* prog; // program buffer
+  const WgProgram* wg;       // [grid] program of each workgroup
   const uint16_t* q;         // [n_q][H_q][d]
   const uint16_t* tail_k;    // [n_q][tail_cap][H_kv][d]
   const uint16_t* tail_v;
@@ -190,7 +211,8 @@ struct AttendArgs {
   int tail_cap;
   int n_slots;
   int qt_stride;             // bf16 row stride of the projected query in LDS
-  int ring_offset;           // byte offset of the per-wave fragment rings in LDS
+  int prog_bytes;            // LDS bytes reserved for the program (the work area follows)
+  int ring_offset;           // byte offset of the per-wave fragment rings in the work area
 };
 
 struct MergeArgs {

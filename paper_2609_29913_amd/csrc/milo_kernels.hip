@@ -3,7 +3,8 @@
 // attention itself is Sec. 4.1 Eq. 1).
 //
 //  pack_kernel    repacks row-major bf16 factors into MFMA-fragment order.
-//  attend_kernel  one workgroup per work item:
+//  attend_kernel  persistent: one workgroup per compute unit runs a host-built
+//                 list of work items, its fragment streams flowing across items:
 //     block item (block b, KV head g, 64-column tile of query columns):
 //       projection  Qt = scale*log2(e) * R^K_b[:, g] q          (MFMA, into LDS)
 //       scores      S  = P^K_b Qt, 256 tokens per tile          (MFMA, 4 waves x 64 tokens)
@@ -38,6 +39,48 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+__device__ __forceinline__ void lds_dma16(const uint16_t* g, __bf16* lds_slot) {
+  __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(g),
+                                   reinterpret_cast<__attribute__((address_space(3))) void*>(
+                                       reinterpret_cast<uintptr_t>(lds_slot)),
+                                   16, 0, 0);
+}
+
+// LDS reads of the workgroup's program (run lists, work items).  The compiler
+// cannot tell these addresses from the slots that in-flight global->LDS loads
+// write, so a plain LDS load here would make it wait for every outstanding
+// fragment load; the program region is never a load target, so the reads are
+// issued directly, waiting only for themselves.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)reinterpret_cast<uintptr_t>(p);  // offset within the LDS aperture
+}
+__device__ __forceinline__ int2 prog_read_b64(const void* p) {
+  int2 v;
+  asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(lds_addr(p)));
+  return v;
+}
+__device__ __forceinline__ int4 prog_read_b128(const void* p) {
+  int4 v;
+  asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(lds_addr(p)));
+  return v;
+}
+
+// Workgroup barrier for the attention kernel: every wave's LDS reads and
+// writes issued before it are complete.  In-flight global->LDS fragment loads
+// are deliberately not waited for (each targets its own wave's ring slots);
+// __syncthreads() would make the compiler drain them (vmcnt(0)) at many
+// barriers.  The "memory" clobber keeps the compiler from moving memory
+// accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt(0xF70 | N);  // vmcnt(N), expcnt/lgkmcnt not waited
+}
+
 // ---------------------------------------------------------------------------
 // Packing
 // ---------------------------------------------------------------------------
@@ -63,261 +106,217 @@ __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
 
 // ---------------------------------------------------------------------------
 // Tail work item: attention of the G query heads of KV head g of request i over
-// tokens [t0, t0 + nt) of that request's uncompressed KV.  The chunk's K and V
-// rows are staged in LDS with coalesced 16-byte loads, then scored and
-// accumulated from LDS.
+// tokens [t0, t0 + nt) of that request's uncompressed KV (nt <= 128 comes with
+// the item).  Wave w takes tokens t0 + 32w .. t0 + 32w + 31; every load of the
+// item is issued up front (rows past the chunk's end re-read its last row and
+// are masked), then:
+//   scores  S = K q^T  (one 32x32x16 MFMA per 16 dims: 32 tokens x 32 head
+//           columns, heads past G read the last head and are discarded)
+//   softmax column max / sum over the 4 waves through LDS, W = 2^(S - m)
+//   values  o[h] = sum_t W[t][h] V[t]  (VALU: lane owns D/64 dims, the weights
+//           of a token are broadcast from LDS), summed over the waves in LDS.
 // ---------------------------------------------------------------------------
-template <int D>
-__device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem) {
-  constexpr int kRow = D + 8;               // bf16 row stride of the staged K / V
-  constexpr int kChunks = D / 8;            // 16-byte pieces per row
-  constexpr int kPairs = D / 2;             // d pairs of the value pass (one per lane)
-  const int i = it.req, slot = it.slot, g = it.g;
-  const int G = a.G;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int t0 = it.sub * kTailChunk;
-  const int nt = min(kTailChunk, a.tail_len[i] - t0);
-  __bf16* kt = reinterpret_cast<__bf16*>(smem);           // [kTailChunk][kRow]
-  __bf16* vt = kt + kTailChunk * kRow;                      // [kTailChunk][kRow]
-  float* qs = reinterpret_cast<float*>(vt + kTailChunk * kRow);  // [kMaxGroup][D]
-  float* sc = qs + kMaxGroup * D;                           // [kTailChunk][kMaxGroup] token-major
-  float2* ml = reinterpret_cast<float2*>(sc + kMaxGroup * kTailChunk);  // [kMaxGroup]
-  float* op = reinterpret_cast<float*>(kt);  // [kWaves][kMaxGroup][D], over K (dead after scoring)
+// Value pass of a tail item for one wave: o[h][e] = sum over the wave's 32
+// tokens of W[t][h] * V[t][e] for NH heads and this lane's D/64 dims, written
+// to the wave's partial-output rows (row stride D).  Fully unrolled, so the
+// per-token registers are addressed statically.
+template <int D, int NH>
+__device__ __forceinline__ void tail_values(const float* wt, const uint32_t (&vraw)[kTailChunk / kWaves],
+                                            float* out) {
+  constexpr int DL = D / 64;
+  float acc[NH][DL];
+#pragma unroll
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int e = 0; e < DL; ++e) acc[h][e] = 0.f;
+#pragma unroll
+  for (int tt = 0; tt < kTailChunk / kWaves; ++tt) {
+    float vf[DL];
+    vf[0] = __uint_as_float(vraw[tt] << 16);
+    if constexpr (DL == 2) vf[1] = __uint_as_float(vraw[tt] & 0xffff0000u);
+    const float4* wr = reinterpret_cast<const float4*>(wt + tt * 32);
+#pragma unroll
+    for (int q4 = 0; q4 < NH / 4; ++q4) {
+      const float4 w4 = wr[q4];
+      const float wv[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < DL; ++e) acc[4 * q4 + u][e] += wv[u] * vf[e];
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int e = 0; e < DL; ++e) out[h * D + e] = acc[h][e];
+}
 
-  const int64_t rstride = (int64_t)a.H_kv * D;
-  const uint16_t* kb = a.tail_k + ((int64_t)i * a.tail_cap + t0) * rstride + (int64_t)g * D;
-  const uint16_t* vb = a.tail_v + ((int64_t)i * a.tail_cap + t0) * rstride + (int64_t)g * D;
-  {
-    // every load of the chunk is issued before the first LDS write; rows past
-    // the chunk's end re-read its last row (never used), so no load is predicated
-    constexpr int kPer = kTailChunk * kChunks / kThreads;
-    constexpr int kQPer = kMaxGroup * D / kThreads;
-    uint4 kv[kPer], vv[kPer];
-    uint16_t qv[kQPer];
+template <int D>
+__device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
+                                          const int tid) {
+  constexpr int NK = D / 16;                // 16-dim steps of the score MFMA
+  constexpr int DL = D / 64;                // dims per lane in the value pass
+  constexpr int kTokW = kTailChunk / kWaves;  // tokens per wave (32)
+  static_assert(kTokW == 32, "one 32-row MFMA tile of tokens per wave");
+  const int i = it.req, slot = it.slot, g = it.g, G = a.G;
+  const int wave = tid >> 6, lane = tid & 63, lrow = lane & 31, lhi = lane >> 5;
+  const int t0 = it.sub * kTailChunk, nt = it.blk.T;
+  float* red = reinterpret_cast<float*>(smem);   // [kWaves][32] column maxima
+  float* lred = red + kWaves * 32;               // [kWaves][32] column sums
+  float* wt = lred + kWaves * 32;                // [kTailChunk][32] weights, token-major
+  float* op = wt + kTailChunk * 32;              // [kWaves][kMaxGroup][D] partial outputs
+
+  const int64_t rs = (int64_t)a.H_kv * D;      // row stride of the tail K / V
+  const int64_t row0 = (int64_t)i * a.tail_cap + t0;
+  const int tk = min(kTokW * wave + lrow, nt - 1);   // this lane's token row (clamped)
+  const int hh = min(lrow, G - 1);                    // this lane's head column (clamped)
+  const uint16_t* krow = a.tail_k + (row0 + tk) * rs + (int64_t)g * D + 8 * lhi;
+  const uint16_t* qrow = a.q + ((int64_t)i * a.H_q + g * G + hh) * D + 8 * lhi;
+  const uint16_t* vcol = a.tail_v + row0 * rs + (int64_t)g * D + DL * lane;
+  bf16x8 kf[NK], qf[NK];
 #pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int x = tid + u * kThreads, t = min(x / kChunks, nt - 1), c = x % kChunks;
-      kv[u] = *reinterpret_cast<const uint4*>(kb + t * rstride + 8 * c);
-      vv[u] = *reinterpret_cast<const uint4*>(vb + t * rstride + 8 * c);
-    }
-#pragma unroll
-    for (int u = 0; u < kQPer; ++u) {
-      const int x = tid + u * kThreads, hh = min(x / D, G - 1), j = x % D;
-      qv[u] = a.q[((int64_t)i * a.H_q + g * G + hh) * D + j];
-    }
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int x = tid + u * kThreads, t = x / kChunks, c = x % kChunks;
-      *reinterpret_cast<uint4*>(kt + t * kRow + 8 * c) = kv[u];
-      *reinterpret_cast<uint4*>(vt + t * kRow + 8 * c) = vv[u];
-    }
-#pragma unroll
-    for (int u = 0; u < kQPer; ++u) qs[tid + u * kThreads] = bf16_to_f32(qv[u]) * a.qscale;
+  for (int k = 0; k < NK; ++k) {
+    kf[k] = ld_bf16x8(krow + 16 * k);
+    qf[k] = ld_bf16x8(qrow + 16 * k);
   }
-  __syncthreads();
-  // scores: thread (token t, head parity hp) covers heads hp, hp+2, ...; the
-  // loops run over the largest group size without branches (heads past G read
-  // the last head's query and are discarded), so the LDS reads pipeline
-  {
-    const int t = tid % kTailChunk, hp = tid / kTailChunk;
-    float acc[kMaxGroup / 2];
+  uint32_t vraw[kTokW];  // V[token][DL*lane .. +DL-1] as bf16 bits
 #pragma unroll
-    for (int u = 0; u < kMaxGroup / 2; ++u) acc[u] = 0.f;
-    const __bf16* kr = kt + t * kRow;
-    const float* qh[kMaxGroup / 2];
-#pragma unroll
-    for (int u = 0; u < kMaxGroup / 2; ++u) qh[u] = qs + min(hp + 2 * u, G - 1) * D;
-#pragma unroll 2
-    for (int j = 0; j < D; j += 8) {
-      const bf16x8 k8 = ld_bf16x8(kr + j);
-      float kf[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kf[e] = (float)k8[e];
-#pragma unroll
-      for (int u = 0; u < kMaxGroup / 2; ++u) {
-        const float4 qa = *reinterpret_cast<const float4*>(qh[u] + j);
-        const float4 qb = *reinterpret_cast<const float4*>(qh[u] + j + 4);
-        acc[u] += kf[0] * qa.x + kf[1] * qa.y + kf[2] * qa.z + kf[3] * qa.w +
-                  kf[4] * qb.x + kf[5] * qb.y + kf[6] * qb.z + kf[7] * qb.w;
-      }
-    }
-    if (t < nt) {
-#pragma unroll
-      for (int u = 0; u < kMaxGroup / 2; ++u) {
-        const int hh = hp + 2 * u;
-        if (hh < G) sc[t * kMaxGroup + hh] = acc[u];
-      }
-    }
+  for (int tt = 0; tt < kTokW; ++tt) {
+    const int64_t r = min(kTokW * wave + tt, nt - 1);
+    if constexpr (DL == 2) vraw[tt] = *reinterpret_cast<const uint32_t*>(vcol + r * rs);
+    else vraw[tt] = vcol[r * rs];
   }
-  __syncthreads();
-  for (int hh = wave; hh < G; hh += kWaves) {
-    float mx = -INFINITY;
-    for (int t = lane; t < nt; t += 64) mx = fmaxf(mx, sc[t * kMaxGroup + hh]);
+  // scores: lane holds head column lrow, token rows 8(v/4) + 4 lhi + v%4 of the wave's 32
+  f32x16 sc = {};
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-    float sum = 0.f;
-    for (int t = lane; t < nt; t += 64) {
-      const float w = fast_exp2(sc[t * kMaxGroup + hh] - mx);
-      sc[t * kMaxGroup + hh] = w;
-      sum += w;
-    }
+  for (int k = 0; k < NK; ++k) sc = mfma32(kf[k], qf[k], sc);
+  float mx = -INFINITY;
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
-    if (lane == 0) ml[hh] = make_float2(mx, sum);
+  for (int v = 0; v < 16; ++v) {
+    const int tw = 8 * (v >> 2) + 4 * lhi + (v & 3);
+    const float x = kTokW * wave + tw < nt ? sc[v] * a.qscale : -INFINITY;
+    sc[v] = x;
+    mx = fmaxf(mx, x);
   }
-  __syncthreads();
-  // values: lane owns the d pair (2*dp, 2*dp+1) for D == 128 (one d for D == 64),
-  // wave w the tokens w, w+4, ...; every head of the group at once
-  {
-    constexpr int kDL = D / 64;  // d values per lane
-    float acc[kMaxGroup][kDL];
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  red[wave * 32 + lrow] = mx;  // both lane halves hold the same value
+  lds_barrier();
+  float m = red[lrow];
 #pragma unroll
-    for (int hh = 0; hh < kMaxGroup; ++hh)
+  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red[w * 32 + lrow]);
+  float lsum = 0.f;
 #pragma unroll
-      for (int e = 0; e < kDL; ++e) acc[hh][e] = 0.f;
-    const int d0 = kDL * lane;
-#pragma unroll 4
-    for (int t = wave; t < nt; t += kWaves) {
-      float v[kDL];
-#pragma unroll
-      for (int e = 0; e < kDL; ++e) v[e] = (float)vt[t * kRow + d0 + e];
-      const float4* wr = reinterpret_cast<const float4*>(sc + t * kMaxGroup);
-#pragma unroll
-      for (int q4 = 0; q4 < kMaxGroup / 4; ++q4) {
-        const float4 w4 = wr[q4];  // weights past G are unset and their sums discarded
-        const float wv[4] = {w4.x, w4.y, w4.z, w4.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int e = 0; e < kDL; ++e) acc[4 * q4 + u][e] += wv[u] * v[e];
-      }
-    }
-#pragma unroll
-    for (int hh = 0; hh < kMaxGroup; ++hh)
-      if (hh < G)
-#pragma unroll
-        for (int e = 0; e < kDL; ++e) op[(wave * kMaxGroup + hh) * D + d0 + e] = acc[hh][e];
+  for (int v = 0; v < 16; ++v) {
+    const int tw = 8 * (v >> 2) + 4 * lhi + (v & 3);
+    const float w = fast_exp2(sc[v] - m);  // masked tokens: 2^-inf = 0
+    lsum += w;
+    wt[(kTokW * wave + tw) * 32 + lrow] = w;
   }
-  __syncthreads();
+  lsum += __shfl_xor(lsum, 32);
+  lred[wave * 32 + lrow] = lsum;
+  lds_barrier();
+  // values over the wave's own tokens (heads rounded up to 8 or 16)
+  if (G <= 8) tail_values<D, 8>(wt + kTokW * wave * 32, vraw, op + wave * kMaxGroup * D + DL * lane);
+  else tail_values<D, kMaxGroup>(wt + kTokW * wave * 32, vraw, op + wave * kMaxGroup * D + DL * lane);
+  lds_barrier();
   for (int x = tid; x < G * D; x += kThreads) {
-    const int hh = x / D, jj = x % D;
-    float s = 0.f;
+    const int h = x / D, dd = x % D;
+    float o = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) s += op[(w * kMaxGroup + hh) * D + jj];
-    const int64_t col = (int64_t)i * a.H_q + g * G + hh;
-    a.part_o[(col * a.n_slots + slot) * D + jj] = s;
-    if (jj == 0) a.part_ml[col * a.n_slots + slot] = ml[hh];
+    for (int w = 0; w < kWaves; ++w) o += op[(w * kMaxGroup + h) * D + dd];
+    const int64_t col = (int64_t)i * a.H_q + g * G + h;
+    a.part_o[(col * a.n_slots + slot) * D + dd] = o;
+    if (dd == 0) {
+      float mm = red[h], ll = 0.f;
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) mm = fmaxf(mm, red[w * 32 + h]);
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) ll += lred[w * 32 + h];
+      a.part_ml[col * a.n_slots + slot] = make_float2(mm, ll);
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
 // Block work item: latent-space attention of one 64-column tile of the query
-// columns of KV head g over all tokens of block b.
+// columns of KV head g over the tiles [tile0, tile0 + ntile) of block b.
 //
 // Waves split the tokens of each 256-token tile for the scores (64 tokens each)
 // and split the rank tiles of the latent accumulator (rank tile rt belongs to
 // wave rt % 4).  Every factor fragment a wave consumes (R^K for the projection,
-// P^K and P^V per tile, R^V for the up-projection) forms one stream per work
-// item.  With NSLOT > 0 the stream is fed through a private ring of NSLOT LDS
-// slots by direct global->LDS loads issued kDepth fragments ahead of use (so
-// each wait is a constant vmcnt); with NSLOT == 0 fragments are loaded
-// straight into registers.  Every loop is software-pipelined: the operands of
-// step k+1 are read while the MFMAs of step k run.
+// P^K and P^V per tile, R^V for the up-projection) comes from the wave's
+// fragment stream (FragRing below).  Every loop is software-pipelined: the
+// operands of step k+1 are read while the MFMAs of step k run.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void lds_dma16(const uint16_t* g, __bf16* lds_slot) {
-  __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(g),
-                                   reinterpret_cast<__attribute__((address_space(3))) void*>(
-                                       reinterpret_cast<uintptr_t>(lds_slot)),
-                                   16, 0, 0);
-}
+// A wave's fragment stream over all block items of its workgroup.  The host
+// lists, per wave, the runs of consecutive packed fragments in the order the
+// wave consumes them (per block item: its R^K run for the projection, then for
+// every 256-token tile its P^K run and its P^V run, then its R^V run for the
+// up-projection); the list sits in LDS and ends with a long sentinel run.
+// With NSLOT > 0 fragments reach the wave through a private ring of NSLOT LDS
+// slots, filled by direct global->LDS loads issued kDepth fragments ahead of
+// use, so every wait is a constant vmcnt; the look-ahead crosses item
+// boundaries, so the next item's first fragments load while the current one
+// finishes.  With NSLOT == 0 fragments are loaded straight into registers.
+// All fields are wave-uniform (scalar registers).
+template <int NSLOT>
+struct FragRing {
+  static constexpr int kDepth = NSLOT > 2 ? NSLOT - 2 : 1;  // fragments in flight
+  const uint16_t* data_lane;  // packed buffer + this lane's 8-element offset
+  __bf16* ring;               // this wave's NSLOT slots
+  const int2* run;            // current entry of this wave's run list (LDS)
+  int64_t off;                // element offset of the next fragment
+  int left;                   // fragments left in the current run
+  int rs, ws;                 // ring slots: next to read, next to fill
+  int lane8;                  // this lane's element offset inside a fragment
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 16, "vmcnt immediate");
-  __builtin_amdgcn_s_waitcnt(0xF70 | N);  // vmcnt(N), expcnt/lgkmcnt not waited
-}
-
-// A wave's fragment stream.  In consumption order it is: the wave's R^K run
-// (projection), then for every 256-token tile the next 2*nks fragments of its
-// P^K run and the next 16*my_nrt fragments of its P^V run, then its R^V run
-// (up-projection).  The packed layout stores each of these runs contiguously,
-// so advancing is an add and a countdown; the phase changes only when a run
-// ends.  Once exhausted, the stream keeps returning its last fragment.  All
-// fields are wave-uniform (scalar registers).
-struct FragStream {
-  int64_t off;        // element offset of the next fragment
-  int64_t step;       // kFragElems while running, 0 once exhausted
-  int left;           // fragments left in the current run
-  int phase, t;       // 0 R^K, 1 P^K of tile t, 2 P^V of tile t, 3 R^V, 4 exhausted
-  int64_t pk, pv, rv; // resume points of the wave's P^K / P^V runs, start of its R^V run
-  int n_pk, n_pv, n_rv, ntiles;
-
-  __device__ __forceinline__ void begin_tile() {
-    phase = 1;
-    off = pk;
-    left = n_pk;
+  __device__ __forceinline__ void load_run() {
+    const int2 v = prog_read_b64(run);
+    off = (int64_t)__builtin_amdgcn_readfirstlane(v.x) * kFragElems;
+    left = __builtin_amdgcn_readfirstlane(v.y);
   }
-  __device__ __forceinline__ void finish() {
-    phase = 4;
-    off -= kFragElems;
-    step = 0;
-    left = 1 << 30;
-  }
-  __device__ __forceinline__ void init(int64_t rk, int n_rk) {
-    t = 0;
-    step = kFragElems;
-    if (n_rk > 0) {
-      phase = 0;
-      off = rk;
-      left = n_rk;
-    } else {
-      begin_tile();
-    }
-  }
-  __device__ void next_tile() {
-    if (++t < ntiles) {
-      begin_tile();
-    } else if (n_rv > 0) {
-      phase = 3;
-      off = rv;
-      left = n_rv;
-    } else {
-      finish();
-    }
-  }
-  __device__ void refill() {
-    switch (phase) {
-      case 0: begin_tile(); break;
-      case 1:
-        pk = off;
-        if (n_pv > 0) {
-          phase = 2;
-          off = pv;
-          left = n_pv;
-        } else {
-          next_tile();
-        }
-        break;
-      case 2: pv = off; next_tile(); break;
-      default: finish(); break;  // end of the R^V run
-    }
-  }
-  // offset of the next fragment; advances the stream
+  // offset of the next fragment of the stream; advances it
   __device__ __forceinline__ int64_t next() {
     const int64_t o = off;
-    off += step;
-    if (--left == 0) refill();
+    off += kFragElems;
+    if (--left == 0) {
+      ++run;
+      load_run();
+    }
     return o;
+  }
+  __device__ __forceinline__ void start() {
+    load_run();
+    rs = 0;
+    ws = 0;
+    if constexpr (NSLOT > 0) {
+#pragma unroll
+      for (int k = 0; k < kDepth; ++k) lds_dma16(data_lane + next(), ring + k * kFragElems);
+      ws = kDepth;
+    }
+  }
+  // the next fragment, in this lane's operand layout
+  __device__ __forceinline__ bf16x8 take() {
+    if constexpr (NSLOT > 0) {
+      wait_vmcnt<kDepth - 1>();
+      const bf16x8 v = ld_bf16x8(ring + rs * kFragElems + lane8);
+      lds_dma16(data_lane + next(), ring + ws * kFragElems);
+      rs = rs + 1 == NSLOT ? 0 : rs + 1;
+      ws = ws + 1 == NSLOT ? 0 : ws + 1;
+      return v;
+    } else {
+      return ld_bf16x8(data_lane + next());
+    }
   }
 };
 
 template <int D, int MAX_RT, int NSLOT>
-__device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem) {
-  constexpr int kDepth = NSLOT > 2 ? NSLOT - 2 : 1;   // fragments in flight per wave
+__device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
+                                           FragRing<NSLOT>& fr, const int tid) {
   constexpr int NK = D / 16;
   const BlockMeta& bm = it.blk;
   const int slot = it.slot, g = it.g, c0 = it.sub * kCols;
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lrow = lane & 31, lhi = lane >> 5;
   const int G = a.G, ncg = a.n_q * G;
@@ -327,45 +326,13 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   const int my_nrt = owned_tiles(nrt_v, wave);
   const int my_nrt_k = owned_tiles(nrt_k, wave);
   const int T = bm.T;
-  const int tiles_all = bm.T_pad / kTile;     // tiles of the whole block (run lengths)
   const int ntiles = it.ntile, tile0 = it.tile0;  // tiles this item covers
   __bf16* qt = reinterpret_cast<__bf16*>(smem);              // [kCols][qsd]
   __bf16* wl = qt + kCols * qsd;                               // [kCols][kWStride]
   float* red = reinterpret_cast<float*>(wl + kCols * kWStride);  // [kWaves][kCols]
-  const uint16_t* data_lane = a.data + lane * 8;
-
-  // ---- start streaming fragments before anything else ----
-  FragStream st;
-  st.pk = bm.off_pk + ((int64_t)wave * tiles_all + tile0) * 2 * nks * kFragElems;
-  st.pv = bm.off_pv + ((int64_t)(bm.T_pad / 16) * owned_before(nrt_v, wave) + (int64_t)tile0 * 16 * my_nrt) * kFragElems;
-  st.rv = bm.off_rv + ((int64_t)g * (D / 32) * nkv + (int64_t)(D / 64) * 4 * owned_before(nrt_v, wave)) * kFragElems;
-  st.n_pk = 2 * nks;
-  st.n_pv = 16 * my_nrt;
-  st.n_rv = (D / 64) * 4 * my_nrt;
-  st.ntiles = ntiles;
-  st.init(bm.off_rk + ((int64_t)g * nrt_k * NK + (int64_t)NK * owned_before(nrt_k, wave)) * kFragElems,
-          NK * my_nrt_k);
-  __bf16* ring = nullptr;
-  int rs = 0, ws = 0;  // ring slots: next to read, next to fill
-  if constexpr (NSLOT > 0) {
-    ring = reinterpret_cast<__bf16*>(smem + a.ring_offset) + (size_t)wave * NSLOT * kFragElems;
-#pragma unroll
-    for (int k = 0; k < kDepth; ++k) lds_dma16(data_lane + st.next(), ring + k * kFragElems);
-    ws = kDepth;
-  }
-  // the next fragment of the stream, in this lane's operand layout
-  auto take = [&]() -> bf16x8 {
-    if constexpr (NSLOT > 0) {
-      wait_vmcnt<kDepth - 1>();
-      const bf16x8 v = ld_bf16x8(ring + rs * kFragElems + lane * 8);
-      lds_dma16(data_lane + st.next(), ring + ws * kFragElems);
-      rs = rs + 1 == NSLOT ? 0 : rs + 1;
-      ws = ws + 1 == NSLOT ? 0 : ws + 1;
-      return v;
-    } else {
-      return ld_bf16x8(data_lane + st.next());
-    }
-  };
+  // the wave's next fragment; the order of take() calls below is the order of
+  // the wave's runs: R^K, then per tile P^K and P^V, then R^V
+  auto take = [&]() -> bf16x8 { return fr.take(); };
 
   // ---- projection: Qt[rank][col] (stored [col][rank]) ----
   {
@@ -408,7 +375,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- scores, online softmax, latent V ----
   f32x16 oacc[MAX_RT][2];
@@ -469,7 +436,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       mx[ch] = fmaxf(mx[ch], __shfl_xor(mx[ch], 32));
       if (lhi == 0) red[wave * kCols + 32 * ch + lrow] = mx[ch];
     }
-    __syncthreads();
+    lds_barrier();
     float alpha[2];
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
@@ -500,7 +467,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
         }
       l_run[ch] = l_run[ch] * alpha[ch] + lsum;
     }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int r = 0; r < MAX_RT; ++r) {
       oacc[r][0] *= alpha[0];
@@ -545,7 +512,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   // ---- up-projection through R^V and the partial (m, l, o) ----
 #pragma unroll
   for (int ch = 0; ch < 2; ++ch) l_run[ch] += __shfl_xor(l_run[ch], 32);
-  __syncthreads();  // every wave is done with qt / wl
+  lds_barrier();  // every wave is done with qt / wl
   float* ored = reinterpret_cast<float*>(smem);       // [kWaves][kCols][kORow]
   float* lred = ored + kWaves * kCols * kORow;        // [kWaves][kCols]
   if (lhi == 0) {
@@ -597,7 +564,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
           *reinterpret_cast<float4*>(ored + (wave * kCols + 32 * ch + lrow) * kORow + 32 * dt + 8 * j +
                                      4 * lhi) = v;
         }
-    __syncthreads();
+    lds_barrier();
     {
       const int col = tid >> 2, dq = (tid & 3) * 16;
       const int c = c0 + col;
@@ -616,7 +583,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
   if (tid < kCols) {
     const int c = c0 + tid;
@@ -629,15 +596,56 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       a.part_ml[colg * a.n_slots + slot] = make_float2(m, l);
     }
   }
-  if constexpr (NSLOT > 0) wait_vmcnt<0>();  // no LDS write may land after the workgroup ends
+}
+
+// a work item read from LDS into wave-uniform registers
+__device__ __forceinline__ WorkItem lds_item(const unsigned char* p) {
+  static_assert(sizeof(WorkItem) % 16 == 0, "work items are whole 16-byte chunks");
+  int32_t w[sizeof(WorkItem) / 4];
+#pragma unroll
+  for (int i = 0; i < (int)sizeof(WorkItem) / 16; ++i) {
+    const int4 v = prog_read_b128(p + 16 * i);
+    w[4 * i + 0] = __builtin_amdgcn_readfirstlane(v.x);
+    w[4 * i + 1] = __builtin_amdgcn_readfirstlane(v.y);
+    w[4 * i + 2] = __builtin_amdgcn_readfirstlane(v.z);
+    w[4 * i + 3] = __builtin_amdgcn_readfirstlane(v.w);
+  }
+  WorkItem it;
+  __builtin_memcpy(&it, w, sizeof(WorkItem));
+  return it;
 }
 
 template <int D, int MAX_RT, int NSLOT>
 __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  const WorkItem it = a.items[blockIdx.x];
-  if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT>(a, it, smem);
-  else if (it.kind == kItemTail) tail_item<D>(a, it, smem);
+  const WgProgram p = a.wg[blockIdx.x];
+  if (p.n_items == 0) return;
+  {
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(a.prog + p.off);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(smem);
+    for (int i = threadIdx.x; i < p.words; i += kThreads) dst[i] = src[i];
+  }
+  lds_barrier();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int run_off = wave == 0 ? p.run_off[0] : wave == 1 ? p.run_off[1] : wave == 2 ? p.run_off[2] : p.run_off[3];
+  unsigned char* work = smem + a.prog_bytes;
+  FragRing<NSLOT> fr;
+  fr.data_lane = a.data + (threadIdx.x & 63) * 8;
+  fr.lane8 = (threadIdx.x & 63) * 8;
+  fr.run = reinterpret_cast<const int2*>(smem + run_off);
+  fr.ring = reinterpret_cast<__bf16*>(work + a.ring_offset) + (size_t)wave * NSLOT * kFragElems;
+  fr.start();
+  for (int k = 0; k < p.n_items; ++k) {
+    const WorkItem it = lds_item(smem + (size_t)k * sizeof(WorkItem));
+    if (k > 0) lds_barrier();  // the previous item's LDS reads are done
+    // the thread index is re-derived per item (opaque to the optimiser), so no
+    // lane-dependent address of one item kind stays live across the other
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT>(a, it, work, fr, tid);
+    else if (it.kind == kItemTail) tail_item<D>(a, it, work, tid);
+  }
+  if constexpr (NSLOT > 0) wait_vmcnt<0>();  // no LDS write may land after the workgroup ends
 }
 
 // ---------------------------------------------------------------------------
@@ -718,10 +726,7 @@ size_t attend_lds_base_bytes(int head_dim, int rk_pad_max) {
   const size_t qsd = (size_t)rk_pad_max + 8;
   const size_t loop = kCols * qsd * 2 + (size_t)kCols * kWStride * 2 + (size_t)kWaves * kCols * 4;
   const size_t epi = ((size_t)kWaves * kCols * kORow + (size_t)kWaves * kCols) * 4;
-  const size_t tail = (size_t)2 * kTailChunk * (head_dim + 8) * 2 +
-                      ((size_t)kMaxGroup * head_dim + (size_t)kMaxGroup * kTailChunk) * 4 + kMaxGroup * 8;
-  static_assert((size_t)kWaves * kMaxGroup * 128 * 4 <= (size_t)kTailChunk * (128 + 8) * 2,
-                "tail value partials must fit over the staged K");
+  const size_t tail = ((size_t)2 * kWaves * 32 + (size_t)kTailChunk * 32 + (size_t)kWaves * kMaxGroup * head_dim) * 4;
   size_t m = loop > epi ? loop : epi;
   m = m > tail ? m : tail;
   return (m + 1023) / 1024 * 1024;  // the fragment rings start here
@@ -745,6 +750,7 @@ static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hip
 template <int D, int MAX_RT>
 static hipError_t launch_attend_r(const AttendArgs& a, int nslot, int grid, size_t lds, hipStream_t s) {
   switch (nslot) {
+    case 14: return launch_attend_t<D, MAX_RT, 14>(a, grid, lds, s);
     case 12: return launch_attend_t<D, MAX_RT, 12>(a, grid, lds, s);
     case 6: return launch_attend_t<D, MAX_RT, 6>(a, grid, lds, s);
     case 0: return launch_attend_t<D, MAX_RT, 0>(a, grid, lds, s);
