@@ -55,7 +55,7 @@ typedef struct milo_cache milo_cache;
  *   head_dim      d, 64 or 128 (others return MILO_ERR_UNSUPPORTED)
  *   block_tokens  [n_blocks] T_b >= 1
  *   rank_k/v      [n_blocks] 1 <= r <= min(T_b, H_kv*d); this library supports
- *                 r <= 960 (larger ranks return MILO_ERR_UNSUPPORTED). */
+ *                 r <= 896 (larger ranks return MILO_ERR_UNSUPPORTED). */
 typedef struct milo_cache_desc {
   int32_t n_blocks;
   int32_t n_kv_heads;

@@ -141,31 +141,42 @@ constexpr int kMaxPartTiles = 8;  // keeps every item's run list short
 
 struct Schedule {
   std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs
-  int n_launch = 0, n_parts = 0, prog_bytes = 0, rk_pad_max = 32, rv_pad_max = 32;
+  int n_launch = 0, n_parts = 0, prog_bytes = 0, rk_pad_max = 32, rv_pad_max = 32, max_own = 1;
 };
 
 // The fragment runs wave w of a block item consumes, in the kernel's order:
-// its R^K rank tiles (projection), then per tile its P^K sub-tiles and its P^V
-// rank tiles, then its R^V rank tiles (up-projection).  Offsets follow the
-// packed layout of each factor.
+// its R^K rank tiles (projection); then per tile its P^K sub-tile and the P^V
+// rank tiles of its rank group over its token segment; then its rank group's
+// R^V rank tiles (up-projection).  Offsets
+// follow the packed layout of each factor.
 void append_runs(const WorkItem& it, int w, int d, std::vector<int2>& out) {
   const BlockMeta& bm = it.blk;
   const int NK = d / 16;
   const int nrt_k = bm.rk_pad / 32, nks = bm.rk_pad / 16, nrt_v = bm.rv_pad / 32, nkv = bm.rv_pad / 16;
-  const int my_k = owned_tiles(nrt_k, w), my_v = owned_tiles(nrt_v, w);
+  const int own_k = owned_tiles(nrt_k, w, kWaves);
+  const int nseg = v_segments(nrt_v), ng = kWaves / nseg, rg = w % ng, sg = w / ng;
+  const int own_v = owned_tiles(nrt_v, rg, ng), nst = 16 / nseg;
   const int tiles_all = bm.T_pad / kTile;
   auto add = [&](int64_t elem_off, int64_t n) {
     if (n > 0) out.push_back(make_int2((int)(elem_off / kFragElems), (int)n));
   };
-  add(bm.off_rk + ((int64_t)it.g * nrt_k * NK + (int64_t)NK * owned_before(nrt_k, w)) * kFragElems,
-      (int64_t)NK * my_k);
+  add(bm.off_rk + ((int64_t)it.g * nrt_k * NK + (int64_t)NK * owned_before(nrt_k, w, kWaves)) * kFragElems,
+      (int64_t)NK * own_k);
+  const int64_t pv_first = (int64_t)(bm.T_pad / 16) * owned_before(nrt_v, rg, ng);
   for (int t = it.tile0; t < it.tile0 + it.ntile; ++t) {
-    add(bm.off_pk + ((int64_t)w * tiles_all + t) * 2 * nks * kFragElems, 2 * nks);
-    add(bm.off_pv + ((int64_t)(bm.T_pad / 16) * owned_before(nrt_v, w) + (int64_t)t * 16 * my_v) * kFragElems,
-        16 * my_v);
+    add(bm.off_pk + ((int64_t)w * tiles_all + t) * nks * kFragElems, nks);
+    add(bm.off_pv + (pv_first + (int64_t)(16 * t + nst * sg) * own_v) * kFragElems, (int64_t)nst * own_v);
   }
-  add(bm.off_rv + ((int64_t)it.g * (d / 32) * nkv + (int64_t)(d / 64) * 4 * owned_before(nrt_v, w)) * kFragElems,
-      (int64_t)(d / 64) * 4 * my_v);
+  add(bm.off_rv + ((int64_t)it.g * (d / 32) * nkv + (int64_t)(d / 64) * 4 * owned_before(nrt_v, rg, ng)) *
+                      kFragElems,
+      (int64_t)(d / 64) * 4 * own_v);
+}
+
+// Latent rank tiles the busiest wave of a block accumulates (projection or value pass).
+int max_owned(const BlockMeta& m) {
+  const int nrt_k = m.rk_pad / 32, nrt_v = m.rv_pad / 32;
+  const int ng = kWaves / v_segments(nrt_v);
+  return std::max((nrt_k + kWaves - 1) / kWaves, (nrt_v + ng - 1) / ng);
 }
 
 int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const std::vector<int32_t>& tl, int n_ct,
@@ -173,8 +184,10 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
   const int NK = c.d / 16;
   auto item_cost = [&](const BlockMeta& m, int nt) {
     const int nrt_k = m.rk_pad / 32, nks = m.rk_pad / 16, nrt_v = m.rv_pad / 32;
-    const int mk = (nrt_k + kWaves - 1) / kWaves, mv = (nrt_v + kWaves - 1) / kWaves;
-    const double frags = (double)NK * mk + nt * (2.0 * nks + 16.0 * mv) + (c.d / 64) * 4.0 * mv;
+    const int nseg = v_segments(nrt_v), ng = kWaves / nseg;
+    const int mk = (nrt_k + kWaves - 1) / kWaves, mv = (nrt_v + ng - 1) / ng;
+    const double frags = (double)NK * mk + nt * ((double)nks + 16.0 / nseg * mv) +
+                         (c.d / 64) * 4.0 * mv;
     return kCostFrag * frags + kCostTile * nt + kCostItem;
   };
   int S = 1;
@@ -206,6 +219,7 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
   }
   const int n_parts = (int)parts.size();
   out->n_parts = n_parts;
+  for (const Part& pt : parts) out->max_own = std::max(out->max_own, max_owned(c.meta[pt.b]));
   struct Job { int part, req, ch, ct, hc; double cost; };
   std::vector<Job> jobs;
   for (int p = 0; p < n_parts; ++p)
@@ -509,15 +523,12 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     Schedule sch;
     const int err = build_schedule(*c, block_table, n_sel, tl, n_ct, &sch);
     if (err != MILO_OK) return err;
-    const int rt_need = (sch.rv_pad_max / 32 + kWaves - 1) / kWaves;
-    int max_rt = 8;
-    for (int cand : {2, 4, 6, 8})
-      if (cand >= rt_need) { max_rt = cand; break; }
+    const int max_rt = sch.max_own <= 2 ? 2 : 4;
     // deepest fragment ring that fits next to the program, projected query and weight tile
     const size_t base = attend_lds_base_bytes(c->d, sch.rk_pad_max);
     const size_t prog = (size_t)sch.prog_bytes;
     int nslot = 0;
-    for (int cand : {14, 12, 6})
+    for (int cand : {8, 6})
       if (prog + base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
     // device buffers
     const int64_t plan_bytes = (int64_t)sch.bytes.size();

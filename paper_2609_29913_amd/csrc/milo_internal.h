@@ -30,29 +30,53 @@ namespace milo {
 // latent accumulator feeds the up-projection straight from registers.
 //
 // Fragment order follows the attention kernel's work split, so that every wave
-// of a workgroup reads each factor as one contiguous run in the order it
-// consumes it.  A 256-token tile t is split over the kWaves waves: wave w owns
-// token sub-tiles tau = 8t + 2w + {0,1}; rank tiles are dealt round-robin, wave
-// w owning rho = w + kWaves*j.
-//   P^K: [w][t][kap][tau%2]
-//   P^V: [w][sig][j]                (wave w's run has owned_tiles(nrt_v, w) per sig)
+// of a workgroup reads each factor as contiguous runs in the order it consumes
+// it.  The kWaves waves split a 256-token tile for the scores: wave w owns token
+// sub-tile tau = 8t + w of tile t.  For the projection, rank tiles are dealt
+// round-robin over all waves (wave w owns rho = w + kWaves*j).  The latent
+// value pass and the up-projection split the waves into nseg = v_segments(nrt)
+// token segments times ng = kWaves / nseg rank groups: wave w works on token
+// segment w / ng (256 / nseg tokens of every tile) and owns the rank tiles
+// rho = (w % ng) + ng*j, so low-rank blocks still keep every wave busy.
+//   P^K: [w][t][kap]
+//   P^V: [rg][sig][j]                (group rg's run has owned_tiles(nrt, rg, ng) per sig)
 //   R^K: [g][w][j][kap]
-//   R^V: [g][w][pass][j][half][dt]  (kap = 2*rho + half, dl = 2*pass + dt, 64-row passes)
+//   R^V: [g][rg][pass][j][half][dt]  (kap = 2*rho + half, dl = 2*pass + dt, 64-row passes)
 // ---------------------------------------------------------------------------
 constexpr int kFragElems = 512;  // 64 lanes x 8 bf16
-constexpr int kWaves = 4;        // waves per attention workgroup
+constexpr int kWaves = 8;        // waves per attention workgroup (two per SIMD)
 constexpr int kTile = 256;       // tokens per attention tile
+constexpr int kMaxOwn = 4;       // most latent rank tiles one wave accumulates
 enum FactorKind : int { kPK = 0, kRK = 1, kPV = 2, kRV = 3 };
 
-// rank tiles dealt round-robin over the waves: how many wave w owns, and how
-// many the waves before it own
-__host__ __device__ inline int owned_tiles(int nrt, int w) {
-  return nrt > w ? (nrt - w + kWaves - 1) / kWaves : 0;
+// rank tiles dealt round-robin over n owners: how many owner w holds, and how
+// many the owners before it hold
+__host__ __device__ inline int owned_tiles(int nrt, int w, int n) {
+  return nrt > w ? (nrt - w + n - 1) / n : 0;
 }
-__host__ __device__ inline int owned_before(int nrt, int w) {
+__host__ __device__ inline int owned_before(int nrt, int w, int n) {
   int s = 0;
-  for (int v = 0; v < w; ++v) s += owned_tiles(nrt, v);
+  for (int v = 0; v < w; ++v) s += owned_tiles(nrt, v, n);
   return s;
+}
+
+// Token segments of the latent value pass for a block with nrt rank tiles of
+// 32: the split (1, 2, 4 or 8 segments) with the least work for the busiest
+// wave, ties going to fewer segments (fewer duplicate R^V reads), with no wave
+// owning more than kMaxOwn rank tiles.
+__host__ __device__ inline int v_segments(int nrt) {
+  int best = 1, best_work = 1 << 30;
+  for (int nseg = 1; nseg <= kWaves; nseg *= 2) {
+    const int ng = kWaves / nseg;
+    const int own = (nrt + ng - 1) / ng;
+    if (own > kMaxOwn) continue;
+    const int work = own * (kTile / nseg);
+    if (work < best_work) {
+      best_work = work;
+      best = nseg;
+    }
+  }
+  return best;
 }
 
 struct FactorGeom {
@@ -71,13 +95,13 @@ __host__ __device__ inline int64_t frag_count(const FactorGeom& f) {
   }
 }
 
-// the wave whose run holds unit u, when wave w's run has per*owned_tiles(nrt, w)
-// units and the runs are stored in wave order; *first = start of that run
-__host__ __device__ inline int run_owner(int nrt, int64_t u, int64_t per, int64_t* first) {
+// the owner whose run holds unit u, when owner w's run has per*owned_tiles(nrt, w, n)
+// units and the runs are stored in owner order; *first = start of that run
+__host__ __device__ inline int run_owner(int nrt, int64_t u, int64_t per, int n, int64_t* first) {
   int w = 0;
   int64_t start = 0;
-  while (w + 1 < kWaves && u >= start + per * owned_tiles(nrt, w)) {
-    start += per * owned_tiles(nrt, w);
+  while (w + 1 < n && u >= start + per * owned_tiles(nrt, w, n)) {
+    start += per * owned_tiles(nrt, w, n);
     ++w;
   }
   *first = start;
@@ -91,24 +115,24 @@ __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, i
   switch (f.kind) {
     case kPK: {
       const int nks = f.r_pad / 16, ntiles = f.T_pad / kTile;
-      const int mt = (int)(frag % 2);
-      const int kap = (int)((frag / 2) % nks);
-      const int t = (int)((frag / (2 * nks)) % ntiles);
-      const int w = (int)(frag / ((int64_t)2 * nks * ntiles));
-      const int tau = 8 * t + 2 * w + mt;
+      const int kap = (int)(frag % nks);
+      const int t = (int)((frag / nks) % ntiles);
+      const int w = (int)(frag / ((int64_t)nks * ntiles));
+      const int tau = kWaves * t + w;
       *row = 32 * tau + m;
       *col = 16 * kap + 8 * c + e;
       return;
     }
     case kPV: {
       const int nrt = f.r_pad / 32, T16 = f.T_pad / 16;
+      const int ng = kWaves / v_segments(nrt);
       int64_t first;
-      const int w = run_owner(nrt, frag, T16, &first);
-      const int own = owned_tiles(nrt, w);
+      const int rg = run_owner(nrt, frag, T16, ng, &first);
+      const int own = owned_tiles(nrt, rg, ng);
       const int64_t local = frag - first;
       const int sig = (int)(local / own), j = (int)(local % own);
       *row = 16 * sig + 8 * c + e;
-      *col = 32 * (w + kWaves * j) + m;
+      *col = 32 * (rg + ng * j) + m;
       return;
     }
     case kRK: {
@@ -116,7 +140,7 @@ __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, i
       const int g = (int)(frag / ((int64_t)nrt * nk));
       const int64_t in_g = frag % ((int64_t)nrt * nk);
       int64_t first;
-      const int w = run_owner(nrt, in_g, nk, &first);
+      const int w = run_owner(nrt, in_g, nk, kWaves, &first);
       const int64_t local = in_g - first;
       const int j = (int)(local / nk), kap = (int)(local % nk);
       *row = 32 * (w + kWaves * j) + m;
@@ -125,16 +149,17 @@ __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, i
     }
     default: {
       const int nrt = f.r_pad / 32, npass = f.d / 64;
+      const int ng = kWaves / v_segments(nrt);
       const int64_t per_g = (int64_t)(f.d / 32) * (f.r_pad / 16);
       const int g = (int)(frag / per_g);
       const int64_t in_g = frag % per_g;
       int64_t first;
-      const int w = run_owner(nrt, in_g, (int64_t)npass * 4, &first);
-      const int own = owned_tiles(nrt, w);
+      const int rg = run_owner(nrt, in_g, (int64_t)npass * 4, ng, &first);
+      const int own = owned_tiles(nrt, rg, ng);
       const int64_t local = in_g - first;
       const int dt = (int)(local % 2), half = (int)((local / 2) % 2);
       const int j = (int)((local / 4) % own), pass = (int)(local / (4 * own));
-      const int kap = 2 * (w + kWaves * j) + half;
+      const int kap = 2 * (rg + ng * j) + half;
       *row = 16 * kap + 8 * (e >> 2) + 4 * c + (e & 3);
       *col = g * f.d + 32 * (2 * pass + dt) + m;
       return;
@@ -177,21 +202,22 @@ struct WgProgram {
   int64_t off;                // byte offset in the program buffer (16-byte aligned)
   int32_t words;              // program size in 4-byte words
   int32_t n_items;            // work items (they start the program)
-  int32_t run_off[4];         // byte offset of wave w's run list within the program
+  int32_t run_off[kWaves];    // byte offset of wave w's run list within the program
 };
-static_assert(sizeof(WgProgram) == 32, "program entry layout");
+static_assert(sizeof(WgProgram) == 16 + 4 * kWaves, "program entry layout");
 constexpr int kSentinelRun = 1 << 30;
 
 // Attention kernel geometry.
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCols = 64;                      // query columns per workgroup
-constexpr int kTokWave = kTile / kWaves;       // tokens per wave per tile
+constexpr int kTokWave = kTile / kWaves;       // tokens per wave per tile (one MFMA row block)
+static_assert(kTokWave == 32, "the score pass gives every wave one 32-token sub-tile");
 constexpr int kWStride = kTile + 8;            // bf16 row stride of the weight tile in LDS
 constexpr int kORow = 68;                      // fp32 row stride of the up-projection reduction
 constexpr int kMaxGroup = 16;                  // max query heads per KV head
-constexpr int kMaxRank = 960;                  // largest supported rank (LDS bound)
+constexpr int kMaxRank = 896;                  // largest supported rank (LDS bound)
 constexpr int kLdsBytes = 160 * 1024;          // LDS per workgroup on gfx950
-constexpr int kTailChunk = 128;                // dense-tail tokens per work item
+constexpr int kTailChunk = kWaves * 32;        // dense-tail tokens per work item
 constexpr int kXcds = 8;                       // XCDs of an MI355X (workgroup b runs on XCD b % 8)
 constexpr int kCUs = 256;                      // compute units; one persistent workgroup each
 constexpr int kProgCap = 8192;                 // largest per-workgroup program (bytes of LDS)

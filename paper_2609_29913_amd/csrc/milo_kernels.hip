@@ -39,11 +39,13 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__device__ __forceinline__ void lds_dma16(const uint16_t* g, __bf16* lds_slot) {
-  __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(g),
-                                   reinterpret_cast<__attribute__((address_space(3))) void*>(
-                                       reinterpret_cast<uintptr_t>(lds_slot)),
-                                   16, 0, 0);
+// Direct global->LDS load of one fragment: lane l's 16 bytes from `src` land at
+// LDS byte address lds_slot + 16 l.  Issued as inline assembly, so the compiler
+// neither counts it nor orders other LDS accesses after it; every consumer
+// waits for it explicitly (wait_vmcnt) before reading the slot.  M0 carries the
+// slot address; no compiler-generated code in these kernels uses M0.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_slot) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_slot), "v"(src) : "memory");
 }
 
 // LDS reads of the workgroup's program (run lists, work items).  The compiler
@@ -65,6 +67,17 @@ __device__ __forceinline__ int4 prog_read_b128(const void* p) {
   return v;
 }
 
+// LDS stores the compiler would otherwise order after every in-flight
+// global->LDS fragment load (it cannot prove they target other addresses).
+__device__ __forceinline__ void lds_store_b128(void* p, float4 v) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  const f32x4 x = {v.x, v.y, v.z, v.w};
+  asm volatile("ds_write_b128 %0, %1" ::"v"(lds_addr(p)), "v"(x) : "memory");
+}
+__device__ __forceinline__ void lds_store_b32(void* p, float v) {
+  asm volatile("ds_write_b32 %0, %1" ::"v"(lds_addr(p)), "v"(v) : "memory");
+}
+
 // Workgroup barrier for the attention kernel: every wave's LDS reads and
 // writes issued before it are complete.  In-flight global->LDS fragment loads
 // are deliberately not waited for (each targets its own wave's ring slots);
@@ -75,10 +88,13 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (they complete in issue order).  The "memory" clobber keeps LDS reads of the
+// slots it guards after it.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 16, "vmcnt immediate");
-  __builtin_amdgcn_s_waitcnt(0xF70 | N);  // vmcnt(N), expcnt/lgkmcnt not waited
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // ---------------------------------------------------------------------------
@@ -237,47 +253,37 @@ __device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& i
   }
 }
 
-// ---------------------------------------------------------------------------
-// Block work item: latent-space attention of one 64-column tile of the query
-// columns of KV head g over the tiles [tile0, tile0 + ntile) of block b.
-//
-// Waves split the tokens of each 256-token tile for the scores (64 tokens each)
-// and split the rank tiles of the latent accumulator (rank tile rt belongs to
-// wave rt % 4).  Every factor fragment a wave consumes (R^K for the projection,
-// P^K and P^V per tile, R^V for the up-projection) comes from the wave's
-// fragment stream (FragRing below).  Every loop is software-pipelined: the
-// operands of step k+1 are read while the MFMAs of step k run.
-// ---------------------------------------------------------------------------
 // A wave's fragment stream over all block items of its workgroup.  The host
 // lists, per wave, the runs of consecutive packed fragments in the order the
 // wave consumes them (per block item: its R^K run for the projection, then for
 // every 256-token tile its P^K run and its P^V run, then its R^V run for the
-// up-projection); the list sits in LDS and ends with a long sentinel run.
-// With NSLOT > 0 fragments reach the wave through a private ring of NSLOT LDS
+// up-projection); the list sits in LDS and ends with a long sentinel run.  A
+// run entry (x, n) is n consecutive fragments starting at fragment x.  With
+// NSLOT > 0 fragments reach the wave through a private ring of NSLOT LDS
 // slots, filled by direct global->LDS loads issued kDepth fragments ahead of
 // use, so every wait is a constant vmcnt; the look-ahead crosses item
 // boundaries, so the next item's first fragments load while the current one
 // finishes.  With NSLOT == 0 fragments are loaded straight into registers.
-// All fields are wave-uniform (scalar registers).
-template <int NSLOT>
+template <int D, int NSLOT>
 struct FragRing {
   static constexpr int kDepth = NSLOT > 2 ? NSLOT - 2 : 1;  // fragments in flight
-  const uint16_t* data_lane;  // packed buffer + this lane's 8-element offset
+  const uint16_t* data_lane;  // packed factor buffer + this lane's 8-element offset
+  int lane8;                  // this lane's element offset inside a fragment
   __bf16* ring;               // this wave's NSLOT slots
+  uint32_t ring_lds;          // LDS byte address of slot 0 (wave-uniform)
   const int2* run;            // current entry of this wave's run list (LDS)
   int64_t off;                // element offset of the next fragment
   int left;                   // fragments left in the current run
   int rs, ws;                 // ring slots: next to read, next to fill
-  int lane8;                  // this lane's element offset inside a fragment
 
   __device__ __forceinline__ void load_run() {
     const int2 v = prog_read_b64(run);
     off = (int64_t)__builtin_amdgcn_readfirstlane(v.x) * kFragElems;
     left = __builtin_amdgcn_readfirstlane(v.y);
   }
-  // offset of the next fragment of the stream; advances it
-  __device__ __forceinline__ int64_t next() {
-    const int64_t o = off;
+  // address of this lane's part of the next fragment; advances the stream
+  __device__ __forceinline__ const uint16_t* next() {
+    const uint16_t* o = data_lane + off;
     off += kFragElems;
     if (--left == 0) {
       ++run;
@@ -291,7 +297,7 @@ struct FragRing {
     ws = 0;
     if constexpr (NSLOT > 0) {
 #pragma unroll
-      for (int k = 0; k < kDepth; ++k) lds_dma16(data_lane + next(), ring + k * kFragElems);
+      for (int k = 0; k < kDepth; ++k) lds_dma16(next(), ring_lds + k * kFragElems * 2);
       ws = kDepth;
     }
   }
@@ -300,20 +306,35 @@ struct FragRing {
     if constexpr (NSLOT > 0) {
       wait_vmcnt<kDepth - 1>();
       const bf16x8 v = ld_bf16x8(ring + rs * kFragElems + lane8);
-      lds_dma16(data_lane + next(), ring + ws * kFragElems);
+      lds_dma16(next(), ring_lds + ws * kFragElems * 2);
       rs = rs + 1 == NSLOT ? 0 : rs + 1;
       ws = ws + 1 == NSLOT ? 0 : ws + 1;
       return v;
     } else {
-      return ld_bf16x8(data_lane + next());
+      return ld_bf16x8(next());
     }
   }
 };
 
+// ---------------------------------------------------------------------------
+// Block work item: latent-space attention of one 64-column tile of the query
+// columns of KV head g over the tiles [tile0, tile0 + ntile) of block b.
+//
+// Eight waves (two per SIMD).  Scores: wave w takes the 32 tokens 32w..32w+31
+// of every 256-token tile against all 64 columns.  Latent V and the
+// up-projection: the waves form nseg token segments x ng rank groups (see the
+// packed layout), so each wave accumulates its own rank tiles over its own
+// tokens; the up-projected partials of all waves are summed in LDS.  Every
+// factor fragment a wave consumes (R^K for the projection, P^K and P^V per
+// tile, R^V for the up-projection) comes from the wave's fragment stream
+// (FragRing above); the item's queries are loaded into LDS at its start.  Every loop is software-pipelined: the operands of
+// step k+1 are read while the MFMAs of step k run.
+// ---------------------------------------------------------------------------
 template <int D, int MAX_RT, int NSLOT>
 __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
-                                           FragRing<NSLOT>& fr, const int tid) {
+                                           FragRing<D, NSLOT>& fr, const int tid) {
   constexpr int NK = D / 16;
+  constexpr int kORed = 4;  // partial-output slots of the up-projection reduction
   const BlockMeta& bm = it.blk;
   const int slot = it.slot, g = it.g, c0 = it.sub * kCols;
   const int lane = tid & 63;
@@ -322,34 +343,53 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   const int G = a.G, ncg = a.n_q * G;
   const int qsd = a.qt_stride;
   const int nrt_k = bm.rk_pad >> 5, nks = bm.rk_pad >> 4;
-  const int nrt_v = bm.rv_pad >> 5, nkv = bm.rv_pad >> 4;
-  const int my_nrt = owned_tiles(nrt_v, wave);
-  const int my_nrt_k = owned_tiles(nrt_k, wave);
+  const int nrt_v = bm.rv_pad >> 5;
+  const int own_k = owned_tiles(nrt_k, wave, kWaves);
+  const int nseg = v_segments(nrt_v), ng = kWaves / nseg;
+  const int rg = wave % ng, sg = wave / ng;
+  const int own_v = owned_tiles(nrt_v, rg, ng);
+  const int nst = 16 / nseg;                // 16-token steps of the wave's segment per tile
   const int T = bm.T;
   const int ntiles = it.ntile, tile0 = it.tile0;  // tiles this item covers
   __bf16* qt = reinterpret_cast<__bf16*>(smem);              // [kCols][qsd]
   __bf16* wl = qt + kCols * qsd;                               // [kCols][kWStride]
   float* red = reinterpret_cast<float*>(wl + kCols * kWStride);  // [kWaves][kCols]
   // the wave's next fragment; the order of take() calls below is the order of
-  // the wave's runs: R^K, then per tile P^K and P^V, then R^V
+  // the wave's runs: R^K (waves that own projection rank tiles), then per tile
+  // P^K and P^V, then R^V
   auto take = [&]() -> bf16x8 { return fr.take(); };
 
-  // ---- projection: Qt[rank][col] (stored [col][rank]) ----
+  // ---- the item's 64 query rows -> LDS (in the weight tile's area, idle until
+  // the first tile).  Row-major [column][D]; the 16-byte chunk j of column c is
+  // stored at chunk position j ^ (c % kRowChunks), so the projection's operand
+  // reads (same chunk, 32 columns) hit distinct banks.  Columns past the last
+  // one re-read the last column's query (their results are never stored).
+  constexpr int kRowChunks = D / 8;              // 16-byte chunks per query row
+  constexpr int kRowsPerLoad = 64 / kRowChunks;  // rows per 1 KiB load
+  const __bf16* qimg = wl;
   {
+    const uint32_t qimg_lds = __builtin_amdgcn_readfirstlane(lds_addr(qimg));
+    const int cl_lane = lane / kRowChunks, pos = lane % kRowChunks;
+    for (int f = wave; f < kCols / kRowsPerLoad; f += kWaves) {
+      const int cl = kRowsPerLoad * f + cl_lane;
+      const int c = min(c0 + cl, ncg - 1);
+      const uint16_t* src =
+          a.q + ((int64_t)(c / G) * a.H_q + g * G + c % G) * D + 8 * (pos ^ (cl % kRowChunks));
+      lds_dma16(src, qimg_lds + f * 1024);
+    }
+    wait_vmcnt<0>();
+    lds_barrier();
+  }
+
+  // ---- projection: Qt[rank][col] (stored [col][rank]) ----
+  if (own_k > 0) {
     bf16x8 qf[NK][2];
 #pragma unroll
-    for (int ch = 0; ch < 2; ++ch) {
-      const int c = c0 + 32 * ch + lrow;
-      const bool ok = c < ncg;
-      const int qi = ok ? c / G : 0, qh = ok ? g * G + c % G : 0;
-      const uint16_t* qrow = a.q + ((int64_t)qi * a.H_q + qh) * D + 8 * lhi;
+    for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-      for (int k = 0; k < NK; ++k) {
-        bf16x8 v = ld_bf16x8(qrow + 16 * k);
-        qf[k][ch] = ok ? v : bf16x8{};
-      }
-    }
-    for (int j = 0; j < my_nrt_k; ++j) {
+      for (int k = 0; k < NK; ++k)
+        qf[k][ch] = ld_bf16x8(qimg + (32 * ch + lrow) * D + 8 * ((2 * k + lhi) ^ (lrow % kRowChunks)));
+    for (int j = 0; j < own_k; ++j) {
       const int rt = wave + kWaves * j;
       f32x16 acc0 = {}, acc1 = {};
       bf16x8 af = take();
@@ -385,56 +425,48 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   float l_run[2] = {0.f, 0.f};
   const __bf16* qr0 = qt + lrow * qsd + 8 * lhi;
   const __bf16* qr1 = qt + (32 + lrow) * qsd + 8 * lhi;
-  const __bf16* wr0 = wl + lrow * kWStride + 8 * lhi;
-  const __bf16* wr1 = wl + (32 + lrow) * kWStride + 8 * lhi;
+  const __bf16* wr0 = wl + lrow * kWStride + 8 * lhi + 16 * nst * sg;
+  const __bf16* wr1 = wl + (32 + lrow) * kWStride + 8 * lhi + 16 * nst * sg;
 
   for (int tt = 0; tt < ntiles; ++tt) {
-    const int t0 = (tile0 + tt) * kTile;
-    const int tw = t0 + wave * kTokWave;
-    f32x16 s00 = {}, s01 = {}, s10 = {}, s11 = {};
+    const int tw = (tile0 + tt) * kTile + wave * kTokWave;
+    f32x16 s0 = {}, s1 = {};
     {
-      // operands of rank step k: a0/a1 (P^K sub-tiles), b0/b1 (Qt column tiles);
+      // operands of rank step k: ak (P^K sub-tile), b0/b1 (Qt column tiles);
       // nks is even (ranks are padded to 32), so the loop runs over step pairs
-      bf16x8 a0 = take(), a1 = take();
+      bf16x8 ak = take();
       bf16x8 b0 = ld_bf16x8(qr0), b1 = ld_bf16x8(qr1);
       for (int k = 0; k < nks; k += 2) {
-        const bf16x8 c0 = take(), c1 = take();
+        const bf16x8 ck = take();
         const bf16x8 d0 = ld_bf16x8(qr0 + 16 * (k + 1));
         const bf16x8 d1 = ld_bf16x8(qr1 + 16 * (k + 1));
-        s00 = mfma32(a0, b0, s00);
-        s01 = mfma32(a0, b1, s01);
-        s10 = mfma32(a1, b0, s10);
-        s11 = mfma32(a1, b1, s11);
+        s0 = mfma32(ak, b0, s0);
+        s1 = mfma32(ak, b1, s1);
         if (k + 2 < nks) {
-          a0 = take();
-          a1 = take();
+          ak = take();
           b0 = ld_bf16x8(qr0 + 16 * (k + 2));
           b1 = ld_bf16x8(qr1 + 16 * (k + 2));
         }
-        s00 = mfma32(c0, d0, s00);
-        s01 = mfma32(c0, d1, s01);
-        s10 = mfma32(c1, d0, s10);
-        s11 = mfma32(c1, d1, s11);
+        s0 = mfma32(ck, d0, s0);
+        s1 = mfma32(ck, d1, s1);
       }
     }
-    f32x16 s[2][2] = {{s00, s01}, {s10, s11}};
+    f32x16 sc[2] = {s0, s1};
     // mask tokens past the end of the block, wave-local column max
     float mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+    for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-      for (int ch = 0; ch < 2; ++ch)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int tok = tw + 32 * mt + 8 * (v >> 2) + 4 * lhi + (v & 3);
-          const float x = tok < T ? s[mt][ch][v] : -INFINITY;
-          s[mt][ch][v] = x;
-          mx[ch] = fmaxf(mx[ch], x);
-        }
+      for (int v = 0; v < 16; ++v) {
+        const int tok = tw + 8 * (v >> 2) + 4 * lhi + (v & 3);
+        const float x = tok < T ? sc[ch][v] : -INFINITY;
+        sc[ch][v] = x;
+        mx[ch] = fmaxf(mx[ch], x);
+      }
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
       mx[ch] = fmaxf(mx[ch], __shfl_xor(mx[ch], 32));
-      if (lhi == 0) red[wave * kCols + 32 * ch + lrow] = mx[ch];
+      red[wave * kCols + 32 * ch + lrow] = mx[ch];  // both lane halves hold the same value
     }
     lds_barrier();
     float alpha[2];
@@ -452,19 +484,16 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
     for (int ch = 0; ch < 2; ++ch) {
       float lsum = 0.f;
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
+      for (int j = 0; j < 4; ++j) {
+        bf16x4 w4;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          bf16x4 w4;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const float w = fast_exp2(s[mt][ch][4 * j + u] - m_run[ch]);
-            lsum += w;
-            w4[u] = (__bf16)w;
-          }
-          *reinterpret_cast<bf16x4*>(wl + (32 * ch + lrow) * kWStride + wave * kTokWave + 32 * mt +
-                                     8 * j + 4 * lhi) = w4;
+        for (int u = 0; u < 4; ++u) {
+          const float w = fast_exp2(sc[ch][4 * j + u] - m_run[ch]);
+          lsum += w;
+          w4[u] = (__bf16)w;
         }
+        *reinterpret_cast<bf16x4*>(wl + (32 * ch + lrow) * kWStride + wave * kTokWave + 8 * j + 4 * lhi) = w4;
+      }
       l_run[ch] = l_run[ch] * alpha[ch] + lsum;
     }
     lds_barrier();
@@ -473,35 +502,36 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       oacc[r][0] *= alpha[0];
       oacc[r][1] *= alpha[1];
     }
-    if (my_nrt > 0) {
-      // operands of 16-token step sg: w0/w1 (weight column tiles), pa[r] (P^V rank tiles)
+    if (own_v > 0) {
+      // operands of 16-token step st: w0/w1 (weight column tiles), pa[r] (P^V rank
+      // tiles); nst is even (at most 8 segments), so the loop runs over step pairs
       bf16x8 pa[MAX_RT], pc[MAX_RT];
       bf16x8 w0 = ld_bf16x8(wr0), w1 = ld_bf16x8(wr1);
 #pragma unroll
       for (int r = 0; r < MAX_RT; ++r)
-        if (r < my_nrt) pa[r] = take();
-      for (int sg = 0; sg < kTile / 16; sg += 2) {
-        const bf16x8 x0 = ld_bf16x8(wr0 + 16 * (sg + 1));
-        const bf16x8 x1 = ld_bf16x8(wr1 + 16 * (sg + 1));
+        if (r < own_v) pa[r] = take();
+      for (int st = 0; st < nst; st += 2) {
+        const bf16x8 x0 = ld_bf16x8(wr0 + 16 * (st + 1));
+        const bf16x8 x1 = ld_bf16x8(wr1 + 16 * (st + 1));
 #pragma unroll
         for (int r = 0; r < MAX_RT; ++r)
-          if (r < my_nrt) pc[r] = take();
+          if (r < own_v) pc[r] = take();
 #pragma unroll
         for (int r = 0; r < MAX_RT; ++r)
-          if (r < my_nrt) {
+          if (r < own_v) {
             oacc[r][0] = mfma32(pa[r], w0, oacc[r][0]);
             oacc[r][1] = mfma32(pa[r], w1, oacc[r][1]);
           }
-        if (sg + 2 < kTile / 16) {
-          w0 = ld_bf16x8(wr0 + 16 * (sg + 2));
-          w1 = ld_bf16x8(wr1 + 16 * (sg + 2));
+        if (st + 2 < nst) {
+          w0 = ld_bf16x8(wr0 + 16 * (st + 2));
+          w1 = ld_bf16x8(wr1 + 16 * (st + 2));
 #pragma unroll
           for (int r = 0; r < MAX_RT; ++r)
-            if (r < my_nrt) pa[r] = take();
+            if (r < own_v) pa[r] = take();
         }
 #pragma unroll
         for (int r = 0; r < MAX_RT; ++r)
-          if (r < my_nrt) {
+          if (r < own_v) {
             oacc[r][0] = mfma32(pc[r], x0, oacc[r][0]);
             oacc[r][1] = mfma32(pc[r], x1, oacc[r][1]);
           }
@@ -513,27 +543,25 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 #pragma unroll
   for (int ch = 0; ch < 2; ++ch) l_run[ch] += __shfl_xor(l_run[ch], 32);
   lds_barrier();  // every wave is done with qt / wl
-  float* ored = reinterpret_cast<float*>(smem);       // [kWaves][kCols][kORow]
-  float* lred = ored + kWaves * kCols * kORow;        // [kWaves][kCols]
-  if (lhi == 0) {
-    lred[wave * kCols + lrow] = l_run[0];
-    lred[wave * kCols + 32 + lrow] = l_run[1];
-  }
+  float* ored = reinterpret_cast<float*>(smem);       // [kORed][kCols][kORow]
+  float* lred = ored + kORed * kCols * kORow;         // [kWaves][kCols]
+  lred[wave * kCols + lrow] = l_run[0];  // both lane halves hold the sums
+  lred[wave * kCols + 32 + lrow] = l_run[1];
 #pragma unroll
   for (int pass = 0; pass < D / 64; ++pass) {
     f32x16 acc[2][2];
     acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = f32x16{};
-    if (my_nrt > 0) {
+    if (own_v > 0) {
       // fragments of (owned rank tile r, rank half, d tile dt), in stream order
       bf16x8 f00 = take(), f01 = take();
 #pragma unroll
       for (int r = 0; r < MAX_RT; ++r) {
-        if (r < my_nrt) {
+        if (r < own_v) {
 #pragma unroll
           for (int half = 0; half < 2; ++half) {
             // prefetch the next (rank tile, half) pair of d-tile fragments
             bf16x8 g00 = f00, g01 = f01;
-            if (half == 0 || r + 1 < my_nrt) {
+            if (half == 0 || r + 1 < own_v) {
               g00 = take();
               g01 = take();
             }
@@ -553,29 +581,48 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
         }
       }
     }
+    // sum the eight waves' partials: waves 0-3 store, then waves 4-7 add in place
+    float* mine = ored + ((wave % kORed) * kCols + lrow) * kORow + 4 * lhi;
+    if (wave < kORed) {
 #pragma unroll
-    for (int dt = 0; dt < 2; ++dt)
+      for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
-      for (int ch = 0; ch < 2; ++ch)
+        for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float4 v = make_float4(acc[dt][ch][4 * j], acc[dt][ch][4 * j + 1], acc[dt][ch][4 * j + 2],
-                                 acc[dt][ch][4 * j + 3]);
-          *reinterpret_cast<float4*>(ored + (wave * kCols + 32 * ch + lrow) * kORow + 32 * dt + 8 * j +
-                                     4 * lhi) = v;
-        }
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<float4*>(mine + 32 * ch * kORow + 32 * dt + 8 * j) =
+                make_float4(acc[dt][ch][4 * j], acc[dt][ch][4 * j + 1], acc[dt][ch][4 * j + 2],
+                            acc[dt][ch][4 * j + 3]);
+    }
+    lds_barrier();
+    if (wave >= kORed) {
+#pragma unroll
+      for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+        for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            float4* p = reinterpret_cast<float4*>(mine + 32 * ch * kORow + 32 * dt + 8 * j);
+            float4 v = *p;
+            v.x += acc[dt][ch][4 * j];
+            v.y += acc[dt][ch][4 * j + 1];
+            v.z += acc[dt][ch][4 * j + 2];
+            v.w += acc[dt][ch][4 * j + 3];
+            *p = v;
+          }
+    }
     lds_barrier();
     {
-      const int col = tid >> 2, dq = (tid & 3) * 16;
+      const int col = tid >> 3, dq = (tid & 7) * 8;
       const int c = c0 + col;
       if (c < ncg) {
         const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
         float* dst = a.part_o + (colg * a.n_slots + slot) * D + 64 * pass + dq;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
+        for (int q4 = 0; q4 < 2; ++q4) {
           float4 sum = *reinterpret_cast<const float4*>(ored + col * kORow + dq + 4 * q4);
 #pragma unroll
-          for (int w = 1; w < kWaves; ++w) {
+          for (int w = 1; w < kORed; ++w) {
             const float4 x = *reinterpret_cast<const float4*>(ored + (w * kCols + col) * kORow + dq + 4 * q4);
             sum.x += x.x; sum.y += x.y; sum.z += x.z; sum.w += x.w;
           }
@@ -627,13 +674,14 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   }
   lds_barrier();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int run_off = wave == 0 ? p.run_off[0] : wave == 1 ? p.run_off[1] : wave == 2 ? p.run_off[2] : p.run_off[3];
+  const int run_off = a.wg[blockIdx.x].run_off[wave];  // scalar load at a wave-uniform index
   unsigned char* work = smem + a.prog_bytes;
-  FragRing<NSLOT> fr;
+  FragRing<D, NSLOT> fr;
   fr.data_lane = a.data + (threadIdx.x & 63) * 8;
   fr.lane8 = (threadIdx.x & 63) * 8;
-  fr.run = reinterpret_cast<const int2*>(smem + run_off);
   fr.ring = reinterpret_cast<__bf16*>(work + a.ring_offset) + (size_t)wave * NSLOT * kFragElems;
+  fr.ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(fr.ring));
+  fr.run = reinterpret_cast<const int2*>(smem + run_off);
   fr.start();
   for (int k = 0; k < p.n_items; ++k) {
     const WorkItem it = lds_item(smem + (size_t)k * sizeof(WorkItem));
@@ -654,18 +702,20 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
 // the slots s = w mod 4 (each lane owns D/64 consecutive outputs); the waves are
 // combined in a fixed order, so the result is deterministic.
 // ---------------------------------------------------------------------------
+constexpr int kMergeWaves = 4;
+constexpr int kMergeThreads = 64 * kMergeWaves;
 template <int D>
-__global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
   constexpr int E = D / 64;  // outputs per lane
-  __shared__ float red[kWaves];
-  __shared__ float dred[kWaves];
-  __shared__ float part[kWaves][D];
+  __shared__ float red[kMergeWaves];
+  __shared__ float dred[kMergeWaves];
+  __shared__ float part[kMergeWaves][D];
   const int col = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int i = col / a.H_q;
   const int n_valid = a.n_block_slots + (a.tail_len[i] + kTailChunk - 1) / kTailChunk;
   const float2* ml = a.part_ml + (int64_t)col * a.n_slots;
   float mx = -INFINITY;
-  for (int s = tid; s < n_valid; s += kThreads) mx = fmaxf(mx, ml[s].x);
+  for (int s = tid; s < n_valid; s += kMergeThreads) mx = fmaxf(mx, ml[s].x);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
   if (lane == 0) red[wave] = mx;
@@ -676,14 +726,14 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
   for (int e = 0; e < E; ++e) num[e] = 0.f;
   const float* po = a.part_o + (int64_t)col * a.n_slots * D + E * lane;
   int s = wave;
-  for (; s + 3 * kWaves < n_valid; s += 4 * kWaves) {
+  for (; s + 3 * kMergeWaves < n_valid; s += 4 * kMergeWaves) {
     float2 m4[4];
     float v4[4][E];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      m4[u] = ml[s + u * kWaves];
+      m4[u] = ml[s + u * kMergeWaves];
 #pragma unroll
-      for (int e = 0; e < E; ++e) v4[u][e] = po[(int64_t)(s + u * kWaves) * D + e];
+      for (int e = 0; e < E; ++e) v4[u][e] = po[(int64_t)(s + u * kMergeWaves) * D + e];
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -693,7 +743,7 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
       for (int e = 0; e < E; ++e) num[e] += v4[u][e] * f;
     }
   }
-  for (; s < n_valid; s += kWaves) {
+  for (; s < n_valid; s += kMergeWaves) {
     const float2 m1 = ml[s];
     const float f = fast_exp2(m1.x - mx);
     den += m1.y * f;
@@ -725,7 +775,7 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
 size_t attend_lds_base_bytes(int head_dim, int rk_pad_max) {
   const size_t qsd = (size_t)rk_pad_max + 8;
   const size_t loop = kCols * qsd * 2 + (size_t)kCols * kWStride * 2 + (size_t)kWaves * kCols * 4;
-  const size_t epi = ((size_t)kWaves * kCols * kORow + (size_t)kWaves * kCols) * 4;
+  const size_t epi = ((size_t)4 * kCols * kORow + (size_t)kWaves * kCols) * 4;
   const size_t tail = ((size_t)2 * kWaves * 32 + (size_t)kTailChunk * 32 + (size_t)kWaves * kMaxGroup * head_dim) * 4;
   size_t m = loop > epi ? loop : epi;
   m = m > tail ? m : tail;
@@ -750,8 +800,7 @@ static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hip
 template <int D, int MAX_RT>
 static hipError_t launch_attend_r(const AttendArgs& a, int nslot, int grid, size_t lds, hipStream_t s) {
   switch (nslot) {
-    case 14: return launch_attend_t<D, MAX_RT, 14>(a, grid, lds, s);
-    case 12: return launch_attend_t<D, MAX_RT, 12>(a, grid, lds, s);
+    case 8: return launch_attend_t<D, MAX_RT, 8>(a, grid, lds, s);
     case 6: return launch_attend_t<D, MAX_RT, 6>(a, grid, lds, s);
     case 0: return launch_attend_t<D, MAX_RT, 0>(a, grid, lds, s);
     default: return hipErrorInvalidValue;
@@ -764,8 +813,6 @@ static hipError_t launch_attend_d(const AttendArgs& a, int max_rt, int nslot, in
   switch (max_rt) {
     case 2: return launch_attend_r<D, 2>(a, nslot, grid, lds, s);
     case 4: return launch_attend_r<D, 4>(a, nslot, grid, lds, s);
-    case 6: return launch_attend_r<D, 6>(a, nslot, grid, lds, s);
-    case 8: return launch_attend_r<D, 8>(a, nslot, grid, lds, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -780,9 +827,9 @@ hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslo
 
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s) {
   if (head_dim == 64) {
-    hipLaunchKernelGGL(merge_kernel<64>, dim3(n_cols), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(merge_kernel<64>, dim3(n_cols), dim3(kMergeThreads), 0, s, a);
   } else if (head_dim == 128) {
-    hipLaunchKernelGGL(merge_kernel<128>, dim3(n_cols), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(merge_kernel<128>, dim3(n_cols), dim3(kMergeThreads), 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }

@@ -54,7 +54,7 @@ def _create(desc, nb=1, null_factor=False):
     (dict(nb=1, T=(300,), rk=(65,), rv=(8,)), milo.MILO_ERR_INVALID_ARG),     # rank > H_kv*d
     (dict(nb=1, T=(64,), rk=(8,), rv=(0,)), milo.MILO_ERR_INVALID_ARG),       # rank 0
     (dict(nb=1, d=96, T=(64,), rk=(8,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # head_dim
-    (dict(nb=1, nkv=8, d=128, T=(2048,), rk=(992,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # rank cap
+    (dict(nb=1, nkv=8, d=128, T=(2048,), rk=(928,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # rank cap
     (dict(nb=1, nkv=0, T=(64,), rk=(8,), rv=(8,)), milo.MILO_ERR_INVALID_ARG),
 ])
 def test_create_rejects(kw, code):

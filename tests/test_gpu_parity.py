@@ -54,7 +54,7 @@ SHAPES = {
                 n_q_heads=16, tail_cap=9, tail_len=[9, 0, 4, 9, 1]),
     "rank768": dict(block_tokens=[1024, 800], rank_k=[768, 640], rank_v=[704, 768], n_kv_heads=8,
                     head_dim=128, n_q=2, n_q_heads=40, tail_cap=64),
-    "rank960": dict(block_tokens=[1000], rank_k=[960], rank_v=[900], n_kv_heads=8, head_dim=128, n_q=1,
+    "rank896": dict(block_tokens=[1000], rank_k=[896], rank_v=[840], n_kv_heads=8, head_dim=128, n_q=1,
                     n_q_heads=16, tail_cap=0),
 }
 

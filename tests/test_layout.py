@@ -8,7 +8,10 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 GEOMS = [
     (1, 1, 1, 64), (45, 33, 3, 64), (256, 64, 2, 128), (300, 100, 4, 128), (1024, 288, 4, 128),
-    (700, 96, 2, 64), (1000, 960, 8, 128), (2048, 512, 8, 128), (513, 160, 1, 64), (100, 40, 4, 128),
+    (700, 96, 2, 64), (1000, 896, 8, 128), (2048, 512, 8, 128), (513, 160, 1, 64), (100, 40, 4, 128),
+    # every split of the latent value pass (1, 2, 4 and 8 token segments)
+    (256, 32, 2, 64), (512, 64, 2, 64), (300, 96, 4, 128), (256, 128, 2, 64), (256, 224, 4, 128),
+    (768, 288, 4, 128), (256, 384, 4, 128), (1024, 768, 8, 128),
 ]
 
 
