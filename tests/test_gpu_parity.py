@@ -72,6 +72,28 @@ def test_parity_q7b_single_layer():
     _check(synth.gen_layer("q7b_1l"), label="q7b_1l")
 
 
+@pytest.mark.parametrize("cfg,layer", [("q7b_28l", 27), ("q14b_48l", 0), ("q32b_64l", 0)])
+def test_parity_full_size_layers_sampled(cfg, layer):
+    """One whole layer of each large workload (all selected blocks, full decode
+    batch, full tails) on the GPU; the oracle checks a seeded sample of columns
+    (every KV head group is represented)."""
+    inp = synth.gen_layer(cfg, layer)
+    gl = GpuLayer(inp)
+    try:
+        got = gl.attend().cpu().numpy()
+    finally:
+        gl.free()
+    assert np.all(np.isfinite(got)), "unwritten or non-finite outputs"
+    rng = np.random.default_rng(zlib.crc32(cfg.encode()) + layer)
+    G = inp.n_q_heads // inp.n_kv_heads
+    cols = [(int(rng.integers(inp.n_q)), g * G + int(rng.integers(G))) for g in range(inp.n_kv_heads)]
+    cols += [(int(rng.integers(inp.n_q)), int(rng.integers(inp.n_q_heads))) for _ in range(4)]
+    ref = oracle.attend_latent(**oracle_args(inp), columns=cols)
+    err = col_rel_l2(np.stack([got[i, h] for i, h in cols]), ref)
+    print(f"[parity] {cfg} layer {layer}: {len(cols)} sampled columns, max rel-L2 = {err.max():.3e}", flush=True)
+    assert err.max() <= TOL_REL_L2
+
+
 def test_subset_and_order_of_blocks():
     inp = synth.make_problem(21, [300, 512, 64, 1000, 7], [32, 64, 16, 256, 7], n_kv_heads=2, head_dim=128,
                              n_q=2, n_q_heads=6, tail_cap=40, tail_len=[40, 13])
