@@ -66,10 +66,12 @@ def to_device(a, dev):
 
 
 class Layer:
+    """One layer's device state: its cache, queries, tails and output (the host
+    copies of the factors are not kept)."""
+
     def __init__(self, inp: synth.LayerInputs, dev):
         import torch
         from paper_2609_29913_amd import milo
-        self.inp = inp
         self.cache = milo.milo_cache_create(inp.block_tokens, inp.rank_k, inp.rank_v, inp.n_kv_heads,
                                             inp.head_dim, inp.pk, inp.rk, inp.pv, inp.rv)
         self.q = to_device(inp.q, dev)
@@ -77,11 +79,12 @@ class Layer:
         self.tv = to_device(inp.tail_v, dev)
         self.out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
         self.table = list(range(inp.n_blocks))
+        self.tail_len = inp.tail_len.copy()
+        self.scale = inp.scale
 
     def step(self, stream):
         from paper_2609_29913_amd import milo
-        inp = self.inp
-        milo.milo_attend_decode(self.cache, self.table, self.q, self.tk, self.tv, inp.tail_len, inp.scale,
+        milo.milo_attend_decode(self.cache, self.table, self.q, self.tk, self.tv, self.tail_len, self.scale,
                                 self.out, stream=stream)
 
 
@@ -152,10 +155,24 @@ def main():
     milo.lib()
 
     cfg = synth.CONFIGS[args.config]
-    layers_inp = [synth.gen_layer(cfg, l) for l in range(cfg.n_layers)]
-    per_step = sum(synth.algorithmic_bytes(x) for x in layers_inp)
+    # layers are generated one at a time and only their device state is kept
+    # (a 64-layer workload's host factors would not fit next to each other)
+    x0 = None
+    per_step = flops_step = out_bytes = 0
+    mean_ranks = []
+    groups = [[]]
+    for l in range(cfg.n_layers):
+        x = synth.gen_layer(cfg, l)
+        per_step += synth.algorithmic_bytes(x)
+        flops_step += synth.latent_flops(x)
+        out_bytes += 4 * x.n_q * x.n_q_heads * x.head_dim
+        mean_ranks.append(float(x.rank_k.mean()))
+        groups[0].append(Layer(x, dev))
+        if l == 0:
+            x0 = x
     copies = max(1, int(np.ceil(args.rotate_bytes / per_step)))
-    groups = [[Layer(x, dev) for x in layers_inp] for _ in range(copies)]
+    for _ in range(1, copies):
+        groups.append([Layer(synth.gen_layer(cfg, l), dev) for l in range(cfg.n_layers)])
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
@@ -186,13 +203,14 @@ def main():
     merge_avg_s = merge_ms / n_calls * 1e-3
 
     # the attention kernel reads every factor once, the tails and the queries
-    out_bytes = sum(4 * x.n_q * x.n_q_heads * x.head_dim for x in layers_inp)
     kern_bytes = (per_step - out_bytes) / cfg.n_layers
-    flops = sum(synth.latent_flops(x) for x in layers_inp) / cfg.n_layers
+    flops = flops_step / cfg.n_layers
     achieved = kern_bytes / att_avg_s / 1e9
+    mfma_tflops = flops / att_avg_s / 1e12
+    # the bound is the roof the kernel's arithmetic intensity meets first
+    bound = "hbm" if flops / kern_bytes < MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
     traffic = counter_traffic(args.config)
 
-    x0 = layers_inp[0]
     ctx_tokens = int(x0.block_tokens.sum()) + int(x0.tail_len.max())
     value = x0.n_q * ctx_tokens / (ms_per_step * 1e-3)
     result = {
@@ -219,25 +237,27 @@ def main():
             "q_heads": x0.n_q_heads,
             "kv_heads": x0.n_kv_heads,
             "head_dim": x0.head_dim,
-            "mean_rank": float(np.mean([x.rank_k.mean() for x in layers_inp])),
+            "mean_rank": float(np.mean(mean_ranks)),
             "accumulation": "fp32",
             "rotated_copies": copies,
             "step_bytes_algorithmic": per_step,
             "hbm_frac_of_step": per_step / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
         },
         "roofline": {
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
+            "bound": bound,
+            "achieved": achieved if bound == "hbm" else mfma_tflops,
+            "peak": HBM_PEAK_GBS if bound == "hbm" else MFMA_BF16_PEAK_TFLOPS,
+            "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+            "frac": achieved / HBM_PEAK_GBS if bound == "hbm" else mfma_tflops / MFMA_BF16_PEAK_TFLOPS,
             "traffic": traffic,
+            "arithmetic_intensity_flop_per_byte": flops / kern_bytes,
             "kernel": "attend_kernel",
             "kernel_avg_us": att_avg_s * 1e6,
             "merge_kernel_avg_us": merge_avg_s * 1e6,
             "algorithmic_bytes_per_launch": kern_bytes,
-            "mfma_tflops": flops / att_avg_s / 1e12,
-            "mfma_frac": flops / att_avg_s / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+            "hbm_gbs": achieved,
+            "mfma_tflops": mfma_tflops,
+            "mfma_frac": mfma_tflops / MFMA_BF16_PEAK_TFLOPS,
             "kernel_source_sha256_16": kernel_source_hash(),
         },
         "cpu_baseline": None,
