@@ -123,20 +123,22 @@ int64_t factor_offset(const BlockMeta& m, int which) {
 //
 // Work is cut into jobs: a block job is one part of a selected block (a range
 // of whole 256-token tiles; large blocks are split so the work evens out) for
-// one 64-column tile of query columns, and a tail job is one 128-token chunk of
+// one 64-column tile of query columns, and a tail job is one 256-token chunk of
 // one request's dense KV.  Each job covers S KV heads at once: the S work items
 // of a job run on a "gang" of S workgroups of one XCD (S = KV heads rounded up
 // to a power of two, at most 32), so a block's P factors are fetched from HBM
 // once and re-read by the other heads from that XCD's L2.  Jobs are dealt to
-// the gangs longest first (each to the gang with the least estimated work);
-// within a gang, tail jobs run first so their latency overlaps the start of the
-// fragment streams.  Workgroup b runs on XCD b % 8 (round-robin dispatch), so
+// the gangs longest first (each to the gang with the least estimated work),
+// then single jobs are moved or swapped between the most and the least loaded
+// gang while that lowers the maximum; of several ways to split the blocks, the
+// one with the smallest estimated makespan is kept.  Within a gang, tail jobs
+// run first so their latency overlaps the start of the fragment streams.  Workgroup b runs on XCD b % 8 (round-robin dispatch), so
 // gang k on XCD k % 8 uses workgroups (k % 8) + 8 * ((k / 8) * S + j), j < S.
 // ---------------------------------------------------------------------------
 // Cost model (microseconds on an MI355X, fitted to kernel timings): one
 // fragment of the slowest wave's stream, the per-tile softmax and barriers, the
 // per-item set-up, and one dense-tail chunk.
-constexpr double kCostFrag = 0.09, kCostTile = 3.0, kCostItem = 5.0, kCostTail = 7.0;
+constexpr double kCostFrag = 0.16, kCostTile = 1.8, kCostItem = 5.0, kCostTail = 9.5;
 constexpr int kMaxPartTiles = 8;  // keeps every item's run list short
 
 struct Schedule {
@@ -146,13 +148,13 @@ struct Schedule {
 
 // The fragment runs wave w of a block item consumes, in the kernel's order:
 // its R^K rank tiles (projection); then per tile its P^K sub-tile and the P^V
-// rank tiles of its rank group over its token segment; then its rank group's
-// R^V rank tiles (up-projection).  Offsets
+// rank tiles of its rank group over its token segment; then R^V for its
+// 16-dim output slice over all ranks (up-projection).  Offsets
 // follow the packed layout of each factor.
 void append_runs(const WorkItem& it, int w, int d, std::vector<int2>& out) {
   const BlockMeta& bm = it.blk;
   const int NK = d / 16;
-  const int nrt_k = bm.rk_pad / 32, nks = bm.rk_pad / 16, nrt_v = bm.rv_pad / 32, nkv = bm.rv_pad / 16;
+  const int nrt_k = bm.rk_pad / 32, nks = bm.rk_pad / 16, nrt_v = bm.rv_pad / 32;
   const int own_k = owned_tiles(nrt_k, w, kWaves);
   const int nseg = v_segments(nrt_v), ng = kWaves / nseg, rg = w % ng, sg = w / ng;
   const int own_v = owned_tiles(nrt_v, rg, ng), nst = 16 / nseg;
@@ -167,9 +169,8 @@ void append_runs(const WorkItem& it, int w, int d, std::vector<int2>& out) {
     add(bm.off_pk + ((int64_t)w * tiles_all + t) * nks * kFragElems, nks);
     add(bm.off_pv + (pv_first + (int64_t)(16 * t + nst * sg) * own_v) * kFragElems, (int64_t)nst * own_v);
   }
-  add(bm.off_rv + ((int64_t)it.g * (d / 32) * nkv + (int64_t)(d / 64) * 4 * owned_before(nrt_v, rg, ng)) *
-                      kFragElems,
-      (int64_t)(d / 64) * 4 * own_v);
+  const int nds = d / 16, ds = w % nds, nkr = bm.rv_pad / 32;
+  add(bm.off_rv + ((int64_t)it.g * nds + ds) * nkr * kFragElems, nkr);
 }
 
 // Latent rank tiles the busiest wave of a block accumulates (projection or value pass).
@@ -186,8 +187,7 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
     const int nrt_k = m.rk_pad / 32, nks = m.rk_pad / 16, nrt_v = m.rv_pad / 32;
     const int nseg = v_segments(nrt_v), ng = kWaves / nseg;
     const int mk = (nrt_k + kWaves - 1) / kWaves, mv = (nrt_v + ng - 1) / ng;
-    const double frags = (double)NK * mk + nt * ((double)nks + 16.0 / nseg * mv) +
-                         (c.d / 64) * 4.0 * mv;
+    const double frags = (double)NK * mk + nt * ((double)nks + 16.0 / nseg * mv) + m.rv_pad / 32.0;
     return kCostFrag * frags + kCostTile * nt + kCostItem;
   };
   int S = 1;
@@ -200,52 +200,118 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
     total += item_cost(m, m.T_pad / kTile) * n_ct * n_hc;
   }
   for (int32_t len : tl) total += kCostTail * ((len + kTailChunk - 1) / kTailChunk) * n_hc;
-  // parts of at most 2/3 of a gang's average work (and at most kMaxPartTiles tiles)
-  const double target = std::max(1e-9, total / n_gangs / 1.5);
   struct Part { int b, tile0, ntile; double cost; };
-  std::vector<Part> parts;
-  for (int j = 0; j < n_sel; ++j) {
-    const int b = table[j];
-    const BlockMeta& m = c.meta[b];
-    const int nt = m.T_pad / kTile;
-    const int np_cost = (int)std::min<double>(nt, std::max(1.0, std::ceil(item_cost(m, nt) / target)));
-    const int np = std::max(np_cost, (nt + kMaxPartTiles - 1) / kMaxPartTiles);
-    for (int p = 0; p < np; ++p) {
-      const int t_a = (int)((int64_t)nt * p / np), t_b = (int)((int64_t)nt * (p + 1) / np);
-      parts.push_back({b, t_a, t_b - t_a, item_cost(m, t_b - t_a)});
+  struct Job { int part, req, ch, ct, hc; double cost; };
+  // Jobs for one way of splitting the blocks: parts of at most `share` of a
+  // gang's average work (and at most kMaxPartTiles tiles), longest first.
+  auto make_jobs = [&](double share, std::vector<Part>& parts, std::vector<Job>& jobs) {
+    const double target = std::max(1e-9, total / n_gangs * share);
+    parts.clear();
+    jobs.clear();
+    for (int j = 0; j < n_sel; ++j) {
+      const int b = table[j];
+      const BlockMeta& m = c.meta[b];
+      const int nt = m.T_pad / kTile;
+      const int np_cost = (int)std::min<double>(nt, std::max(1.0, std::ceil(item_cost(m, nt) / target)));
+      const int np = std::max(np_cost, (nt + kMaxPartTiles - 1) / kMaxPartTiles);
+      for (int p = 0; p < np; ++p) {
+        const int t_a = (int)((int64_t)nt * p / np), t_b = (int)((int64_t)nt * (p + 1) / np);
+        parts.push_back({b, t_a, t_b - t_a, item_cost(m, t_b - t_a)});
+      }
     }
-    out->rk_pad_max = std::max(out->rk_pad_max, m.rk_pad);
-    out->rv_pad_max = std::max(out->rv_pad_max, m.rv_pad);
+    for (int p = 0; p < (int)parts.size(); ++p)
+      for (int ct = 0; ct < n_ct; ++ct)
+        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({p, -1, -1, ct, hc, parts[p].cost});
+    for (int i = 0; i < (int)tl.size(); ++i)
+      for (int ch = 0; ch * kTailChunk < tl[i]; ++ch)
+        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({-1, i, ch, 0, hc, kCostTail});
+    std::stable_sort(jobs.begin(), jobs.end(), [](const Job& x, const Job& y) { return x.cost > y.cost; });
+  };
+  // Deal jobs (indices `idx`, longest first) to the gangs: each to the least
+  // loaded gang, then improve by moving or swapping single jobs between the
+  // most and the least loaded gang while that lowers the maximum.  Returns the
+  // largest gang load.
+  auto deal = [&](const std::vector<Job>& jobs, const std::vector<int>& idx,
+                  std::vector<std::vector<int>>& lists) -> double {
+    lists.assign(n_gangs, {});
+    std::vector<double> load(n_gangs, 0.0);
+    for (int k : idx) {
+      const int best = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+      load[best] += jobs[k].cost;
+      lists[best].push_back(k);
+    }
+    for (int iter = 0; iter < 4 * n_gangs; ++iter) {
+      const int hi = (int)(std::max_element(load.begin(), load.end()) - load.begin());
+      const int lo = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+      double best_max = load[hi];
+      int bi = -1, bj = -1;  // job position in hi, and in lo (-1: move only)
+      for (int i = 0; i < (int)lists[hi].size(); ++i) {
+        const double ci = jobs[lists[hi][i]].cost;
+        const double mv = std::max(load[hi] - ci, load[lo] + ci);
+        if (mv < best_max - 1e-9) { best_max = mv; bi = i; bj = -1; }
+        for (int j = 0; j < (int)lists[lo].size(); ++j) {
+          const double cj = jobs[lists[lo][j]].cost;
+          if (cj >= ci) continue;
+          const double sw = std::max(load[hi] - ci + cj, load[lo] + ci - cj);
+          if (sw < best_max - 1e-9) { best_max = sw; bi = i; bj = j; }
+        }
+      }
+      if (bi < 0) break;
+      const int ki = lists[hi][bi];
+      lists[hi].erase(lists[hi].begin() + bi);
+      load[hi] -= jobs[ki].cost;
+      if (bj >= 0) {
+        const int kj = lists[lo][bj];
+        lists[lo].erase(lists[lo].begin() + bj);
+        load[lo] -= jobs[kj].cost;
+        lists[hi].push_back(kj);
+        load[hi] += jobs[kj].cost;
+      }
+      lists[lo].push_back(ki);
+      load[lo] += jobs[ki].cost;
+    }
+    for (auto& l : lists)  // tail jobs first, then the longest block jobs
+      std::stable_sort(l.begin(), l.end(), [&](int x, int y) {
+        if ((jobs[x].part < 0) != (jobs[y].part < 0)) return jobs[x].part < 0;
+        return jobs[x].cost > jobs[y].cost;
+      });
+    return *std::max_element(load.begin(), load.end());
+  };
+  // the split whose dealt schedule has the smallest estimated makespan
+  std::vector<Part> parts;
+  std::vector<Job> jobs;
+  {
+    double best = 1e300, best_share = 1.0;
+    for (double share : {1.5, 1.0, 0.8, 0.67, 0.5, 0.33}) {
+      make_jobs(share, parts, jobs);
+      std::vector<int> idx(jobs.size());
+      std::iota(idx.begin(), idx.end(), 0);
+      std::vector<std::vector<int>> lists;
+      const double mk = deal(jobs, idx, lists);
+      if (mk < best - 1e-9) { best = mk; best_share = share; }
+    }
+    make_jobs(best_share, parts, jobs);
   }
   const int n_parts = (int)parts.size();
   out->n_parts = n_parts;
-  for (const Part& pt : parts) out->max_own = std::max(out->max_own, max_owned(c.meta[pt.b]));
-  struct Job { int part, req, ch, ct, hc; double cost; };
-  std::vector<Job> jobs;
-  for (int p = 0; p < n_parts; ++p)
-    for (int ct = 0; ct < n_ct; ++ct)
-      for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({p, -1, -1, ct, hc, parts[p].cost});
-  for (int i = 0; i < (int)tl.size(); ++i)
-    for (int ch = 0; ch * kTailChunk < tl[i]; ++ch)
-      for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({-1, i, ch, 0, hc, kCostTail});
-  std::stable_sort(jobs.begin(), jobs.end(), [](const Job& x, const Job& y) { return x.cost > y.cost; });
+  for (const Part& pt : parts) {
+    out->rk_pad_max = std::max(out->rk_pad_max, c.meta[pt.b].rk_pad);
+    out->rv_pad_max = std::max(out->rv_pad_max, c.meta[pt.b].rv_pad);
+    out->max_own = std::max(out->max_own, max_owned(c.meta[pt.b]));
+  }
 
-  const size_t base = attend_lds_base_bytes(c.d, out->rk_pad_max);
+  const size_t base = attend_lds_base_bytes(c.d, out->rk_pad_max, out->rv_pad_max);
   const size_t cap = std::min<size_t>(kProgCap, base < (size_t)kLdsBytes ? kLdsBytes - base : 0);
   for (int L = 1; L <= (1 << 20); L *= 2) {
     std::vector<std::vector<unsigned char>> progs((size_t)L * kCUs);
     std::vector<WgProgram> entries((size_t)L * kCUs);
     size_t max_prog = 0;
     for (int l = 0; l < L; ++l) {
-      std::vector<std::vector<int>> lists(n_gangs);
-      std::vector<double> load(n_gangs, 0.0);
-      for (size_t k = l; k < jobs.size(); k += L) {
-        const int best = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-        load[best] += jobs[k].cost;
-        lists[best].push_back((int)k);
-      }
+      std::vector<int> idx;
+      for (size_t k = l; k < jobs.size(); k += L) idx.push_back((int)k);
+      std::vector<std::vector<int>> lists;
+      deal(jobs, idx, lists);
       for (int gang = 0; gang < n_gangs; ++gang) {
-        std::stable_partition(lists[gang].begin(), lists[gang].end(), [&](int k) { return jobs[k].part < 0; });
         for (int j = 0; j < S; ++j) {
           const int wg = (gang % kXcds) + kXcds * ((gang / kXcds) * S + j);
           std::vector<WorkItem> items;
@@ -525,7 +591,7 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     if (err != MILO_OK) return err;
     const int max_rt = sch.max_own <= 2 ? 2 : 4;
     // deepest fragment ring that fits next to the program, projected query and weight tile
-    const size_t base = attend_lds_base_bytes(c->d, sch.rk_pad_max);
+    const size_t base = attend_lds_base_bytes(c->d, sch.rk_pad_max, sch.rv_pad_max);
     const size_t prog = (size_t)sch.prog_bytes;
     int nslot = 0;
     for (int cand : {8, 6})

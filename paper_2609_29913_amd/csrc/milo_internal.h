@@ -12,8 +12,8 @@ namespace milo {
 // ---------------------------------------------------------------------------
 // Packed layout.  Every factor is stored as a sequence of 1 KiB "fragments":
 // 64 lanes x 8 bf16, exactly the per-lane operand of one
-// v_mfma_f32_32x32x16_bf16, so one wave loads one fragment with one fully
-// coalesced 16-byte load per lane.  Rows beyond T_b and ranks beyond r are
+// v_mfma_f32_32x32x16_bf16 (R^V: of one v_mfma_f32_16x16x32_bf16), so one
+// wave loads one fragment with one fully coalesced 16-byte load per lane.  Rows beyond T_b and ranks beyond r are
 // stored as zeros (tokens padded to whole 256-token tiles, ranks to 32).
 //
 // Lane l = 32*c + m (c = lane group 0/1, m = 0..31), element e = 0..7.
@@ -23,11 +23,8 @@ namespace milo {
 //       P^V[16*sig + 8*c + e][32*rho + m]                         (A: rank x tokens)
 //   R^K fragment (KV head g, rank tile rho, d step kap):
 //       R^K[32*rho + m][g*d + 16*kap + 8*c + e]                   (A: rank x d)
-//   R^V fragment (KV head g, d tile dl, rank step kap):
-//       R^V[16*kap + 8*(e/4) + 4*c + e%4][g*d + 32*dl + m]        (A: d x rank)
-// The R^V rank order inside a 16-rank step matches the rows that one lane holds
-// in the fp32 accumulator of a 32x32 MFMA (rows 8*(v/4) + 4*c + v%4), so the
-// latent accumulator feeds the up-projection straight from registers.
+//   R^V fragment (KV head g, 16-dim slice ds, 32-rank step kap), lane l = 16*qq + n:
+//       R^V[32*kap + 8*qq + e][g*d + 16*ds + n]                   (A: d x rank, 16x16x32)
 //
 // Fragment order follows the attention kernel's work split, so that every wave
 // of a workgroup reads each factor as contiguous runs in the order it consumes
@@ -37,11 +34,12 @@ namespace milo {
 // value pass and the up-projection split the waves into nseg = v_segments(nrt)
 // token segments times ng = kWaves / nseg rank groups: wave w works on token
 // segment w / ng (256 / nseg tokens of every tile) and owns the rank tiles
-// rho = (w % ng) + ng*j, so low-rank blocks still keep every wave busy.
+// rho = (w % ng) + ng*j, so low-rank blocks still keep every wave busy.  The
+// up-projection gives every wave a 16-dim slice of the output over all ranks.
 //   P^K: [w][t][kap]
 //   P^V: [rg][sig][j]                (group rg's run has owned_tiles(nrt, rg, ng) per sig)
 //   R^K: [g][w][j][kap]
-//   R^V: [g][rg][pass][j][half][dt]  (kap = 2*rho + half, dl = 2*pass + dt, 64-row passes)
+//   R^V: [g][ds][kap]
 // ---------------------------------------------------------------------------
 constexpr int kFragElems = 512;  // 64 lanes x 8 bf16
 constexpr int kWaves = 8;        // waves per attention workgroup (two per SIMD)
@@ -62,7 +60,7 @@ __host__ __device__ inline int owned_before(int nrt, int w, int n) {
 
 // Token segments of the latent value pass for a block with nrt rank tiles of
 // 32: the split (1, 2, 4 or 8 segments) with the least work for the busiest
-// wave, ties going to fewer segments (fewer duplicate R^V reads), with no wave
+// wave, ties going to fewer segments (fewer partial sums to combine), with no wave
 // owning more than kMaxOwn rank tiles.
 __host__ __device__ inline int v_segments(int nrt) {
   int best = 1, best_work = 1 << 30;
@@ -91,7 +89,7 @@ __host__ __device__ inline int64_t frag_count(const FactorGeom& f) {
     case kPK: return (int64_t)(f.T_pad / 32) * (f.r_pad / 16);
     case kPV: return (int64_t)(f.T_pad / 16) * (f.r_pad / 32);
     case kRK: return (int64_t)f.n_kv * (f.r_pad / 32) * (f.d / 16);
-    default:  return (int64_t)f.n_kv * (f.d / 32) * (f.r_pad / 16);
+    default:  return (int64_t)f.n_kv * (f.d / 16) * (f.r_pad / 32);
   }
 }
 
@@ -148,20 +146,12 @@ __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, i
       return;
     }
     default: {
-      const int nrt = f.r_pad / 32, npass = f.d / 64;
-      const int ng = kWaves / v_segments(nrt);
-      const int64_t per_g = (int64_t)(f.d / 32) * (f.r_pad / 16);
-      const int g = (int)(frag / per_g);
-      const int64_t in_g = frag % per_g;
-      int64_t first;
-      const int rg = run_owner(nrt, in_g, (int64_t)npass * 4, ng, &first);
-      const int own = owned_tiles(nrt, rg, ng);
-      const int64_t local = in_g - first;
-      const int dt = (int)(local % 2), half = (int)((local / 2) % 2);
-      const int j = (int)((local / 4) % own), pass = (int)(local / (4 * own));
-      const int kap = 2 * (rg + ng * j) + half;
-      *row = 16 * kap + 8 * (e >> 2) + 4 * c + (e & 3);
-      *col = g * f.d + 32 * (2 * pass + dt) + m;
+      const int nks = f.r_pad / 32, nds = f.d / 16;
+      const int kap = (int)(frag % nks);
+      const int ds = (int)((frag / nks) % nds);
+      const int g = (int)(frag / ((int64_t)nks * nds));
+      *row = 32 * kap + 8 * (lane >> 4) + e;
+      *col = g * f.d + 16 * ds + (lane & 15);
       return;
     }
   }
@@ -213,7 +203,6 @@ constexpr int kCols = 64;                      // query columns per workgroup
 constexpr int kTokWave = kTile / kWaves;       // tokens per wave per tile (one MFMA row block)
 static_assert(kTokWave == 32, "the score pass gives every wave one 32-token sub-tile");
 constexpr int kWStride = kTile + 8;            // bf16 row stride of the weight tile in LDS
-constexpr int kORow = 68;                      // fp32 row stride of the up-projection reduction
 constexpr int kMaxGroup = 16;                  // max query heads per KV head
 constexpr int kMaxRank = 896;                  // largest supported rank (LDS bound)
 constexpr int kLdsBytes = 160 * 1024;          // LDS per workgroup on gfx950
@@ -263,7 +252,7 @@ hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslo
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s);
 // LDS of the attention kernel: a base region (projected query, weight tile and
 // reductions, or the tail item's buffers) followed by kWaves rings of nslot fragments.
-size_t attend_lds_base_bytes(int head_dim, int rk_pad_max);
+size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max);
 size_t attend_ring_bytes(int nslot);
 
 }  // namespace milo

@@ -26,11 +26,15 @@ namespace milo {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8 ld_bf16x8(const void* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
@@ -70,7 +74,6 @@ __device__ __forceinline__ int4 prog_read_b128(const void* p) {
 // LDS stores the compiler would otherwise order after every in-flight
 // global->LDS fragment load (it cannot prove they target other addresses).
 __device__ __forceinline__ void lds_store_b128(void* p, float4 v) {
-  typedef float f32x4 __attribute__((ext_vector_type(4)));
   const f32x4 x = {v.x, v.y, v.z, v.w};
   asm volatile("ds_write_b128 %0, %1" ::"v"(lds_addr(p)), "v"(x) : "memory");
 }
@@ -543,94 +546,87 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 #pragma unroll
   for (int ch = 0; ch < 2; ++ch) l_run[ch] += __shfl_xor(l_run[ch], 32);
   lds_barrier();  // every wave is done with qt / wl
-  float* ored = reinterpret_cast<float*>(smem);       // [kORed][kCols][kORow]
-  float* lred = ored + kORed * kCols * kORow;         // [kWaves][kCols]
+  float* lred = reinterpret_cast<float*>(smem + a.ring_offset) - kWaves * kCols;  // [kWaves][kCols]
   lred[wave * kCols + lrow] = l_run[0];  // both lane halves hold the sums
   lred[wave * kCols + 32 + lrow] = l_run[1];
+  // combine the token segments' latent partials (pairwise rounds through LDS,
+  // fp32): the waves of segments [h, 2h) hand theirs to segments [0, h)
+  if (nseg > 1) {
+    float* segbuf = reinterpret_cast<float*>(smem);  // [slot][owned tile][ch][16][64 lanes]
+    const int own_max = (nrt_v + ng - 1) / ng;        // slot size: the largest rank group's tiles
+    for (int h = nseg / 2; h >= 1; h /= 2) {
+      if (sg >= h && sg < 2 * h) {
+        float* dst = segbuf + (int64_t)((sg - h) * ng + rg) * own_max * 2 * 16 * 64 + lane;
 #pragma unroll
-  for (int pass = 0; pass < D / 64; ++pass) {
-    f32x16 acc[2][2];
-    acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = f32x16{};
-    if (own_v > 0) {
-      // fragments of (owned rank tile r, rank half, d tile dt), in stream order
-      bf16x8 f00 = take(), f01 = take();
+        for (int r = 0; r < MAX_RT; ++r)
+          if (r < own_v)
 #pragma unroll
-      for (int r = 0; r < MAX_RT; ++r) {
-        if (r < own_v) {
+            for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            // prefetch the next (rank tile, half) pair of d-tile fragments
-            bf16x8 g00 = f00, g01 = f01;
-            if (half == 0 || r + 1 < own_v) {
-              g00 = take();
-              g01 = take();
-            }
-            bf16x8 b0, b1;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              b0[e] = (__bf16)oacc[r][0][8 * half + e];
-              b1[e] = (__bf16)oacc[r][1][8 * half + e];
-            }
-            acc[0][0] = mfma32(f00, b0, acc[0][0]);
-            acc[0][1] = mfma32(f00, b1, acc[0][1]);
-            acc[1][0] = mfma32(f01, b0, acc[1][0]);
-            acc[1][1] = mfma32(f01, b1, acc[1][1]);
-            f00 = g00;
-            f01 = g01;
-          }
-        }
+              for (int v = 0; v < 16; ++v) dst[((r * 2 + ch) * 16 + v) * 64] = oacc[r][ch][v];
       }
-    }
-    // sum the eight waves' partials: waves 0-3 store, then waves 4-7 add in place
-    float* mine = ored + ((wave % kORed) * kCols + lrow) * kORow + 4 * lhi;
-    if (wave < kORed) {
+      lds_barrier();
+      if (sg < h) {
+        const float* src = segbuf + (int64_t)(sg * ng + rg) * own_max * 2 * 16 * 64 + lane;
 #pragma unroll
-      for (int dt = 0; dt < 2; ++dt)
+        for (int r = 0; r < MAX_RT; ++r)
+          if (r < own_v)
+#pragma unroll
+            for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+              for (int v = 0; v < 16; ++v) oacc[r][ch][v] += src[((r * 2 + ch) * 16 + v) * 64];
+      }
+      lds_barrier();
+    }
+  }
+  // the latent accumulator of every rank tile -> LDS as bf16 [col][rank]
+  __bf16* olat = reinterpret_cast<__bf16*>(smem);
+  const int ols = bm.rv_pad + 8;
+  if (sg == 0) {
+#pragma unroll
+    for (int r = 0; r < MAX_RT; ++r)
+      if (r < own_v) {
+        const int rt = rg + ng * r;
 #pragma unroll
         for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            *reinterpret_cast<float4*>(mine + 32 * ch * kORow + 32 * dt + 8 * j) =
-                make_float4(acc[dt][ch][4 * j], acc[dt][ch][4 * j + 1], acc[dt][ch][4 * j + 2],
-                            acc[dt][ch][4 * j + 3]);
-    }
-    lds_barrier();
-    if (wave >= kORed) {
+          for (int jj = 0; jj < 4; ++jj) {
+            bf16x4 v;
 #pragma unroll
-      for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-        for (int ch = 0; ch < 2; ++ch)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            float4* p = reinterpret_cast<float4*>(mine + 32 * ch * kORow + 32 * dt + 8 * j);
-            float4 v = *p;
-            v.x += acc[dt][ch][4 * j];
-            v.y += acc[dt][ch][4 * j + 1];
-            v.z += acc[dt][ch][4 * j + 2];
-            v.w += acc[dt][ch][4 * j + 3];
-            *p = v;
+            for (int u = 0; u < 4; ++u) v[u] = (__bf16)oacc[r][ch][4 * jj + u];
+            *reinterpret_cast<bf16x4*>(olat + (32 * ch + lrow) * ols + 32 * rt + 8 * jj + 4 * lhi) = v;
           }
-    }
-    lds_barrier();
-    {
-      const int col = tid >> 3, dq = (tid & 7) * 8;
-      const int c = c0 + col;
-      if (c < ncg) {
-        const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
-        float* dst = a.part_o + (colg * a.n_slots + slot) * D + 64 * pass + dq;
-#pragma unroll
-        for (int q4 = 0; q4 < 2; ++q4) {
-          float4 sum = *reinterpret_cast<const float4*>(ored + col * kORow + dq + 4 * q4);
-#pragma unroll
-          for (int w = 1; w < kORed; ++w) {
-            const float4 x = *reinterpret_cast<const float4*>(ored + (w * kCols + col) * kORow + dq + 4 * q4);
-            sum.x += x.x; sum.y += x.y; sum.z += x.z; sum.w += x.w;
-          }
-          *reinterpret_cast<float4*>(dst + 4 * q4) = sum;
-        }
       }
+  }
+  lds_barrier();
+  // every wave: output dims [16 ds, 16 ds + 16) of its 16-column blocks, over
+  // all ranks (16x16x32 MFMAs: R^V fragment x latent columns from LDS)
+  constexpr int NDS = D / 16;              // 16-dim slices
+  constexpr int NCB = 4 * NDS / kWaves;    // 16-column blocks per wave
+  const int ds = wave % NDS, cb0 = (wave / NDS) * NCB;
+  f32x4 uacc[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) uacc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  {
+    const int nk = bm.rv_pad >> 5;
+    const __bf16* ob = olat + (16 * cb0 + (lane & 15)) * ols + 8 * (lane >> 4);
+    bf16x8 af = take();
+    for (int k = 0; k < nk; ++k) {
+      bf16x8 an = af;
+      if (k + 1 < nk) an = take();
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) uacc[cb] = mfma16(af, ld_bf16x8(ob + 16 * cb * ols + 32 * k), uacc[cb]);
+      af = an;
     }
-    lds_barrier();
+  }
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    const int c = c0 + 16 * (cb0 + cb) + (lane & 15);
+    if (c < ncg) {
+      const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
+      *reinterpret_cast<float4*>(a.part_o + (colg * a.n_slots + slot) * D + 16 * ds + 4 * (lane >> 4)) =
+          make_float4(uacc[cb][0], uacc[cb][1], uacc[cb][2], uacc[cb][3]);
+    }
   }
   if (tid < kCols) {
     const int c = c0 + tid;
@@ -772,10 +768,15 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t attend_lds_base_bytes(int head_dim, int rk_pad_max) {
+size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max) {
   const size_t qsd = (size_t)rk_pad_max + 8;
   const size_t loop = kCols * qsd * 2 + (size_t)kCols * kWStride * 2 + (size_t)kWaves * kCols * 4;
-  const size_t epi = ((size_t)4 * kCols * kORow + (size_t)kWaves * kCols) * 4;
+  // up-projection: the latent accumulator as bf16 [col][rank], or the segment
+  // partials being combined (at most 4 slots x 3 rank tiles x 8 KiB), then the
+  // per-wave column sums at the end of the region
+  const size_t olat = (size_t)kCols * (rv_pad_max + 8) * 2;
+  const size_t segs = (size_t)4 * 3 * 2 * 16 * 64 * 4;
+  const size_t epi = (olat > segs ? olat : segs) + (size_t)kWaves * kCols * 4;
   const size_t tail = ((size_t)2 * kWaves * 32 + (size_t)kTailChunk * 32 + (size_t)kWaves * kMaxGroup * head_dim) * 4;
   size_t m = loop > epi ? loop : epi;
   m = m > tail ? m : tail;

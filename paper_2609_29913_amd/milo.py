@@ -45,6 +45,10 @@ def lib() -> ctypes.CDLL:
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build()")
+        # PyTorch ships its own HIP runtime; loading it first makes the library
+        # bind to that same runtime (one runtime per process), so torch tensors
+        # and streams can be passed across the boundary
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         vp = ctypes.c_void_p
         L.milo_cache_create.argtypes = [ctypes.POINTER(milo_cache_desc), ctypes.POINTER(vp),
