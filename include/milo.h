@@ -132,9 +132,10 @@ int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which
                            uint16_t* dst);
 
 /* Kernel timing for measurement.  While enabled, every milo_attend_decode
- * records HIP events on its stream around its attention kernel (the fused
- * projection / score / latent-V / up-projection / tail kernel) and around its
- * merge kernel.  milo_timing_read synchronises on those events, returns the
+ * has its attention kernel (the fused projection / score / latent-V /
+ * up-projection / tail kernel) and its merge kernel record HIP events at their
+ * own start and end (the launches record them, so launch gaps are not counted).
+ * milo_timing_read synchronises on those events, returns the
  * summed durations in milliseconds and the number of calls, and clears them.
  * Any argument of milo_timing_read may be NULL. */
 int milo_timing_enable(int enable);

@@ -61,7 +61,7 @@ struct TimingState {
   std::mutex mu;
   bool enabled = false;
   std::vector<hipEvent_t> pool;
-  std::vector<hipEvent_t> recorded;  // groups of 3: start, after attend kernel, after merge
+  std::vector<hipEvent_t> recorded;  // groups of 4: attend kernel start / end, merge kernel start / end
 };
 TimingState g_timing;
 
@@ -676,12 +676,13 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   aa.ring_offset = c->ring_offset;
   MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out, n_q_heads, c->n_block_slots, c->n_slots};
 
-  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+  // timing: events recorded by the launches themselves at kernel start and end
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};  // attend start / end, merge start / end
   bool timed = false;
   {
     std::lock_guard<std::mutex> lk(g_timing.mu);
     if (g_timing.enabled) {
-      for (int k = 0; k < 3; ++k) {
+      for (int k = 0; k < 4; ++k) {
         if (g_timing.pool.empty()) {
           hipEvent_t e;
           MILO_HIP(hipEventCreate(&e));
@@ -693,20 +694,18 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
       timed = true;
     }
   }
-  if (timed) MILO_HIP(hipEventRecord(ev[0], s));
   hipError_t e = hipSuccess;
   for (int l = 0; l < c->n_launch; ++l) {
     aa.wg = reinterpret_cast<const WgProgram*>(c->plan_d) + (size_t)l * kCUs;
-    e = launch_attend(aa, c->d, c->max_rt, c->nslot, kCUs, c->lds, s);
+    e = launch_attend(aa, c->d, c->max_rt, c->nslot, kCUs, c->lds, s, l == 0 ? ev[0] : nullptr,
+                      l == c->n_launch - 1 ? ev[1] : nullptr);
     if (e != hipSuccess) return hip_fail(e, "attend kernel launch");
   }
-  if (timed) MILO_HIP(hipEventRecord(ev[1], s));
-  e = launch_merge(ma, c->d, n_cols, s);
+  e = launch_merge(ma, c->d, n_cols, s, ev[2], ev[3]);
   if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   if (timed) {
-    MILO_HIP(hipEventRecord(ev[2], s));
     std::lock_guard<std::mutex> lk(g_timing.mu);
-    g_timing.recorded.insert(g_timing.recorded.end(), ev, ev + 3);
+    g_timing.recorded.insert(g_timing.recorded.end(), ev, ev + 4);
   }
   return MILO_OK;
 }
@@ -722,13 +721,13 @@ int milo_timing_read(double* attend_kernel_ms, double* merge_kernel_ms, int64_t*
   g_err.clear();
   std::lock_guard<std::mutex> lk(g_timing.mu);
   double ta = 0.0, tm = 0.0;
-  const size_t n = g_timing.recorded.size() / 3;
+  const size_t n = g_timing.recorded.size() / 4;
   for (size_t k = 0; k < n; ++k) {
-    hipEvent_t* e = &g_timing.recorded[3 * k];
-    MILO_HIP(hipEventSynchronize(e[2]));
+    hipEvent_t* e = &g_timing.recorded[4 * k];
+    MILO_HIP(hipEventSynchronize(e[3]));
     float a = 0.f, m = 0.f;
     MILO_HIP(hipEventElapsedTime(&a, e[0], e[1]));
-    MILO_HIP(hipEventElapsedTime(&m, e[1], e[2]));
+    MILO_HIP(hipEventElapsedTime(&m, e[2], e[3]));
     ta += a;
     tm += m;
   }

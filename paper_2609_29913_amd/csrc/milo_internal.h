@@ -247,9 +247,12 @@ struct PackArgs {
 
 // Launchers (defined in milo_kernels.hip).
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+// e0 / e1 (may be null): events recorded when the kernel starts and ends
+// (hipExtLaunchKernelGGL), so they time the kernel itself.
 hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, int grid, size_t lds_bytes,
-                         hipStream_t s);
-hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s);
+                         hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s, hipEvent_t e0 = nullptr,
+                        hipEvent_t e1 = nullptr);
 // LDS of the attention kernel: a base region (projected query, weight tile and
 // reductions, or the tail item's buffers) followed by kWaves rings of nslot fragments.
 size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max);

@@ -19,6 +19,8 @@
 //
 // Scores are kept in log2 units (the scale folds log2(e)), so every exponential
 // is one v_exp_f32.
+#include <hip/hip_ext.h>
+
 #include "milo_internal.h"
 
 namespace milo {
@@ -694,66 +696,84 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
 
 // ---------------------------------------------------------------------------
 // Log-sum-exp merge: one workgroup per query column (i, h).  Slots [0, n_sel)
-// are the selected blocks, then request i's tail chunks.  Wave w accumulates
-// the slots s = w mod 4 (each lane owns D/64 consecutive outputs); the waves are
-// combined in a fixed order, so the result is deterministic.
+// are the selected blocks, then request i's tail chunks.  Thread t takes the
+// 4 output dims 4 (t % (D/4)) of the slots s = t / (D/4) (mod slots per pass),
+// so every load is one 16-byte vector and a wave reads whole slots; the loads
+// of kMergeUnroll passes are issued before any is used, and each thread keeps
+// a running (max, sum, output) over its slots.  The slot lanes are then merged
+// in a fixed order through LDS, so the result is deterministic.
 // ---------------------------------------------------------------------------
-constexpr int kMergeWaves = 4;
-constexpr int kMergeThreads = 64 * kMergeWaves;
+constexpr int kMergeThreads = 256;
+constexpr int kMergeUnroll = 8;
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
-  constexpr int E = D / 64;  // outputs per lane
-  __shared__ float red[kMergeWaves];
-  __shared__ float dred[kMergeWaves];
-  __shared__ float part[kMergeWaves][D];
-  const int col = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  constexpr int TPS = D / 4;                // threads per slot
+  constexpr int SPP = kMergeThreads / TPS;  // slots per pass
+  __shared__ float red_m[SPP], red_l[SPP];
+  __shared__ float4 red_o[SPP][TPS];
+  const int col = blockIdx.x, tid = threadIdx.x;
+  const int dq = tid % TPS, sl = tid / TPS;
   const int i = col / a.H_q;
   const int n_valid = a.n_block_slots + (a.tail_len[i] + kTailChunk - 1) / kTailChunk;
   const float2* ml = a.part_ml + (int64_t)col * a.n_slots;
-  float mx = -INFINITY;
-  for (int s = tid; s < n_valid; s += kMergeThreads) mx = fmaxf(mx, ml[s].x);
+  const float4* po = reinterpret_cast<const float4*>(a.part_o + (int64_t)col * a.n_slots * D) + dq;
+  float m = -INFINITY, l = 0.f;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = sl; s0 < n_valid; s0 += SPP * kMergeUnroll) {
+    float2 mm[kMergeUnroll];
+    float4 oo[kMergeUnroll];
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  float num[E], den = 0.f;
-#pragma unroll
-  for (int e = 0; e < E; ++e) num[e] = 0.f;
-  const float* po = a.part_o + (int64_t)col * a.n_slots * D + E * lane;
-  int s = wave;
-  for (; s + 3 * kMergeWaves < n_valid; s += 4 * kMergeWaves) {
-    float2 m4[4];
-    float v4[4][E];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      m4[u] = ml[s + u * kMergeWaves];
-#pragma unroll
-      for (int e = 0; e < E; ++e) v4[u][e] = po[(int64_t)(s + u * kMergeWaves) * D + e];
+    for (int u = 0; u < kMergeUnroll; ++u) {
+      const int s = s0 + u * SPP;
+      if (s < n_valid) {
+        mm[u] = ml[s];
+        oo[u] = po[(int64_t)s * TPS];
+      } else {
+        mm[u] = make_float2(-INFINITY, 0.f);
+        oo[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float f = fast_exp2(m4[u].x - mx);
-      den += m4[u].y * f;
-#pragma unroll
-      for (int e = 0; e < E; ++e) num[e] += v4[u][e] * f;
+    for (int u = 0; u < kMergeUnroll; ++u) {
+      if (mm[u].x == -INFINITY) continue;  // past the last slot
+      const float mn = fmaxf(m, mm[u].x);
+      const float fo = fast_exp2(m - mn);  // m = -inf before the first slot: 0
+      const float fn = fast_exp2(mm[u].x - mn);
+      l = l * fo + mm[u].y * fn;
+      o.x = o.x * fo + oo[u].x * fn;
+      o.y = o.y * fo + oo[u].y * fn;
+      o.z = o.z * fo + oo[u].z * fn;
+      o.w = o.w * fo + oo[u].w * fn;
+      m = mn;
     }
   }
-  for (; s < n_valid; s += kMergeWaves) {
-    const float2 m1 = ml[s];
-    const float f = fast_exp2(m1.x - mx);
-    den += m1.y * f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) num[e] += po[(int64_t)s * D + e] * f;
+  // every thread of a slot lane holds the same (m, l)
+  if (dq == 0) {
+    red_m[sl] = m;
+    red_l[sl] = l;
   }
-#pragma unroll
-  for (int e = 0; e < E; ++e) part[wave][E * lane + e] = num[e];
-  if (lane == 0) dred[wave] = den;
+  red_o[sl][dq] = o;
   __syncthreads();
-  if (tid < D) {
-    const float dsum = dred[0] + dred[1] + dred[2] + dred[3];
-    const float nsum = part[0][tid] + part[1][tid] + part[2][tid] + part[3][tid];
-    a.out[(int64_t)col * D + tid] = nsum / dsum;
+  if (tid < TPS) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < SPP; ++k) mx = fmaxf(mx, red_m[k]);
+    float den = 0.f;
+    float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int k = 0; k < SPP; ++k) {
+      if (red_m[k] == -INFINITY) continue;  // a lane without slots
+      const float f = fast_exp2(red_m[k] - mx);
+      den += red_l[k] * f;
+      const float4 v = red_o[k][tid];
+      num.x += v.x * f;
+      num.y += v.y * f;
+      num.z += v.z * f;
+      num.w += v.w * f;
+    }
+    const float inv = 1.f / den;
+    reinterpret_cast<float4*>(a.out + (int64_t)col * D)[tid] =
+        make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
   }
 }
 
@@ -786,7 +806,8 @@ size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max) {
 size_t attend_ring_bytes(int nslot) { return (size_t)kWaves * nslot * kFragElems * 2; }
 
 template <int D, int MAX_RT, int NSLOT>
-static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hipStream_t s) {
+static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
+                                  hipEvent_t e1) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_kernel<D, MAX_RT, NSLOT>),
@@ -794,43 +815,44 @@ static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hip
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT>), dim3(grid), dim3(kThreads), lds, s, a);
+  hipExtLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT>), dim3(grid), dim3(kThreads), (uint32_t)lds, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 
 template <int D, int MAX_RT>
-static hipError_t launch_attend_r(const AttendArgs& a, int nslot, int grid, size_t lds, hipStream_t s) {
+static hipError_t launch_attend_r(const AttendArgs& a, int nslot, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
+                                  hipEvent_t e1) {
   switch (nslot) {
-    case 8: return launch_attend_t<D, MAX_RT, 8>(a, grid, lds, s);
-    case 6: return launch_attend_t<D, MAX_RT, 6>(a, grid, lds, s);
-    case 0: return launch_attend_t<D, MAX_RT, 0>(a, grid, lds, s);
+    case 8: return launch_attend_t<D, MAX_RT, 8>(a, grid, lds, s, e0, e1);
+    case 6: return launch_attend_t<D, MAX_RT, 6>(a, grid, lds, s, e0, e1);
+    case 0: return launch_attend_t<D, MAX_RT, 0>(a, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int D>
 static hipError_t launch_attend_d(const AttendArgs& a, int max_rt, int nslot, int grid, size_t lds,
-                                  hipStream_t s) {
+                                  hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   switch (max_rt) {
-    case 2: return launch_attend_r<D, 2>(a, nslot, grid, lds, s);
-    case 4: return launch_attend_r<D, 4>(a, nslot, grid, lds, s);
+    case 2: return launch_attend_r<D, 2>(a, nslot, grid, lds, s, e0, e1);
+    case 4: return launch_attend_r<D, 4>(a, nslot, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, int grid, size_t lds_bytes,
-                         hipStream_t s) {
+                         hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (grid == 0) return hipSuccess;
-  if (head_dim == 64) return launch_attend_d<64>(a, max_rt, nslot, grid, lds_bytes, s);
-  if (head_dim == 128) return launch_attend_d<128>(a, max_rt, nslot, grid, lds_bytes, s);
+  if (head_dim == 64) return launch_attend_d<64>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
+  if (head_dim == 128) return launch_attend_d<128>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s) {
+hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (head_dim == 64) {
-    hipLaunchKernelGGL(merge_kernel<64>, dim3(n_cols), dim3(kMergeThreads), 0, s, a);
+    hipExtLaunchKernelGGL(merge_kernel<64>, dim3(n_cols), dim3(kMergeThreads), 0, s, e0, e1, 0, a);
   } else if (head_dim == 128) {
-    hipLaunchKernelGGL(merge_kernel<128>, dim3(n_cols), dim3(kMergeThreads), 0, s, a);
+    hipExtLaunchKernelGGL(merge_kernel<128>, dim3(n_cols), dim3(kMergeThreads), 0, s, e0, e1, 0, a);
   } else {
     return hipErrorInvalidValue;
   }
