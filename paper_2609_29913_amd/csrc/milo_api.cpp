@@ -135,10 +135,13 @@ int64_t factor_offset(const BlockMeta& m, int which) {
 // run first so their latency overlaps the start of the fragment streams.  Workgroup b runs on XCD b % 8 (round-robin dispatch), so
 // gang k on XCD k % 8 uses workgroups (k % 8) + 8 * ((k / 8) * S + j), j < S.
 // ---------------------------------------------------------------------------
-// Cost model (microseconds on an MI355X, fitted to kernel timings): one
-// fragment of the slowest wave's stream, the per-tile softmax and barriers, the
-// per-item set-up, and one dense-tail chunk.
-constexpr double kCostFrag = 0.16, kCostTile = 1.8, kCostItem = 5.0, kCostTail = 9.5;
+// Cost model (microseconds on an MI355X, least-squares fit to per-item kernel
+// timings of the 7B-shaped layer, rms error 0.5 us): one fragment of the
+// slowest wave's projection and up-projection streams, one fragment of its
+// tile stream, the per-tile softmax and barriers, the per-item set-up, one
+// round of the token-segment reduction, and one dense-tail chunk.
+constexpr double kCostFragItem = 0.19, kCostFragTile = 0.173, kCostTile = 1.52, kCostItem = 2.33,
+                 kCostSegRound = 1.36, kCostTail = 9.7;
 constexpr int kMaxPartTiles = 8;  // keeps every item's run list short
 
 struct Schedule {
@@ -187,8 +190,12 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
     const int nrt_k = m.rk_pad / 32, nks = m.rk_pad / 16, nrt_v = m.rv_pad / 32;
     const int nseg = v_segments(nrt_v), ng = kWaves / nseg;
     const int mk = (nrt_k + kWaves - 1) / kWaves, mv = (nrt_v + ng - 1) / ng;
-    const double frags = (double)NK * mk + nt * ((double)nks + 16.0 / nseg * mv) + m.rv_pad / 32.0;
-    return kCostFrag * frags + kCostTile * nt + kCostItem;
+    int rounds = 0;
+    for (int h = nseg; h > 1; h /= 2) ++rounds;
+    const double item_frags = (double)NK * mk + m.rv_pad / 32.0;
+    const double tile_frags = nt * ((double)nks + 16.0 / nseg * mv);
+    return kCostFragItem * item_frags + kCostFragTile * tile_frags + kCostTile * nt + kCostItem +
+           kCostSegRound * rounds;
   };
   int S = 1;
   while (S < c.n_kv && S < 32) S *= 2;
