@@ -502,10 +502,15 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       l_run[ch] = l_run[ch] * alpha[ch] + lsum;
     }
     lds_barrier();
+    // rescale the latent accumulators to the new running maximum; skipped on
+    // the first tile (they are zero) and when no column's maximum moved
+    if (tt > 0 && own_v > 0 && __any(alpha[0] != 1.f || alpha[1] != 1.f)) {
 #pragma unroll
-    for (int r = 0; r < MAX_RT; ++r) {
-      oacc[r][0] *= alpha[0];
-      oacc[r][1] *= alpha[1];
+      for (int r = 0; r < MAX_RT; ++r)
+        if (r < own_v) {
+          oacc[r][0] *= alpha[0];
+          oacc[r][1] *= alpha[1];
+        }
     }
     if (own_v > 0) {
       // operands of 16-token step st: w0/w1 (weight column tiles), pa[r] (P^V rank

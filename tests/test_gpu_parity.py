@@ -94,6 +94,27 @@ def test_parity_full_size_layers_sampled(cfg, layer):
     assert err.max() <= TOL_REL_L2
 
 
+def test_score_outliers_in_late_tiles():
+    """Keys whose scores dwarf the rest arrive late: one in the last token tile
+    of a block, one in a block processed after another, one in a tail.  The
+    running maximum jumps (every earlier contribution must be rescaled by about
+    2^-100), columns where the same key scores very negatively underflow, and
+    nothing may overflow (Sec. 4.1 Eq. 1: softmax is shift-invariant)."""
+    inp = synth.make_problem(25, [1024, 700], [128, 64], n_kv_heads=2, head_dim=128, n_q=2, n_q_heads=4,
+                             tail_cap=50)
+    pk0 = synth.bf16_to_f32(inp.pk[0]).copy()
+    pk0[900] *= 40.0
+    inp.pk[0] = synth.f32_to_bf16(pk0)
+    pk1 = synth.bf16_to_f32(inp.pk[1]).copy()
+    pk1[650] *= 25.0
+    inp.pk[1] = synth.f32_to_bf16(pk1)
+    tk = synth.bf16_to_f32(inp.tail_k).copy()
+    tk[1, 30] *= 30.0
+    inp.tail_k = synth.f32_to_bf16(tk)
+    _check(inp, label="late outliers")
+    _check(inp, table=[1, 0], label="late outliers, blocks reversed")
+
+
 def test_subset_and_order_of_blocks():
     inp = synth.make_problem(21, [300, 512, 64, 1000, 7], [32, 64, 16, 256, 7], n_kv_heads=2, head_dim=128,
                              n_q=2, n_q_heads=6, tail_cap=40, tail_len=[40, 13])
