@@ -44,7 +44,7 @@ namespace milo {
 constexpr int kFragElems = 512;  // 64 lanes x 8 bf16
 constexpr int kWaves = 8;        // waves per attention workgroup (two per SIMD)
 constexpr int kTile = 256;       // tokens per attention tile
-constexpr int kMaxOwn = 4;       // most latent rank tiles one wave accumulates
+constexpr int kMaxOwn = 2;       // most latent rank tiles one wave accumulates (see v_segments)
 enum FactorKind : int { kPK = 0, kRK = 1, kPV = 2, kRV = 3 };
 
 // rank tiles dealt round-robin over n owners: how many owner w holds, and how
@@ -61,7 +61,8 @@ __host__ __device__ inline int owned_before(int nrt, int w, int n) {
 // Token segments of the latent value pass for a block with nrt rank tiles of
 // 32: the split (1, 2, 4 or 8 segments) with the least work for the busiest
 // wave, ties going to fewer segments (fewer partial sums to combine), with no wave
-// owning more than kMaxOwn rank tiles.
+// owning more than kMaxOwn rank tiles; past 8 * kMaxOwn rank tiles no split
+// qualifies and the block uses one segment (every wave owns nrt / 8 tiles).
 __host__ __device__ inline int v_segments(int nrt) {
   int best = 1, best_work = 1 << 30;
   for (int nseg = 1; nseg <= kWaves; nseg *= 2) {
