@@ -161,8 +161,12 @@ def main():
     per_step = flops_step = out_bytes = 0
     mean_ranks = []
     groups = [[]]
+    t_gen = time.perf_counter()
     for l in range(cfg.n_layers):
         x = synth.gen_layer(cfg, l)
+        if cfg.n_layers > 1:
+            print(f"bench: layer {l + 1}/{cfg.n_layers} generated ({time.perf_counter() - t_gen:.0f} s)",
+                  file=sys.stderr, flush=True)
         per_step += synth.algorithmic_bytes(x)
         flops_step += synth.latent_flops(x)
         out_bytes += 4 * x.n_q * x.n_q_heads * x.head_dim

@@ -123,11 +123,14 @@ int64_t factor_offset(const BlockMeta& m, int which) {
 //
 // Work is cut into jobs: a block job is one part of a selected block (a range
 // of whole 256-token tiles; large blocks are split so the work evens out) for
-// one 64-column tile of query columns, and a tail job is one 256-token chunk of
-// one request's dense KV.  Each job covers S KV heads at once: the S work items
-// of a job run on a "gang" of S workgroups of one XCD (S = KV heads rounded up
-// to a power of two, at most 32), so a block's P factors are fetched from HBM
-// once and re-read by the other heads from that XCD's L2.  Jobs are dealt to
+// a group of C 64-column tiles of query columns, and a tail job is C 256-token
+// chunks of one request's dense KV.  Each job covers S_kv KV heads x C at once:
+// its S = S_kv * C work items run on a "gang" of S workgroups of one XCD
+// (S_kv = KV heads rounded up to a power of two; C = the largest power of two
+// dividing the number of column tiles with S <= 32), so a block's P factors are
+// fetched from HBM once and re-read by the other heads and column tiles from
+// that XCD's L2.  Workgroup j of a gang takes head j % S_kv and column tile
+// (or tail chunk) j / S_kv of the job's group.  Jobs are dealt to
 // the gangs longest first (each to the gang with the least estimated work),
 // then single jobs are moved or swapped between the most and the least loaded
 // gang while that lowers the maximum; of several ways to split the blocks, the
@@ -197,16 +200,21 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
     return kCostFragItem * item_frags + kCostFragTile * tile_frags + kCostTile * nt + kCostItem +
            kCostSegRound * rounds;
   };
-  int S = 1;
-  while (S < c.n_kv && S < 32) S *= 2;
-  const int n_hc = (c.n_kv + S - 1) / S;
+  int S_kv = 1;
+  while (S_kv < c.n_kv && S_kv < 32) S_kv *= 2;
+  int C = 1;
+  while (n_ct % (2 * C) == 0 && S_kv * 2 * C <= 32) C *= 2;
+  const int S = S_kv * C;
+  const int n_hc = (c.n_kv + S_kv - 1) / S_kv;
+  const int n_cg = n_ct / C;  // column-tile groups
   const int n_gangs = kCUs / S;
   double total = 0.0;
   for (int j = 0; j < n_sel; ++j) {
     const BlockMeta& m = c.meta[table[j]];
-    total += item_cost(m, m.T_pad / kTile) * n_ct * n_hc;
+    total += item_cost(m, m.T_pad / kTile) * n_cg * n_hc;
   }
-  for (int32_t len : tl) total += kCostTail * ((len + kTailChunk - 1) / kTailChunk) * n_hc;
+  for (int32_t len : tl)
+    total += kCostTail * ((len + kTailChunk * C - 1) / (kTailChunk * C)) * n_hc;
   struct Part { int b, tile0, ntile; double cost; };
   struct Job { int part, req, ch, ct, hc; double cost; };
   // Jobs for one way of splitting the blocks: parts of at most `share` of a
@@ -227,11 +235,11 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
       }
     }
     for (int p = 0; p < (int)parts.size(); ++p)
-      for (int ct = 0; ct < n_ct; ++ct)
-        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({p, -1, -1, ct, hc, parts[p].cost});
+      for (int cg = 0; cg < n_cg; ++cg)
+        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({p, -1, -1, cg, hc, parts[p].cost});
     for (int i = 0; i < (int)tl.size(); ++i)
-      for (int ch = 0; ch * kTailChunk < tl[i]; ++ch)
-        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({-1, i, ch, 0, hc, kCostTail});
+      for (int chg = 0; chg * C * kTailChunk < tl[i]; ++chg)
+        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({-1, i, chg, 0, hc, kCostTail});
     std::stable_sort(jobs.begin(), jobs.end(), [](const Job& x, const Job& y) { return x.cost > y.cost; });
   };
   // Deal jobs (indices `idx`, longest first) to the gangs: each to the least
@@ -323,9 +331,10 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
           const int wg = (gang % kXcds) + kXcds * ((gang / kXcds) * S + j);
           std::vector<WorkItem> items;
           std::vector<int2> runs[kWaves];
+          const int sub = j / S_kv;  // column tile (or tail chunk) within the job's group
           for (int k : lists[gang]) {
             const Job& jb = jobs[k];
-            const int g = jb.hc * S + j;
+            const int g = jb.hc * S_kv + j % S_kv;
             if (g >= c.n_kv) continue;
             WorkItem w{};
             w.g = g;
@@ -334,16 +343,18 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
               w.blk = c.meta[pt.b];
               w.kind = kItemBlock;
               w.slot = jb.part;
-              w.sub = jb.ct;
+              w.sub = jb.ct * C + sub;
               w.tile0 = pt.tile0;
               w.ntile = pt.ntile;
               for (int v = 0; v < kWaves; ++v) append_runs(w, v, c.d, runs[v]);
             } else {
+              const int ch = jb.ch * C + sub;
+              if (ch * kTailChunk >= tl[jb.req]) continue;
               w.kind = kItemTail;
-              w.blk.T = std::min(kTailChunk, tl[jb.req] - jb.ch * kTailChunk);  // tokens of the chunk
+              w.blk.T = std::min(kTailChunk, tl[jb.req] - ch * kTailChunk);  // tokens of the chunk
               w.req = jb.req;
-              w.slot = n_parts + jb.ch;
-              w.sub = jb.ch;
+              w.slot = n_parts + ch;
+              w.sub = ch;
             }
             items.push_back(w);
           }

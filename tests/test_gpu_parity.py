@@ -46,6 +46,9 @@ SHAPES = {
     "d64_g7_two_col_tiles": dict(block_tokens=[513, 64, 700], rank_k=[64, 64, 64], rank_v=[32, 64, 96],
                                  n_kv_heads=2, head_dim=64, n_q=10, n_q_heads=14, tail_cap=200,
                                  tail_len=[200, 129, 1, 0, 128, 127, 50, 3, 200, 77]),
+    "two_col_tiles_long_tails": dict(block_tokens=[600, 300], rank_k=[64, 96], n_kv_heads=2, head_dim=128,
+                                     n_q=10, n_q_heads=14, tail_cap=600,
+                                     tail_len=[600, 513, 257, 256, 1, 0, 300, 599, 512, 128]),
     "q7b_shape_5_blocks": dict(block_tokens=[1024] * 5, rank_k=[64, 288, 512, 96, 352], n_kv_heads=4,
                                head_dim=128, n_q=8, n_q_heads=28, tail_cap=256),
     "g1_mha": dict(block_tokens=[100, 900], rank_k=[40, 512], n_kv_heads=4, head_dim=128, n_q=2,
