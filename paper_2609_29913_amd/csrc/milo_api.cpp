@@ -86,7 +86,8 @@ struct milo_cache {
   int32_t* tail_len_pinned = nullptr;
   // the plan of the previous call
   std::vector<int32_t> plan_key;
-  int n_launch = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0;
+  int n_launch = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0, n_ct = 0;
+  int64_t count_off = 0;  // byte offset of the plan's slot counts
   int prog_bytes = 0, ring_offset = 0;
   size_t lds = 0;
 };
@@ -150,6 +151,8 @@ constexpr int kMaxPartTiles = 8;  // keeps every item's run list short
 struct Schedule {
   std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs
   int n_launch = 0, n_parts = 0, prog_bytes = 0, rk_pad_max = 32, rv_pad_max = 32, max_own = 1;
+  int n_block_slots = 0;  // block-group slots of the busiest (KV head, column tile)
+  int64_t count_off = 0;  // byte offset of the int32 [H_kv][n_ct] slot counts in `bytes`
 };
 
 // The fragment runs wave w of a block item consumes, in the kernel's order:
@@ -315,11 +318,16 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
     out->max_own = std::max(out->max_own, max_owned(c.meta[pt.b]));
   }
 
+  // a workgroup folds consecutive block items of one (KV head, column tile)
+  // into one partial where the kernel keeps that partial in registers (at most
+  // two latent rank tiles per wave)
+  const bool fold = out->max_own <= 2;
   const size_t base = attend_lds_base_bytes(c.d, out->rk_pad_max, out->rv_pad_max);
   const size_t cap = std::min<size_t>(kProgCap, base < (size_t)kLdsBytes ? kLdsBytes - base : 0);
   for (int L = 1; L <= (1 << 20); L *= 2) {
     std::vector<std::vector<unsigned char>> progs((size_t)L * kCUs);
     std::vector<WgProgram> entries((size_t)L * kCUs);
+    std::vector<int32_t> slot_count((size_t)c.n_kv * n_ct, 0);
     size_t max_prog = 0;
     for (int l = 0; l < L; ++l) {
       std::vector<int> idx;
@@ -353,11 +361,29 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
               w.kind = kItemTail;
               w.blk.T = std::min(kTailChunk, tl[jb.req] - ch * kTailChunk);  // tokens of the chunk
               w.req = jb.req;
-              w.slot = n_parts + ch;
+              w.slot = ch;
               w.sub = ch;
             }
             items.push_back(w);
           }
+          // groups of consecutive block items with one (KV head, column tile)
+          // share a slot; slots of a (head, tile) are numbered densely
+          int first = -1, last = -1;
+          for (int i = 0; i < (int)items.size(); ++i) {
+            WorkItem& w = items[i];
+            if (w.kind != kItemBlock) continue;
+            const bool cont = fold && first >= 0 && items[first].g == w.g && items[first].sub == w.sub;
+            if (cont) {
+              w.slot = items[first].slot;
+            } else {
+              if (last >= 0) items[last].flags |= kItemFlush;
+              first = i;
+              w.flags |= kItemFirst;
+              w.slot = slot_count[(size_t)w.g * n_ct + w.sub]++;
+            }
+            last = i;
+          }
+          if (last >= 0) items[last].flags |= kItemFlush;
           WgProgram& e = entries[(size_t)l * kCUs + wg];
           e = WgProgram{};
           if (items.empty()) continue;
@@ -380,16 +406,22 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
     }
     const size_t prog_bytes = (size_t)round_up((int64_t)max_prog, 256);
     if (prog_bytes > cap) continue;
-    // assemble: the entry table, then every program at a 16-byte aligned offset
+    // assemble: the entry table, every program at a 16-byte aligned offset,
+    // then the slot counts
     size_t off = entries.size() * sizeof(WgProgram);
     for (size_t k = 0; k < progs.size(); ++k) {
       entries[k].off = (int64_t)off;
       off += progs[k].size();
     }
+    out->count_off = (int64_t)round_up((int64_t)off, 16);
+    off = (size_t)out->count_off + slot_count.size() * sizeof(int32_t);
     out->bytes.assign(std::max<size_t>(off, 16), 0);
     std::memcpy(out->bytes.data(), entries.data(), entries.size() * sizeof(WgProgram));
     for (size_t k = 0; k < progs.size(); ++k)
       if (!progs[k].empty()) std::memcpy(out->bytes.data() + entries[k].off, progs[k].data(), progs[k].size());
+    std::memcpy(out->bytes.data() + out->count_off, slot_count.data(), slot_count.size() * sizeof(int32_t));
+    out->n_block_slots = 0;
+    for (int32_t k : slot_count) out->n_block_slots = std::max(out->n_block_slots, (int)k);
     out->n_launch = L;
     out->prog_bytes = (int)prog_bytes;
     return MILO_OK;
@@ -645,8 +677,10 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     MILO_HIP(hipMemcpyAsync(c->plan_d, c->plan_pinned, (size_t)plan_bytes, hipMemcpyHostToDevice, s));
     MILO_HIP(hipMemcpyAsync(c->tail_len_d, c->tail_len_pinned, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
     c->n_launch = sch.n_launch;
-    c->n_slots = sch.n_parts + max_chunks;
-    c->n_block_slots = sch.n_parts;
+    c->n_slots = sch.n_block_slots + max_chunks;
+    c->n_block_slots = sch.n_block_slots;
+    c->count_off = sch.count_off;
+    c->n_ct = n_ct;
     c->max_rt = max_rt;
     c->nslot = nslot;
     c->rk_pad_max = sch.rk_pad_max;
@@ -689,10 +723,13 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   aa.G = G;
   aa.tail_cap = tail_cap;
   aa.n_slots = c->n_slots;
+  aa.n_block_slots = c->n_block_slots;
   aa.qt_stride = c->rk_pad_max + 8;
   aa.prog_bytes = c->prog_bytes;
   aa.ring_offset = c->ring_offset;
-  MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out, n_q_heads, c->n_block_slots, c->n_slots};
+  MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out,
+               reinterpret_cast<const int32_t*>(c->plan_d + c->count_off), n_q_heads, G, c->n_ct,
+               c->n_block_slots, c->n_slots};
 
   // timing: events recorded by the launches themselves at kernel start and end
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};  // attend start / end, merge start / end

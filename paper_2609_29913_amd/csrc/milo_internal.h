@@ -172,15 +172,23 @@ struct WorkItem {
   BlockMeta blk;      // block items: the block's packed offsets and padded sizes;
                       // tail items: blk.T = tokens of the chunk
   int32_t kind;       // ItemKind
-  int32_t slot;       // partial slot written for every column of the item
+  int32_t slot;       // block items: the group's partial slot (see kItemFirst);
+                      // tail items: chunk index (slot n_block_slots + slot)
   int32_t g;          // KV head
-  int32_t sub;        // block items: 64-column tile; tail items: 128-token chunk
+  int32_t sub;        // block items: 64-column tile; tail items: kTailChunk-token chunk
   int32_t req;        // tail items: request index
   int32_t tile0;      // block items: first 256-token tile of the block covered
   int32_t ntile;      // block items: number of tiles covered
-  int32_t pad;
+  int32_t flags;      // block items: kItemFirst / kItemFlush (see below)
 };
 static_assert(sizeof(WorkItem) == 80, "work item layout");
+// Consecutive block items of a workgroup for the same KV head and column tile
+// form a group that shares one partial slot: the first item starts the
+// workgroup's running (max, sum, output) per column, every item folds its own
+// partial into it (log-sum-exp), and the last one writes it out.  Slots of a
+// (head, column tile) are numbered densely from 0; tail items write slot
+// n_block_slots + their chunk index.
+enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2 };
 
 // The attention kernel is persistent: workgroup b runs the program of entry b,
 // a byte range of the program buffer holding its work items in order, followed
@@ -226,6 +234,7 @@ struct AttendArgs {
   int n_q, H_q, H_kv, G;
   int tail_cap;
   int n_slots;
+  int n_block_slots;         // slots [0, n_block_slots) hold block groups, the rest tail chunks
   int qt_stride;             // bf16 row stride of the projected query in LDS
   int prog_bytes;            // LDS bytes reserved for the program (the work area follows)
   int ring_offset;           // byte offset of the per-wave fragment rings in the work area
@@ -236,7 +245,8 @@ struct MergeArgs {
   const float2* part_ml;
   const int32_t* tail_len;   // device [n_q]
   float* out;                // [n_q][H_q][d]
-  int H_q, n_block_slots, n_slots;
+  const int32_t* slot_count;  // device [H_kv][n_ct]: block-group slots used per (KV head, column tile)
+  int H_q, G, n_ct, n_block_slots, n_slots;
 };
 
 struct PackArgs {

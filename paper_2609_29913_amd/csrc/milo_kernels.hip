@@ -3,18 +3,23 @@
 // attention itself is Sec. 4.1 Eq. 1).
 //
 //  pack_kernel    repacks row-major bf16 factors into MFMA-fragment order.
-//  attend_kernel  persistent: one workgroup per compute unit runs a host-built
-//                 list of work items, its fragment streams flowing across items:
-//     block item (block b, KV head g, 64-column tile of query columns):
+//  attend_kernel  persistent: one workgroup (8 waves) per compute unit runs a
+//                 host-built list of work items, its fragment streams flowing
+//                 across items:
+//     block item (block b, KV head g, 64-column tile of query columns, a run
+//     of 256-token tiles):
 //       projection  Qt = scale*log2(e) * R^K_b[:, g] q          (MFMA, into LDS)
-//       scores      S  = P^K_b Qt, 256 tokens per tile          (MFMA, 4 waves x 64 tokens)
+//       scores      S  = P^K_b Qt, 32 tokens per wave and tile  (MFMA)
 //       softmax     running max per column shared by the waves, W = 2^(S - m)
-//       latent V    Ot = sum_t W_t P^V_b[t]                      (MFMA, waves split the rank)
-//       up-project  o  = R^V_b[:, g]^T Ot                        (MFMA from registers)
-//       -> partial (m, l, o) per column
-//     tail item (request i, KV head g, 128-token chunk of the request's own KV):
-//       plain attention of the group's query heads over the chunk (VALU, LDS-staged)
-//       -> partial (m, l, o) per column
+//       latent V    Ot = sum_t W_t P^V_b[t]                      (MFMA, waves split
+//                   token segments x rank tiles)
+//       up-project  o  = R^V_b[:, g]^T Ot                        (MFMA, 16-dim slice
+//                   per wave)
+//       -> folded into the workgroup's partial (m, l, o) per column for its
+//          current (KV head, column tile); written when the group ends
+//     tail item (request i, KV head g, kTailChunk-token chunk of the request's
+//     own KV): plain attention of the group's query heads over the chunk
+//     (MFMA scores, VALU values) -> partial (m, l, o) per column
 //  merge_kernel   log-sum-exp merge of every partial of a column into O (fp32).
 //
 // Scores are kept in log2 units (the scale folds log2(e)), so every exponential
@@ -179,7 +184,7 @@ __device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& i
   constexpr int DL = D / 64;                // dims per lane in the value pass
   constexpr int kTokW = kTailChunk / kWaves;  // tokens per wave (32)
   static_assert(kTokW == 32, "one 32-row MFMA tile of tokens per wave");
-  const int i = it.req, slot = it.slot, g = it.g, G = a.G;
+  const int i = it.req, slot = a.n_block_slots + it.slot, g = it.g, G = a.G;
   const int wave = tid >> 6, lane = tid & 63, lrow = lane & 31, lhi = lane >> 5;
   const int t0 = it.sub * kTailChunk, nt = it.blk.T;
   float* red = reinterpret_cast<float*>(smem);   // [kWaves][32] column maxima
@@ -321,23 +326,42 @@ struct FragRing {
   }
 };
 
+// A workgroup's running partial for its current group of block items (one KV
+// head and column tile): the output in the up-projection's lane layout (NCB
+// 16-column blocks of the wave's 16-dim slice), the per-column maximum in the
+// score layout (32 ch + lane % 32; every wave holds it), the per-column sum
+// in wave 0 (thread t: column t).
+template <int NCB>
+struct GroupAcc {
+  f32x4 o[NCB];
+  float m[2];
+  float l;
+};
+template <int D>
+constexpr int up_col_blocks() {
+  return 4 * (D / 16) / kWaves;  // 16-column blocks per wave in the up-projection
+}
+
 // ---------------------------------------------------------------------------
 // Block work item: latent-space attention of one 64-column tile of the query
 // columns of KV head g over the tiles [tile0, tile0 + ntile) of block b.
 //
 // Eight waves (two per SIMD).  Scores: wave w takes the 32 tokens 32w..32w+31
-// of every 256-token tile against all 64 columns.  Latent V and the
-// up-projection: the waves form nseg token segments x ng rank groups (see the
-// packed layout), so each wave accumulates its own rank tiles over its own
-// tokens; the up-projected partials of all waves are summed in LDS.  Every
-// factor fragment a wave consumes (R^K for the projection, P^K and P^V per
-// tile, R^V for the up-projection) comes from the wave's fragment stream
-// (FragRing above); the item's queries are loaded into LDS at its start.  Every loop is software-pipelined: the operands of
-// step k+1 are read while the MFMAs of step k run.
+// of every 256-token tile against all 64 columns.  Latent V: the waves form
+// nseg token segments x ng rank groups (see the packed layout), so each wave
+// accumulates its own rank tiles over its own tokens; the segments' partial
+// sums are then combined in LDS and the latent result goes to LDS as bf16.
+// Up-projection: each wave computes a 16-dim slice of the output for all 64
+// columns over all ranks.  Every factor fragment a wave consumes (R^K for the
+// projection, P^K and P^V per tile, R^V for the up-projection) comes from the
+// wave's fragment stream (FragRing above); the item's queries are loaded into
+// LDS at its start.  Every loop is software-pipelined: the operands of step
+// k+1 are read while the MFMAs of step k run.
 // ---------------------------------------------------------------------------
 template <int D, int MAX_RT, int NSLOT>
 __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
-                                           FragRing<D, NSLOT>& fr, const int tid) {
+                                           FragRing<D, NSLOT>& fr, GroupAcc<up_col_blocks<D>()>& acc,
+                                           const int tid) {
   constexpr int NK = D / 16;
   constexpr int kORed = 4;  // partial-output slots of the up-projection reduction
   const BlockMeta& bm = it.blk;
@@ -609,7 +633,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   // every wave: output dims [16 ds, 16 ds + 16) of its 16-column blocks, over
   // all ranks (16x16x32 MFMAs: R^V fragment x latent columns from LDS)
   constexpr int NDS = D / 16;              // 16-dim slices
-  constexpr int NCB = 4 * NDS / kWaves;    // 16-column blocks per wave
+  constexpr int NCB = up_col_blocks<D>();  // 16-column blocks per wave
   const int ds = wave % NDS, cb0 = (wave / NDS) * NCB;
   f32x4 uacc[NCB];
 #pragma unroll
@@ -626,25 +650,58 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       af = an;
     }
   }
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
-    const int c = c0 + 16 * (cb0 + cb) + (lane & 15);
-    if (c < ncg) {
-      const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
-      *reinterpret_cast<float4*>(a.part_o + (colg * a.n_slots + slot) * D + 16 * ds + 4 * (lane >> 4)) =
-          make_float4(uacc[cb][0], uacc[cb][1], uacc[cb][2], uacc[cb][3]);
-    }
-  }
+  // the item's partial: per-column maximum m_run (score layout), sum (thread
+  // tid < kCols: column tid), output uacc (up-projection layout)
+  float l_item = 0.f;
   if (tid < kCols) {
-    const int c = c0 + tid;
-    if (c < ncg) {
-      float l = 0.f;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) l += lred[w * kCols + tid];
-      const float m = tid < 32 ? m_run[0] : m_run[1];
-      const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
-      a.part_ml[colg * a.n_slots + slot] = make_float2(m, l);
+    for (int w = 0; w < kWaves; ++w) l_item += lred[w * kCols + tid];
+  }
+  auto store = [&](const f32x4 (&o)[NCB], const float (&m)[2], float l) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const int c = c0 + 16 * (cb0 + cb) + (lane & 15);
+      if (c < ncg) {
+        const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
+        *reinterpret_cast<float4*>(a.part_o + (colg * a.n_slots + slot) * D + 16 * ds + 4 * (lane >> 4)) =
+            make_float4(o[cb][0], o[cb][1], o[cb][2], o[cb][3]);
+      }
     }
+    if (tid < kCols) {
+      const int c = c0 + tid;
+      if (c < ncg) {
+        const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
+        a.part_ml[colg * a.n_slots + slot] = make_float2(tid < 32 ? m[0] : m[1], l);
+      }
+    }
+  };
+  if constexpr (MAX_RT <= 2) {
+    // fold into the group's running partial (log-sum-exp); the group's last
+    // item writes it out
+    const bool first = (it.flags & kItemFirst) != 0;
+    float fa[2], fb[2];
+#pragma unroll
+    for (int ch = 0; ch < 2; ++ch) {
+      const float mn = first ? m_run[ch] : fmaxf(acc.m[ch], m_run[ch]);
+      fa[ch] = first ? 0.f : fast_exp2(acc.m[ch] - mn);
+      fb[ch] = fast_exp2(m_run[ch] - mn);
+      acc.m[ch] = mn;
+    }
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const int cc = 16 * (cb0 + cb) + (lane & 15);  // column within the tile
+      const bool hi = ((cb0 + cb) >> 1) != 0;        // wave-uniform: column half
+      const float sa = __shfl(hi ? fa[1] : fa[0], cc & 31);
+      const float sb = __shfl(hi ? fb[1] : fb[0], cc & 31);
+      acc.o[cb] = first ? uacc[cb] * sb : acc.o[cb] * sa + uacc[cb] * sb;
+    }
+    if (tid < kCols) {
+      const int ch = tid >> 5;
+      acc.l = first ? l_item * fb[ch] : acc.l * fa[ch] + l_item * fb[ch];
+    }
+    if (it.flags & kItemFlush) store(acc.o, acc.m, acc.l);
+  } else {
+    store(uacc, m_run, l_item);
   }
 }
 
@@ -680,6 +737,7 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   const int run_off = a.wg[blockIdx.x].run_off[wave];  // scalar load at a wave-uniform index
   unsigned char* work = smem + a.prog_bytes;
   FragRing<D, NSLOT> fr;
+  GroupAcc<up_col_blocks<D>()> acc;
   fr.data_lane = a.data + (threadIdx.x & 63) * 8;
   fr.lane8 = (threadIdx.x & 63) * 8;
   fr.ring = reinterpret_cast<__bf16*>(work + a.ring_offset) + (size_t)wave * NSLOT * kFragElems;
@@ -693,15 +751,16 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
     // lane-dependent address of one item kind stays live across the other
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
-    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT>(a, it, work, fr, tid);
+    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT>(a, it, work, fr, acc, tid);
     else if (it.kind == kItemTail) tail_item<D>(a, it, work, tid);
   }
   if constexpr (NSLOT > 0) wait_vmcnt<0>();  // no LDS write may land after the workgroup ends
 }
 
 // ---------------------------------------------------------------------------
-// Log-sum-exp merge: one workgroup per query column (i, h).  Slots [0, n_sel)
-// are the selected blocks, then request i's tail chunks.  Thread t takes the
+// Log-sum-exp merge: one workgroup per query column (i, h).  Its partials are
+// the block-group slots [0, nb) of its (KV head, column tile), then request i's
+// tail chunks at n_block_slots + chunk.  Thread t takes the
 // 4 output dims 4 (t % (D/4)) of the slots s = t / (D/4) (mod slots per pass),
 // so every load is one 16-byte vector and a wave reads whole slots; the loads
 // of kMergeUnroll passes are issued before any is used, and each thread keeps
@@ -718,8 +777,10 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
   __shared__ float4 red_o[SPP][TPS];
   const int col = blockIdx.x, tid = threadIdx.x;
   const int dq = tid % TPS, sl = tid / TPS;
-  const int i = col / a.H_q;
-  const int n_valid = a.n_block_slots + (a.tail_len[i] + kTailChunk - 1) / kTailChunk;
+  const int i = col / a.H_q, h = col % a.H_q;
+  const int ct = (i * a.G + h % a.G) / kCols;                   // the column's tile within its KV head
+  const int nb = a.slot_count[(h / a.G) * a.n_ct + ct];        // block-group slots of that (head, tile)
+  const int n_valid = nb + (a.tail_len[i] + kTailChunk - 1) / kTailChunk;
   const float2* ml = a.part_ml + (int64_t)col * a.n_slots;
   const float4* po = reinterpret_cast<const float4*>(a.part_o + (int64_t)col * a.n_slots * D) + dq;
   float m = -INFINITY, l = 0.f;
@@ -729,8 +790,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
     float4 oo[kMergeUnroll];
 #pragma unroll
     for (int u = 0; u < kMergeUnroll; ++u) {
-      const int s = s0 + u * SPP;
-      if (s < n_valid) {
+      const int v = s0 + u * SPP;
+      if (v < n_valid) {
+        const int s = v < nb ? v : a.n_block_slots + (v - nb);
         mm[u] = ml[s];
         oo[u] = po[(int64_t)s * TPS];
       } else {
