@@ -144,8 +144,8 @@ int64_t factor_offset(const BlockMeta& m, int which) {
 // slowest wave's projection and up-projection streams, one fragment of its
 // tile stream, the per-tile softmax and barriers, the per-item set-up, one
 // round of the token-segment reduction, and one dense-tail chunk.
-constexpr double kCostFragItem = 0.19, kCostFragTile = 0.173, kCostTile = 1.52, kCostItem = 2.33,
-                 kCostSegRound = 1.36, kCostTail = 9.7;
+constexpr double kCostFragItem = 0.206, kCostFragTile = 0.153, kCostTile = 1.75, kCostItem = 2.43,
+                 kCostSegRound = 0.61, kCostTail = 9.4;
 constexpr int kMaxPartTiles = 8;  // keeps every item's run list short
 
 struct Schedule {
