@@ -146,7 +146,6 @@ int64_t factor_offset(const BlockMeta& m, int which) {
 // round of the token-segment reduction, and one dense-tail chunk.
 constexpr double kCostFragItem = 0.206, kCostFragTile = 0.153, kCostTile = 1.75, kCostItem = 2.43,
                  kCostSegRound = 0.61, kCostTail = 9.4;
-constexpr int kMaxPartTiles = 8;  // keeps every item's run list short
 
 struct Schedule {
   std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs
@@ -154,33 +153,6 @@ struct Schedule {
   int n_block_slots = 0;  // block-group slots of the busiest (KV head, column tile)
   int64_t count_off = 0;  // byte offset of the int32 [H_kv][n_ct] slot counts in `bytes`
 };
-
-// The fragment runs wave w of a block item consumes, in the kernel's order:
-// its R^K rank tiles (projection); then per tile its P^K sub-tile and the P^V
-// rank tiles of its rank group over its token segment; then R^V for its
-// 16-dim output slice over all ranks (up-projection).  Offsets
-// follow the packed layout of each factor.
-void append_runs(const WorkItem& it, int w, int d, std::vector<int2>& out) {
-  const BlockMeta& bm = it.blk;
-  const int NK = d / 16;
-  const int nrt_k = bm.rk_pad / 32, nks = bm.rk_pad / 16, nrt_v = bm.rv_pad / 32;
-  const int own_k = owned_tiles(nrt_k, w, kWaves);
-  const int nseg = v_segments(nrt_v), ng = kWaves / nseg, rg = w % ng, sg = w / ng;
-  const int own_v = owned_tiles(nrt_v, rg, ng), nst = 16 / nseg;
-  const int tiles_all = bm.T_pad / kTile;
-  auto add = [&](int64_t elem_off, int64_t n) {
-    if (n > 0) out.push_back(make_int2((int)(elem_off / kFragElems), (int)n));
-  };
-  add(bm.off_rk + ((int64_t)it.g * nrt_k * NK + (int64_t)NK * owned_before(nrt_k, w, kWaves)) * kFragElems,
-      (int64_t)NK * own_k);
-  const int64_t pv_first = (int64_t)(bm.T_pad / 16) * owned_before(nrt_v, rg, ng);
-  for (int t = it.tile0; t < it.tile0 + it.ntile; ++t) {
-    add(bm.off_pk + ((int64_t)w * tiles_all + t) * nks * kFragElems, nks);
-    add(bm.off_pv + (pv_first + (int64_t)(16 * t + nst * sg) * own_v) * kFragElems, (int64_t)nst * own_v);
-  }
-  const int nds = d / 16, ds = w % nds, nkr = bm.rv_pad / 32;
-  add(bm.off_rv + ((int64_t)it.g * nds + ds) * nkr * kFragElems, nkr);
-}
 
 // Latent rank tiles the busiest wave of a block accumulates (projection or value pass).
 int max_owned(const BlockMeta& m) {
@@ -322,8 +294,14 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
   // into one partial where the kernel keeps that partial in registers (at most
   // two latent rank tiles per wave)
   const bool fold = out->max_own <= 2;
+  // LDS left for the program: all that the projected query, weight tile and
+  // a 6-slot fragment ring leave (fewer launches would cost the ring), or all
+  // but the first two when even a short program leaves no room for the ring
   const size_t base = attend_lds_base_bytes(c.d, out->rk_pad_max, out->rv_pad_max);
-  const size_t cap = std::min<size_t>(kProgCap, base < (size_t)kLdsBytes ? kLdsBytes - base : 0);
+  const size_t ring6 = attend_ring_bytes(6);
+  const size_t short_prog = 16 * sizeof(WorkItem) + (size_t)kWaves * kRunBufs * kRunCap * sizeof(int2);
+  const size_t room = base < (size_t)kLdsBytes ? kLdsBytes - base : 0;
+  const size_t cap = room >= ring6 + short_prog ? room - ring6 : room;
   for (int L = 1; L <= (1 << 20); L *= 2) {
     std::vector<std::vector<unsigned char>> progs((size_t)L * kCUs);
     std::vector<WgProgram> entries((size_t)L * kCUs);
@@ -338,7 +316,6 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
         for (int j = 0; j < S; ++j) {
           const int wg = (gang % kXcds) + kXcds * ((gang / kXcds) * S + j);
           std::vector<WorkItem> items;
-          std::vector<int2> runs[kWaves];
           const int sub = j / S_kv;  // column tile (or tail chunk) within the job's group
           for (int k : lists[gang]) {
             const Job& jb = jobs[k];
@@ -354,7 +331,7 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
               w.sub = jb.ct * C + sub;
               w.tile0 = pt.tile0;
               w.ntile = pt.ntile;
-              for (int v = 0; v < kWaves; ++v) append_runs(w, v, c.d, runs[v]);
+              w.flags = lg_rank_groups(w.blk.rv_pad / 32) << kItemLgNgShift;
             } else {
               const int ch = jb.ch * C + sub;
               if (ch * kTailChunk >= tl[jb.req]) continue;
@@ -390,17 +367,10 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
           std::vector<unsigned char>& pb = progs[(size_t)l * kCUs + wg];
           pb.resize(items.size() * sizeof(WorkItem));
           std::memcpy(pb.data(), items.data(), pb.size());
-          for (int v = 0; v < kWaves; ++v) {
-            runs[v].push_back(make_int2(0, kSentinelRun));
-            e.run_off[v] = (int32_t)pb.size();
-            const size_t at = pb.size();
-            pb.resize(at + runs[v].size() * sizeof(int2));
-            std::memcpy(pb.data() + at, runs[v].data(), runs[v].size() * sizeof(int2));
-          }
-          pb.resize(round_up((int64_t)pb.size(), 16), 0);
           e.n_items = (int32_t)items.size();
           e.words = (int32_t)(pb.size() / 4);
-          max_prog = std::max(max_prog, pb.size());
+          // LDS: the items, then every wave's run buffer
+          max_prog = std::max(max_prog, pb.size() + (size_t)kWaves * kRunBufs * kRunCap * sizeof(int2));
         }
       }
     }

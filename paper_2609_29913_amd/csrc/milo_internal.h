@@ -53,9 +53,8 @@ __host__ __device__ inline int owned_tiles(int nrt, int w, int n) {
   return nrt > w ? (nrt - w + n - 1) / n : 0;
 }
 __host__ __device__ inline int owned_before(int nrt, int w, int n) {
-  int s = 0;
-  for (int v = 0; v < w; ++v) s += owned_tiles(nrt, v, n);
-  return s;
+  // owners v < nrt % n hold one tile more than nrt / n
+  return w * (nrt / n) + (w < nrt % n ? w : nrt % n);
 }
 
 // Token segments of the latent value pass for a block with nrt rank tiles of
@@ -76,6 +75,59 @@ __host__ __device__ inline int v_segments(int nrt) {
     }
   }
   return best;
+}
+
+struct BlockMeta {
+  int64_t off_pk, off_rk, off_pv, off_rv;
+  int32_t T, T_pad, rk_pad, rv_pad;
+};
+
+// Most 256-token tiles in one block item (parts of larger blocks are split),
+// and so the most fragment runs one item gives a wave (plus an end marker).
+constexpr int kMaxPartTiles = 8;
+constexpr int kRunCap = 2 + 2 * kMaxPartTiles + 2;
+constexpr int kRunBufs = 4;  // run buffers per wave in the attention kernel
+
+// log2 of the rank groups (kWaves / nseg) of a block with nrt V rank tiles
+__host__ __device__ inline int lg_rank_groups(int nrt) {
+  const int nseg = v_segments(nrt);
+  return nseg == 1 ? 3 : nseg == 2 ? 2 : nseg == 4 ? 1 : 0;
+}
+
+// The fragment runs wave w consumes for a block item (block bm, KV head g,
+// tiles [tile0, tile0 + ntile)) of head dimension d, in the attention kernel's
+// order: its R^K rank tiles (projection); then per tile its P^K sub-tile and
+// the P^V rank tiles of its rank group over its token segment; then R^V for
+// its 16-dim output slice over all ranks (up-projection).  lg_ng =
+// lg_rank_groups(rv_pad / 32) (passed in, so the kernel derives runs with
+// shifts only).  emit(first fragment index, count) is called for every
+// non-empty run; offsets follow the packed layout above.
+template <typename Emit>
+__host__ __device__ inline void block_runs(const BlockMeta& bm, int g, int tile0, int ntile, int w, int d,
+                                           int lg_ng, Emit&& emit) {
+  static_assert(kWaves == 8, "rank tiles are dealt over 8 waves");
+  const int NK = d / 16;
+  const int nrt_k = bm.rk_pad >> 5, nks = bm.rk_pad >> 4, nrt_v = bm.rv_pad >> 5;
+  // owner w of tiles dealt round-robin over n = 2^lg owners: nrt >> lg tiles,
+  // one more if w < nrt mod n; the owners before it hold w (nrt >> lg) + min(w, nrt mod n)
+  const int own_k = (nrt_k >> 3) + (w < (nrt_k & 7) ? 1 : 0);
+  const int before_k = w * (nrt_k >> 3) + (w < (nrt_k & 7) ? w : (nrt_k & 7));
+  const int ng = 1 << lg_ng, rg = w & (ng - 1), sg = w >> lg_ng;
+  const int rem_v = nrt_v & (ng - 1);
+  const int own_v = (nrt_v >> lg_ng) + (rg < rem_v ? 1 : 0);
+  const int before_v = rg * (nrt_v >> lg_ng) + (rg < rem_v ? rg : rem_v);
+  const int nst = 2 << lg_ng;  // 16-token steps of a segment per tile (16 / nseg)
+  const int tiles_all = bm.T_pad / kTile;
+  const int rk0 = (int)(bm.off_rk / kFragElems), pk0 = (int)(bm.off_pk / kFragElems);
+  const int pv0 = (int)(bm.off_pv / kFragElems), rv0 = (int)(bm.off_rv / kFragElems);
+  if (own_k > 0) emit(rk0 + g * nrt_k * NK + NK * before_k, NK * own_k);
+  const int pv_first = (bm.T_pad / 16) * before_v;
+  for (int t = tile0; t < tile0 + ntile; ++t) {
+    emit(pk0 + (w * tiles_all + t) * nks, nks);
+    if (own_v > 0) emit(pv0 + pv_first + (16 * t + nst * sg) * own_v, nst * own_v);
+  }
+  const int nds = d / 16, nkr = bm.rv_pad >> 5;
+  emit(rv0 + (g * nds + w % nds) * nkr, nkr);
 }
 
 struct FactorGeom {
@@ -160,10 +212,6 @@ __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, i
 
 // Per-block metadata in device memory; offsets are in bf16 elements from the
 // start of the cache's packed buffer.
-struct BlockMeta {
-  int64_t off_pk, off_rk, off_pv, off_rv;
-  int32_t T, T_pad, rk_pad, rv_pad;
-};
 
 // Work item of the attention kernel.  Block items carry their block's metadata
 // inline, so an item is self-contained.
@@ -189,21 +237,23 @@ static_assert(sizeof(WorkItem) == 80, "work item layout");
 // (head, column tile) are numbered densely from 0; tail items write slot
 // n_block_slots + their chunk index.
 enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2 };
+// bits 8-9 of a block item's flags: lg_rank_groups of its block
+constexpr int kItemLgNgShift = 8;
 
 // The attention kernel is persistent: workgroup b runs the program of entry b,
-// a byte range of the program buffer holding its work items in order, followed
-// by one fragment-run list per wave.  A run is (first fragment index, count):
-// the fragments the wave consumes, in consumption order, over all of the
-// workgroup's block items (tail items consume none).  Each list ends with a
-// sentinel run (fragment 0, 2^30) that feeds the look-ahead loads issued past
-// the last real fragment.  The program is copied into LDS at kernel start.
+// a byte range of the program buffer holding its work items in order; it is
+// copied into LDS at kernel start.  Each wave derives, item by item, the runs
+// of consecutive packed fragments it consumes (a run is (first fragment index,
+// count); block_runs below), into a per-wave run buffer of kRunCap entries
+// that follows the items in LDS; after the last block item a sentinel run
+// (fragment 0, 2^30) feeds the look-ahead loads issued past the last fragment.
 struct WgProgram {
   int64_t off;                // byte offset in the program buffer (16-byte aligned)
   int32_t words;              // program size in 4-byte words
   int32_t n_items;            // work items (they start the program)
-  int32_t run_off[kWaves];    // byte offset of wave w's run list within the program
+  int32_t pad[2];
 };
-static_assert(sizeof(WgProgram) == 16 + 4 * kWaves, "program entry layout");
+static_assert(sizeof(WgProgram) == 24, "program entry layout");
 constexpr int kSentinelRun = 1 << 30;
 
 // Attention kernel geometry.
@@ -218,7 +268,6 @@ constexpr int kLdsBytes = 160 * 1024;          // LDS per workgroup on gfx950
 constexpr int kTailChunk = kWaves * 32;        // dense-tail tokens per work item
 constexpr int kXcds = 8;                       // XCDs of an MI355X (workgroup b runs on XCD b % 8)
 constexpr int kCUs = 256;                      // compute units; one persistent workgroup each
-constexpr int kProgCap = 8192;                 // largest per-workgroup program (bytes of LDS)
 
 struct AttendArgs {
   const uint16_t* data;      // packed factors

@@ -84,6 +84,9 @@ __device__ __forceinline__ void lds_store_b128(void* p, float4 v) {
   const f32x4 x = {v.x, v.y, v.z, v.w};
   asm volatile("ds_write_b128 %0, %1" ::"v"(lds_addr(p)), "v"(x) : "memory");
 }
+__device__ __forceinline__ void lds_store_b64(void* p, int2 v) {
+  asm volatile("ds_write_b64 %0, %1" ::"v"(lds_addr(p)), "v"(v) : "memory");
+}
 __device__ __forceinline__ void lds_store_b32(void* p, float v) {
   asm volatile("ds_write_b32 %0, %1" ::"v"(lds_addr(p)), "v"(v) : "memory");
 }
@@ -263,13 +266,42 @@ __device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& i
   }
 }
 
-// A wave's fragment stream over all block items of its workgroup.  The host
-// lists, per wave, the runs of consecutive packed fragments in the order the
-// wave consumes them (per block item: its R^K run for the projection, then for
-// every 256-token tile its P^K run and its P^V run, then its R^V run for the
-// up-projection); the list sits in LDS and ends with a long sentinel run.  A
-// run entry (x, n) is n consecutive fragments starting at fragment x.  With
-// NSLOT > 0 fragments reach the wave through a private ring of NSLOT LDS
+// a work item read from LDS into wave-uniform registers
+__device__ __forceinline__ WorkItem lds_item(const unsigned char* p) {
+  static_assert(sizeof(WorkItem) == 80, "a work item is five 16-byte chunks");
+  int4 v0, v1, v2, v3, v4;
+  const uint32_t a = lds_addr(p);
+  asm volatile(
+      "ds_read_b128 %0, %5\n\tds_read_b128 %1, %5 offset:16\n\tds_read_b128 %2, %5 offset:32\n\t"
+      "ds_read_b128 %3, %5 offset:48\n\tds_read_b128 %4, %5 offset:64\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(v0), "=&v"(v1), "=&v"(v2), "=&v"(v3), "=&v"(v4)  // early clobber: the address
+      : "v"(a));                                                // must survive the first reads
+  const int4 vv[5] = {v0, v1, v2, v3, v4};
+  int32_t w[20];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    w[4 * i + 0] = __builtin_amdgcn_readfirstlane(vv[i].x);
+    w[4 * i + 1] = __builtin_amdgcn_readfirstlane(vv[i].y);
+    w[4 * i + 2] = __builtin_amdgcn_readfirstlane(vv[i].z);
+    w[4 * i + 3] = __builtin_amdgcn_readfirstlane(vv[i].w);
+  }
+  WorkItem it;
+  __builtin_memcpy(&it, w, sizeof(WorkItem));
+  return it;
+}
+
+// A wave's fragment stream over all block items of its workgroup: the runs of
+// consecutive packed fragments in the order the wave consumes them (per block
+// item: its R^K run for the projection, then for every 256-token tile its P^K
+// run and its P^V run, then its R^V run for the up-projection; block_runs).
+// Wave 0 derives them item by item for all waves (RunDeriver below) into four
+// LDS run buffers per wave used in turn (entry (x, n): n consecutive fragments
+// from fragment x; (x, 0) ends a buffer), staying two block items ahead of the
+// item being computed: every item gives every wave at least three fragments
+// and the look-ahead loads run at most kDepth <= 6 fragments ahead, so they
+// never reach a buffer that is not ready, and the buffer being refilled is two
+// items behind.  Runs are read when their first fragment is issued.  After the
+// last block item a long sentinel run follows.  With NSLOT > 0 fragments reach the wave through a private ring of NSLOT LDS
 // slots, filled by direct global->LDS loads issued kDepth fragments ahead of
 // use, so every wait is a constant vmcnt; the look-ahead crosses item
 // boundaries, so the next item's first fragments load while the current one
@@ -277,31 +309,42 @@ __device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& i
 template <int D, int NSLOT>
 struct FragRing {
   static constexpr int kDepth = NSLOT > 2 ? NSLOT - 2 : 1;  // fragments in flight
+  static_assert(kDepth <= 6, "run buffers are derived two block items (>= 6 fragments) ahead");
   const uint16_t* data_lane;  // packed factor buffer + this lane's 8-element offset
   int lane8;                  // this lane's element offset inside a fragment
   __bf16* ring;               // this wave's NSLOT slots
   uint32_t ring_lds;          // LDS byte address of slot 0 (wave-uniform)
-  const int2* run;            // current entry of this wave's run list (LDS)
+  const int2* run;            // current entry of the run buffers (LDS)
+  int2* rbuf;                 // this wave's kRunBufs run buffers of kRunCap entries
+  int rb;                     // buffer the stream reads
   int64_t off;                // element offset of the next fragment
   int left;                   // fragments left in the current run
   int rs, ws;                 // ring slots: next to read, next to fill
 
   __device__ __forceinline__ void load_run() {
-    const int2 v = prog_read_b64(run);
+    int2 v = prog_read_b64(run);
+    if (__builtin_amdgcn_readfirstlane(v.y) == 0) {  // end of a buffer: the next one
+      rb = (rb + 1) % kRunBufs;
+      run = rbuf + rb * kRunCap;
+      v = prog_read_b64(run);
+    }
     off = (int64_t)__builtin_amdgcn_readfirstlane(v.x) * kFragElems;
     left = __builtin_amdgcn_readfirstlane(v.y);
   }
   // address of this lane's part of the next fragment; advances the stream
   __device__ __forceinline__ const uint16_t* next() {
-    const uint16_t* o = data_lane + off;
-    off += kFragElems;
-    if (--left == 0) {
+    if (left == 0) {
       ++run;
       load_run();
     }
+    const uint16_t* o = data_lane + off;
+    off += kFragElems;
+    --left;
     return o;
   }
   __device__ __forceinline__ void start() {
+    rb = 0;
+    run = rbuf;
     load_run();
     rs = 0;
     ws = 0;
@@ -323,6 +366,45 @@ struct FragRing {
     } else {
       return ld_bf16x8(next());
     }
+  }
+};
+
+// Derivation of the fragment runs, done by wave 0 for all eight waves (lane w
+// derives wave w's runs, in vector registers): the runs of the workgroup's
+// next block item, or the sentinel run after the last one, into every wave's
+// buffer gb.  Runs are read by their wave only after a later workgroup
+// barrier.
+template <int D>
+struct RunDeriver {
+  const unsigned char* items;  // the workgroup's work items (LDS)
+  int n_items;
+  int gk;                      // next item to look at
+  int gb;                      // buffer the next derivation fills
+  int2* rbuf;                  // all waves' run buffers: [wave][kRunBufs][kRunCap]
+
+  __device__ void derive(int lane) {
+    WorkItem it{};
+    bool found = false;
+    while (gk < n_items) {
+      it = lds_item(items + (size_t)gk * sizeof(WorkItem));
+      ++gk;
+      if (it.kind == kItemBlock) {
+        found = true;
+        break;
+      }
+    }
+    if (lane < kWaves) {
+      int2* out = rbuf + ((size_t)lane * kRunBufs + gb) * kRunCap;
+      int n = 0;
+      auto put = [&](int x, int cnt) {
+        lds_store_b64(out + n, make_int2(x, cnt));
+        ++n;
+      };
+      if (found) block_runs(it.blk, it.g, it.tile0, it.ntile, lane, D, (it.flags >> kItemLgNgShift) & 3, put);
+      else put(0, kSentinelRun);
+      put(0, 0);
+    }
+    gb = (gb + 1) % kRunBufs;
   }
 };
 
@@ -360,8 +442,8 @@ constexpr int up_col_blocks() {
 // ---------------------------------------------------------------------------
 template <int D, int MAX_RT, int NSLOT>
 __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
-                                           FragRing<D, NSLOT>& fr, GroupAcc<up_col_blocks<D>()>& acc,
-                                           const int tid) {
+                                           FragRing<D, NSLOT>& fr, RunDeriver<D>& rd,
+                                           GroupAcc<up_col_blocks<D>()>& acc, const int tid) {
   constexpr int NK = D / 16;
   constexpr int kORed = 4;  // partial-output slots of the up-projection reduction
   const BlockMeta& bm = it.blk;
@@ -406,6 +488,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
           a.q + ((int64_t)(c / G) * a.H_q + g * G + c % G) * D + 8 * (pos ^ (cl % kRowChunks));
       lds_dma16(src, qimg_lds + f * 1024);
     }
+    if (wave == 0) rd.derive(lane);  // the runs of the block item two ahead, while the rows load
     wait_vmcnt<0>();
     lds_barrier();
   }
@@ -705,23 +788,6 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   }
 }
 
-// a work item read from LDS into wave-uniform registers
-__device__ __forceinline__ WorkItem lds_item(const unsigned char* p) {
-  static_assert(sizeof(WorkItem) % 16 == 0, "work items are whole 16-byte chunks");
-  int32_t w[sizeof(WorkItem) / 4];
-#pragma unroll
-  for (int i = 0; i < (int)sizeof(WorkItem) / 16; ++i) {
-    const int4 v = prog_read_b128(p + 16 * i);
-    w[4 * i + 0] = __builtin_amdgcn_readfirstlane(v.x);
-    w[4 * i + 1] = __builtin_amdgcn_readfirstlane(v.y);
-    w[4 * i + 2] = __builtin_amdgcn_readfirstlane(v.z);
-    w[4 * i + 3] = __builtin_amdgcn_readfirstlane(v.w);
-  }
-  WorkItem it;
-  __builtin_memcpy(&it, w, sizeof(WorkItem));
-  return it;
-}
-
 template <int D, int MAX_RT, int NSLOT>
 __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -734,7 +800,6 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   }
   lds_barrier();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int run_off = a.wg[blockIdx.x].run_off[wave];  // scalar load at a wave-uniform index
   unsigned char* work = smem + a.prog_bytes;
   FragRing<D, NSLOT> fr;
   GroupAcc<up_col_blocks<D>()> acc;
@@ -742,7 +807,18 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   fr.lane8 = (threadIdx.x & 63) * 8;
   fr.ring = reinterpret_cast<__bf16*>(work + a.ring_offset) + (size_t)wave * NSLOT * kFragElems;
   fr.ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(fr.ring));
-  fr.run = reinterpret_cast<const int2*>(smem + run_off);
+  RunDeriver<D> rd;
+  rd.items = smem;
+  rd.n_items = p.n_items;
+  rd.gk = 0;
+  rd.gb = 0;
+  rd.rbuf = reinterpret_cast<int2*>(smem + (size_t)p.n_items * sizeof(WorkItem));
+  if (wave == 0) {
+    rd.derive(threadIdx.x & 63);
+    rd.derive(threadIdx.x & 63);
+  }
+  lds_barrier();
+  fr.rbuf = rd.rbuf + (size_t)wave * kRunBufs * kRunCap;
   fr.start();
   for (int k = 0; k < p.n_items; ++k) {
     const WorkItem it = lds_item(smem + (size_t)k * sizeof(WorkItem));
@@ -751,7 +827,7 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
     // lane-dependent address of one item kind stays live across the other
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
-    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT>(a, it, work, fr, acc, tid);
+    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT>(a, it, work, fr, rd, acc, tid);
     else if (it.kind == kItemTail) tail_item<D>(a, it, work, tid);
   }
   if constexpr (NSLOT > 0) wait_vmcnt<0>();  // no LDS write may land after the workgroup ends

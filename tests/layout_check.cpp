@@ -4,6 +4,8 @@
 // (fragment, lane, element) maps inside the padded block.
 #include <cstdio>
 #include <cstdlib>
+#include <string>
+#include <utility>
 #include <vector>
 
 #include "milo_internal.h"
@@ -52,8 +54,79 @@ static int check(int kind, int T, int r, int n_kv, int d) {
   return 0;
 }
 
+// The fragment runs every wave derives for one whole block (block_runs):
+// over the eight waves, each fragment of P^K, P^V and of head g's slices of
+// R^K and R^V is read the expected number of times (once; R^V once per wave
+// sharing a 16-dim slice), and each wave's run lengths match what the kernel
+// consumes per phase.
+static int check_runs(int T, int rk, int rv, int n_kv, int d) {
+  const int T_pad = (T + kTile - 1) / kTile * kTile;
+  BlockMeta bm{};
+  bm.T = T;
+  bm.T_pad = T_pad;
+  bm.rk_pad = (rk + 31) / 32 * 32;
+  bm.rv_pad = (rv + 31) / 32 * 32;
+  const long long n_pk = (long long)T_pad * bm.rk_pad / kFragElems, n_pv = (long long)T_pad * bm.rv_pad / kFragElems;
+  const long long n_rk = (long long)bm.rk_pad * n_kv * d / kFragElems, n_rv = (long long)bm.rv_pad * n_kv * d / kFragElems;
+  bm.off_pk = 0;
+  bm.off_rk = n_pk * kFragElems;
+  bm.off_pv = (n_pk + n_rk) * kFragElems;
+  bm.off_rv = (n_pk + n_rk + n_pv) * kFragElems;
+  const long long total = n_pk + n_rk + n_pv + n_rv;
+  const int ntile = T_pad / kTile, nds = d / 16;
+  const int lg_ng = lg_rank_groups(bm.rv_pad / 32);
+  for (int g = 0; g < n_kv; ++g) {
+    std::vector<int> seen((size_t)total, 0);
+    for (int w = 0; w < kWaves; ++w) {
+      std::vector<std::pair<int, int>> runs;
+      block_runs(bm, g, 0, ntile, w, d, lg_ng, [&](int x, int n) { runs.push_back({x, n}); });
+      for (auto& r : runs)
+        for (int k = 0; k < r.second; ++k) {
+          if (r.first + k < 0 || r.first + k >= total) {
+            std::printf("runs: fragment %d outside the block\n", r.first + k);
+            return 1;
+          }
+          seen[(size_t)(r.first + k)]++;
+        }
+      // per-phase lengths the kernel takes
+      const int nrt_k = bm.rk_pad / 32, nrt_v = bm.rv_pad / 32, nseg = v_segments(nrt_v), ng = kWaves / nseg;
+      const int own_k = owned_tiles(nrt_k, w, kWaves), own_v = owned_tiles(nrt_v, w % ng, ng);
+      size_t i = 0;
+      if (own_k > 0 && (runs[i++].second != d / 16 * own_k)) { std::printf("runs: R^K length\n"); return 1; }
+      for (int t = 0; t < ntile; ++t) {
+        if (runs[i++].second != bm.rk_pad / 16) { std::printf("runs: P^K length\n"); return 1; }
+        if (own_v > 0 && runs[i++].second != kTile / 16 / nseg * own_v) { std::printf("runs: P^V length\n"); return 1; }
+      }
+      if (runs[i++].second != bm.rv_pad / 32 || i != runs.size()) { std::printf("runs: R^V / count\n"); return 1; }
+      if ((int)runs.size() > kRunCap - 1) { std::printf("runs: more than the run buffer holds\n"); return 1; }
+    }
+    for (long long f = 0; f < total; ++f) {
+      int want = 0;
+      if (f < n_pk) want = 1;
+      else if (f < n_pk + n_rk) want = (f - n_pk) / (n_rk / n_kv) == g;
+      else if (f < n_pk + n_rk + n_pv) want = 1;
+      else want = (f - n_pk - n_rk - n_pv) / (n_rv / n_kv) == g ? kWaves / nds : 0;
+      if (seen[(size_t)f] != want) {
+        std::printf("runs: head %d fragment %lld read %d times, want %d\n", g, f, seen[(size_t)f], want);
+        return 1;
+      }
+    }
+  }
+  return 0;
+}
+
 int main(int argc, char** argv) {
-  // argv: groups of (T, r, n_kv, d)
+  // argv: groups of (T, r, n_kv, d); with --runs first: groups of (T, rk, rv, n_kv, d)
+  if (argc > 1 && std::string(argv[1]) == "--runs") {
+    int bad = 0, n = 0;
+    for (int i = 2; i + 4 < argc; i += 5) {
+      bad |= check_runs(std::atoi(argv[i]), std::atoi(argv[i + 1]), std::atoi(argv[i + 2]), std::atoi(argv[i + 3]),
+                        std::atoi(argv[i + 4]));
+      ++n;
+    }
+    std::printf("%s (%d geometries)\n", bad ? "FAIL" : "OK", n);
+    return bad;
+  }
   int bad = 0, n = 0;
   for (int i = 1; i + 3 < argc; i += 4) {
     const int T = std::atoi(argv[i]), r = std::atoi(argv[i + 1]), nkv = std::atoi(argv[i + 2]),

@@ -32,3 +32,24 @@ def test_fragment_layout_is_a_bijection(checker):
     res = subprocess.run([checker, *args], capture_output=True, text=True)
     assert res.returncode == 0, res.stdout + res.stderr
     assert res.stdout.startswith("OK")
+
+
+# (T, rank_k, rank_v, KV heads, head dim): ragged tokens, K/V ranks that
+# differ, every token-segment split of the value pass, ranks beyond 512
+RUN_GEOMS = [
+    (1, 1, 1, 1, 64), (45, 33, 17, 3, 64), (256, 64, 64, 2, 128), (300, 100, 257, 4, 128),
+    (1024, 288, 288, 4, 128), (700, 96, 32, 2, 64), (1000, 896, 840, 8, 128), (2048, 512, 512, 8, 128),
+    (513, 160, 224, 1, 64), (256, 32, 32, 2, 64), (512, 64, 128, 2, 64), (768, 288, 384, 4, 128),
+    (1024, 768, 704, 8, 128),
+]
+
+
+def test_derived_fragment_runs_cover_each_block_once(checker):
+    """The runs each wave derives for a block item (block_runs) read every
+    P^K / P^V fragment once over the eight waves and every fragment of the
+    item's head slices of R^K once and of R^V once per wave sharing its
+    16-dim slice, with per-phase run lengths equal to what the kernel takes."""
+    args = [str(x) for g in RUN_GEOMS for x in g]
+    res = subprocess.run([checker, "--runs", *args], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert res.stdout.startswith("OK")
