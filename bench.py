@@ -127,8 +127,11 @@ def calibrate_copy(dev, n_bytes=1 << 30, reps=5):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 500 for a single-layer workload, else 10)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps first (default 200 for a single-layer workload, else 2); the "
+                         "kernels reach their steady-state speed after ~100 back-to-back steps")
     ap.add_argument("--config", default="q7b_1l", choices=sorted(synth.CONFIGS))
     ap.add_argument("--rotate-bytes", type=float, default=512e6,
                     help="minimum bytes of distinct layer copies rotated over (defeats the Infinity Cache)")
@@ -155,6 +158,10 @@ def main():
     milo.lib()
 
     cfg = synth.CONFIGS[args.config]
+    if args.steps is None:
+        args.steps = 500 if cfg.n_layers == 1 else 10
+    if args.warmup is None:
+        args.warmup = 200 if cfg.n_layers == 1 else 2
     # layers are generated one at a time and only their device state is kept
     # (a 64-layer workload's host factors would not fit next to each other)
     x0 = None
