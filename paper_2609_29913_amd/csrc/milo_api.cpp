@@ -151,6 +151,7 @@ struct Schedule {
   std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs
   int n_launch = 0, n_parts = 0, prog_bytes = 0, rk_pad_max = 32, rv_pad_max = 32, max_own = 1;
   int n_block_slots = 0;  // block-group slots of the busiest (KV head, column tile)
+  bool half_w = false;    // the weight tile in 128-token halves (LDS is short)
   int64_t count_off = 0;  // byte offset of the int32 [H_kv][n_ct] slot counts in `bytes`
 };
 
@@ -294,14 +295,26 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
   // into one partial where the kernel keeps that partial in registers (at most
   // two latent rank tiles per wave)
   const bool fold = out->max_own <= 2;
-  // LDS left for the program: all that the projected query, weight tile and
-  // a 6-slot fragment ring leave (fewer launches would cost the ring), or all
-  // but the first two when even a short program leaves no room for the ring
-  const size_t base = attend_lds_base_bytes(c.d, out->rk_pad_max, out->rv_pad_max);
-  const size_t ring6 = attend_ring_bytes(6);
+  // LDS plan: the projected query, weight tile and a 6-slot fragment ring,
+  // the rest for the program (fewer launches would cost the ring); when even a
+  // short program leaves no room for that (ranks above 512), the weight tile
+  // in two 128-token halves and a 4-slot ring; failing that, no ring
   const size_t short_prog = 16 * sizeof(WorkItem) + (size_t)kWaves * kRunBufs * kRunCap * sizeof(int2);
-  const size_t room = base < (size_t)kLdsBytes ? kLdsBytes - base : 0;
-  const size_t cap = room >= ring6 + short_prog ? room - ring6 : room;
+  auto room_for = [&](bool half_w) {
+    const size_t b = attend_lds_base_bytes(c.d, out->rk_pad_max, out->rv_pad_max, half_w);
+    return b < (size_t)kLdsBytes ? kLdsBytes - b : 0;
+  };
+  size_t cap;
+  if (room_for(false) >= attend_ring_bytes(6) + short_prog) {
+    out->half_w = false;
+    cap = room_for(false) - attend_ring_bytes(6);
+  } else if (room_for(true) >= attend_ring_bytes(4) + short_prog) {
+    out->half_w = true;
+    cap = room_for(true) - attend_ring_bytes(4);
+  } else {
+    out->half_w = false;
+    cap = room_for(false);
+  }
   for (int L = 1; L <= (1 << 20); L *= 2) {
     std::vector<std::vector<unsigned char>> progs((size_t)L * kCUs);
     std::vector<WgProgram> entries((size_t)L * kCUs);
@@ -610,12 +623,20 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     const int err = build_schedule(*c, block_table, n_sel, tl, n_ct, &sch);
     if (err != MILO_OK) return err;
     const int max_rt = sch.max_own <= 2 ? 2 : 4;
-    // deepest fragment ring that fits next to the program, projected query and weight tile
-    const size_t base = attend_lds_base_bytes(c->d, sch.rk_pad_max, sch.rv_pad_max);
+    // deepest fragment ring that fits next to the program, projected query and
+    // weight tile (4 slots go with the half weight tile)
+    const size_t base = attend_lds_base_bytes(c->d, sch.rk_pad_max, sch.rv_pad_max, sch.half_w);
     const size_t prog = (size_t)sch.prog_bytes;
     int nslot = 0;
-    for (int cand : {8, 6})
-      if (prog + base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
+    if (sch.half_w) {
+      // the program was sized to leave room for this ring
+      if (prog + base + attend_ring_bytes(4) > (size_t)kLdsBytes)
+        return fail(MILO_ERR_UNSUPPORTED, "work schedule does not fit in LDS");
+      nslot = 4;
+    } else {
+      for (int cand : {8, 6})
+        if (prog + base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
+    }
     // device buffers
     const int64_t plan_bytes = (int64_t)sch.bytes.size();
     if (plan_bytes > c->plan_cap) {

@@ -315,7 +315,7 @@ hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_
                         hipEvent_t e1 = nullptr);
 // LDS of the attention kernel: a base region (projected query, weight tile and
 // reductions, or the tail item's buffers) followed by kWaves rings of nslot fragments.
-size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max);
+size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max, bool half_w);
 size_t attend_ring_bytes(int nslot);
 
 }  // namespace milo

@@ -440,7 +440,7 @@ constexpr int up_col_blocks() {
 // LDS at its start.  Every loop is software-pipelined: the operands of step
 // k+1 are read while the MFMAs of step k run.
 // ---------------------------------------------------------------------------
-template <int D, int MAX_RT, int NSLOT>
+template <int D, int MAX_RT, int NSLOT, bool WH>
 __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
                                            FragRing<D, NSLOT>& fr, RunDeriver<D>& rd,
                                            GroupAcc<up_col_blocks<D>()>& acc, const int tid) {
@@ -463,8 +463,11 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   const int T = bm.T;
   const int ntiles = it.ntile, tile0 = it.tile0;  // tiles this item covers
   __bf16* qt = reinterpret_cast<__bf16*>(smem);              // [kCols][qsd]
-  __bf16* wl = qt + kCols * qsd;                               // [kCols][kWStride]
-  float* red = reinterpret_cast<float*>(wl + kCols * kWStride);  // [kWaves][kCols]
+  // the weight tile: [kCols][kWS] bf16, all 256 tokens of a tile, or (WH) one
+  // 128-token half at a time when LDS is short (ranks above 512)
+  constexpr int kWS = WH ? kTile / 2 + 8 : kWStride;
+  __bf16* wl = qt + kCols * qsd;                          // [kCols][kWS]
+  float* red = reinterpret_cast<float*>(wl + kCols * kWS);  // [kWaves][kCols]
   // the wave's next fragment; the order of take() calls below is the order of
   // the wave's runs: R^K (waves that own projection rank tiles), then per tile
   // P^K and P^V, then R^V
@@ -537,8 +540,9 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   float l_run[2] = {0.f, 0.f};
   const __bf16* qr0 = qt + lrow * qsd + 8 * lhi;
   const __bf16* qr1 = qt + (32 + lrow) * qsd + 8 * lhi;
-  const __bf16* wr0 = wl + lrow * kWStride + 8 * lhi + 16 * nst * sg;
-  const __bf16* wr1 = wl + (32 + lrow) * kWStride + 8 * lhi + 16 * nst * sg;
+  // weight operand rows of the wave's segment (relative step st at 16 st)
+  const __bf16* wr0 = wl + lrow * kWS + 8 * lhi + 16 * nst * sg;
+  const __bf16* wr1 = wl + (32 + lrow) * kWS + 8 * lhi + 16 * nst * sg;
 
   for (int tt = 0; tt < ntiles; ++tt) {
     const int tw = (tile0 + tt) * kTile + wave * kTokWave;
@@ -591,45 +595,43 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       alpha[ch] = fast_exp2(m_run[ch] - mn);
       m_run[ch] = mn;
     }
-    // weights -> LDS as [col][token] bf16
+    // weights W = 2^(s - m) (bf16) in registers, then to LDS as [col][token]
+    bf16x4 wv[2][4];
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
       float lsum = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        bf16x4 w4;
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const float w = fast_exp2(sc[ch][4 * j + u] - m_run[ch]);
           lsum += w;
-          w4[u] = (__bf16)w;
+          wv[ch][j][u] = (__bf16)w;
         }
-        *reinterpret_cast<bf16x4*>(wl + (32 * ch + lrow) * kWStride + wave * kTokWave + 8 * j + 4 * lhi) = w4;
-      }
       l_run[ch] = l_run[ch] * alpha[ch] + lsum;
     }
-    lds_barrier();
-    // rescale the latent accumulators to the new running maximum; skipped on
-    // the first tile (they are zero) and when no column's maximum moved
-    if (tt > 0 && own_v > 0 && __any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+    auto write_w = [&]() {
+      const int tcol = (WH ? (wave & 3) : wave) * kTokWave;  // the wave's tokens in the (half) tile
 #pragma unroll
-      for (int r = 0; r < MAX_RT; ++r)
-        if (r < own_v) {
-          oacc[r][0] *= alpha[0];
-          oacc[r][1] *= alpha[1];
-        }
-    }
-    if (own_v > 0) {
+      for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<bf16x4*>(wl + (32 * ch + lrow) * kWS + tcol + 8 * j + 4 * lhi) = wv[ch][j];
+    };
+    // latent V over the wave's relative steps [lo, hi) (even bounds), weights
+    // of relative step st at w0p / w1p + 16 st
+    auto vpass = [&](int lo, int hi, const __bf16* w0p, const __bf16* w1p) {
+      if (own_v <= 0 || lo >= hi) return;
       // operands of 16-token step st: w0/w1 (weight column tiles), pa[r] (P^V rank
-      // tiles); nst is even (at most 8 segments), so the loop runs over step pairs
+      // tiles); the loop runs over step pairs
       bf16x8 pa[MAX_RT], pc[MAX_RT];
-      bf16x8 w0 = ld_bf16x8(wr0), w1 = ld_bf16x8(wr1);
+      bf16x8 w0 = ld_bf16x8(w0p + 16 * lo), w1 = ld_bf16x8(w1p + 16 * lo);
 #pragma unroll
       for (int r = 0; r < MAX_RT; ++r)
         if (r < own_v) pa[r] = take();
-      for (int st = 0; st < nst; st += 2) {
-        const bf16x8 x0 = ld_bf16x8(wr0 + 16 * (st + 1));
-        const bf16x8 x1 = ld_bf16x8(wr1 + 16 * (st + 1));
+      for (int st = lo; st < hi; st += 2) {
+        const bf16x8 x0 = ld_bf16x8(w0p + 16 * (st + 1));
+        const bf16x8 x1 = ld_bf16x8(w1p + 16 * (st + 1));
 #pragma unroll
         for (int r = 0; r < MAX_RT; ++r)
           if (r < own_v) pc[r] = take();
@@ -639,9 +641,9 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
             oacc[r][0] = mfma32(pa[r], w0, oacc[r][0]);
             oacc[r][1] = mfma32(pa[r], w1, oacc[r][1]);
           }
-        if (st + 2 < nst) {
-          w0 = ld_bf16x8(wr0 + 16 * (st + 2));
-          w1 = ld_bf16x8(wr1 + 16 * (st + 2));
+        if (st + 2 < hi) {
+          w0 = ld_bf16x8(w0p + 16 * (st + 2));
+          w1 = ld_bf16x8(w1p + 16 * (st + 2));
 #pragma unroll
           for (int r = 0; r < MAX_RT; ++r)
             if (r < own_v) pa[r] = take();
@@ -653,6 +655,35 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
             oacc[r][1] = mfma32(pc[r], x1, oacc[r][1]);
           }
       }
+    };
+    auto rescale = [&]() {
+      // rescale the latent accumulators to the new running maximum; skipped on
+      // the first tile (they are zero) and when no column's maximum moved
+      if (tt > 0 && own_v > 0 && __any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+#pragma unroll
+        for (int r = 0; r < MAX_RT; ++r)
+          if (r < own_v) {
+            oacc[r][0] *= alpha[0];
+            oacc[r][1] *= alpha[1];
+          }
+      }
+    };
+    if constexpr (!WH) {
+      write_w();
+      lds_barrier();
+      rescale();
+      vpass(0, nst, wr0, wr1);
+    } else {
+      // half h holds the tokens of waves 4h .. 4h+3, i.e. tile steps [8h, 8h + 8);
+      // the wave's segment covers tile steps [nst sg, nst sg + nst)
+      if (wave < 4) write_w();
+      lds_barrier();
+      rescale();
+      vpass(0, min(nst, 8 - nst * sg), wr0, wr1);
+      lds_barrier();  // every wave is done with the first half's weights
+      if (wave >= 4) write_w();
+      lds_barrier();
+      vpass(max(0, 8 - nst * sg), nst, wr0 - 16 * 8, wr1 - 16 * 8);
     }
   }
 
@@ -788,7 +819,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   }
 }
 
-template <int D, int MAX_RT, int NSLOT>
+template <int D, int MAX_RT, int NSLOT, bool WH>
 __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const WgProgram p = a.wg[blockIdx.x];
@@ -827,7 +858,7 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
     // lane-dependent address of one item kind stays live across the other
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
-    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT>(a, it, work, fr, rd, acc, tid);
+    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT, WH>(a, it, work, fr, rd, acc, tid);
     else if (it.kind == kItemTail) tail_item<D>(a, it, work, tid);
   }
   if constexpr (NSLOT > 0) wait_vmcnt<0>();  // no LDS write may land after the workgroup ends
@@ -931,9 +962,10 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max) {
+size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max, bool half_w) {
   const size_t qsd = (size_t)rk_pad_max + 8;
-  const size_t loop = kCols * qsd * 2 + (size_t)kCols * kWStride * 2 + (size_t)kWaves * kCols * 4;
+  const size_t ws = half_w ? kTile / 2 + 8 : kWStride;
+  const size_t loop = kCols * qsd * 2 + (size_t)kCols * ws * 2 + (size_t)kWaves * kCols * 4;
   // up-projection: the latent accumulator as bf16 [col][rank], or the segment
   // partials being combined (at most 4 slots x 3 rank tiles x 8 KiB), then the
   // per-wave column sums at the end of the region
@@ -948,27 +980,30 @@ size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max) {
 
 size_t attend_ring_bytes(int nslot) { return (size_t)kWaves * nslot * kFragElems * 2; }
 
-template <int D, int MAX_RT, int NSLOT>
+template <int D, int MAX_RT, int NSLOT, bool WH>
 static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                                   hipEvent_t e1) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_kernel<D, MAX_RT, NSLOT>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_kernel<D, MAX_RT, NSLOT, WH>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipExtLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT>), dim3(grid), dim3(kThreads), (uint32_t)lds, s, e0, e1, 0, a);
+  hipExtLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT, WH>), dim3(grid), dim3(kThreads), (uint32_t)lds, s, e0, e1, 0,
+                        a);
   return hipGetLastError();
 }
 
+// ring slots 8 / 6 / none with the whole weight tile; 4 with the half tile
 template <int D, int MAX_RT>
 static hipError_t launch_attend_r(const AttendArgs& a, int nslot, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                                   hipEvent_t e1) {
   switch (nslot) {
-    case 8: return launch_attend_t<D, MAX_RT, 8>(a, grid, lds, s, e0, e1);
-    case 6: return launch_attend_t<D, MAX_RT, 6>(a, grid, lds, s, e0, e1);
-    case 0: return launch_attend_t<D, MAX_RT, 0>(a, grid, lds, s, e0, e1);
+    case 8: return launch_attend_t<D, MAX_RT, 8, false>(a, grid, lds, s, e0, e1);
+    case 6: return launch_attend_t<D, MAX_RT, 6, false>(a, grid, lds, s, e0, e1);
+    case 4: return launch_attend_t<D, MAX_RT, 4, true>(a, grid, lds, s, e0, e1);
+    case 0: return launch_attend_t<D, MAX_RT, 0, false>(a, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
