@@ -568,17 +568,22 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       }
     }
     f32x16 sc[2] = {s0, s1};
-    // mask tokens past the end of the block, wave-local column max
+    // mask tokens past the end of the block (only the block's last tile can
+    // hold any; the test is wave-uniform), wave-local column max
     float mx[2] = {-INFINITY, -INFINITY};
+    if (tw + kTokWave > T) {
+#pragma unroll
+      for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int tok = tw + 8 * (v >> 2) + 4 * lhi + (v & 3);
+          if (tok >= T) sc[ch][v] = -INFINITY;
+        }
+    }
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int tok = tw + 8 * (v >> 2) + 4 * lhi + (v & 3);
-        const float x = tok < T ? sc[ch][v] : -INFINITY;
-        sc[ch][v] = x;
-        mx[ch] = fmaxf(mx[ch], x);
-      }
+      for (int v = 0; v < 16; ++v) mx[ch] = fmaxf(mx[ch], sc[ch][v]);
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
       mx[ch] = fmaxf(mx[ch], __shfl_xor(mx[ch], 32));
