@@ -12,7 +12,9 @@ the 256 MB Infinity Cache, so steps rotate over independent copies of the layer
 (each with its own cache, queries and tails) until the rotation exceeds 512 MB.
 
 Prints one JSON line (see the fields below).  --gpus above 1 is rejected: this
-path runs on one GPU.
+path runs on one GPU.  --prefill N measures instead the causal prefill of one
+request's chunk of N tokens (milo_attend_prefill) on the workload's first layer,
+after the workload's tail length of earlier tokens, and prints one JSON line for it.
 """
 from __future__ import annotations
 
@@ -88,6 +90,90 @@ class Layer:
                                 self.out, stream=stream)
 
 
+class PrefillLayer(Layer):
+    """A layer's cache plus one request's chunk of n_tok query tokens and its one
+    shared tail (tail_base earlier rows, then the chunk's own rows)."""
+
+    def __init__(self, inp: synth.LayerInputs, dev, n_tok: int, tail_base: int, seed: int):
+        super().__init__(inp, dev)
+        import torch
+        rng = np.random.Generator(np.random.Philox(key=[0x50524546, seed]))
+        D = inp.n_kv_heads * inp.head_dim
+        q = synth.f32_to_bf16(rng.standard_normal((n_tok, inp.n_q_heads, inp.head_dim), dtype=np.float32))
+        rows = tail_base + n_tok
+        tk = synth.f32_to_bf16(rng.standard_normal((rows, inp.n_kv_heads, inp.head_dim), dtype=np.float32))
+        tv = synth.f32_to_bf16(rng.standard_normal((rows, inp.n_kv_heads, inp.head_dim), dtype=np.float32))
+        self.q, self.tk, self.tv = to_device(q, dev), to_device(tk, dev), to_device(tv, dev)
+        self.out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+        self.tail_base = tail_base
+        self.bytes = (2 * int(sum((t + D) * (a + b) for t, a, b in zip(inp.block_tokens, inp.rank_k, inp.rank_v)))
+                      + 4 * rows * D + 2 * q.size)
+        self.flops = (sum(2 * n_tok * inp.n_q_heads * (int(a) + int(b)) * (int(t) + inp.head_dim)
+                          for t, a, b in zip(inp.block_tokens, inp.rank_k, inp.rank_v))
+                      + 4 * inp.n_q_heads * inp.head_dim * sum(tail_base + j + 1 for j in range(n_tok)))
+        self.ctx_tokens = sum(int(inp.block_tokens.sum()) + tail_base + j + 1 for j in range(n_tok))
+
+    def step(self, stream):
+        from paper_2609_29913_amd import milo
+        milo.milo_attend_prefill(self.cache, self.table, self.q, self.tk, self.tv, self.tail_base, self.scale,
+                                 self.out, stream=stream)
+
+
+def run_prefill(args, cfg, dev):
+    """Time the causal prefill of one chunk of args.prefill tokens (see the module text)."""
+    import torch
+    from paper_2609_29913_amd import milo
+    x = synth.gen_layer(cfg, 0)
+    tail_base = int(x.tail_len.max())
+    first = PrefillLayer(x, dev, args.prefill, tail_base, 0)
+    copies = max(1, int(np.ceil(args.rotate_bytes / first.bytes)))
+    layers = [first] + [PrefillLayer(x, dev, args.prefill, tail_base, k) for k in range(1, copies)]
+    stream = torch.cuda.current_stream()
+    for k in range(args.warmup):
+        layers[k % copies].step(stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        layers[k % copies].step(stream)
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    milo.milo_timing_enable(True)
+    for k in range(args.steps):
+        layers[k % copies].step(stream)
+    torch.cuda.synchronize()
+    att_ms, merge_ms, n_calls = milo.milo_timing_read()
+    milo.milo_timing_enable(False)
+    att_s = att_ms / n_calls * 1e-3
+    kern_bytes = first.bytes  # the attention kernel reads every factor, the tail and the queries once
+    flops = first.flops
+    bound = "hbm" if flops / kern_bytes < MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
+    gbs, tfs = kern_bytes / att_s / 1e9, flops / att_s / 1e12
+    result = {
+        "metric": "effective context tokens/s per prefill chunk (1 GPU) + % of HBM roofline",
+        "value": first.ctx_tokens / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) factors / N(0,1/r) R, queries and tail, bf16)",
+        "config": {"workload": f"{cfg.name}_prefill{args.prefill}", "mode": "prefill",
+                   "chunk_tokens": args.prefill, "tail_rows_before_chunk": tail_base,
+                   "context_tokens": int(x.block_tokens.sum()), "blocks": x.n_blocks, "q_heads": x.n_q_heads,
+                   "kv_heads": x.n_kv_heads, "head_dim": x.head_dim, "rotated_copies": copies},
+        "roofline": {"bound": bound, "achieved": gbs if bound == "hbm" else tfs,
+                     "peak": HBM_PEAK_GBS if bound == "hbm" else MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+                     "frac": gbs / HBM_PEAK_GBS if bound == "hbm" else tfs / MFMA_BF16_PEAK_TFLOPS,
+                     "traffic": None, "arithmetic_intensity_flop_per_byte": flops / kern_bytes,
+                     "kernel": "attend_kernel", "kernel_avg_us": att_s * 1e6,
+                     "merge_kernel_avg_us": merge_ms / n_calls * 1e3, "algorithmic_bytes_per_launch": kern_bytes,
+                     "hbm_gbs": gbs, "mfma_tflops": tfs, "mfma_frac": tfs / MFMA_BF16_PEAK_TFLOPS,
+                     "kernel_source_sha256_16": kernel_source_hash()},
+        "cpu_baseline": None,
+    }
+    for layer in layers:
+        milo.milo_cache_free(layer.cache)
+    print(json.dumps(result), flush=True)
+
+
 def cpu_baseline(inp: synth.LayerInputs, n_layers: int, budget_s: float):
     """The CPU oracle (fp64 numpy, latent order) timed on this host on the same
     workload: whole layer steps repeated until ~budget_s of CPU work."""
@@ -138,6 +224,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true", help="only run a 1 GiB device copy (counter scaling)")
+    ap.add_argument("--prefill", type=int, default=0, metavar="N",
+                    help="time the causal prefill of an N-token chunk of one request instead (first layer)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -162,6 +250,9 @@ def main():
         args.steps = 500 if cfg.n_layers == 1 else 10
     if args.warmup is None:
         args.warmup = 200 if cfg.n_layers == 1 else 2
+    if args.prefill > 0:
+        run_prefill(args, cfg, dev)
+        return
     # layers are generated one at a time and only their device state is kept
     # (a 64-layer workload's host factors would not fit next to each other)
     x0 = None

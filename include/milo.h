@@ -112,6 +112,27 @@ int milo_attend_decode(milo_cache* cache, const int32_t* block_table, int32_t n_
                        const int32_t* tail_len, int32_t tail_cap, float scale, float* out,
                        void* hip_stream);
 
+/* Prefill of one request: a chunk of n_tok consecutive query tokens attends to
+ * the selected blocks plus the request's dense tail, causally among its own
+ * tokens (Alg. 1 inference stage with a multi-token input query Q; Eq. 1).
+ * Token j (0-based) sees the blocks and tail rows [0, tail_base + j + 1): the
+ * tail_base rows that precede the chunk and the chunk's own first j + 1 tokens,
+ * whose keys and values the caller has stored at rows tail_base ..
+ * tail_base + n_tok - 1.
+ *   n_tok         tokens in the chunk, >= 1.
+ *   q             device bf16 [n_tok][H_q][d].
+ *   tail_k/v      device bf16 [tail_cap][H_kv][d], one tail read by every token.
+ *   tail_base     rows of the tail before the chunk, >= 0; tail_base + n_tok <= tail_cap.
+ *   out           device fp32 [n_tok][H_q][d], fully overwritten.
+ * cache, block_table, n_sel, n_q_heads, scale, hip_stream, ownership and errors
+ * as for milo_attend_decode (the work is that of a decode step whose n_tok
+ * requests share one tail with lengths tail_base + 1 .. tail_base + n_tok). */
+int milo_attend_prefill(milo_cache* cache, const int32_t* block_table, int32_t n_sel,
+                        int32_t n_tok, int32_t n_q_heads, const uint16_t* q,
+                        const uint16_t* tail_k, const uint16_t* tail_v,
+                        int32_t tail_base, int32_t tail_cap, float scale, float* out,
+                        void* hip_stream);
+
 /* Release the cache and its device memory (synchronises the device first).
  * NULL is accepted and ignored. */
 void milo_cache_free(milo_cache* cache);

@@ -18,6 +18,9 @@ What it computes (the method's result, written out plainly in fp64):
 * Query head h reads KV head g = floor(h / G), G = H_q / H_kv.
 
 `attend_dense` is that definition: rebuild K and V, then softmax attention.
+`attend_prefill` is the same definition for a multi-token input query of one
+request whose tokens attend causally among themselves (a chunk of new tokens
+sharing one tail).
 `attend_latent` reaches the same numbers by exact reassociation,
 q.(P R)_t = P_t.(R q) and sum_t w_t (P R)_t = (sum_t w_t P_t) R, which is the
 order the GPU path follows: project the query per block, score against P^K
@@ -30,7 +33,7 @@ from __future__ import annotations
 
 import numpy as np
 
-__all__ = ["attend_dense", "attend_latent", "reconstruct"]
+__all__ = ["attend_dense", "attend_latent", "attend_prefill", "reconstruct"]
 
 
 def reconstruct(p: np.ndarray, r: np.ndarray) -> np.ndarray:
@@ -154,3 +157,19 @@ def attend_latent(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale,
     if all_cols:
         out = out.reshape(n_q, n_q_heads, d)
     return (out, weights) if return_weights else out
+
+
+def attend_prefill(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_base, scale):
+    """Causal prefill of one request (Alg. 1 inference stage with a multi-token
+    input query Q, Eq. 1 with the causal mask of an autoregressive model over
+    Q's own tokens): token j of the chunk q [n_tok, H_q, d] attends to the
+    selected blocks and to the first tail_base + j + 1 rows of the one tail
+    tail_k / tail_v [tail_cap, H_kv, d] (the rows before the chunk, then the
+    chunk's own tokens up to and including j).  Returns [n_tok, H_q, d]."""
+    n_tok = q.shape[0]
+    if tail_base + n_tok > tail_k.shape[0]:
+        raise ValueError("the tail must hold tail_base + n_tok rows")
+    tk = np.broadcast_to(tail_k, (n_tok,) + tail_k.shape)
+    tv = np.broadcast_to(tail_v, (n_tok,) + tail_v.shape)
+    tail_len = tail_base + 1 + np.arange(n_tok)
+    return attend_dense(pk, rk, pv, rv, table, q, tk, tv, tail_len, scale)

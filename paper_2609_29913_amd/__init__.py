@@ -5,6 +5,6 @@ declared in include/milo.h); `milo` is a thin ctypes binding with the same
 entry-point names.
 """
 from . import milo  # noqa: F401
-from .milo import (MiloError, lib, milo_attend_decode, milo_cache_create,  # noqa: F401
+from .milo import (MiloError, lib, milo_attend_decode, milo_attend_prefill, milo_cache_create,  # noqa: F401
                    milo_cache_device_bytes, milo_cache_free, milo_cache_read_factor,
                    milo_last_error, milo_timing_enable, milo_timing_read)

@@ -562,10 +562,12 @@ int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which
   return MILO_OK;
 }
 
-int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_q, int32_t n_q_heads,
-                       const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
-                       int32_t tail_cap, float scale, float* out, void* hip_stream) {
-  g_err.clear();
+// Attention of n_q query tokens over the selected blocks plus their dense tails:
+// query i reads tail rows [i * tail_stride, i * tail_stride + tail_len[i]) of
+// tail_k / tail_v (tail_stride = tail_cap: one tail per request; 0: one shared tail).
+static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_q, int32_t n_q_heads,
+                  const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
+                  int32_t tail_cap, int64_t tail_stride, float scale, float* out, void* hip_stream) {
   // ---- validation (host only, nothing queued yet) ----
   if (!c) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
   if (n_sel < 0) return fail(MILO_ERR_INVALID_ARG, "n_sel must be >= 0");
@@ -712,7 +714,7 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
   aa.H_q = n_q_heads;
   aa.H_kv = c->n_kv;
   aa.G = G;
-  aa.tail_cap = tail_cap;
+  aa.tail_stride = tail_stride;
   aa.n_slots = c->n_slots;
   aa.n_block_slots = c->n_block_slots;
   aa.qt_stride = c->rk_pad_max + 8;
@@ -754,6 +756,31 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
     g_timing.recorded.insert(g_timing.recorded.end(), ev, ev + 4);
   }
   return MILO_OK;
+}
+
+int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_q, int32_t n_q_heads,
+                       const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
+                       int32_t tail_cap, float scale, float* out, void* hip_stream) {
+  g_err.clear();
+  return attend(c, block_table, n_sel, n_q, n_q_heads, q, tail_k, tail_v, tail_len, tail_cap, tail_cap, scale, out,
+                hip_stream);
+}
+
+int milo_attend_prefill(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_tok, int32_t n_q_heads,
+                        const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, int32_t tail_base,
+                        int32_t tail_cap, float scale, float* out, void* hip_stream) {
+  g_err.clear();
+  if (n_tok < 1) return fail(MILO_ERR_INVALID_ARG, "n_tok must be >= 1");
+  if (tail_base < 0) return fail(MILO_ERR_INVALID_ARG, "tail_base must be >= 0");
+  if ((int64_t)tail_base + n_tok > tail_cap)
+    return fail(MILO_ERR_INVALID_ARG, "tail_cap (%d) must hold tail_base + n_tok = %lld rows", tail_cap,
+                (long long)tail_base + n_tok);
+  if (!tail_k || !tail_v) return fail(MILO_ERR_INVALID_ARG, "tail_k / tail_v must be non-NULL");
+  // token j sees the tail_base rows before the chunk and the chunk's first j + 1 tokens
+  std::vector<int32_t> tl(n_tok);
+  for (int j = 0; j < n_tok; ++j) tl[j] = tail_base + j + 1;
+  return attend(c, block_table, n_sel, n_tok, n_q_heads, q, tail_k, tail_v, tl.data(), tail_cap, 0, scale, out,
+                hip_stream);
 }
 
 int milo_timing_enable(int enable) {

@@ -274,14 +274,14 @@ struct AttendArgs {
   const unsigned char* prog; // program buffer
   const WgProgram* wg;       // [grid] program of each workgroup
   const uint16_t* q;         // [n_q][H_q][d]
-  const uint16_t* tail_k;    // [n_q][tail_cap][H_kv][d]
+  const uint16_t* tail_k;    // request i's tail rows start at row i * tail_stride; [row][H_kv][d]
   const uint16_t* tail_v;
   const int32_t* tail_len;   // device [n_q]
   float* part_o;             // [n_q*H_q][n_slots][d]
   float2* part_ml;           // [n_q*H_q][n_slots] (max in log2 units, sum)
   float qscale;              // scale * log2(e)
   int n_q, H_q, H_kv, G;
-  int tail_cap;
+  int64_t tail_stride;      // rows between consecutive requests' tails (0: one tail shared by all)
   int n_slots;
   int n_block_slots;         // slots [0, n_block_slots) hold block groups, the rest tail chunks
   int qt_stride;             // bf16 row stride of the projected query in LDS

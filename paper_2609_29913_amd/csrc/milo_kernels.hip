@@ -196,7 +196,7 @@ __device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& i
   float* op = wt + kTailChunk * 32;              // [kWaves][kMaxGroup][D] partial outputs
 
   const int64_t rs = (int64_t)a.H_kv * D;      // row stride of the tail K / V
-  const int64_t row0 = (int64_t)i * a.tail_cap + t0;
+  const int64_t row0 = (int64_t)i * a.tail_stride + t0;
   const int tk = min(kTokW * wave + lrow, nt - 1);   // this lane's token row (clamped)
   const int hh = min(lrow, G - 1);                    // this lane's head column (clamped)
   const uint16_t* krow = a.tail_k + (row0 + tk) * rs + (int64_t)g * D + 8 * lhi;

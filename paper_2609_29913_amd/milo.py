@@ -58,6 +58,9 @@ def lib() -> ctypes.CDLL:
         L.milo_attend_decode.argtypes = [vp, _c_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                          vp, vp, vp, _c_i32p, ctypes.c_int32, ctypes.c_float, vp, vp]
         L.milo_attend_decode.restype = ctypes.c_int
+        L.milo_attend_prefill.argtypes = [vp, _c_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                          vp, vp, vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, vp, vp]
+        L.milo_attend_prefill.restype = ctypes.c_int
         L.milo_cache_free.argtypes = [vp]
         L.milo_cache_free.restype = None
         L.milo_last_error.argtypes = []
@@ -159,6 +162,22 @@ def milo_attend_decode(cache: int, block_table, q, tail_k, tail_v, tail_len, sca
     _check(lib().milo_attend_decode(
         ctypes.c_void_p(cache), _i32(table) if n_sel else None, n_sel, n_q, n_q_heads,
         _addr(q), _addr(tail_k), _addr(tail_v), _i32(tail_len), tail_cap, float(scale), _addr(out),
+        _stream(stream)))
+
+
+def milo_attend_prefill(cache: int, block_table, q, tail_k, tail_v, tail_base: int, scale: float, out,
+                        stream=None) -> None:
+    """Queue the causal prefill of one request's chunk of n_tok tokens.  q: bf16
+    [n_tok][H_q][d], tail_k/v: bf16 [tail_cap][H_kv][d] (one shared tail whose rows
+    tail_base .. tail_base + n_tok - 1 are the chunk's own keys / values), out: fp32
+    [n_tok][H_q][d] (device tensors)."""
+    n_tok, n_q_heads = int(q.shape[0]), int(q.shape[1])
+    tail_cap = int(tail_k.shape[0])
+    table = None if block_table is None else list(block_table)
+    n_sel = 0 if table is None else len(table)
+    _check(lib().milo_attend_prefill(
+        ctypes.c_void_p(cache), _i32(table) if n_sel else None, n_sel, n_tok, n_q_heads,
+        _addr(q), _addr(tail_k), _addr(tail_v), int(tail_base), tail_cap, float(scale), _addr(out),
         _stream(stream)))
 
 

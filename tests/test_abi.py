@@ -88,6 +88,10 @@ def test_create_byte_cap_is_out_of_memory(monkeypatch):
 def test_attend_null_cache_and_free_null():
     rc = milo.lib().milo_attend_decode(None, None, 0, 1, 1, None, None, None, None, 0, 1.0, None, None)
     assert rc == milo.MILO_ERR_INVALID_ARG
+    rc = milo.lib().milo_attend_prefill(None, None, 0, 1, 1, None, None, None, 0, 1, 1.0, None, None)
+    assert rc == milo.MILO_ERR_INVALID_ARG
+    rc = milo.lib().milo_attend_prefill(None, None, 0, 4, 1, None, None, None, 2, 5, 1.0, None, None)
+    assert rc == milo.MILO_ERR_INVALID_ARG and "tail_cap" in milo.milo_last_error()
     milo.milo_cache_free(None)
     v = ctypes.c_int64()
     assert milo.lib().milo_cache_device_bytes(None, ctypes.byref(v)) == milo.MILO_ERR_INVALID_ARG

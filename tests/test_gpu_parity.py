@@ -230,3 +230,72 @@ def test_error_profile_is_bf16_sized():
     e = col_rel_l2(got, oracle.attend_latent(**oracle_args(inp)))
     print(f"[parity] tiny per-head rel-L2: median {np.median(e):.2e} max {e.max():.2e}", flush=True)
     assert np.median(e) < 5e-3
+
+
+# ----------------------------------------------------------------------------------
+# prefill: a chunk of one request's tokens, causal over its own tail rows
+# ----------------------------------------------------------------------------------
+PREFILL = {
+    # the chunk's tail lengths 251..270 cross a 256-token tail chunk
+    "blocks_chunk_crosses_tail_chunk": dict(block_tokens=[300, 1024], rank_k=[64, 288], n_kv_heads=4,
+                                            head_dim=128, n_q_heads=28, n_tok=20, tail_base=250,
+                                            extra_rows=10),
+    # no blocks: causal self-attention of 300 tokens (two tail chunks), G = 7
+    "tail_only_causal_300": dict(block_tokens=[], rank_k=[], n_kv_heads=2, head_dim=64, n_q_heads=14,
+                                 n_tok=300, tail_base=0, extra_rows=0),
+    # 7B-shaped heads, 64-token chunk after 192 tail rows
+    "q7b_heads_chunk64": dict(block_tokens=[1024] * 4, rank_k=[64, 512, 288, 160], n_kv_heads=4,
+                              head_dim=128, n_q_heads=28, n_tok=64, tail_base=192, extra_rows=0),
+}
+
+
+@pytest.mark.parametrize("name", list(PREFILL))
+def test_prefill_parity(name):
+    import torch
+    from helpers import to_device
+    from paper_2609_29913_amd import milo
+    c = dict(PREFILL[name])
+    n_tok, tail_base, extra = c.pop("n_tok"), c.pop("tail_base"), c.pop("extra_rows")
+    blocks = c.pop("block_tokens")
+    ranks = c.pop("rank_k")
+    tail_cap = tail_base + n_tok + extra
+    # a problem whose request 0 supplies the shared tail; a placeholder block when there is none
+    inp = synth.make_problem(zlib.crc32(name.encode()) % 1000, blocks or [1], ranks or [1], n_q=n_tok,
+                             tail_cap=tail_cap, **c)
+    table = list(range(len(blocks)))
+    gl = GpuLayer(inp)
+    try:
+        tk, tv = to_device(inp.tail_k[0]), to_device(inp.tail_v[0])
+        out = torch.full(inp.q.shape, float("nan"), dtype=torch.float32, device="cuda")
+        milo.milo_attend_prefill(gl.cache, table, gl.q, tk, tv, tail_base, inp.scale, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+    finally:
+        gl.free()
+    assert np.all(np.isfinite(got)), "unwritten or non-finite outputs"
+    a = oracle_args(inp, table)
+    ref = oracle.attend_prefill(a["pk"], a["rk"], a["pv"], a["rv"], table, a["q"], a["tail_k"][0],
+                                a["tail_v"][0], tail_base, inp.scale)
+    err = max_rel_l2(got, ref)
+    print(f"[parity] prefill {name} max rel-L2 = {err:.3e}", flush=True)
+    assert err <= TOL_REL_L2
+
+
+def test_prefill_rejects_bad_arguments():
+    import torch
+    from helpers import to_device
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(28, [64], [16], n_kv_heads=2, head_dim=64, n_q=4, n_q_heads=4, tail_cap=6)
+    gl = GpuLayer(inp)
+    out = torch.empty(inp.q.shape, dtype=torch.float32, device="cuda")
+    tk, tv = to_device(inp.tail_k[0]), to_device(inp.tail_v[0])
+    try:
+        for tail_base in (3, -1):  # 3 + 4 tokens > 6 rows; negative base
+            with pytest.raises(milo.MiloError) as ei:
+                milo.milo_attend_prefill(gl.cache, [0], gl.q, tk, tv, tail_base, inp.scale, out)
+            assert ei.value.code == milo.MILO_ERR_INVALID_ARG
+        milo.milo_attend_prefill(gl.cache, [0], gl.q, tk, tv, 2, inp.scale, out)  # 2 + 4 rows fit
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(out).all())
+    finally:
+        gl.free()

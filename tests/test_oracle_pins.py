@@ -349,3 +349,66 @@ def test_planted_mistake_is_caught(name, old, new):
         except Exception:  # an assertion or a crash both expose the mistake
             failed.append(pin.__name__)
     assert failed, f"planted mistake '{name}' passed every external pin"
+
+
+# ----------------------------------------------------------------------------------
+# prefill (a multi-token query of one request, causal over its own tokens)
+# ----------------------------------------------------------------------------------
+def _prefill_case(seed, n_tok, tail_base, extra_rows, n_kv=2, G=3, d=16, blocks=((4, 2), (9, 5))):
+    """A prefill problem: blocks (T_b, r_b), one shared tail of tail_base + n_tok
+    + extra_rows rows, n_tok query tokens."""
+    tail_cap = tail_base + n_tok + extra_rows
+    base = _case(seed, [t for t, _ in blocks] or [1], [r for _, r in blocks] or [1],
+                 n_kv_heads=n_kv, head_dim=d, n_q=n_tok, n_q_heads=n_kv * G, tail_cap=tail_cap)
+    args = {k: base[k] for k in ("pk", "rk", "pv", "rv", "q", "scale")}
+    args["table"] = list(range(len(blocks)))
+    args["tail_k"], args["tail_v"] = base["tail_k"][0], base["tail_v"][0]  # request 0's tail, shared
+    args["tail_base"] = tail_base
+    return args
+
+
+def _causal_sdpa(a, n_tok, G):
+    """torch's attention of the chunk over the shared tail with the causal mask
+    (fp64, CPU; KV heads repeated for the GQA groups)."""
+    tail_base = a["tail_base"]
+    n_keys = tail_base + n_tok
+    q = torch.from_numpy(np.ascontiguousarray(a["q"].transpose(1, 0, 2)))[None]       # [1, H_q, n_tok, d]
+    k = torch.from_numpy(np.ascontiguousarray(a["tail_k"][:n_keys].transpose(1, 0, 2)))
+    v = torch.from_numpy(np.ascontiguousarray(a["tail_v"][:n_keys].transpose(1, 0, 2)))
+    k = k.repeat_interleave(G, dim=0)[None]
+    v = v.repeat_interleave(G, dim=0)[None]
+    if tail_base == 0:
+        o = torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=a["scale"], is_causal=True)
+    else:
+        mask = torch.arange(n_keys)[None, :] < (tail_base + 1 + torch.arange(n_tok))[:, None]
+        o = torch.nn.functional.scaled_dot_product_attention(q, k, v, attn_mask=mask, scale=a["scale"])
+    return o[0].numpy().transpose(1, 0, 2)
+
+
+@pytest.mark.parametrize("tail_base,extra", [(0, 0), (5, 3)])
+def test_prefill_tail_only_matches_causal_sdpa(tail_base, extra):
+    """No blocks: the chunk's attention over its tail is textbook causal attention
+    (torch's is_causal when the chunk is the whole tail; an explicit mask with
+    earlier rows); rows past tail_base + n_tok are never read."""
+    n_tok, G = 7, 3
+    a = _prefill_case(21, n_tok, tail_base, extra, G=G)
+    a["table"] = []
+    ref = _causal_sdpa(a, n_tok, G)
+    o = oracle.attend_prefill(**a)
+    assert np.allclose(o, ref, rtol=1e-12, atol=1e-14)
+    a["tail_k"] = a["tail_k"].copy()
+    a["tail_k"][tail_base + n_tok:] = 1e6  # unused rows
+    assert np.array_equal(oracle.attend_prefill(**a), o)
+
+
+def test_prefill_token_rows_match_latent_route():
+    """With blocks: token j of the chunk is a decode query whose tail is the
+    shared tail's first tail_base + j + 1 rows (checked through the latent route,
+    which shares no code with the dense definition the prefill wrapper uses)."""
+    n_tok, tail_base = 5, 4
+    a = _prefill_case(22, n_tok, tail_base, 2)
+    o = oracle.attend_prefill(**a)
+    for j in range(n_tok):
+        ref = oracle.attend_latent(a["pk"], a["rk"], a["pv"], a["rv"], a["table"], a["q"][j:j + 1],
+                                   a["tail_k"][None], a["tail_v"][None], [tail_base + j + 1], a["scale"])
+        assert _col_rel(o[j:j + 1], ref) < 1e-12
