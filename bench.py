@@ -199,6 +199,31 @@ def cpu_baseline(inp: synth.LayerInputs, n_layers: int, budget_s: float):
                       + (f", x{n_layers} layers" if n_layers > 1 else "")}
 
 
+def device_env(dev, n_bytes=1 << 30, reps=5):
+    """Host, software and device facts for the record, plus the bandwidth of a plain
+    1 GiB device copy (bytes read + written per second: what HBM sustains here)."""
+    import platform
+    import socket
+    import torch
+    props = torch.cuda.get_device_properties(dev)
+    a = torch.empty(n_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    st.record()
+    for _ in range(reps):
+        b.copy_(a)
+    en.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * n_bytes * reps / (st.elapsed_time(en) * 1e-3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return {"host": socket.gethostname(), "python": platform.python_version(), "torch": torch.__version__,
+            "hip": getattr(torch.version, "hip", None), "gpu": props.name,
+            "arch": getattr(props, "gcnArchName", None), "compute_units": props.multi_processor_count,
+            "device_copy_gbs": copy_gbs}
+
+
 def calibrate_copy(dev, n_bytes=1 << 30, reps=5):
     """Plain device copy of known size (for scaling HBM byte counters)."""
     import torch
@@ -304,6 +329,16 @@ def main():
     att_avg_s = att_ms / n_calls * 1e-3
     merge_avg_s = merge_ms / n_calls * 1e-3
 
+    # third pass: each step between HIP events on the launch stream (distribution)
+    import torch
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for k in range(args.steps):
+        run_step(k)
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    step_us = np.array([evs[k].elapsed_time(evs[k + 1]) * 1e3 for k in range(args.steps)])
+
     # the attention kernel reads every factor once, the tails and the queries
     kern_bytes = (per_step - out_bytes) / cfg.n_layers
     flops = flops_step / cfg.n_layers
@@ -312,6 +347,7 @@ def main():
     # the bound is the roof the kernel's arithmetic intensity meets first
     bound = "hbm" if flops / kern_bytes < MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
     traffic = counter_traffic(args.config)
+    t_roof = max(kern_bytes / (HBM_PEAK_GBS * 1e9), flops / (MFMA_BF16_PEAK_TFLOPS * 1e12))
 
     ctx_tokens = int(x0.block_tokens.sum()) + int(x0.tail_len.max())
     value = x0.n_q * ctx_tokens / (ms_per_step * 1e-3)
@@ -345,6 +381,8 @@ def main():
             "step_bytes_algorithmic": per_step,
             "hbm_frac_of_step": per_step / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
         },
+        "step_us": {"median": float(np.median(step_us)), "min": float(step_us.min()),
+                    "p90": float(np.percentile(step_us, 90)), "timing": "HIP events between steps"},
         "roofline": {
             "bound": bound,
             "achieved": achieved if bound == "hbm" else mfma_tflops,
@@ -360,6 +398,7 @@ def main():
             "hbm_gbs": achieved,
             "mfma_tflops": mfma_tflops,
             "mfma_frac": mfma_tflops / MFMA_BF16_PEAK_TFLOPS,
+            "attainable_frac": t_roof / att_avg_s,
             "kernel_source_sha256_16": kernel_source_hash(),
         },
         "cpu_baseline": None,
@@ -367,6 +406,7 @@ def main():
     for grp in groups:
         for layer in grp:
             milo.milo_cache_free(layer.cache)
+    result["env"] = device_env(dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(x0, cfg.n_layers, args.cpu_budget)
     print(json.dumps(result), flush=True)
