@@ -84,7 +84,10 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk,
                       milo_cache** out);
 
 /* One decode step of attention over the selected blocks plus each request's
- * dense tail (Alg. 1 inference stage; Eq. 1).
+ * dense tail (Alg. 1 inference stage; Eq. 1).  The step's work plan gives every
+ * workgroup a program that must fit in LDS; when the programs would not fit
+ * (or exceed the byte cap in the MILO_MAX_PROGRAM_BYTES environment variable,
+ * read when a plan is built) the work is split over several launches.
  *   cache         from milo_cache_create, on the current device.
  *   block_table   host [n_sel] distinct block ids in [0, n_blocks) (the retriever's
  *                 selection; any order gives the same result up to rounding).

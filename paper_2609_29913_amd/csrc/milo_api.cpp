@@ -56,6 +56,15 @@ int64_t env_byte_cap() {
   return std::strtoll(s, nullptr, 10);
 }
 
+// LDS bytes a workgroup program may use at most, from MILO_MAX_PROGRAM_BYTES
+// (unset: no cap beyond what LDS leaves).  A small cap splits a step's work
+// over several attention launches; it exists so that path can be exercised.
+int64_t env_program_cap() {
+  const char* s = std::getenv("MILO_MAX_PROGRAM_BYTES");
+  if (!s || !*s) return -1;
+  return std::strtoll(s, nullptr, 10);
+}
+
 // Timing hooks (measurement only).
 struct TimingState {
   std::mutex mu;
@@ -315,6 +324,7 @@ int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const s
     out->half_w = false;
     cap = room_for(false);
   }
+  if (const int64_t pc = env_program_cap(); pc >= 0) cap = std::min(cap, (size_t)pc);
   for (int L = 1; L <= (1 << 20); L *= 2) {
     std::vector<std::vector<unsigned char>> progs((size_t)L * kCUs);
     std::vector<WgProgram> entries((size_t)L * kCUs);

@@ -147,6 +147,27 @@ def test_plan_changes_between_calls():
         gl.free()
 
 
+def test_work_split_over_several_launches(monkeypatch):
+    """When the workgroup programs do not fit in LDS the step runs as several
+    attention launches.  A cap of 5376 program bytes holds the run buffers and
+    at most three 80-byte items per workgroup; 1200 one-tile blocks on one KV
+    head give some workgroup at least five items in a single launch, so the
+    plan needs two or more launches."""
+    monkeypatch.setenv("MILO_MAX_PROGRAM_BYTES", "5376")
+    n = 1200
+    inp = synth.make_problem(31, [32] * n, [16] * n, rank_v=[8] * n, n_kv_heads=1, head_dim=64, n_q=2,
+                             n_q_heads=2, tail_cap=40, tail_len=[40, 3])
+    gl = GpuLayer(inp)
+    try:
+        got = gl.attend().cpu().numpy()
+    finally:
+        gl.free()
+    ref = oracle.attend_latent(**oracle_args(inp))
+    err = max_rel_l2(got, ref)
+    print(f"[parity] several launches max rel-L2 = {err:.3e}", flush=True)
+    assert err <= TOL_REL_L2
+
+
 def test_deterministic_and_fully_written():
     inp = synth.make_problem(24, [1024, 333], [256, 96], n_kv_heads=4, head_dim=128, n_q=3, n_q_heads=28,
                              tail_cap=100)
