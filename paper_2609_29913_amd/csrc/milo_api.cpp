@@ -629,6 +629,10 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
   int max_chunks = 0;
   for (int i = 0; i < n_q; ++i) max_chunks = std::max(max_chunks, (tl[i] + kTailChunk - 1) / kTailChunk);
   if (key != c->plan_key) {
+    // no plan is valid until this one is complete: a failure below (an
+    // allocation, an upload) must not leave the old key pointing at buffers
+    // that were freed or half rewritten
+    c->plan_key.clear();
     const int ncg = n_q * G;
     const int n_ct = (ncg + kCols - 1) / kCols;
     Schedule sch;
@@ -743,7 +747,11 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
       for (int k = 0; k < 4; ++k) {
         if (g_timing.pool.empty()) {
           hipEvent_t e;
-          MILO_HIP(hipEventCreate(&e));
+          const hipError_t ce = hipEventCreate(&e);
+          if (ce != hipSuccess) {
+            for (int j = 0; j < k; ++j) g_timing.pool.push_back(ev[j]);
+            return hip_fail(ce, "hipEventCreate");
+          }
           g_timing.pool.push_back(e);
         }
         ev[k] = g_timing.pool.back();
@@ -752,15 +760,23 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
       timed = true;
     }
   }
+  // a failed launch hands the call's events back to the pool
+  auto launch_fail = [&](hipError_t err, const char* what) {
+    if (timed) {
+      std::lock_guard<std::mutex> lk(g_timing.mu);
+      g_timing.pool.insert(g_timing.pool.end(), ev, ev + 4);
+    }
+    return hip_fail(err, what);
+  };
   hipError_t e = hipSuccess;
   for (int l = 0; l < c->n_launch; ++l) {
     aa.wg = reinterpret_cast<const WgProgram*>(c->plan_d) + (size_t)l * kCUs;
     e = launch_attend(aa, c->d, c->max_rt, c->nslot, kCUs, c->lds, s, l == 0 ? ev[0] : nullptr,
                       l == c->n_launch - 1 ? ev[1] : nullptr);
-    if (e != hipSuccess) return hip_fail(e, "attend kernel launch");
+    if (e != hipSuccess) return launch_fail(e, "attend kernel launch");
   }
   e = launch_merge(ma, c->d, n_cols, s, ev[2], ev[3]);
-  if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+  if (e != hipSuccess) return launch_fail(e, "merge kernel launch");
   if (timed) {
     std::lock_guard<std::mutex> lk(g_timing.mu);
     g_timing.recorded.insert(g_timing.recorded.end(), ev, ev + 4);
