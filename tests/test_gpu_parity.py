@@ -320,3 +320,33 @@ def test_prefill_rejects_bad_arguments():
         assert bool(torch.isfinite(out).all())
     finally:
         gl.free()
+
+
+def _random_case(seed):
+    """A seeded random problem: head dim, KV heads, group size, batch, ragged
+    blocks and ranks (K and V apart), a random subset of the blocks in random
+    order, ragged tails (some empty)."""
+    rng = np.random.default_rng(1000 + seed)
+    d = int(rng.choice([64, 128]))
+    n_kv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 5, 7, 16]))
+    n_q = int(rng.integers(1, 7))
+    n_blocks = int(rng.integers(1, 9))
+    T = rng.integers(1, 1400, n_blocks)
+    D = n_kv * d
+    rk = [int(rng.integers(1, min(int(t), D, 1024) + 1)) for t in T]
+    rv = [int(rng.integers(1, min(int(t), D, 1024) + 1)) for t in T]
+    tail_cap = int(rng.choice([0, 1, 70, 300]))
+    tail_len = [int(rng.integers(0, tail_cap + 1)) for _ in range(n_q)]
+    inp = synth.make_problem(500 + seed, [int(t) for t in T], rk, rv, n_kv_heads=n_kv, head_dim=d, n_q=n_q,
+                             n_q_heads=n_kv * G, tail_cap=tail_cap, tail_len=tail_len)
+    k = int(rng.integers(0 if tail_cap and min(tail_len) > 0 else 1, n_blocks + 1))
+    table = [int(b) for b in rng.permutation(n_blocks)[:k]]
+    return inp, table
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_parity_random_shapes(seed):
+    inp, table = _random_case(seed)
+    _check(inp, table=table, label=f"random seed {seed} (d={inp.head_dim}, H_kv={inp.n_kv_heads}, "
+                                   f"G={inp.n_q_heads // inp.n_kv_heads}, blocks {len(table)}/{inp.n_blocks})")
