@@ -638,7 +638,7 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
     Schedule sch;
     const int err = build_schedule(*c, block_table, n_sel, tl, n_ct, &sch);
     if (err != MILO_OK) return err;
-    const int max_rt = sch.max_own <= 2 ? 2 : 4;
+    const int max_rt = sch.max_own <= 2 ? 2 : sch.max_own == 3 ? 3 : 4;
     // deepest fragment ring that fits next to the program, projected query and
     // weight tile (4 slots go with the half weight tile)
     const size_t base = attend_lds_base_bytes(c->d, sch.rk_pad_max, sch.rv_pad_max, sch.half_w);

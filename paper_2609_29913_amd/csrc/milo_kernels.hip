@@ -1018,6 +1018,7 @@ static hipError_t launch_attend_d(const AttendArgs& a, int max_rt, int nslot, in
                                   hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   switch (max_rt) {
     case 2: return launch_attend_r<D, 2>(a, nslot, grid, lds, s, e0, e1);
+    case 3: return launch_attend_r<D, 3>(a, nslot, grid, lds, s, e0, e1);
     case 4: return launch_attend_r<D, 4>(a, nslot, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
