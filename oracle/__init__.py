@@ -21,6 +21,11 @@ What it computes (the method's result, written out plainly in fp64):
 `attend_prefill` is the same definition for a multi-token input query of one
 request whose tokens attend causally among themselves (a chunk of new tokens
 sharing one tail).
+`allocate_ranks` is the encoder's rank allocation (Sec. 4.3): per-block ranks
+that maximise the retained spectral information (Eq. 5) under a total rank
+budget and per-block bounds (Eq. 6), found by the greedy over marginal gains
+(Eq. 7) that the paper describes.
+
 `attend_latent` reaches the same numbers by exact reassociation,
 q.(P R)_t = P_t.(R q) and sum_t w_t (P R)_t = (sum_t w_t P_t) R, which is the
 order the GPU path follows: project the query per block, score against P^K
@@ -33,7 +38,8 @@ from __future__ import annotations
 
 import numpy as np
 
-__all__ = ["attend_dense", "attend_latent", "attend_prefill", "reconstruct"]
+__all__ = ["allocate_ranks", "attend_dense", "attend_latent", "attend_prefill", "reconstruct",
+           "spectral_information"]
 
 
 def reconstruct(p: np.ndarray, r: np.ndarray) -> np.ndarray:
@@ -173,3 +179,56 @@ def attend_prefill(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_base, scale):
     tv = np.broadcast_to(tail_v, (n_tok,) + tail_v.shape)
     tail_len = tail_base + 1 + np.arange(n_tok)
     return attend_dense(pk, rk, pv, rv, table, q, tk, tv, tail_len, scale)
+
+
+# --------------------------------------------------------------------------
+# Rank allocation (Sec. 4.3, Eqs. 5-7)
+# --------------------------------------------------------------------------
+def spectral_information(sigma, r: int, eps: float) -> float:
+    """Eq. 5: H(r) = sum over the r largest singular values of log(1 + sigma^2 / eps^2).
+    sigma: one block's singular values, non-increasing."""
+    s = np.asarray(sigma, dtype=np.float64)[:r]
+    return float(np.sum(np.log1p(s * s / (eps * eps))))
+
+
+def allocate_ranks(sigmas, r_total: int, r_min: int, r_max: int, eps: float = 1e-3) -> np.ndarray:
+    """Eq. 6 solved by the greedy of Eq. 7: every block starts at r_min; each
+    remaining rank unit goes to the block whose next singular value brings the
+    largest gain log(1 + sigma_{i,r+1}^2 / eps^2); stop when the ranks sum to the
+    budget or no block can grow.
+
+    Readings where the text leaves it open: a block cannot take more ranks than
+    it has singular values (min(T_b, D)), so its floor is min(r_min, n_i) and its
+    cap min(r_max, n_i); if every block reaches its cap first the sum stays below
+    the budget (the constraint of Eq. 6 is an inequality); equal gains go to the
+    lower block index.
+
+    sigmas: list of 1-D arrays, block i's singular values, non-increasing
+    returns int64 ranks [n_blocks]; raises ValueError when even the floors exceed
+    the budget (Eq. 6 has no feasible point)."""
+    n = len(sigmas)
+    sig = [np.asarray(s, dtype=np.float64) for s in sigmas]
+    for i, s in enumerate(sig):
+        if s.ndim != 1 or np.any(~np.isfinite(s)) or np.any(s < 0) or np.any(np.diff(s) > 0):
+            raise ValueError(f"block {i}: singular values must be finite, non-negative, non-increasing")
+    cap = np.array([min(r_max, len(s)) for s in sig], dtype=np.int64)
+    r = np.array([min(r_min, len(s)) for s in sig], dtype=np.int64)
+    if int(r.sum()) > r_total:
+        raise ValueError("the budget is below the sum of the per-block floors")
+
+    def gain(i):  # Delta H_{i, r_i}: the gain of block i's next singular value
+        if r[i] >= cap[i]:
+            return -np.inf
+        x = sig[i][r[i]]
+        return np.log1p(x * x / (eps * eps))
+
+    nxt = np.array([gain(i) for i in range(n)])
+    left = r_total - int(r.sum())
+    while left > 0:
+        i = int(np.argmax(nxt))          # first index among equal maxima
+        if nxt[i] == -np.inf:
+            break                        # every block is at its cap
+        r[i] += 1
+        left -= 1
+        nxt[i] = gain(i)
+    return r

@@ -26,12 +26,12 @@ import numpy as np
 __all__ = [
     "Config", "CONFIGS", "LayerInputs", "f32_to_bf16", "bf16_to_f32",
     "bf16_to_f64", "gen_layer", "make_problem", "draw_block_tokens",
-    "draw_ranks", "algorithmic_bytes", "latent_flops",
+    "draw_ranks", "algorithmic_bytes", "latent_flops", "gen_spectra", "Spectra",
 ]
 
 _MAGIC = 0x4D494C4F  # "MILO"
 # tensor ids inside one layer's key space
-T_META, T_PK, T_RK, T_PV, T_RV, T_TAILK, T_TAILV, T_Q = range(8)
+T_META, T_PK, T_RK, T_PV, T_RV, T_TAILK, T_TAILV, T_Q, T_SIGMA = range(9)
 _SHARED_LAYER = 0xFFFFF  # key slot for draws shared by every layer
 
 
@@ -272,3 +272,48 @@ def latent_flops(inp: LayerInputs, table=None) -> int:
     G = inp.n_q_heads // inp.n_kv_heads
     tail = 4 * int(np.sum(inp.tail_len)) * G * inp.n_kv_heads * d
     return blk + tail
+
+
+# --------------------------------------------------------------------------
+# Singular-value spectra for the rank allocation (encoder input)
+# --------------------------------------------------------------------------
+@dataclass
+class Spectra:
+    """Per-block singular values of one layer's keys (or values), fp32, each row
+    non-increasing; row b holds n_sv[b] = min(T_b, D) values, padded with zeros
+    to ld columns; plus the allocation's budget and bounds."""
+    sigma: np.ndarray       # float32 [n_blocks][ld]
+    n_sv: np.ndarray        # int32 [n_blocks]
+    r_total: int
+    r_min: int
+    r_max: int
+
+
+def gen_spectra(cfg: Config | str, layer: int = 0, rho: float = 0.5, r_min: int = 32,
+                r_max: int = 896) -> Spectra:
+    """Seeded synthetic spectra with the block structure of a workload: block b
+    decays as a power law sigma_j = s_b (j + 1)^(-a_b) with a_b ~ U(0.2, 1.6) and
+    s_b ~ LogNormal(0, 0.5), so blocks range from flat (information-dense) to
+    steep (redundant).  About one value in 64 is copied from its predecessor, so
+    equal values (ties) occur inside rows.  The budget is the rank sum at which
+    Eq. 4's ratio equals rho when every block has the same rank:
+    r_total = floor(rho * N * D * B / (B + D)) with B the mean block size."""
+    if isinstance(cfg, str):
+        cfg = CONFIGS[cfg]
+    T = draw_block_tokens(cfg)
+    D = cfg.d_kv
+    n_sv = np.minimum(T, D).astype(np.int32)
+    ld = int(n_sv.max())
+    rng = _rng(cfg.cfg_id, layer, T_SIGMA)
+    a = rng.uniform(0.2, 1.6, size=len(T))
+    s0 = np.exp(rng.normal(0.0, 0.5, size=len(T)))
+    sigma = np.zeros((len(T), ld), dtype=np.float32)
+    for b, n in enumerate(n_sv):
+        row = (s0[b] * np.arange(1, n + 1, dtype=np.float64) ** -a[b]).astype(np.float32)
+        dup = np.flatnonzero(rng.random(n) < 1.0 / 64)
+        dup = dup[dup > 0]
+        row[dup] = row[dup - 1]
+        sigma[b, :n] = np.minimum.accumulate(row)
+    B = float(T.mean())
+    r_total = int(np.floor(rho * len(T) * D * B / (B + D)))
+    return Spectra(sigma, n_sv, r_total, r_min, r_max)
