@@ -136,6 +136,38 @@ int milo_attend_prefill(milo_cache* cache, const int32_t* block_table, int32_t n
                         int32_t tail_base, int32_t tail_cap, float scale, float* out,
                         void* hip_stream);
 
+/* Entropy-based rank allocation of the encoder (Sec. 4.3): the per-block ranks
+ * r_b that maximise the retained spectral information sum_b H_b(r_b), with
+ * H_b(r) = sum_{j<=r} log(1 + sigma_{b,j}^2 / eps^2) (Eq. 5), subject to
+ * sum_b r_b <= r_total and r_min <= r_b <= r_max (Eq. 6), as the greedy over
+ * marginal gains of Eq. 7 assigns them: every block starts at its floor and
+ * each further unit goes to the block with the largest next singular value.
+ * The result does not depend on eps (the gain is increasing in sigma), so eps
+ * is not an argument.  A block cannot exceed its own number of singular values:
+ * its floor is min(r_min, n_sv[b]) and its cap min(r_max, n_sv[b]); when every
+ * block reaches its cap the sum stays below r_total; equal singular values go
+ * to the lower block index first.  Run it once for the key spectra and once for
+ * the value spectra (Eq. 4 counts both) to get rank_k and rank_v for
+ * milo_cache_create.
+ *   sigma      device fp32 [n_blocks][ld]; row b holds block b's singular values
+ *              in its first n_sv[b] columns, finite, >= 0 and non-increasing
+ *              (the rest of the row is not read).
+ *   ld         row stride in elements, >= 1 and >= every n_sv[b].
+ *   n_blocks   >= 1.
+ *   n_sv       host [n_blocks], 0 <= n_sv[b] <= ld (min(T_b, H_kv*d) for an SVD).
+ *   r_total    rank budget R_tot, at least sum_b min(r_min, n_sv[b]).
+ *   r_min/max  0 <= r_min <= r_max.
+ *   ranks      host [n_blocks] out.
+ *   hip_stream stream the kernels run on; the call waits for them (synchronous).
+ * Allocates and frees a small device workspace per call.  Errors: INVALID_ARG
+ * (NULL pointer, bad bounds, budget below the floors, or a row that is not
+ * finite, non-negative and non-increasing: the message names the lowest such
+ * block; ranks is then untouched), UNSUPPORTED (2^31 or more candidate values),
+ * OUT_OF_MEMORY, HIP_ERROR. */
+int milo_allocate_ranks(const float* sigma, int64_t ld, int32_t n_blocks, const int32_t* n_sv,
+                        int64_t r_total, int32_t r_min, int32_t r_max, int32_t* ranks,
+                        void* hip_stream);
+
 /* Release the cache and its device memory (synchronises the device first).
  * NULL is accepted and ignored. */
 void milo_cache_free(milo_cache* cache);
@@ -164,6 +196,10 @@ int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which
  * Any argument of milo_timing_read may be NULL. */
 int milo_timing_enable(int enable);
 int milo_timing_read(double* attend_kernel_ms, double* merge_kernel_ms, int64_t* n_calls);
+/* The same for milo_allocate_ranks calls made while timing is enabled: summed
+ * milliseconds of the whole kernel chain and of its histogram passes, and the
+ * number of calls, since the last read (then cleared). */
+int milo_timing_read_alloc(double* chain_ms, double* hist_ms, int64_t* n_calls);
 
 #ifdef __cplusplus
 }

@@ -61,6 +61,12 @@ def lib() -> ctypes.CDLL:
         L.milo_attend_prefill.argtypes = [vp, _c_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                           vp, vp, vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, vp, vp]
         L.milo_attend_prefill.restype = ctypes.c_int
+        L.milo_allocate_ranks.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, _c_i32p, ctypes.c_int64,
+                                          ctypes.c_int32, ctypes.c_int32, _c_i32p, vp]
+        L.milo_allocate_ranks.restype = ctypes.c_int
+        L.milo_timing_read_alloc.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                             ctypes.POINTER(ctypes.c_int64)]
+        L.milo_timing_read_alloc.restype = ctypes.c_int
         L.milo_cache_free.argtypes = [vp]
         L.milo_cache_free.restype = None
         L.milo_last_error.argtypes = []
@@ -181,6 +187,17 @@ def milo_attend_prefill(cache: int, block_table, q, tail_k, tail_v, tail_base: i
         _stream(stream)))
 
 
+def milo_allocate_ranks(sigma, n_sv, r_total: int, r_min: int, r_max: int, stream=None) -> np.ndarray:
+    """Per-block ranks (Sec. 4.3 allocation).  sigma: device fp32 [n_blocks][ld]
+    tensor of non-increasing singular values, n_sv: host [n_blocks] counts.
+    Returns int32 [n_blocks]; synchronous."""
+    n_blocks, ld = int(sigma.shape[0]), int(sigma.shape[1])
+    out = (ctypes.c_int32 * max(1, n_blocks))()
+    _check(lib().milo_allocate_ranks(_addr(sigma), ld, n_blocks, _i32(n_sv), int(r_total), int(r_min),
+                                     int(r_max), out, _stream(stream)))
+    return np.frombuffer(out, dtype=np.int32, count=n_blocks).copy()
+
+
 def milo_cache_free(cache: int | None) -> None:
     lib().milo_cache_free(ctypes.c_void_p(cache) if cache else None)
 
@@ -199,6 +216,13 @@ def milo_cache_read_factor(cache: int, block: int, which: int, shape) -> np.ndar
 
 def milo_timing_enable(enable: bool) -> None:
     _check(lib().milo_timing_enable(1 if enable else 0))
+
+
+def milo_timing_read_alloc():
+    """(allocation kernel-chain ms, histogram-pass ms, number of calls) since the last read."""
+    a, h, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+    _check(lib().milo_timing_read_alloc(ctypes.byref(a), ctypes.byref(h), ctypes.byref(n)))
+    return a.value, h.value, n.value
 
 
 def milo_timing_read():

@@ -101,3 +101,27 @@ def test_attend_null_cache_and_free_null():
 def test_timing_read_without_calls():
     milo.milo_timing_enable(False)
     assert milo.milo_timing_read() == (0.0, 0.0, 0)
+
+
+def test_allocate_rejects_on_the_host():
+    L = milo.lib()
+    nsv = (ctypes.c_int32 * 2)(4, 3)
+    out = (ctypes.c_int32 * 2)(-7, -7)
+    fake = 4096  # never dereferenced: every case fails its host check first
+    cases = [
+        ((None, 4, 2, nsv, 5, 1, 4, out, None), "non-NULL"),
+        ((fake, 4, 2, None, 5, 1, 4, out, None), "non-NULL"),
+        ((fake, 4, 2, nsv, 5, 1, 4, None, None), "non-NULL"),
+        ((fake, 4, 0, nsv, 5, 1, 4, out, None), "n_blocks"),
+        ((fake, 0, 2, nsv, 5, 1, 4, out, None), "ld"),
+        ((fake, 4, 2, nsv, 5, 3, 2, out, None), "r_min"),
+        ((fake, 4, 2, nsv, 5, -1, 2, out, None), "r_min"),
+        ((fake, 3, 2, (ctypes.c_int32 * 2)(4, 3), 5, 1, 4, out, None), "n_sv"),
+        ((fake, 4, 2, (ctypes.c_int32 * 2)(4, -1), 5, 1, 4, out, None), "n_sv"),
+        ((fake, 4, 2, nsv, 5, 3, 4, out, None), "floors"),   # floors 3 + 3 = 6 > 5
+    ]
+    for args, word in cases:
+        assert L.milo_allocate_ranks(*args) == milo.MILO_ERR_INVALID_ARG, args
+        assert word in milo.milo_last_error(), (word, milo.milo_last_error())
+    assert list(out) == [-7, -7]
+    assert milo.milo_timing_read_alloc() == (0.0, 0.0, 0)

@@ -1,0 +1,144 @@
+"""GPU parity of the entropy rank allocation (Sec. 4.3, Eqs. 5-7): the ranks
+from milo_allocate_ranks must equal the oracle's greedy exactly (integer
+output), on the workloads' block structures, on random ragged problems with
+many equal values, at the edges of the budget, and the allocated ranks must
+drive a decode step that matches the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import GpuLayer, max_rel_l2, oracle_args
+from paper_2609_29913_amd import milo
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu(sigma, n_sv, r_total, r_min, r_max):
+    dev = torch.from_numpy(np.ascontiguousarray(sigma, dtype=np.float32)).cuda()
+    return milo.milo_allocate_ranks(dev, n_sv, r_total, r_min, r_max)
+
+
+def _ref(sigma, n_sv, r_total, r_min, r_max):
+    return oracle.allocate_ranks([sigma[b, :n].astype(np.float64) for b, n in enumerate(n_sv)],
+                                 r_total, r_min, r_max)
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "q7b_1l", "q14b_48l", "q32b_64l"])
+def test_alloc_parity_workloads(cfg):
+    sp = synth.gen_spectra(cfg)
+    print(f"allocation {cfg}: {sp.sigma.shape} budget {sp.r_total}", flush=True)
+    got = _gpu(sp.sigma, sp.n_sv, sp.r_total, sp.r_min, sp.r_max)
+    ref = _ref(sp.sigma, sp.n_sv, sp.r_total, sp.r_min, sp.r_max)
+    assert np.array_equal(got, ref)
+    assert got.sum() == sp.r_total
+
+
+def _random_problem(seed):
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(1, 400))
+    ld = int(rng.integers(1, 1100))
+    n_sv = rng.integers(0, ld + 1, n).astype(np.int32)
+    n_sv[rng.random(n) < 0.1] = 0
+    sigma = np.full((n, ld + int(rng.integers(0, 3))), np.nan, dtype=np.float32)  # padding is never read
+    for b in range(n):
+        m = int(n_sv[b])
+        if seed % 3 == 0:   # few distinct values: ties inside and across blocks, zeros
+            v = rng.choice(np.array([0.0, 0.25, 1.0, 3.0], dtype=np.float32), m)
+        else:
+            v = rng.exponential(1.0, m).astype(np.float32) * np.float32(rng.uniform(0.1, 10))
+        sigma[b, :m] = np.sort(v)[::-1]
+    r_min = int(rng.integers(0, 40))
+    r_max = int(rng.integers(r_min, ld + 2))
+    floor = int(np.minimum(r_min, n_sv).sum())
+    cap = int(np.minimum(r_max, n_sv).sum())
+    r_total = int(rng.integers(floor, cap + 10))
+    return sigma, n_sv, r_total, r_min, r_max
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_alloc_parity_random(seed):
+    sigma, n_sv, r_total, r_min, r_max = _random_problem(seed)
+    print(f"allocation seed {seed}: {sigma.shape} budget {r_total} bounds ({r_min}, {r_max})", flush=True)
+    got = _gpu(sigma, n_sv, r_total, r_min, r_max)
+    assert np.array_equal(got, _ref(sigma, n_sv, r_total, r_min, r_max))
+
+
+def test_alloc_budget_edges_and_ties():
+    sp = synth.gen_spectra("q7b_1l")
+    lo = np.minimum(sp.r_min, sp.n_sv)
+    hi = np.minimum(sp.r_max, sp.n_sv)
+    for r_total in (int(lo.sum()), int(lo.sum()) + 1, int(hi.sum()) - 1, int(hi.sum()), int(hi.sum()) + 100):
+        got = _gpu(sp.sigma, sp.n_sv, r_total, sp.r_min, sp.r_max)
+        assert np.array_equal(got, _ref(sp.sigma, sp.n_sv, r_total, sp.r_min, sp.r_max)), r_total
+    # identical rows: units go round-robin in block order
+    row = np.linspace(4.0, 1.0, 64, dtype=np.float32)
+    sigma = np.tile(row, (7, 1))
+    n_sv = np.full(7, 64, np.int32)
+    for extra in (0, 3, 7, 10):
+        got = _gpu(sigma, n_sv, 7 * 5 + extra, 5, 64)
+        assert np.array_equal(got, _ref(sigma, n_sv, 7 * 5 + extra, 5, 64)), extra
+    # one block with all of the largest values, all values equal, single block
+    sigma = np.zeros((3, 16), np.float32)
+    sigma[1] = 9.0
+    got = _gpu(sigma, np.full(3, 16, np.int32), 20, 2, 16)
+    assert list(got) == [2, 16, 2]
+    got = _gpu(np.full((1, 8), 2.0, np.float32), np.array([8], np.int32), 5, 0, 8)
+    assert list(got) == [5]
+
+
+@pytest.mark.parametrize("bad,block", [("increasing", 2), ("negative", 1), ("nan", 3), ("inf", 0)])
+def test_alloc_rejects_bad_rows(bad, block):
+    sigma = np.tile(np.linspace(3.0, 0.0, 32, dtype=np.float32), (5, 1))
+    if bad == "increasing":
+        sigma[block, 10] = sigma[block, 9] + 0.5
+    elif bad == "negative":
+        sigma[block, 31] = -1.0
+    elif bad == "nan":
+        sigma[block, 4] = np.nan
+    else:
+        sigma[block, 0] = np.inf
+    if bad != "increasing":
+        sigma[4, 20] = sigma[4, 19] + 1.0   # a later bad block: the message names the lowest
+    with pytest.raises(milo.MiloError) as ei:
+        _gpu(sigma, np.full(5, 32, np.int32), 60, 4, 20)
+    assert ei.value.code == milo.MILO_ERR_INVALID_ARG
+    assert f"block {block}:" in str(ei.value)
+    # the same rows after the bad block is fixed allocate normally
+    ok = np.tile(np.linspace(3.0, 0.0, 32, dtype=np.float32), (5, 1))
+    assert np.array_equal(_gpu(ok, np.full(5, 32, np.int32), 60, 4, 20),
+                          _ref(ok, np.full(5, 32, np.int32), 60, 4, 20))
+
+
+def test_allocated_ranks_drive_a_decode_step():
+    # the encoder's output feeds the cache: allocate K and V ranks from two
+    # spectra of the tiny workload's shape, then a decode step over factors of
+    # those ranks matches the oracle
+    cfg = synth.CONFIGS["tiny"]
+    sk, sv = synth.gen_spectra(cfg, layer=0), synth.gen_spectra(cfg, layer=1)
+    rk = _gpu(sk.sigma, sk.n_sv, sk.r_total, sk.r_min, sk.r_max)
+    rv = _gpu(sv.sigma, sv.n_sv, sv.r_total, sv.r_min, sv.r_max)
+    assert np.array_equal(rk, _ref(sk.sigma, sk.n_sv, sk.r_total, sk.r_min, sk.r_max))
+    inp = synth.make_problem(11, synth.draw_block_tokens(cfg).tolist(), rk.tolist(), rv.tolist(),
+                             n_kv_heads=cfg.n_kv_heads, head_dim=cfg.head_dim, n_q=2, n_q_heads=cfg.n_q_heads,
+                             tail_cap=cfg.tail)
+    gl = GpuLayer(inp)
+    try:
+        got = gl.attend().cpu().numpy()
+    finally:
+        gl.free()
+    assert max_rel_l2(got, oracle.attend_latent(**oracle_args(inp))) <= 1e-2
+
+
+def test_alloc_timing_counts_calls():
+    sp = synth.gen_spectra("tiny")
+    milo.milo_timing_read_alloc()
+    milo.milo_timing_enable(True)
+    try:
+        for _ in range(3):
+            _gpu(sp.sigma, sp.n_sv, sp.r_total, sp.r_min, sp.r_max)
+    finally:
+        milo.milo_timing_enable(False)
+    chain, hist, n = milo.milo_timing_read_alloc()
+    assert n == 3 and 0 < hist <= chain
