@@ -15,6 +15,8 @@ Prints one JSON line (see the fields below).  --gpus above 1 is rejected: this
 path runs on one GPU.  --prefill N measures instead the causal prefill of one
 request's chunk of N tokens (milo_attend_prefill) on the workload's first layer,
 after the workload's tail length of earlier tokens, and prints one JSON line for it.
+--alloc measures instead the encoder's entropy rank allocation (milo_allocate_ranks)
+on one layer's synthetic key spectra with the workload's block sizes.
 """
 from __future__ import annotations
 
@@ -174,6 +176,71 @@ def run_prefill(args, cfg, dev):
     print(json.dumps(result), flush=True)
 
 
+def run_alloc(args, cfg, dev):
+    """Time the encoder's entropy rank allocation (milo_allocate_ranks) on one
+    layer's synthetic key spectra of the workload's block structure."""
+    import torch
+    from paper_2609_29913_amd import milo
+    import oracle
+    sp = synth.gen_spectra(cfg, 0)
+    sig = torch.from_numpy(sp.sigma).to(dev)
+    call = lambda: milo.milo_allocate_ranks(sig, sp.n_sv, sp.r_total, sp.r_min, sp.r_max)
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ranks = call()
+    ms_per_call = (time.perf_counter() - t0) * 1e3 / args.steps
+    milo.milo_timing_read_alloc()
+    milo.milo_timing_enable(True)
+    for _ in range(args.steps):
+        call()
+    milo.milo_timing_enable(False)
+    chain_ms, hist_ms, n_calls = milo.milo_timing_read_alloc()
+    n_values = int(sp.n_sv.sum())
+    # one histogram pass must read every singular value once (the first pass
+    # checks them all, the others select among the candidates of the same rows)
+    pass_bytes = 4 * n_values
+    hist_s = hist_ms / (4 * n_calls) * 1e-3
+    chain_s = chain_ms / n_calls * 1e-3
+    alloc_bytes = 4 * n_values + 4 * len(sp.n_sv)  # the whole allocation: values once, ranks out
+    gbs = pass_bytes / hist_s / 1e9
+    budget = 10.0 if args.cpu_budget is None else args.cpu_budget
+    cpu = None
+    if not args.no_cpu_baseline:
+        rows = [sp.sigma[b, :n].astype(np.float64) for b, n in enumerate(sp.n_sv)]
+        times, t_start = [], time.perf_counter()
+        while not times or (time.perf_counter() - t_start < budget and len(times) < 20):
+            t1 = time.perf_counter()
+            ref = oracle.allocate_ranks(rows, sp.r_total, sp.r_min, sp.r_max)
+            times.append(time.perf_counter() - t1)
+        if not np.array_equal(ref, ranks):
+            raise RuntimeError("allocation differs from the oracle")
+        cpu = {"value": 1.0 / float(np.median(times)), "unit": "allocations/s", "cores": 1, "kind": "oracle",
+               "sample": f"the same allocation (greedy over marginal gains, numpy, one thread), "
+                         f"{len(times)} runs, median"}
+    result = {
+        "metric": "entropy rank allocations per second (one layer's blocks, 1 GPU) + % of HBM roofline",
+        "value": 1e3 / ms_per_call, "unit": "allocations/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_call, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic power-law singular-value spectra with ties (seeded), the workload's block sizes",
+        "config": {"workload": f"{cfg.name}_rank_allocation", "mode": "allocation", "blocks": len(sp.n_sv),
+                   "singular_values": n_values, "budget": sp.r_total, "r_min": sp.r_min, "r_max": sp.r_max,
+                   "ms_per_call_includes": "host checks, workspace hipMalloc/hipFree, upload, kernels, "
+                                           "read-back, synchronisation"},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None, "kernel": "alloc_hist_kernel",
+                     "kernel_avg_us": hist_s * 1e6, "algorithmic_bytes_per_launch": pass_bytes,
+                     "chain_avg_us": chain_s * 1e6, "chain_algorithmic_bytes": alloc_bytes,
+                     "chain_hbm_frac": alloc_bytes / chain_s / 1e9 / HBM_PEAK_GBS,
+                     "kernel_source_sha256_16": kernel_source_hash()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def cpu_baseline(inp: synth.LayerInputs, n_layers: int, budget_s: float):
     """The CPU oracle (fp64 numpy, latent order) timed on this host on the same
     workload: whole layer steps repeated until ~budget_s of CPU work."""
@@ -251,6 +318,8 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true", help="only run a 1 GiB device copy (counter scaling)")
     ap.add_argument("--prefill", type=int, default=0, metavar="N",
                     help="time the causal prefill of an N-token chunk of one request instead (first layer)")
+    ap.add_argument("--alloc", action="store_true",
+                    help="time the encoder's entropy rank allocation on the workload's block structure instead")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -272,11 +341,14 @@ def main():
 
     cfg = synth.CONFIGS[args.config]
     if args.steps is None:
-        args.steps = 500 if cfg.n_layers == 1 else 10
+        args.steps = 200 if args.alloc else 500 if cfg.n_layers == 1 else 10
     if args.warmup is None:
-        args.warmup = 200 if cfg.n_layers == 1 else 2
+        args.warmup = 20 if args.alloc else 200 if cfg.n_layers == 1 else 2
     if args.prefill > 0:
         run_prefill(args, cfg, dev)
+        return
+    if args.alloc:
+        run_alloc(args, cfg, dev)
         return
     # layers are generated one at a time and only their device state is kept
     # (a 64-layer workload's host factors would not fit next to each other)

@@ -1,6 +1,7 @@
 // Device side of the entropy rank allocation (Sec. 4.3, Eqs. 5-7): a radix
-// select of the k-th largest candidate singular value over all blocks, then
-// per-block counts and the block-ordered hand-out of equal values.
+// select of the k-th largest candidate singular value over all blocks (four
+// histogram passes of 8 bits), then per-block counts and the block-ordered
+// hand-out of equal values.
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -18,61 +19,97 @@ constexpr int kAssignThreads = 1024;
 // their bit patterns.
 __device__ inline uint32_t sv_key(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }
 
+constexpr int kHistGrid = 1024;  // histogram workgroups at most (grid-stride over row chunks)
+
 __global__ __launch_bounds__(kSelThreads) void alloc_init_kernel(AllocState* st, uint32_t k) {
-  st->hist[threadIdx.x] = 0;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) st->hist[p][threadIdx.x] = 0;
   if (threadIdx.x == 0) {
-    st->prefix = 0;
-    st->mask = 0;
-    st->k_rem = k;
+    st->k = k;
     st->bad_block = INT_MAX;
   }
 }
 
-// One radix pass: histogram of digit (key >> shift) & 255 over the candidates
-// whose higher bits match the prefix fixed so far.  One workgroup covers 256
-// columns of one row; the first pass also checks every value of the row.
-__global__ __launch_bounds__(kSelThreads) void alloc_hist_kernel(AllocArgs a, int shift, int check) {
-  __shared__ uint32_t h[256];
-  const int b = blockIdx.x / a.chunks;
-  const int j = (blockIdx.x % a.chunks) * kSelThreads + threadIdx.x;
-  h[threadIdx.x] = 0;
-  __syncthreads();
-  const AllocBounds bd = a.bounds[b];
-  const uint32_t prefix = a.st->prefix, mask = a.st->mask;
-  if (j < bd.n_sv) {
-    const float* row = a.sigma + (int64_t)b * a.ld;
-    const float x = row[j];
-    if (check) {
-      bool bad = !(x >= 0.0f) || !(x < __builtin_huge_valf());  // negative, infinite or NaN
-      if (j + 1 < bd.n_sv && row[j + 1] > x) bad = true;         // increasing
-      if (bad) atomicMin(&a.st->bad_block, b);
+// The digits picked by the first `passes` radix passes, derived by one wave
+// (every lane gets the result): in pass p, the digit is the one whose bin holds
+// the k_rem-th largest key among those matching the prefix fixed so far; k_rem
+// then drops by the keys in higher bins.  Lane l holds bins 4l .. 4l+3.
+__device__ inline void replay_picks(const AllocState* st, int passes, uint32_t& prefix, uint32_t& mask,
+                                    uint32_t& k_rem) {
+  const int lane = threadIdx.x & 63;
+  uint32_t k = st->k;
+  prefix = 0;
+  mask = 0;
+  uint4 hp[4];  // every pass's bins first: the loads do not depend on the picks
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+    if (p < passes) hp[p] = *reinterpret_cast<const uint4*>(&st->hist[p][4 * lane]);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    if (p >= passes) break;
+    const uint4 h = hp[p];
+    const uint32_t own = h.x + h.y + h.z + h.w;
+    uint32_t suf = own;  // keys in bins >= 4 * lane
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_down(suf, o);
+      if (lane + o < 64) suf += y;
     }
-    const uint32_t key = sv_key(x);
-    if (j >= bd.lo && j < bd.hi && (key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
+    // suf does not increase with the lane and lane 0 holds every matching key
+    // (>= k), so the lanes with suf >= k are 0 .. L
+    const int L = __popcll(__ballot(suf >= k)) - 1;
+    uint32_t above = __shfl(suf - own, L);
+    const uint32_t b3 = __shfl(h.w, L), b2 = __shfl(h.z, L), b1 = __shfl(h.y, L);
+    int d = 4 * L + 3;
+    if (above + b3 < k) {
+      above += b3;
+      --d;
+      if (above + b2 < k) {
+        above += b2;
+        --d;
+        if (above + b1 < k) {
+          above += b1;
+          --d;
+        }
+      }
+    }
+    k -= above;
+    prefix |= (uint32_t)d << (24 - 8 * p);
+    mask |= 255u << (24 - 8 * p);
+  }
+  k_rem = k;
+}
+
+// Radix pass `pass`: histogram of digit (key >> (24 - 8 pass)) & 255 over the
+// candidates whose higher bits match the digits picked so far.  A workgroup
+// walks 256-column chunks of the rows; the first pass also checks every value.
+__global__ __launch_bounds__(kSelThreads) void alloc_hist_kernel(AllocArgs a, int pass) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  uint32_t prefix, mask, k_rem;
+  replay_picks(a.st, pass, prefix, mask, k_rem);
+  __syncthreads();
+  const int shift = 24 - 8 * pass;
+  const int items = a.n_blocks * a.chunks;
+  for (int it = blockIdx.x; it < items; it += gridDim.x) {
+    const int b = it / a.chunks;
+    const int j = (it % a.chunks) * kSelThreads + threadIdx.x;
+    const AllocBounds bd = a.bounds[b];
+    if (j < bd.n_sv) {
+      const float* row = a.sigma + (int64_t)b * a.ld;
+      const float x = row[j];
+      if (pass == 0) {
+        bool bad = !(x >= 0.0f) || !(x < __builtin_huge_valf());  // negative, infinite or NaN
+        if (j + 1 < bd.n_sv && row[j + 1] > x) bad = true;         // increasing
+        if (bad) atomicMin(&a.st->bad_block, b);
+      }
+      const uint32_t key = sv_key(x);
+      if (j >= bd.lo && j < bd.hi && (key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
+    }
   }
   __syncthreads();
   const uint32_t v = h[threadIdx.x];
-  if (v) atomicAdd(&a.st->hist[threadIdx.x], v);
-}
-
-// Picks the digit that holds the k_rem-th largest matching key, fixes it in
-// the prefix and clears the histogram for the next pass.
-__global__ __launch_bounds__(64) void alloc_pick_kernel(AllocState* st, int shift) {
-  if (threadIdx.x == 0) {
-    const uint32_t k = st->k_rem;
-    uint32_t above = 0;
-    int d = 255;
-    for (; d > 0; --d) {
-      const uint32_t c = st->hist[d];
-      if (above + c >= k) break;
-      above += c;
-    }
-    st->k_rem = k - above;
-    st->prefix |= (uint32_t)d << shift;
-    st->mask |= 255u << shift;
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < 256; i += 64) st->hist[i] = 0;
+  if (v) atomicAdd(&a.st->hist[pass][threadIdx.x], v);
 }
 
 // Per block (one wave each): candidates above and equal to the selected key.
@@ -81,7 +118,8 @@ __global__ __launch_bounds__(kSelThreads) void alloc_count_kernel(AllocArgs a) {
   const int lane = threadIdx.x & 63;
   if (b >= a.n_blocks) return;
   const AllocBounds bd = a.bounds[b];
-  const uint32_t tau = a.st->prefix;
+  uint32_t tau, mask, k_rem;
+  replay_picks(a.st, 4, tau, mask, k_rem);
   const float* row = a.sigma + (int64_t)b * a.ld;
   int gt = 0, eq = 0;
   for (int j = bd.lo + lane; j < bd.hi; j += 64) {
@@ -105,7 +143,9 @@ __global__ __launch_bounds__(kSelThreads) void alloc_count_kernel(AllocArgs a) {
 __global__ __launch_bounds__(kAssignThreads) void alloc_assign_kernel(AllocArgs a) {
   __shared__ int64_t wsum[kAssignThreads / 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t units = a.st->k_rem;
+  uint32_t tau, mask, k_rem;
+  replay_picks(a.st, 4, tau, mask, k_rem);
+  const int64_t units = k_rem;
   int64_t carry = 0;
   for (int base = 0; base < a.n_blocks; base += kAssignThreads) {
     const int b = base + threadIdx.x;
@@ -141,17 +181,13 @@ hipError_t launch_allocate(const AllocArgs& a, uint32_t k, hipStream_t s, hipEve
   if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return e;
   alloc_init_kernel<<<1, kSelThreads, 0, s>>>(a.st, k);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const unsigned grid = (unsigned)a.n_blocks * (unsigned)a.chunks;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    if (pass > 0 && k == 0) break;  // only the check
+  const int items = a.n_blocks * a.chunks;
+  const unsigned grid = (unsigned)(items < kHistGrid ? items : kHistGrid);
+  for (int pass = 0; pass < (k == 0 ? 1 : 4); ++pass) {
     if (ev && (e = hipEventRecord(ev[1 + 2 * pass], s)) != hipSuccess) return e;
-    alloc_hist_kernel<<<grid, kSelThreads, 0, s>>>(a, shift, pass == 0 ? 1 : 0);
+    alloc_hist_kernel<<<grid, kSelThreads, 0, s>>>(a, pass);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(ev[2 + 2 * pass], s)) != hipSuccess) return e;
-    if (k == 0) break;
-    alloc_pick_kernel<<<1, 64, 0, s>>>(a.st, shift);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (k > 0) {
     alloc_count_kernel<<<(a.n_blocks + 3) / 4, kSelThreads, 0, s>>>(a);

@@ -314,11 +314,10 @@ struct PackArgs {
 // then counts per block the candidates above it and hands the remaining units
 // at that value out in block order.
 struct AllocState {
-  uint32_t prefix;     // high bits of the k-th largest key fixed so far
-  uint32_t mask;       // which bits of prefix are fixed
-  uint32_t k_rem;      // rank of the wanted key among the keys that match prefix
-  int32_t bad_block;   // lowest block whose row breaks the precondition (INT32_MAX: none)
-  uint32_t hist[256];  // digit histogram of the current pass
+  uint32_t k;              // units to hand out beyond the floors
+  int32_t bad_block;       // lowest block whose row breaks the precondition (INT32_MAX: none)
+  uint32_t pad[62];
+  uint32_t hist[4][256];   // digit histogram of each radix pass (most significant first)
 };
 
 struct AllocBounds {
@@ -340,9 +339,10 @@ struct AllocArgs {
 };
 
 // Queues the whole selection (k units over the candidates, 0 < k < candidates)
-// or, with k == 0, only the state reset and the precondition check.  ev, when
-// non-NULL, receives 10 events: chain start, (start, end) of each of the four
-// histogram passes, chain end.
+// or, with k == 0, only the state reset and the precondition check.  Each pass
+// re-derives the digits picked so far from the earlier passes' histograms.  ev,
+// when non-NULL, receives 10 events: chain start, (start, end) of each of the
+// four histogram passes, chain end.
 hipError_t launch_allocate(const AllocArgs& a, uint32_t k, hipStream_t s, hipEvent_t* ev);
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
