@@ -862,7 +862,9 @@ int milo_allocate_ranks(const float* sigma, int64_t ld, int32_t n_blocks, const 
     std::lock_guard<std::mutex> lk(g_timing.mu);
     timed = g_timing.enabled;
   }
+  bool queued = false;  // once work is queued, it must finish before the workspace is freed
   auto done = [&](int code) {
+    if (queued) (void)hipStreamSynchronize(s);
     for (hipEvent_t e : ev)
       if (e) (void)hipEventDestroy(e);
     (void)hipFree(ws);
@@ -881,6 +883,7 @@ int milo_allocate_ranks(const float* sigma, int64_t ld, int32_t n_blocks, const 
   a.st = (AllocState*)(ws + off_state);
   a.cnt = (int32_t*)(ws + off_cnt);
   a.ranks = (int32_t*)(ws + off_rank);
+  queued = true;
   if ((e = hipMemcpyAsync(ws + off_b, bounds.data(), bounds.size() * sizeof(AllocBounds), hipMemcpyHostToDevice,
                           s)) != hipSuccess)
     return done(hip_fail(e, "hipMemcpyAsync(bounds)"));
