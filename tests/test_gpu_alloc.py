@@ -142,3 +142,51 @@ def test_alloc_timing_counts_calls():
         milo.milo_timing_enable(False)
     chain, hist, n = milo.milo_timing_read_alloc()
     assert n == 3 and 0 < hist <= chain
+
+
+def _check_threshold_property(sigma, n_sv, ranks, r_total, r_min, r_max):
+    """Properties of the greedy's result that hold at any size: bounds, the sum,
+    and every handed-out candidate is >= every candidate left out, with equal
+    values handed out in block order."""
+    lo, hi = np.minimum(r_min, n_sv), np.minimum(r_max, n_sv)
+    assert np.all(ranks >= lo) and np.all(ranks <= hi)
+    assert ranks.sum() == min(r_total, int(hi.sum()))
+    taken_min, left_max = np.inf, -np.inf
+    taken_min_block, left_max_block = -1, -1
+    for b in range(len(n_sv)):
+        if ranks[b] > lo[b]:
+            v = float(sigma[b, ranks[b] - 1])   # the smallest value block b took
+            if v < taken_min or (v == taken_min and b > taken_min_block):
+                taken_min, taken_min_block = v, b
+        if ranks[b] < hi[b]:
+            v = float(sigma[b, ranks[b]])       # the largest value block b left
+            if v > left_max or (v == left_max and b < left_max_block):
+                left_max, left_max_block = v, b
+    assert taken_min >= left_max
+    if taken_min == left_max:                   # a tie split between blocks: lower index first
+        assert taken_min_block <= left_max_block or taken_min_block == -1
+
+
+def test_alloc_at_large_size_by_properties():
+    # 16384 blocks x 1024 values: past what the step-by-step oracle finishes in
+    # seconds, so the result is checked by the properties above
+    rng = np.random.default_rng(77)
+    n, ld = 16384, 1024
+    n_sv = rng.choice(np.array([256, 512, 1024], dtype=np.int32), n)
+    expo = rng.uniform(0.2, 1.6, n)[:, None]
+    sigma = (rng.lognormal(0, 0.5, n)[:, None] * np.arange(1, ld + 1)[None, :] ** -expo).astype(np.float32)
+    sigma = np.round(sigma * 4096) / 4096          # coarse grid: many ties across blocks
+    sigma = np.minimum.accumulate(sigma, axis=1).astype(np.float32)
+    sigma[np.arange(ld)[None, :] >= n_sv[:, None]] = np.nan
+    r_total = int(0.3 * n_sv.sum())
+    print(f"allocation {n} blocks, {int(n_sv.sum())} values, budget {r_total}", flush=True)
+    got = _gpu(sigma, n_sv, r_total, 16, 896)
+    _check_threshold_property(sigma, n_sv, got, r_total, 16, 896)
+
+
+def test_threshold_property_holds_for_the_oracle():
+    # the property check itself against the oracle on a mid-size problem
+    sigma, n_sv, r_total, r_min, r_max = _random_problem(3)
+    ref = _ref(sigma, n_sv, r_total, r_min, r_max)
+    _check_threshold_property(sigma, n_sv, ref, r_total, r_min, r_max)
+    assert np.array_equal(_gpu(sigma, n_sv, r_total, r_min, r_max), ref)

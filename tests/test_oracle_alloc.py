@@ -174,3 +174,24 @@ def test_workload_spectra_are_valid():
     r = oracle.allocate_ranks([sp.sigma[b, :n] for b, n in enumerate(sp.n_sv)], sp.r_total, sp.r_min,
                               sp.r_max)
     assert r.sum() == sp.r_total and r.min() >= sp.r_min and r.max() <= sp.r_max
+
+
+def test_exhaustive_search_hypothesis():
+    # random small problems drawn by hypothesis, with equal values allowed: the
+    # greedy reaches the exhaustive optimum of Eq. 6 (several maximisers may tie)
+    hyp = pytest.importorskip("hypothesis")
+    st = pytest.importorskip("hypothesis.strategies")
+
+    @hyp.settings(max_examples=150, deadline=None, derandomize=True)
+    @hyp.given(st.lists(st.lists(st.integers(0, 6), min_size=0, max_size=5), min_size=1, max_size=3),
+               st.integers(0, 3), st.integers(0, 5), st.integers(0, 9))
+    def check(rows, r_min, r_span, extra):
+        sig = [np.array(sorted(r, reverse=True), dtype=np.float64) for r in rows]
+        r_max = r_min + r_span
+        floor = sum(min(r_min, len(s)) for s in sig)
+        best, arg = _exhaustive(sig, floor + extra, r_min, r_max, 1.0)
+        got = oracle.allocate_ranks(sig, floor + extra, r_min, r_max, 1.0)
+        h = sum(oracle.spectral_information(s, int(r), 1.0) for s, r in zip(sig, got))
+        assert abs(h - best) <= 1e-9 and tuple(int(x) for x in got) in arg
+
+    check()
