@@ -288,7 +288,28 @@ def device_env(dev, n_bytes=1 << 30, reps=5):
     return {"host": socket.gethostname(), "python": platform.python_version(), "torch": torch.__version__,
             "hip": getattr(torch.version, "hip", None), "gpu": props.name,
             "arch": getattr(props, "gcnArchName", None), "compute_units": props.multi_processor_count,
-            "device_copy_gbs": copy_gbs}
+            "device_copy_gbs": copy_gbs, "gpu_clocks": gpu_clocks()}
+
+
+def gpu_clocks():
+    """Graphics clock levels the driver supports (rocm-smi --showclkfrq, MHz) and the
+    level active when read (between runs the GPU idles at its lowest), or None."""
+    import shutil
+    import subprocess
+    exe = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
+    try:
+        out = subprocess.run([exe, "--showclkfrq"], capture_output=True, text=True, timeout=30).stdout
+    except (OSError, subprocess.SubprocessError):
+        return None
+    sec = out.split("Supported sclk frequencies", 1)
+    if len(sec) < 2:
+        return None
+    body = sec[1].split("Supported", 1)[0]
+    levels = [(int(m.group(1)), "*" in m.group(0)) for m in re.finditer(r"(\d+)\s*Mhz\s*\*?", body, re.I)]
+    if not levels:
+        return None
+    return {"sclk_levels_mhz": [v for v, _ in levels], "sclk_max_mhz": max(v for v, _ in levels),
+            "sclk_active_when_read_mhz": next((v for v, cur in levels if cur), None)}
 
 
 def calibrate_copy(dev, n_bytes=1 << 30, reps=5):
