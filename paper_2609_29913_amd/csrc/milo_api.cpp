@@ -71,9 +71,6 @@ struct TimingState {
   bool enabled = false;
   std::vector<hipEvent_t> pool;
   std::vector<hipEvent_t> recorded;  // groups of 4: attend kernel start / end, merge kernel start / end
-  double alloc_chain_ms = 0.0;       // rank allocation: whole kernel chain
-  double alloc_hist_ms = 0.0;        // rank allocation: the histogram passes
-  int64_t alloc_calls = 0;
 };
 TimingState g_timing;
 
@@ -445,6 +442,15 @@ void destroy(milo_cache* c) {
 
 }  // namespace
 
+namespace milo {
+void clear_error() { g_err.clear(); }
+int report_error(int code, const char* msg) { return fail(code, "%s", msg); }
+bool timing_enabled() {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  return g_timing.enabled;
+}
+}  // namespace milo
+
 extern "C" {
 
 const char* milo_last_error(void) { return g_err.c_str(); }
@@ -812,111 +818,6 @@ int milo_attend_prefill(milo_cache* c, const int32_t* block_table, int32_t n_sel
                 hip_stream);
 }
 
-int milo_allocate_ranks(const float* sigma, int64_t ld, int32_t n_blocks, const int32_t* n_sv, int64_t r_total,
-                        int32_t r_min, int32_t r_max, int32_t* ranks, void* hip_stream) {
-  g_err.clear();
-  if (!sigma || !n_sv || !ranks) return fail(MILO_ERR_INVALID_ARG, "sigma, n_sv and ranks must be non-NULL");
-  if (n_blocks < 1) return fail(MILO_ERR_INVALID_ARG, "n_blocks must be >= 1 (got %d)", n_blocks);
-  if (ld < 1) return fail(MILO_ERR_INVALID_ARG, "ld must be >= 1");
-  if (r_min < 0 || r_max < r_min)
-    return fail(MILO_ERR_INVALID_ARG, "need 0 <= r_min <= r_max (got %d, %d)", r_min, r_max);
-  std::vector<AllocBounds> bounds(n_blocks);
-  int64_t floor_sum = 0, cand = 0;
-  int32_t max_sv = 0;
-  for (int b = 0; b < n_blocks; ++b) {
-    if (n_sv[b] < 0 || n_sv[b] > ld)
-      return fail(MILO_ERR_INVALID_ARG, "block %d: n_sv %d outside [0, ld=%lld]", b, n_sv[b], (long long)ld);
-    AllocBounds& bd = bounds[b];
-    bd.n_sv = n_sv[b];
-    bd.lo = std::min(r_min, n_sv[b]);
-    bd.hi = std::min(r_max, n_sv[b]);
-    bd.pad = 0;
-    floor_sum += bd.lo;
-    cand += bd.hi - bd.lo;
-    max_sv = std::max(max_sv, n_sv[b]);
-  }
-  if (r_total < floor_sum)
-    return fail(MILO_ERR_INVALID_ARG, "budget %lld is below the sum of the floors %lld (no feasible allocation)",
-                (long long)r_total, (long long)floor_sum);
-  if (cand >= ((int64_t)1 << 31))
-    return fail(MILO_ERR_UNSUPPORTED, "%lld candidate singular values exceed the supported 2^31", (long long)cand);
-  const int32_t chunks = std::max(1, (max_sv + 255) / 256);
-  if ((int64_t)n_blocks * chunks >= ((int64_t)1 << 31))
-    return fail(MILO_ERR_UNSUPPORTED, "too many rows for one launch");
-  // k units go to the largest candidates; none or all of them is the closed form
-  // (floors or caps), but the values are still checked on the device
-  const int64_t k = r_total - floor_sum;
-  const bool select = k > 0 && k < cand;
-  hipStream_t s = (hipStream_t)hip_stream;
-  const size_t off_state = 0;  // workspace: state, bounds, counts, ranks
-  const size_t st_bytes = (sizeof(AllocState) + 255) / 256 * 256;
-  const size_t off_b = off_state + st_bytes;
-  const size_t off_cnt = off_b + (size_t)n_blocks * sizeof(AllocBounds);
-  const size_t off_rank = off_cnt + 2 * (size_t)n_blocks * sizeof(int32_t);
-  const size_t total = off_rank + (size_t)n_blocks * sizeof(int32_t);
-  char* ws = nullptr;
-  MILO_HIP(hipMalloc((void**)&ws, total));
-  hipEvent_t ev[10] = {};
-  bool timed = false;
-  {
-    std::lock_guard<std::mutex> lk(g_timing.mu);
-    timed = g_timing.enabled;
-  }
-  bool queued = false;  // once work is queued, it must finish before the workspace is freed
-  auto done = [&](int code) {
-    if (queued) (void)hipStreamSynchronize(s);
-    for (hipEvent_t e : ev)
-      if (e) (void)hipEventDestroy(e);
-    (void)hipFree(ws);
-    return code;
-  };
-  hipError_t e;
-  if (timed)
-    for (hipEvent_t& x : ev)
-      if ((e = hipEventCreate(&x)) != hipSuccess) return done(hip_fail(e, "hipEventCreate"));
-  AllocArgs a{};
-  a.sigma = sigma;
-  a.ld = ld;
-  a.n_blocks = n_blocks;
-  a.chunks = chunks;
-  a.bounds = (const AllocBounds*)(ws + off_b);
-  a.st = (AllocState*)(ws + off_state);
-  a.cnt = (int32_t*)(ws + off_cnt);
-  a.ranks = (int32_t*)(ws + off_rank);
-  queued = true;
-  if ((e = hipMemcpyAsync(ws + off_b, bounds.data(), bounds.size() * sizeof(AllocBounds), hipMemcpyHostToDevice,
-                          s)) != hipSuccess)
-    return done(hip_fail(e, "hipMemcpyAsync(bounds)"));
-  if ((e = launch_allocate(a, select ? (uint32_t)k : 0u, s, timed ? ev : nullptr)) != hipSuccess)
-    return done(hip_fail(e, "allocation kernels"));
-  int32_t bad = INT32_MAX;
-  if ((e = hipMemcpyAsync(&bad, &a.st->bad_block, sizeof bad, hipMemcpyDeviceToHost, s)) != hipSuccess)
-    return done(hip_fail(e, "hipMemcpyAsync(check)"));
-  std::vector<int32_t> got(select ? n_blocks : 0);
-  if (select && (e = hipMemcpyAsync(got.data(), a.ranks, got.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
-                    hipSuccess)
-    return done(hip_fail(e, "hipMemcpyAsync(ranks)"));
-  if ((e = hipStreamSynchronize(s)) != hipSuccess) return done(hip_fail(e, "hipStreamSynchronize"));
-  if (bad != INT32_MAX)
-    return done(fail(MILO_ERR_INVALID_ARG,
-                     "block %d: singular values must be finite, non-negative and non-increasing", bad));
-  if (timed) {
-    float chain = 0.f, hist = 0.f, t = 0.f;
-    if ((e = hipEventElapsedTime(&chain, ev[0], ev[9])) != hipSuccess) return done(hip_fail(e, "hipEventElapsedTime"));
-    for (int p = 0; p < (select ? 4 : 1); ++p) {
-      if ((e = hipEventElapsedTime(&t, ev[1 + 2 * p], ev[2 + 2 * p])) != hipSuccess)
-        return done(hip_fail(e, "hipEventElapsedTime"));
-      hist += t;
-    }
-    std::lock_guard<std::mutex> lk(g_timing.mu);
-    g_timing.alloc_chain_ms += chain;
-    g_timing.alloc_hist_ms += hist;
-    g_timing.alloc_calls += 1;
-  }
-  for (int b = 0; b < n_blocks; ++b) ranks[b] = select ? got[b] : (k == 0 ? bounds[b].lo : bounds[b].hi);
-  return done(MILO_OK);
-}
-
 int milo_timing_enable(int enable) {
   g_err.clear();
   std::lock_guard<std::mutex> lk(g_timing.mu);
@@ -946,15 +847,5 @@ int milo_timing_read(double* attend_kernel_ms, double* merge_kernel_ms, int64_t*
   return MILO_OK;
 }
 
-int milo_timing_read_alloc(double* chain_ms, double* hist_ms, int64_t* n_calls) {
-  g_err.clear();
-  std::lock_guard<std::mutex> lk(g_timing.mu);
-  if (chain_ms) *chain_ms = g_timing.alloc_chain_ms;
-  if (hist_ms) *hist_ms = g_timing.alloc_hist_ms;
-  if (n_calls) *n_calls = g_timing.alloc_calls;
-  g_timing.alloc_chain_ms = g_timing.alloc_hist_ms = 0.0;
-  g_timing.alloc_calls = 0;
-  return MILO_OK;
-}
 
 }  // extern "C"
