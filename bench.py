@@ -43,9 +43,12 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_29913_amd", "csrc", f)
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "attend_kernel_q7b_1l_counters.md")
 
 
-def kernel_source_hash() -> str:
+ALLOC_SOURCES = [os.path.join(ROOT, "paper_2609_29913_amd", "csrc", f) for f in ("milo_alloc.hip", "milo_alloc.h")]
+
+
+def kernel_source_hash(sources=None) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in (KERNEL_SOURCES if sources is None else sources):
         with open(p, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -235,7 +238,7 @@ def run_alloc(args, cfg, dev):
                      "kernel_avg_us": hist_s * 1e6, "algorithmic_bytes_per_launch": pass_bytes,
                      "chain_avg_us": chain_s * 1e6, "chain_algorithmic_bytes": alloc_bytes,
                      "chain_hbm_frac": alloc_bytes / chain_s / 1e9 / HBM_PEAK_GBS,
-                     "kernel_source_sha256_16": kernel_source_hash()},
+                     "kernel_source_sha256_16": kernel_source_hash(ALLOC_SOURCES)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)
