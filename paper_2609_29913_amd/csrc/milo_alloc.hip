@@ -1,7 +1,8 @@
-// Device side of the entropy rank allocation (Sec. 4.3, Eqs. 5-7): a radix
-// select of the k-th largest candidate singular value over all blocks (four
-// histogram passes of 8 bits), then per-block counts and the block-ordered
-// hand-out of equal values.
+// Entropy rank allocation of the encoder (Sec. 4.3, Eqs. 5-7): the device side
+// (a radix select of the k-th largest candidate singular value over all blocks
+// in four histogram passes of 8 bits, then per-block counts and the
+// block-ordered hand-out of equal values) and the host entry point
+// milo_allocate_ranks of the C ABI.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
