@@ -5,11 +5,14 @@ One step = one milo_attend_decode per layer of the workload: latent query
 projection, scores + online softmax + latent V, up-projection, dense tail and
 the log-sum-exp merge, for every query column of the decode batch.  Inputs are
 seeded synthetic tensors with the workload's shapes, resident in HBM before the
-timed region.  The default workload is a Qwen2.5-7B-shaped layer (28 query /
-4 KV heads, d=128, 64 blocks x 1024 tokens, ranks 64..512, 256-token dense tail
-per request, 8 decode queries).  A single-layer working set (~117 MB) fits in
-the 256 MB Infinity Cache, so steps rotate over independent copies of the layer
-(each with its own cache, queries and tails) until the rotation exceeds 512 MB.
+timed region.  The default workload is the largest that fits one GPU: a
+Qwen2.5-32B-shaped step of 64 layers (40 query / 8 KV heads, d=128, 1,048,576
+context tokens in ragged blocks of 512/1024/2048, ranks 128..512, 2048-token
+dense tail per request, 16 decode queries; ~170 GB of factors in HBM).  Other
+workloads via --config; a single-layer working set (e.g. the 7B-shaped layer,
+~117 MB) fits in the 256 MB Infinity Cache, so its steps rotate over
+independent copies of the layer (each with its own cache, queries and tails)
+until the rotation exceeds 512 MB.
 
 Prints one JSON line (see the fields below).  --gpus above 1 is rejected: this
 path runs on one GPU.  --prefill N measures instead the causal prefill of one
@@ -39,8 +42,7 @@ METRIC = "effective context tokens/s per decode step (1 GPU) + % of HBM roofline
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, AMD published
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_29913_amd", "csrc", f)
-                  for f in ("milo_kernels.hip", "milo_internal.h", "milo_api.cpp")]
-COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "attend_kernel_q7b_1l_counters.md")
+                  for f in ("milo_kernels.hip", "milo_internal.h", "milo_api.cpp", "milo_plan.cpp", "milo_plan.h")]
 
 
 ALLOC_SOURCES = [os.path.join(ROOT, "paper_2609_29913_amd", "csrc", f) for f in ("milo_alloc.hip", "milo_alloc.h")]
@@ -54,12 +56,18 @@ def kernel_source_hash(sources=None) -> str:
     return h.hexdigest()[:16]
 
 
+def counter_summary(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"attend_kernel_{workload}_counters.md")
+
+
 def counter_traffic(workload: str):
     """HBM bytes per attention-kernel launch from the committed rocprofv3 counter
-    summary, or None when absent or taken on different kernel sources."""
-    if workload != "q7b_1l" or not os.path.exists(COUNTER_SUMMARY):
+    summary of this workload, or None when absent or taken on different kernel
+    sources."""
+    path = counter_summary(workload)
+    if not os.path.exists(path):
         return None
-    txt = open(COUNTER_SUMMARY).read()
+    txt = open(path).read()
     m = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
     hsh = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", txt)
     if not m or not hsh or hsh.group(1) != kernel_source_hash():
@@ -85,12 +93,17 @@ class Layer:
         self.tk = to_device(inp.tail_k, dev)
         self.tv = to_device(inp.tail_v, dev)
         self.out = torch.empty(inp.q.shape, dtype=torch.float32, device=dev)
-        self.table = list(range(inp.n_blocks))
+        self.table = np.arange(inp.n_blocks, dtype=np.int32)
         self.tail_len = inp.tail_len.copy()
+        self.tail_cap = inp.tail_cap
         self.scale = inp.scale
 
-    def step(self, stream):
+    def step(self, stream, grow: int = 0):
+        """One decode call; grow > 0 lengthens every request's tail by that many
+        tokens first (a decode loop appending each step's key and value)."""
         from paper_2609_29913_amd import milo
+        if grow:
+            self.tail_len = np.minimum(self.tail_len + grow, self.tail_cap)
         milo.milo_attend_decode(self.cache, self.table, self.q, self.tk, self.tv, self.tail_len, self.scale,
                                 self.out, stream=stream)
 
@@ -245,28 +258,38 @@ def run_alloc(args, cfg, dev):
 
 
 def cpu_baseline(inp: synth.LayerInputs, n_layers: int, budget_s: float):
-    """The CPU oracle (fp64 numpy, latent order) timed on this host on the same
-    workload: whole layer steps repeated until ~budget_s of CPU work."""
+    """The CPU oracle (numpy, latent order, run in fp32 on fp32 copies of the
+    bf16 inputs) timed on this host on the same workload.  A single-layer
+    workload is timed whole; a multi-layer one on layer 0 for query 0 with all
+    its heads, then scaled linearly by (n_q * H_q / H_q) columns and by the
+    layers (labelled extrapolated).  Repeated until ~budget_s of CPU work."""
     import oracle
     from threadpoolctl import threadpool_info
-    f64 = synth.bf16_to_f64
-    args = dict(pk=[f64(x) for x in inp.pk], rk=[f64(x) for x in inp.rk], pv=[f64(x) for x in inp.pv],
-                rv=[f64(x) for x in inp.rv], table=list(range(inp.n_blocks)), q=f64(inp.q),
-                tail_k=f64(inp.tail_k), tail_v=f64(inp.tail_v), tail_len=inp.tail_len, scale=inp.scale)
+    f32 = synth.bf16_to_f32
+    args = dict(pk=[f32(x) for x in inp.pk], rk=[f32(x) for x in inp.rk], pv=[f32(x) for x in inp.pv],
+                rv=[f32(x) for x in inp.rv], table=list(range(inp.n_blocks)), q=f32(inp.q),
+                tail_k=f32(inp.tail_k), tail_v=f32(inp.tail_v), tail_len=inp.tail_len, scale=inp.scale)
+    sampled = n_layers > 1
+    if sampled:
+        args["columns"] = [(0, h) for h in range(inp.n_q_heads)]
     times = []
     t_start = time.perf_counter()
     while not times or (time.perf_counter() - t_start < budget_s and len(times) < 50):
         t0 = time.perf_counter()
         oracle.attend_latent(**args)
         times.append(time.perf_counter() - t0)
-    t_layer = float(np.median(times))
+    t_run = float(np.median(times))
+    scale_up = inp.n_q * n_layers if sampled else 1          # columns and layers the sample stands for
+    t_step = t_run * scale_up
     tokens = inp.n_q * (int(inp.block_tokens.sum()) + int(inp.tail_len.max()))
     threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    return {"value": tokens / (t_layer * n_layers), "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"full layer step of the workload (fp64 numpy oracle, latent order), {len(times)} "
-                      f"repetitions, median {t_layer * 1e3:.1f} ms per layer"
-                      + (f", x{n_layers} layers" if n_layers > 1 else "")}
+    sample = (f"layer 0, query 0 with all {inp.n_q_heads} heads (fp32 numpy oracle, latent order), "
+              f"{len(times)} repetitions, median {t_run * 1e3:.1f} ms, extrapolated x{inp.n_q} queries "
+              f"x{n_layers} layers" if sampled else
+              f"full layer step (fp32 numpy oracle, latent order), {len(times)} repetitions, median "
+              f"{t_run * 1e3:.1f} ms")
+    return {"value": tokens / t_step, "unit": "tokens/s", "cores": int(threads), "host_cores": os.cpu_count(),
+            "kind": "oracle", "precision": "fp32", "extrapolated": sampled, "sample": sample}
 
 
 def device_env(dev, n_bytes=1 << 30, reps=5):
@@ -334,7 +357,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps first (default 200 for a single-layer workload, else 2); the "
                          "kernels reach their steady-state speed after ~100 back-to-back steps")
-    ap.add_argument("--config", default="q7b_1l", choices=sorted(synth.CONFIGS))
+    ap.add_argument("--config", default="q32b_64l", choices=sorted(synth.CONFIGS),
+                    help="workload (default: the largest that fits one GPU, the 32B-shaped 64-layer step)")
+    ap.add_argument("--grow-tails", action="store_true",
+                    help="decode loop: every request's tail grows by one token per step (warm-up and timed "
+                         "steps), ending at the workload's tail length")
     ap.add_argument("--rotate-bytes", type=float, default=512e6,
                     help="minimum bytes of distinct layer copies rotated over (defeats the Infinity Cache)")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
@@ -376,6 +403,9 @@ def main():
         return
     # layers are generated one at a time and only their device state is kept
     # (a 64-layer workload's host factors would not fit next to each other)
+    grow_from = 0
+    if args.grow_tails:
+        grow_from = max(1, cfg.tail - (args.warmup + args.steps) + 1)
     x0 = None
     per_step = flops_step = out_bytes = 0
     mean_ranks = []
@@ -397,23 +427,50 @@ def main():
     for _ in range(1, copies):
         groups.append([Layer(synth.gen_layer(cfg, l), dev) for l in range(cfg.n_layers)])
     stream = torch.cuda.current_stream()
+    if args.grow_tails:
+        for grp in groups:
+            for layer in grp:
+                layer.tail_len = np.full_like(layer.tail_len, grow_from - 1)
     torch.cuda.synchronize()
+    host_s = [0.0]
 
-    def run_step(k):
+    def run_step(k, grow=0):
         for layer in groups[k % copies]:
-            layer.step(stream)
+            h0 = time.perf_counter()
+            layer.step(stream, grow)
+            host_s[0] += time.perf_counter() - h0
 
+    grow = 1 if args.grow_tails else 0
     for k in range(args.warmup):
-        run_step(k)
+        run_step(k, grow)
     torch.cuda.synchronize()
 
     # timed region: exactly `steps` decode steps, host wall clock between synchronisations
+    builds0 = sum(milo.milo_cache_plan_builds(layer.cache) for grp in groups for layer in grp)
+    host_s[0] = 0.0
+    tail_sum = 0
     t0 = time.perf_counter()
     for k in range(args.steps):
-        run_step(k)
+        run_step(k, grow)
+        tail_sum += int(groups[k % copies][0].tail_len.max())
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
+    host_us_per_call = host_s[0] * 1e6 / (args.steps * cfg.n_layers)
+    plan_builds = sum(milo.milo_cache_plan_builds(layer.cache) for grp in groups for layer in grp) - builds0
+    mean_tail = tail_sum / args.steps
+
+    # host cost of a call with the device idle: one step enqueued after a
+    # synchronisation, a few times (the timed loop above runs ahead of the GPU
+    # until launches wait for queue space, so it cannot show this)
+    enq = []
+    for k in range(min(args.steps, 5)):
+        torch.cuda.synchronize()
+        h0 = time.perf_counter()
+        run_step(k)
+        enq.append(time.perf_counter() - h0)
+    torch.cuda.synchronize()
+    host_idle_us_per_call = float(np.median(enq)) * 1e6 / cfg.n_layers
 
     # second pass with HIP events around the attention kernel on the launch stream
     milo.milo_timing_enable(True)
@@ -445,7 +502,7 @@ def main():
     traffic = counter_traffic(args.config)
     t_roof = max(kern_bytes / (HBM_PEAK_GBS * 1e9), flops / (MFMA_BF16_PEAK_TFLOPS * 1e12))
 
-    ctx_tokens = int(x0.block_tokens.sum()) + int(x0.tail_len.max())
+    ctx_tokens = int(x0.block_tokens.sum()) + (mean_tail if args.grow_tails else int(x0.tail_len.max()))
     value = x0.n_q * ctx_tokens / (ms_per_step * 1e-3)
     result = {
         "metric": METRIC,
@@ -479,6 +536,13 @@ def main():
         },
         "step_us": {"median": float(np.median(step_us)), "min": float(step_us.min()),
                     "p90": float(np.percentile(step_us, 90)), "timing": "HIP events between steps"},
+        "host": {"us_per_call": host_idle_us_per_call, "us_per_call_in_timed_loop": host_us_per_call,
+                 "plan_builds_in_timed_steps": plan_builds,
+                 "tails": (f"growing one token per step, {grow_from}..{cfg.tail} (mean {mean_tail:.0f} in the "
+                           f"timed steps)") if args.grow_tails else "fixed",
+                 "timing": "host wall time inside milo_attend_decode calls (binding, checks, launches): "
+                           "us_per_call with the device idle (median over 5 steps enqueued after a "
+                           "synchronisation); in the timed loop it also holds waits for launch-queue space"},
         "roofline": {
             "bound": bound,
             "achieved": achieved if bound == "hbm" else mfma_tflops,

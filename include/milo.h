@@ -105,9 +105,15 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk,
  *   hip_stream    stream the work is queued on.
  * q, tail_k, tail_v and out are borrowed until the queued work completes.  The
  * cache's workspace is shared by its calls: calls on one cache must be ordered on
- * one stream (calls on different streams race).  Workspace growth and a change of
- * (block_table, n_q, H_q, tail_len, tail_cap) since the previous call allocate or
- * upload synchronously; repeated calls with the same arguments do neither.
+ * one stream (calls on different streams race).
+ * Work plan: built on the host when the block table, n_q, H_q or the planned
+ * tail capacity changes, where the capacity is the longest tail rounded up to a
+ * power of two of 256-token chunks, at most tail_cap.  A decode loop whose tails
+ * grow by a token per call therefore reuses its plan until the longest tail
+ * doubles: the tail lengths themselves travel in the kernel arguments (for
+ * n_q <= 256; larger batches copy them to the device in stream order).  A
+ * rebuild uploads in stream order without waiting for the device, unless the
+ * plan outgrows its buffer; workspace growth also waits for the stream.
  * Errors: INVALID_ARG, UNSUPPORTED, OUT_OF_MEMORY, HIP_ERROR. */
 int milo_attend_decode(milo_cache* cache, const int32_t* block_table, int32_t n_sel,
                        int32_t n_q, int32_t n_q_heads, const uint16_t* q,
@@ -179,6 +185,12 @@ const char* milo_last_error(void);
 /* Bytes of device memory the cache holds for its packed factors. Returns
  * INVALID_ARG for NULL arguments. */
 int milo_cache_device_bytes(const milo_cache* cache, int64_t* bytes);
+
+/* Number of work plans milo_attend_decode / milo_attend_prefill have built for
+ * this cache so far (a plan is rebuilt when the block table, the batch shape or
+ * the planned tail-chunk capacity changes; see milo_attend_decode).  Returns
+ * INVALID_ARG for NULL arguments. */
+int milo_cache_plan_builds(const milo_cache* cache, int64_t* builds);
 
 /* Copy one stored factor of one block back to host memory in the caller's
  * row-major layout (for checking the packed layout).  which: 0 = P^K, 1 = R^K,

@@ -18,6 +18,7 @@
 
 #include "milo.h"
 #include "milo_internal.h"
+#include "milo_plan.h"
 
 using namespace milo;
 
@@ -90,12 +91,15 @@ struct milo_cache {
   unsigned char* plan_d = nullptr;       // program table + programs of the attention launches
   unsigned char* plan_pinned = nullptr;  // staging copy for the upload
   int64_t plan_cap = 0;
-  int32_t* tail_len_d = nullptr;
+  hipEvent_t plan_evt = nullptr;         // recorded after the last upload from plan_pinned
+  bool plan_evt_live = false;
+  int32_t* tail_len_d = nullptr;         // tail lengths of batches above kInlineTails requests
   int64_t tail_len_cap = 0;
-  int32_t* tail_len_pinned = nullptr;
   // the plan of the previous call
   std::vector<int32_t> plan_key;
-  int n_launch = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0, n_ct = 0;
+  int64_t plan_builds = 0;
+  int n_launch = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0, n_chunks = 0;
+  TileGeom tiles{};
   int64_t count_off = 0;  // byte offset of the plan's slot counts
   int prog_bytes = 0, ring_offset = 0;
   size_t lds = 0;
@@ -128,300 +132,6 @@ int64_t factor_offset(const BlockMeta& m, int which) {
   }
 }
 
-// ---------------------------------------------------------------------------
-// Work schedule of one attention call.
-//
-// Work is cut into jobs: a block job is one part of a selected block (a range
-// of whole 256-token tiles; large blocks are split so the work evens out) for
-// a group of C 64-column tiles of query columns, and a tail job is C 256-token
-// chunks of one request's dense KV.  Each job covers S_kv KV heads x C at once:
-// its S = S_kv * C work items run on a "gang" of S workgroups of one XCD
-// (S_kv = KV heads rounded up to a power of two; C = the largest power of two
-// dividing the number of column tiles with S <= 32), so a block's P factors are
-// fetched from HBM once and re-read by the other heads and column tiles from
-// that XCD's L2.  Workgroup j of a gang takes head j % S_kv and column tile
-// (or tail chunk) j / S_kv of the job's group.  Jobs are dealt to
-// the gangs longest first (each to the gang with the least estimated work),
-// then single jobs are moved or swapped between the most and the least loaded
-// gang while that lowers the maximum; of several ways to split the blocks, the
-// one with the smallest estimated makespan is kept.  Within a gang, tail jobs
-// run first so their latency overlaps the start of the fragment streams.  Workgroup b runs on XCD b % 8 (round-robin dispatch), so
-// gang k on XCD k % 8 uses workgroups (k % 8) + 8 * ((k / 8) * S + j), j < S.
-// ---------------------------------------------------------------------------
-// Cost model (microseconds on an MI355X, least-squares fit to per-item kernel
-// timings of the 7B-shaped layer, rms error 0.5 us): one fragment of the
-// slowest wave's projection and up-projection streams, one fragment of its
-// tile stream, the per-tile softmax and barriers, the per-item set-up, one
-// round of the token-segment reduction, and one dense-tail chunk.
-constexpr double kCostFragItem = 0.206, kCostFragTile = 0.153, kCostTile = 1.75, kCostItem = 2.43,
-                 kCostSegRound = 0.61, kCostTail = 9.4;
-
-struct Schedule {
-  std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs
-  int n_launch = 0, n_parts = 0, prog_bytes = 0, rk_pad_max = 32, rv_pad_max = 32, max_own = 1;
-  int n_block_slots = 0;  // block-group slots of the busiest (KV head, column tile)
-  bool half_w = false;    // the weight tile in 128-token halves (LDS is short)
-  int64_t count_off = 0;  // byte offset of the int32 [H_kv][n_ct] slot counts in `bytes`
-};
-
-// Latent rank tiles the busiest wave of a block accumulates (projection or value pass).
-int max_owned(const BlockMeta& m) {
-  const int nrt_k = m.rk_pad / 32, nrt_v = m.rv_pad / 32;
-  const int ng = kWaves / v_segments(nrt_v);
-  return std::max((nrt_k + kWaves - 1) / kWaves, (nrt_v + ng - 1) / ng);
-}
-
-int build_schedule(const milo_cache& c, const int32_t* table, int n_sel, const std::vector<int32_t>& tl, int n_ct,
-                   Schedule* out) {
-  const int NK = c.d / 16;
-  auto item_cost = [&](const BlockMeta& m, int nt) {
-    const int nrt_k = m.rk_pad / 32, nks = m.rk_pad / 16, nrt_v = m.rv_pad / 32;
-    const int nseg = v_segments(nrt_v), ng = kWaves / nseg;
-    const int mk = (nrt_k + kWaves - 1) / kWaves, mv = (nrt_v + ng - 1) / ng;
-    int rounds = 0;
-    for (int h = nseg; h > 1; h /= 2) ++rounds;
-    const double item_frags = (double)NK * mk + m.rv_pad / 32.0;
-    const double tile_frags = nt * ((double)nks + 16.0 / nseg * mv);
-    return kCostFragItem * item_frags + kCostFragTile * tile_frags + kCostTile * nt + kCostItem +
-           kCostSegRound * rounds;
-  };
-  int S_kv = 1;
-  while (S_kv < c.n_kv && S_kv < 32) S_kv *= 2;
-  int C = 1;
-  while (n_ct % (2 * C) == 0 && S_kv * 2 * C <= 32) C *= 2;
-  const int S = S_kv * C;
-  const int n_hc = (c.n_kv + S_kv - 1) / S_kv;
-  const int n_cg = n_ct / C;  // column-tile groups
-  const int n_gangs = kCUs / S;
-  double total = 0.0;
-  for (int j = 0; j < n_sel; ++j) {
-    const BlockMeta& m = c.meta[table[j]];
-    total += item_cost(m, m.T_pad / kTile) * n_cg * n_hc;
-  }
-  for (int32_t len : tl)
-    total += kCostTail * ((len + kTailChunk * C - 1) / (kTailChunk * C)) * n_hc;
-  struct Part { int b, tile0, ntile; double cost; };
-  struct Job { int part, req, ch, ct, hc; double cost; };
-  // Jobs for one way of splitting the blocks: parts of at most `share` of a
-  // gang's average work (and at most kMaxPartTiles tiles), longest first.
-  auto make_jobs = [&](double share, std::vector<Part>& parts, std::vector<Job>& jobs) {
-    const double target = std::max(1e-9, total / n_gangs * share);
-    parts.clear();
-    jobs.clear();
-    for (int j = 0; j < n_sel; ++j) {
-      const int b = table[j];
-      const BlockMeta& m = c.meta[b];
-      const int nt = m.T_pad / kTile;
-      const int np_cost = (int)std::min<double>(nt, std::max(1.0, std::ceil(item_cost(m, nt) / target)));
-      const int np = std::max(np_cost, (nt + kMaxPartTiles - 1) / kMaxPartTiles);
-      for (int p = 0; p < np; ++p) {
-        const int t_a = (int)((int64_t)nt * p / np), t_b = (int)((int64_t)nt * (p + 1) / np);
-        parts.push_back({b, t_a, t_b - t_a, item_cost(m, t_b - t_a)});
-      }
-    }
-    for (int p = 0; p < (int)parts.size(); ++p)
-      for (int cg = 0; cg < n_cg; ++cg)
-        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({p, -1, -1, cg, hc, parts[p].cost});
-    for (int i = 0; i < (int)tl.size(); ++i)
-      for (int chg = 0; chg * C * kTailChunk < tl[i]; ++chg)
-        for (int hc = 0; hc < n_hc; ++hc) jobs.push_back({-1, i, chg, 0, hc, kCostTail});
-    std::stable_sort(jobs.begin(), jobs.end(), [](const Job& x, const Job& y) { return x.cost > y.cost; });
-  };
-  // Deal jobs (indices `idx`, longest first) to the gangs: each to the least
-  // loaded gang, then improve by moving or swapping single jobs between the
-  // most and the least loaded gang while that lowers the maximum.  Returns the
-  // largest gang load.
-  auto deal = [&](const std::vector<Job>& jobs, const std::vector<int>& idx,
-                  std::vector<std::vector<int>>& lists) -> double {
-    lists.assign(n_gangs, {});
-    std::vector<double> load(n_gangs, 0.0);
-    for (int k : idx) {
-      const int best = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-      load[best] += jobs[k].cost;
-      lists[best].push_back(k);
-    }
-    for (int iter = 0; iter < 4 * n_gangs; ++iter) {
-      const int hi = (int)(std::max_element(load.begin(), load.end()) - load.begin());
-      const int lo = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-      double best_max = load[hi];
-      int bi = -1, bj = -1;  // job position in hi, and in lo (-1: move only)
-      for (int i = 0; i < (int)lists[hi].size(); ++i) {
-        const double ci = jobs[lists[hi][i]].cost;
-        const double mv = std::max(load[hi] - ci, load[lo] + ci);
-        if (mv < best_max - 1e-9) { best_max = mv; bi = i; bj = -1; }
-        for (int j = 0; j < (int)lists[lo].size(); ++j) {
-          const double cj = jobs[lists[lo][j]].cost;
-          if (cj >= ci) continue;
-          const double sw = std::max(load[hi] - ci + cj, load[lo] + ci - cj);
-          if (sw < best_max - 1e-9) { best_max = sw; bi = i; bj = j; }
-        }
-      }
-      if (bi < 0) break;
-      const int ki = lists[hi][bi];
-      lists[hi].erase(lists[hi].begin() + bi);
-      load[hi] -= jobs[ki].cost;
-      if (bj >= 0) {
-        const int kj = lists[lo][bj];
-        lists[lo].erase(lists[lo].begin() + bj);
-        load[lo] -= jobs[kj].cost;
-        lists[hi].push_back(kj);
-        load[hi] += jobs[kj].cost;
-      }
-      lists[lo].push_back(ki);
-      load[lo] += jobs[ki].cost;
-    }
-    for (auto& l : lists)  // tail jobs first, then the longest block jobs
-      std::stable_sort(l.begin(), l.end(), [&](int x, int y) {
-        if ((jobs[x].part < 0) != (jobs[y].part < 0)) return jobs[x].part < 0;
-        return jobs[x].cost > jobs[y].cost;
-      });
-    return *std::max_element(load.begin(), load.end());
-  };
-  // the split whose dealt schedule has the smallest estimated makespan
-  std::vector<Part> parts;
-  std::vector<Job> jobs;
-  {
-    double best = 1e300, best_share = 1.0;
-    for (double share : {1.5, 1.0, 0.8, 0.67, 0.5, 0.33}) {
-      make_jobs(share, parts, jobs);
-      std::vector<int> idx(jobs.size());
-      std::iota(idx.begin(), idx.end(), 0);
-      std::vector<std::vector<int>> lists;
-      const double mk = deal(jobs, idx, lists);
-      if (mk < best - 1e-9) { best = mk; best_share = share; }
-    }
-    make_jobs(best_share, parts, jobs);
-  }
-  const int n_parts = (int)parts.size();
-  out->n_parts = n_parts;
-  for (const Part& pt : parts) {
-    out->rk_pad_max = std::max(out->rk_pad_max, c.meta[pt.b].rk_pad);
-    out->rv_pad_max = std::max(out->rv_pad_max, c.meta[pt.b].rv_pad);
-    out->max_own = std::max(out->max_own, max_owned(c.meta[pt.b]));
-  }
-
-  // a workgroup folds consecutive block items of one (KV head, column tile)
-  // into one partial where the kernel keeps that partial in registers (at most
-  // two latent rank tiles per wave)
-  const bool fold = out->max_own <= 2;
-  // LDS plan: the projected query, weight tile and a 6-slot fragment ring,
-  // the rest for the program (fewer launches would cost the ring); when even a
-  // short program leaves no room for that (ranks above 512), the weight tile
-  // in two 128-token halves and a 4-slot ring; failing that, no ring
-  const size_t short_prog = 16 * sizeof(WorkItem) + (size_t)kWaves * kRunBufs * kRunCap * sizeof(int2);
-  auto room_for = [&](bool half_w) {
-    const size_t b = attend_lds_base_bytes(c.d, out->rk_pad_max, out->rv_pad_max, half_w);
-    return b < (size_t)kLdsBytes ? kLdsBytes - b : 0;
-  };
-  size_t cap;
-  if (room_for(false) >= attend_ring_bytes(6) + short_prog) {
-    out->half_w = false;
-    cap = room_for(false) - attend_ring_bytes(6);
-  } else if (room_for(true) >= attend_ring_bytes(4) + short_prog) {
-    out->half_w = true;
-    cap = room_for(true) - attend_ring_bytes(4);
-  } else {
-    out->half_w = false;
-    cap = room_for(false);
-  }
-  if (const int64_t pc = env_program_cap(); pc >= 0) cap = std::min(cap, (size_t)pc);
-  for (int L = 1; L <= (1 << 20); L *= 2) {
-    std::vector<std::vector<unsigned char>> progs((size_t)L * kCUs);
-    std::vector<WgProgram> entries((size_t)L * kCUs);
-    std::vector<int32_t> slot_count((size_t)c.n_kv * n_ct, 0);
-    size_t max_prog = 0;
-    for (int l = 0; l < L; ++l) {
-      std::vector<int> idx;
-      for (size_t k = l; k < jobs.size(); k += L) idx.push_back((int)k);
-      std::vector<std::vector<int>> lists;
-      deal(jobs, idx, lists);
-      for (int gang = 0; gang < n_gangs; ++gang) {
-        for (int j = 0; j < S; ++j) {
-          const int wg = (gang % kXcds) + kXcds * ((gang / kXcds) * S + j);
-          std::vector<WorkItem> items;
-          const int sub = j / S_kv;  // column tile (or tail chunk) within the job's group
-          for (int k : lists[gang]) {
-            const Job& jb = jobs[k];
-            const int g = jb.hc * S_kv + j % S_kv;
-            if (g >= c.n_kv) continue;
-            WorkItem w{};
-            w.g = g;
-            if (jb.part >= 0) {
-              const Part& pt = parts[jb.part];
-              w.blk = c.meta[pt.b];
-              w.kind = kItemBlock;
-              w.slot = jb.part;
-              w.sub = jb.ct * C + sub;
-              w.tile0 = pt.tile0;
-              w.ntile = pt.ntile;
-              w.flags = lg_rank_groups(w.blk.rv_pad / 32) << kItemLgNgShift;
-            } else {
-              const int ch = jb.ch * C + sub;
-              if (ch * kTailChunk >= tl[jb.req]) continue;
-              w.kind = kItemTail;
-              w.blk.T = std::min(kTailChunk, tl[jb.req] - ch * kTailChunk);  // tokens of the chunk
-              w.req = jb.req;
-              w.slot = ch;
-              w.sub = ch;
-            }
-            items.push_back(w);
-          }
-          // groups of consecutive block items with one (KV head, column tile)
-          // share a slot; slots of a (head, tile) are numbered densely
-          int first = -1, last = -1;
-          for (int i = 0; i < (int)items.size(); ++i) {
-            WorkItem& w = items[i];
-            if (w.kind != kItemBlock) continue;
-            const bool cont = fold && first >= 0 && items[first].g == w.g && items[first].sub == w.sub;
-            if (cont) {
-              w.slot = items[first].slot;
-            } else {
-              if (last >= 0) items[last].flags |= kItemFlush;
-              first = i;
-              w.flags |= kItemFirst;
-              w.slot = slot_count[(size_t)w.g * n_ct + w.sub]++;
-            }
-            last = i;
-          }
-          if (last >= 0) items[last].flags |= kItemFlush;
-          WgProgram& e = entries[(size_t)l * kCUs + wg];
-          e = WgProgram{};
-          if (items.empty()) continue;
-          std::vector<unsigned char>& pb = progs[(size_t)l * kCUs + wg];
-          pb.resize(items.size() * sizeof(WorkItem));
-          std::memcpy(pb.data(), items.data(), pb.size());
-          e.n_items = (int32_t)items.size();
-          e.words = (int32_t)(pb.size() / 4);
-          // LDS: the items, then every wave's run buffer
-          max_prog = std::max(max_prog, pb.size() + (size_t)kWaves * kRunBufs * kRunCap * sizeof(int2));
-        }
-      }
-    }
-    const size_t prog_bytes = (size_t)round_up((int64_t)max_prog, 256);
-    if (prog_bytes > cap) continue;
-    // assemble: the entry table, every program at a 16-byte aligned offset,
-    // then the slot counts
-    size_t off = entries.size() * sizeof(WgProgram);
-    for (size_t k = 0; k < progs.size(); ++k) {
-      entries[k].off = (int64_t)off;
-      off += progs[k].size();
-    }
-    out->count_off = (int64_t)round_up((int64_t)off, 16);
-    off = (size_t)out->count_off + slot_count.size() * sizeof(int32_t);
-    out->bytes.assign(std::max<size_t>(off, 16), 0);
-    std::memcpy(out->bytes.data(), entries.data(), entries.size() * sizeof(WgProgram));
-    for (size_t k = 0; k < progs.size(); ++k)
-      if (!progs[k].empty()) std::memcpy(out->bytes.data() + entries[k].off, progs[k].data(), progs[k].size());
-    std::memcpy(out->bytes.data() + out->count_off, slot_count.data(), slot_count.size() * sizeof(int32_t));
-    out->n_block_slots = 0;
-    for (int32_t k : slot_count) out->n_block_slots = std::max(out->n_block_slots, (int)k);
-    out->n_launch = L;
-    out->prog_bytes = (int)prog_bytes;
-    return MILO_OK;
-  }
-  return fail(MILO_ERR_UNSUPPORTED, "work schedule does not fit in LDS");
-}
-
 void destroy(milo_cache* c) {
   if (!c) return;
   if (c->device >= 0) {
@@ -434,7 +144,7 @@ void destroy(milo_cache* c) {
     (void)hipFree(c->plan_d);
     (void)hipFree(c->tail_len_d);
     (void)hipHostFree(c->plan_pinned);
-    (void)hipHostFree(c->tail_len_pinned);
+    if (c->plan_evt) (void)hipEventDestroy(c->plan_evt);
     if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
   }
   delete c;
@@ -561,6 +271,13 @@ int milo_cache_device_bytes(const milo_cache* cache, int64_t* bytes) {
   return MILO_OK;
 }
 
+int milo_cache_plan_builds(const milo_cache* cache, int64_t* builds) {
+  g_err.clear();
+  if (!cache || !builds) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
+  *builds = cache->plan_builds;
+  return MILO_OK;
+}
+
 int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which, uint16_t* dst) {
   g_err.clear();
   if (!cache || !dst) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
@@ -582,11 +299,14 @@ int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which
 }
 
 // Attention of n_q query tokens over the selected blocks plus their dense tails:
-// query i reads tail rows [i * tail_stride, i * tail_stride + tail_len[i]) of
-// tail_k / tail_v (tail_stride = tail_cap: one tail per request; 0: one shared tail).
+// query i reads tail rows [i * tail_stride, i * tail_stride + len_i) of tail_k /
+// tail_v (tail_stride = tail_cap: one tail per request; 0: one shared tail),
+// with len_i = tail_len[i] (host array), or tail_base + i + 1 when tail_len is
+// NULL (the causal lengths of a prefill chunk).
 static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_q, int32_t n_q_heads,
                   const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
-                  int32_t tail_cap, int64_t tail_stride, float scale, float* out, void* hip_stream) {
+                  int32_t tail_base, int32_t tail_cap, int64_t tail_stride, float scale, float* out,
+                  void* hip_stream) {
   // ---- validation (host only, nothing queued yet) ----
   if (!c) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
   if (n_sel < 0) return fail(MILO_ERR_INVALID_ARG, "n_sel must be >= 0");
@@ -599,16 +319,18 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
   if (G > kMaxGroup) return fail(MILO_ERR_UNSUPPORTED, "more than %d query heads per KV head", kMaxGroup);
   if (!q || !out) return fail(MILO_ERR_INVALID_ARG, "q / out must be non-NULL");
   if (tail_cap < 0) return fail(MILO_ERR_INVALID_ARG, "tail_cap must be >= 0");
-  if (tail_cap > 0 && (!tail_k || !tail_v || !tail_len))
+  const bool causal = tail_len == nullptr && tail_base >= 0;
+  if (tail_cap > 0 && (!tail_k || !tail_v || (!tail_len && !causal)))
     return fail(MILO_ERR_INVALID_ARG, "tail_k / tail_v / tail_len must be non-NULL when tail_cap > 0");
   if (!std::isfinite(scale)) return fail(MILO_ERR_INVALID_ARG, "scale must be finite");
   if ((int64_t)n_q * n_q_heads > (int64_t)1 << 24) return fail(MILO_ERR_UNSUPPORTED, "too many query columns");
-  std::vector<int32_t> tl(n_q, 0);
+  int max_len = 0;
   for (int i = 0; i < n_q; ++i) {
-    if (tail_cap > 0) tl[i] = tail_len[i];
-    if (tl[i] < 0 || tl[i] > tail_cap)
-      return fail(MILO_ERR_INVALID_ARG, "tail_len[%d]=%d outside [0, tail_cap=%d]", i, tl[i], tail_cap);
-    if (n_sel == 0 && tl[i] == 0) return fail(MILO_ERR_INVALID_ARG, "request %d has no keys to attend to", i);
+    const int len = causal ? tail_base + i + 1 : tail_cap > 0 ? tail_len[i] : 0;
+    if (len < 0 || len > tail_cap)
+      return fail(MILO_ERR_INVALID_ARG, "tail_len[%d]=%d outside [0, tail_cap=%d]", i, len, tail_cap);
+    if (n_sel == 0 && len == 0) return fail(MILO_ERR_INVALID_ARG, "request %d has no keys to attend to", i);
+    max_len = std::max(max_len, len);
   }
   if (n_sel > 0) {
     std::vector<char> seen(c->n_blocks, 0);
@@ -625,28 +347,35 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
   if (dev != c->device) return fail(MILO_ERR_INVALID_ARG, "cache lives on device %d, current device is %d", c->device, dev);
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
 
-  // ---- plan (rebuilt only when the call's shape changes) ----
+  // ---- plan: rebuilt only when the block table, the batch shape or the tail
+  // chunk capacity changes (the longest tail rounded up to a power of two of
+  // chunks, at most tail_cap), not when tails merely grow ----
+  const int need_chunks = (max_len + kTailChunk - 1) / kTailChunk;
+  int n_chunks = 0;
+  if (need_chunks > 0) {
+    n_chunks = 1;
+    while (n_chunks < need_chunks) n_chunks *= 2;
+    n_chunks = std::min(n_chunks, (tail_cap + kTailChunk - 1) / kTailChunk);
+  }
   std::vector<int32_t> key;
-  key.reserve(6 + n_sel + n_q);
+  key.reserve(4 + n_sel);
   key.push_back(n_sel);
   key.push_back(n_q);
   key.push_back(n_q_heads);
-  key.push_back(tail_cap);
+  key.push_back(n_chunks);
   key.insert(key.end(), block_table, block_table + n_sel);
-  key.insert(key.end(), tl.begin(), tl.end());
   const int n_cols = n_q * n_q_heads;
-  int max_chunks = 0;
-  for (int i = 0; i < n_q; ++i) max_chunks = std::max(max_chunks, (tl[i] + kTailChunk - 1) / kTailChunk);
   if (key != c->plan_key) {
     // no plan is valid until this one is complete: a failure below (an
     // allocation, an upload) must not leave the old key pointing at buffers
     // that were freed or half rewritten
     c->plan_key.clear();
-    const int ncg = n_q * G;
-    const int n_ct = (ncg + kCols - 1) / kCols;
+    const Tiling til = make_tiling(c->n_kv, n_q * G);
     Schedule sch;
-    const int err = build_schedule(*c, block_table, n_sel, tl, n_ct, &sch);
-    if (err != MILO_OK) return err;
+    std::string why;
+    if (!build_schedule(PlanInput{c->meta.data(), c->n_kv, c->d}, block_table, n_sel, n_q, n_chunks, til,
+                        env_program_cap(), &sch, &why))
+      return fail(MILO_ERR_UNSUPPORTED, "%s", why.c_str());
     const int max_rt = sch.max_own <= 2 ? 2 : sch.max_own == 3 ? 3 : 4;
     // deepest fragment ring that fits next to the program, projected query and
     // weight tile (4 slots go with the half weight tile)
@@ -662,7 +391,10 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
       for (int cand : {8, 6})
         if (prog + base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
     }
-    // device buffers
+    // upload in stream order: the kernels of earlier calls, queued before the
+    // copy, read the old plan first.  Only growth of the device buffer waits for
+    // the stream (the old buffer may still be read); the pinned staging buffer
+    // is rewritten once its previous upload has been consumed.
     const int64_t plan_bytes = (int64_t)sch.bytes.size();
     if (plan_bytes > c->plan_cap) {
       MILO_HIP(hipStreamSynchronize(s));
@@ -671,32 +403,25 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
       c->plan_d = nullptr;
       c->plan_pinned = nullptr;
       c->plan_cap = 0;
-      MILO_HIP(hipMalloc(&c->plan_d, (size_t)plan_bytes));
-      MILO_HIP(hipHostMalloc(&c->plan_pinned, (size_t)plan_bytes, hipHostMallocDefault));
-      c->plan_cap = plan_bytes;
+      c->plan_evt_live = false;
+      const int64_t cap = plan_bytes + plan_bytes / 4;
+      MILO_HIP(hipMalloc(&c->plan_d, (size_t)cap));
+      MILO_HIP(hipHostMalloc(&c->plan_pinned, (size_t)cap, hipHostMallocDefault));
+      c->plan_cap = cap;
     }
-    if (n_q > c->tail_len_cap) {
-      MILO_HIP(hipStreamSynchronize(s));
-      (void)hipFree(c->tail_len_d);
-      (void)hipHostFree(c->tail_len_pinned);
-      c->tail_len_d = nullptr;
-      c->tail_len_pinned = nullptr;
-      c->tail_len_cap = 0;
-      MILO_HIP(hipMalloc(&c->tail_len_d, sizeof(int32_t) * n_q));
-      MILO_HIP(hipHostMalloc(&c->tail_len_pinned, sizeof(int32_t) * n_q, hipHostMallocDefault));
-      c->tail_len_cap = n_q;
-    }
-    // the pinned staging buffers may still feed an earlier upload
-    MILO_HIP(hipStreamSynchronize(s));
+    if (!c->plan_evt) MILO_HIP(hipEventCreateWithFlags(&c->plan_evt, hipEventDisableTiming));
+    if (c->plan_evt_live) MILO_HIP(hipEventSynchronize(c->plan_evt));
+    c->plan_evt_live = false;
     std::memcpy(c->plan_pinned, sch.bytes.data(), (size_t)plan_bytes);
-    std::memcpy(c->tail_len_pinned, tl.data(), sizeof(int32_t) * n_q);
     MILO_HIP(hipMemcpyAsync(c->plan_d, c->plan_pinned, (size_t)plan_bytes, hipMemcpyHostToDevice, s));
-    MILO_HIP(hipMemcpyAsync(c->tail_len_d, c->tail_len_pinned, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
+    MILO_HIP(hipEventRecord(c->plan_evt, s));
+    c->plan_evt_live = true;
     c->n_launch = sch.n_launch;
-    c->n_slots = sch.n_block_slots + max_chunks;
+    c->n_chunks = n_chunks;
+    c->n_slots = sch.n_block_slots + n_chunks;
     c->n_block_slots = sch.n_block_slots;
     c->count_off = sch.count_off;
-    c->n_ct = n_ct;
+    c->tiles = til.geom;
     c->max_rt = max_rt;
     c->nslot = nslot;
     c->rk_pad_max = sch.rk_pad_max;
@@ -704,6 +429,7 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
     c->ring_offset = (int)base;
     c->lds = prog + base + attend_ring_bytes(nslot);
     c->plan_key.swap(key);
+    ++c->plan_builds;
   }
   const int64_t need = (int64_t)n_cols * c->n_slots;
   if (need > c->part_cols_slots) {
@@ -721,6 +447,29 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
     MILO_HIP(hipMalloc(&c->part_ml, (size_t)need * sizeof(float2)));
     c->part_cols_slots = need;
   }
+  // this call's tail lengths travel in the kernel arguments; a batch above
+  // kInlineTails requests copies them to the device in stream order
+  TailLens tls{};
+  if (causal || tail_cap == 0) {
+    tls.mode = kTailAffine;
+    tls.base = causal ? tail_base + 1 : 0;
+    tls.step = causal ? 1 : 0;
+  } else if (n_q <= kInlineTails) {
+    tls.mode = kTailInline;
+    for (int i = 0; i < n_q; ++i) tls.v[i] = tail_len[i];
+  } else {
+    tls.mode = kTailDevice;
+    if (n_q > c->tail_len_cap) {
+      MILO_HIP(hipStreamSynchronize(s));
+      (void)hipFree(c->tail_len_d);
+      c->tail_len_d = nullptr;
+      c->tail_len_cap = 0;
+      MILO_HIP(hipMalloc(&c->tail_len_d, sizeof(int32_t) * n_q));
+      c->tail_len_cap = n_q;
+    }
+    MILO_HIP(hipMemcpyAsync(c->tail_len_d, tail_len, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
+    tls.dev = c->tail_len_d;
+  }
 
   // ---- launches ----
   AttendArgs aa{};
@@ -729,7 +478,6 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
   aa.q = q;
   aa.tail_k = tail_k;
   aa.tail_v = tail_v;
-  aa.tail_len = c->tail_len_d;
   aa.part_o = c->part_o;
   aa.part_ml = c->part_ml;
   aa.qscale = scale * 1.4426950408889634f;
@@ -743,9 +491,19 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
   aa.qt_stride = c->rk_pad_max + 8;
   aa.prog_bytes = c->prog_bytes;
   aa.ring_offset = c->ring_offset;
-  MergeArgs ma{c->part_o, c->part_ml, c->tail_len_d, out,
-               reinterpret_cast<const int32_t*>(c->plan_d + c->count_off), n_q_heads, G, c->n_ct,
-               c->n_block_slots, c->n_slots};
+  aa.N_g = n_q * G;
+  aa.tl = tls;
+  MergeArgs ma{};
+  ma.part_o = c->part_o;
+  ma.part_ml = c->part_ml;
+  ma.out = out;
+  ma.slot_count = reinterpret_cast<const int32_t*>(c->plan_d + c->count_off);
+  ma.H_q = n_q_heads;
+  ma.G = G;
+  ma.n_block_slots = c->n_block_slots;
+  ma.n_slots = c->n_slots;
+  ma.tiles = c->tiles;
+  ma.tl = tls;
 
   // timing: events recorded by the launches themselves at kernel start and end
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};  // attend start / end, merge start / end
@@ -797,8 +555,9 @@ int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel,
                        const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
                        int32_t tail_cap, float scale, float* out, void* hip_stream) {
   g_err.clear();
-  return attend(c, block_table, n_sel, n_q, n_q_heads, q, tail_k, tail_v, tail_len, tail_cap, tail_cap, scale, out,
-                hip_stream);
+  if (tail_cap > 0 && !tail_len) return fail(MILO_ERR_INVALID_ARG, "tail_len must be non-NULL when tail_cap > 0");
+  return attend(c, block_table, n_sel, n_q, n_q_heads, q, tail_k, tail_v, tail_len, -1, tail_cap, tail_cap, scale,
+                out, hip_stream);
 }
 
 int milo_attend_prefill(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_tok, int32_t n_q_heads,
@@ -812,10 +571,8 @@ int milo_attend_prefill(milo_cache* c, const int32_t* block_table, int32_t n_sel
                 (long long)tail_base + n_tok);
   if (!tail_k || !tail_v) return fail(MILO_ERR_INVALID_ARG, "tail_k / tail_v must be non-NULL");
   // token j sees the tail_base rows before the chunk and the chunk's first j + 1 tokens
-  std::vector<int32_t> tl(n_tok);
-  for (int j = 0; j < n_tok; ++j) tl[j] = tail_base + j + 1;
-  return attend(c, block_table, n_sel, n_tok, n_q_heads, q, tail_k, tail_v, tl.data(), tail_cap, 0, scale, out,
-                hip_stream);
+  return attend(c, block_table, n_sel, n_tok, n_q_heads, q, tail_k, tail_v, nullptr, tail_base, tail_cap, 0, scale,
+                out, hip_stream);
 }
 
 int milo_timing_enable(int enable) {

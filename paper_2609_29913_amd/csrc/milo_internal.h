@@ -83,9 +83,11 @@ struct BlockMeta {
 };
 
 // Most 256-token tiles in one block item (parts of larger blocks are split),
-// and so the most fragment runs one item gives a wave (plus an end marker).
+// most KV heads one 64-column tile may span, and so the most fragment runs
+// one item gives a wave (plus an end marker).
 constexpr int kMaxPartTiles = 8;
-constexpr int kRunCap = 2 + 2 * kMaxPartTiles + 2;
+constexpr int kMaxTileHeads = 4;
+constexpr int kRunCap = 2 * kMaxTileHeads + 2 * kMaxPartTiles + 2;
 constexpr int kRunBufs = 4;  // run buffers per wave in the attention kernel
 
 // log2 of the rank groups (kWaves / nseg) of a block with nrt V rank tiles
@@ -94,16 +96,18 @@ __host__ __device__ inline int lg_rank_groups(int nrt) {
   return nseg == 1 ? 3 : nseg == 2 ? 2 : nseg == 4 ? 1 : 0;
 }
 
-// The fragment runs wave w consumes for a block item (block bm, KV head g,
-// tiles [tile0, tile0 + ntile)) of head dimension d, in the attention kernel's
-// order: its R^K rank tiles (projection); then per tile its P^K sub-tile and
-// the P^V rank tiles of its rank group over its token segment; then R^V for
-// its 16-dim output slice over all ranks (up-projection).  lg_ng =
-// lg_rank_groups(rv_pad / 32) (passed in, so the kernel derives runs with
-// shifts only).  emit(first fragment index, count) is called for every
-// non-empty run; offsets follow the packed layout above.
+// The fragment runs wave w consumes for a block item (block bm, the nh KV
+// heads g0 .. g0+nh-1 whose query columns the item's column tile holds, tiles
+// [tile0, tile0 + ntile)) of head dimension d, in the attention kernel's
+// order: its R^K rank tiles of every head in turn (projection); then per tile
+// its P^K sub-tile and the P^V rank tiles of its rank group over its token
+// segment; then R^V for its 16-dim output slice over all ranks, every head in
+// turn (up-projection).  lg_ng = lg_rank_groups(rv_pad / 32) (passed in, so
+// the kernel derives runs with shifts only).  emit(first fragment index,
+// count) is called for every non-empty run; offsets follow the packed layout
+// above.
 template <typename Emit>
-__host__ __device__ inline void block_runs(const BlockMeta& bm, int g, int tile0, int ntile, int w, int d,
+__host__ __device__ inline void block_runs(const BlockMeta& bm, int g0, int nh, int tile0, int ntile, int w, int d,
                                            int lg_ng, Emit&& emit) {
   static_assert(kWaves == 8, "rank tiles are dealt over 8 waves");
   const int NK = d / 16;
@@ -120,14 +124,15 @@ __host__ __device__ inline void block_runs(const BlockMeta& bm, int g, int tile0
   const int tiles_all = bm.T_pad / kTile;
   const int rk0 = (int)(bm.off_rk / kFragElems), pk0 = (int)(bm.off_pk / kFragElems);
   const int pv0 = (int)(bm.off_pv / kFragElems), rv0 = (int)(bm.off_rv / kFragElems);
-  if (own_k > 0) emit(rk0 + g * nrt_k * NK + NK * before_k, NK * own_k);
+  if (own_k > 0)
+    for (int h = 0; h < nh; ++h) emit(rk0 + (g0 + h) * nrt_k * NK + NK * before_k, NK * own_k);
   const int pv_first = (bm.T_pad / 16) * before_v;
   for (int t = tile0; t < tile0 + ntile; ++t) {
     emit(pk0 + (w * tiles_all + t) * nks, nks);
     if (own_v > 0) emit(pv0 + pv_first + (16 * t + nst * sg) * own_v, nst * own_v);
   }
   const int nds = d / 16, nkr = bm.rv_pad >> 5;
-  emit(rv0 + (g * nds + w % nds) * nkr, nkr);
+  for (int h = 0; h < nh; ++h) emit(rv0 + ((g0 + h) * nds + w % nds) * nkr, nkr);
 }
 
 struct FactorGeom {
@@ -216,18 +221,22 @@ __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, i
 // Work item of the attention kernel.  Block items carry their block's metadata
 // inline, so an item is self-contained.
 enum ItemKind : int32_t { kItemBlock = 0, kItemTail = 1 };
+//
+// Query columns are numbered head-major: column c = g * N_g + i * G + (h mod G)
+// of KV head g = h / G, request i, query head h (N_g = n_q * G columns per KV
+// head).  A block item works on one column tile, a range of at most kCols
+// consecutive columns that may span up to kMaxTileHeads KV heads.
 struct WorkItem {
-  BlockMeta blk;      // block items: the block's packed offsets and padded sizes;
-                      // tail items: blk.T = tokens of the chunk
+  BlockMeta blk;      // block items: the block's packed offsets and padded sizes
   int32_t kind;       // ItemKind
   int32_t slot;       // block items: the group's partial slot (see kItemFirst);
                       // tail items: chunk index (slot n_block_slots + slot)
-  int32_t g;          // KV head
-  int32_t sub;        // block items: 64-column tile; tail items: kTailChunk-token chunk
-  int32_t req;        // tail items: request index
+  int32_t g;          // tail items: KV head; block items: first KV head of the column tile
+  int32_t sub;        // block items: column tile index; tail items: kTailChunk-token chunk
+  int32_t req;        // tail items: request index; block items: first column of the tile
   int32_t tile0;      // block items: first 256-token tile of the block covered
   int32_t ntile;      // block items: number of tiles covered
-  int32_t flags;      // block items: kItemFirst / kItemFlush (see below)
+  int32_t flags;      // block items: kItemFirst / kItemFlush and the packed fields below
 };
 static_assert(sizeof(WorkItem) == 80, "work item layout");
 // Consecutive block items of a workgroup for the same KV head and column tile
@@ -237,8 +246,11 @@ static_assert(sizeof(WorkItem) == 80, "work item layout");
 // (head, column tile) are numbered densely from 0; tail items write slot
 // n_block_slots + their chunk index.
 enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2 };
-// bits 8-9 of a block item's flags: lg_rank_groups of its block
+// packed fields of a block item's flags: bits 8-9 lg_rank_groups of its block,
+// bits 16-21 the tile's column count - 1, bits 24-26 its KV head count - 1
 constexpr int kItemLgNgShift = 8;
+constexpr int kItemColsShift = 16;
+constexpr int kItemHeadsShift = 24;
 
 // The attention kernel is persistent: workgroup b runs the program of entry b,
 // a byte range of the program buffer holding its work items in order; it is
@@ -269,6 +281,56 @@ constexpr int kTailChunk = kWaves * 32;        // dense-tail tokens per work ite
 constexpr int kXcds = 8;                       // XCDs of an MI355X (workgroup b runs on XCD b % 8)
 constexpr int kCUs = 256;                      // compute units; one persistent workgroup each
 
+// Per-request dense-tail lengths of one call, carried in the kernel arguments
+// so that a call whose tails grew needs no upload: inline values (n_q <=
+// kInlineTails), an affine rule base + step * i (the causal lengths of a
+// prefill chunk, or no tails at all), or a device array for larger batches.
+constexpr int kInlineTails = 256;
+enum TailLenMode : int32_t { kTailInline = 0, kTailAffine = 1, kTailDevice = 2 };
+struct TailLens {
+  int32_t mode;
+  int32_t base, step;        // kTailAffine: request i has base + step * i rows
+  const int32_t* dev;        // kTailDevice: device [n_q]
+  int32_t v[kInlineTails];   // kTailInline
+};
+__host__ __device__ inline int tail_len_of(const TailLens& t, int i) {
+  return t.mode == kTailInline ? t.v[i] : t.mode == kTailAffine ? t.base + t.step * i : t.dev[i];
+}
+
+// How the head-major query columns are cut into column tiles:
+//   kTilePacked  (N_g < kCols) every tile holds `a` whole KV heads
+//   kTileHead    (N_g >= kCols) every KV head is cut into `a` tiles of kCols
+//                columns, the last one partial
+//   kTileFlat    (N_g >= kCols) tile t is columns [kCols t, kCols t + kCols),
+//                spanning at most two KV heads
+enum TileMode : int32_t { kTilePacked = 0, kTileHead = 1, kTileFlat = 2 };
+struct TileGeom {
+  int32_t mode, a, N_g, N;
+};
+// tile index of head-major column c, and the tile's first column and count
+__host__ __device__ inline int tile_of(const TileGeom& t, int c) {
+  return t.mode == kTilePacked ? (c / t.N_g) / t.a
+         : t.mode == kTileHead ? (c / t.N_g) * t.a + (c % t.N_g) / kCols
+                               : c / kCols;
+}
+__host__ __device__ inline void tile_range(const TileGeom& t, int tile, int* c0, int* cn) {
+  int lo, hi;
+  if (t.mode == kTilePacked) {
+    lo = tile * t.a * t.N_g;
+    hi = lo + t.a * t.N_g;
+  } else if (t.mode == kTileHead) {
+    const int g = tile / t.a, k = tile % t.a;
+    lo = g * t.N_g + kCols * k;
+    hi = lo + kCols < (g + 1) * t.N_g ? lo + kCols : (g + 1) * t.N_g;
+  } else {
+    lo = kCols * tile;
+    hi = lo + kCols;
+  }
+  if (hi > t.N) hi = t.N;
+  *c0 = lo;
+  *cn = hi - lo;
+}
+
 struct AttendArgs {
   const uint16_t* data;      // packed factors
   const unsigned char* prog; // program buffer
@@ -276,7 +338,6 @@ struct AttendArgs {
   const uint16_t* q;         // [n_q][H_q][d]
   const uint16_t* tail_k;    // request i's tail rows start at row i * tail_stride; [row][H_kv][d]
   const uint16_t* tail_v;
-  const int32_t* tail_len;   // device [n_q]
   float* part_o;             // [n_q*H_q][n_slots][d]
   float2* part_ml;           // [n_q*H_q][n_slots] (max in log2 units, sum)
   float qscale;              // scale * log2(e)
@@ -287,15 +348,18 @@ struct AttendArgs {
   int qt_stride;             // bf16 row stride of the projected query in LDS
   int prog_bytes;            // LDS bytes reserved for the program (the work area follows)
   int ring_offset;           // byte offset of the per-wave fragment rings in the work area
+  int N_g;                   // query columns per KV head, n_q * G
+  TailLens tl;               // tail lengths of this call
 };
 
 struct MergeArgs {
   const float* part_o;
   const float2* part_ml;
-  const int32_t* tail_len;   // device [n_q]
-  float* out;                // [n_q][H_q][d]
-  const int32_t* slot_count;  // device [H_kv][n_ct]: block-group slots used per (KV head, column tile)
-  int H_q, G, n_ct, n_block_slots, n_slots;
+  float* out;                 // [n_q][H_q][d]
+  const int32_t* slot_count;  // device [n_ct]: block-group slots used per column tile
+  int H_q, G, n_block_slots, n_slots;
+  TileGeom tiles;
+  TailLens tl;
 };
 
 struct PackArgs {

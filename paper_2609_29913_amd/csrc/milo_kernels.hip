@@ -6,17 +6,18 @@
 //  attend_kernel  persistent: one workgroup (8 waves) per compute unit runs a
 //                 host-built list of work items, its fragment streams flowing
 //                 across items:
-//     block item (block b, KV head g, 64-column tile of query columns, a run
-//     of 256-token tiles):
-//       projection  Qt = scale*log2(e) * R^K_b[:, g] q          (MFMA, into LDS)
+//     block item (block b, a tile of up to 64 head-major query columns of
+//     one or more KV heads, a run of 256-token tiles):
+//       projection  Qt = scale*log2(e) * R^K_b[:, g] q          (MFMA, into LDS;
+//                   per KV head g of the tile)
 //       scores      S  = P^K_b Qt, 32 tokens per wave and tile  (MFMA)
 //       softmax     running max per column shared by the waves, W = 2^(S - m)
 //       latent V    Ot = sum_t W_t P^V_b[t]                      (MFMA, waves split
 //                   token segments x rank tiles)
 //       up-project  o  = R^V_b[:, g]^T Ot                        (MFMA, 16-dim slice
-//                   per wave)
+//                   per wave; per KV head g of the tile)
 //       -> folded into the workgroup's partial (m, l, o) per column for its
-//          current (KV head, column tile); written when the group ends
+//          current column tile; written when the group ends
 //     tail item (request i, KV head g, kTailChunk-token chunk of the request's
 //     own KV): plain attention of the group's query heads over the chunk
 //     (MFMA scores, VALU values) -> partial (m, l, o) per column
@@ -49,6 +50,12 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// query row i * H_q + h of head-major column c = g * N_g + i * G + (h mod G)
+__device__ __forceinline__ int64_t query_row(int c, int N_g, int G, int H_q) {
+  const int g = c / N_g, rem = c - g * N_g, i = rem / G;
+  return (int64_t)i * H_q + g * G + (rem - i * G);
+}
 
 // Direct global->LDS load of one fragment: lane l's 16 bytes from `src` land at
 // LDS byte address lds_slot + 16 l.  Issued as inline assembly, so the compiler
@@ -135,8 +142,8 @@ __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
 
 // ---------------------------------------------------------------------------
 // Tail work item: attention of the G query heads of KV head g of request i over
-// tokens [t0, t0 + nt) of that request's uncompressed KV (nt <= 128 comes with
-// the item).  Wave w takes tokens t0 + 32w .. t0 + 32w + 31; every load of the
+// tokens [t0, t0 + nt) of that request's uncompressed KV (nt <= kTailChunk
+// follows from the call's tail length; an item past the tail does nothing).  Wave w takes tokens t0 + 32w .. t0 + 32w + 31; every load of the
 // item is issued up front (rows past the chunk's end re-read its last row and
 // are masked), then:
 //   scores  S = K q^T  (one 32x32x16 MFMA per 16 dims: 32 tokens x 32 head
@@ -189,7 +196,11 @@ __device__ __forceinline__ void tail_item(const AttendArgs& a, const WorkItem& i
   static_assert(kTokW == 32, "one 32-row MFMA tile of tokens per wave");
   const int i = it.req, slot = a.n_block_slots + it.slot, g = it.g, G = a.G;
   const int wave = tid >> 6, lane = tid & 63, lrow = lane & 31, lhi = lane >> 5;
-  const int t0 = it.sub * kTailChunk, nt = it.blk.T;
+  // the chunk's rows come from this call's tail length: the plan holds chunks
+  // up to its planned capacity, and chunks past the request's tail are empty
+  const int t0 = it.sub * kTailChunk;
+  const int nt = min(kTailChunk, tail_len_of(a.tl, i) - t0);
+  if (nt <= 0) return;
   float* red = reinterpret_cast<float*>(smem);   // [kWaves][32] column maxima
   float* lred = red + kWaves * 32;               // [kWaves][32] column sums
   float* wt = lred + kWaves * 32;                // [kTailChunk][32] weights, token-major
@@ -400,7 +411,9 @@ struct RunDeriver {
         lds_store_b64(out + n, make_int2(x, cnt));
         ++n;
       };
-      if (found) block_runs(it.blk, it.g, it.tile0, it.ntile, lane, D, (it.flags >> kItemLgNgShift) & 3, put);
+      if (found)
+        block_runs(it.blk, it.g, ((it.flags >> kItemHeadsShift) & 7) + 1, it.tile0, it.ntile, lane, D,
+                   (it.flags >> kItemLgNgShift) & 3, put);
       else put(0, kSentinelRun);
       put(0, 0);
     }
@@ -425,8 +438,12 @@ constexpr int up_col_blocks() {
 }
 
 // ---------------------------------------------------------------------------
-// Block work item: latent-space attention of one 64-column tile of the query
-// columns of KV head g over the tiles [tile0, tile0 + ntile) of block b.
+// Block work item: latent-space attention of one column tile (at most 64
+// consecutive head-major query columns, of up to kMaxTileHeads KV heads) over
+// the tiles [tile0, tile0 + ntile) of block b.  The scores and the latent
+// value pass do not depend on the head (P^K and P^V are shared by all KV
+// heads); the projection and the up-projection run once per KV head of the
+// tile, each column keeping the result of its own head.
 //
 // Eight waves (two per SIMD).  Scores: wave w takes the 32 tokens 32w..32w+31
 // of every 256-token tile against all 64 columns.  Latent V: the waves form
@@ -447,11 +464,13 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   constexpr int NK = D / 16;
   constexpr int kORed = 4;  // partial-output slots of the up-projection reduction
   const BlockMeta& bm = it.blk;
-  const int slot = it.slot, g = it.g, c0 = it.sub * kCols;
+  const int slot = it.slot, g0 = it.g, c0 = it.req;
+  const int cn = ((it.flags >> kItemColsShift) & 63) + 1;  // columns of the tile
+  const int nh = ((it.flags >> kItemHeadsShift) & 7) + 1;  // KV heads of the tile
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lrow = lane & 31, lhi = lane >> 5;
-  const int G = a.G, ncg = a.n_q * G;
+  const int G = a.G, N_g = a.N_g;
   const int qsd = a.qt_stride;
   const int nrt_k = bm.rk_pad >> 5, nks = bm.rk_pad >> 4;
   const int nrt_v = bm.rv_pad >> 5;
@@ -476,8 +495,9 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   // ---- the item's 64 query rows -> LDS (in the weight tile's area, idle until
   // the first tile).  Row-major [column][D]; the 16-byte chunk j of column c is
   // stored at chunk position j ^ (c % kRowChunks), so the projection's operand
-  // reads (same chunk, 32 columns) hit distinct banks.  Columns past the last
-  // one re-read the last column's query (their results are never stored).
+  // reads (same chunk, 32 columns) hit distinct banks.  Columns past the tile's
+  // last one re-read the last column's query and count as its head (their
+  // results are never stored).
   constexpr int kRowChunks = D / 8;              // 16-byte chunks per query row
   constexpr int kRowsPerLoad = 64 / kRowChunks;  // rows per 1 KiB load
   const __bf16* qimg = wl;
@@ -486,9 +506,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
     const int cl_lane = lane / kRowChunks, pos = lane % kRowChunks;
     for (int f = wave; f < kCols / kRowsPerLoad; f += kWaves) {
       const int cl = kRowsPerLoad * f + cl_lane;
-      const int c = min(c0 + cl, ncg - 1);
-      const uint16_t* src =
-          a.q + ((int64_t)(c / G) * a.H_q + g * G + c % G) * D + 8 * (pos ^ (cl % kRowChunks));
+      const uint16_t* src = a.q + query_row(c0 + min(cl, cn - 1), N_g, G, a.H_q) * D + 8 * (pos ^ (cl % kRowChunks));
       lds_dma16(src, qimg_lds + f * 1024);
     }
     if (wave == 0) rd.derive(lane);  // the runs of the block item two ahead, while the rows load
@@ -496,7 +514,8 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
     lds_barrier();
   }
 
-  // ---- projection: Qt[rank][col] (stored [col][rank]) ----
+  // ---- projection: Qt[rank][col] (stored [col][rank]), once per KV head of
+  // the tile; each column stores its own head's result ----
   if (own_k > 0) {
     bf16x8 qf[NK][2];
 #pragma unroll
@@ -504,8 +523,11 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 #pragma unroll
       for (int k = 0; k < NK; ++k)
         qf[k][ch] = ld_bf16x8(qimg + (32 * ch + lrow) * D + 8 * ((2 * k + lhi) ^ (lrow % kRowChunks)));
-    for (int j = 0; j < own_k; ++j) {
-      const int rt = wave + kWaves * j;
+    // KV head (relative to g0) of this lane's two columns 32 ch + lrow
+    const int hq0 = (c0 + min(lrow, cn - 1)) / N_g - g0;
+    const int hq1 = (c0 + min(32 + lrow, cn - 1)) / N_g - g0;
+    for (int x = 0; x < nh * own_k; ++x) {
+      const int hh = x / own_k, rt = wave + kWaves * (x - hh * own_k);
       f32x16 acc0 = {}, acc1 = {};
       bf16x8 af = take();
 #pragma unroll
@@ -525,8 +547,8 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
           v1[u] = (__bf16)(acc1[4 * jj + u] * a.qscale);
         }
         const int r = 32 * rt + 8 * jj + 4 * lhi;
-        *reinterpret_cast<bf16x4*>(qt + lrow * qsd + r) = v0;
-        *reinterpret_cast<bf16x4*>(qt + (32 + lrow) * qsd + r) = v1;
+        if (hq0 == hh) *reinterpret_cast<bf16x4*>(qt + lrow * qsd + r) = v0;
+        if (hq1 == hh) *reinterpret_cast<bf16x4*>(qt + (32 + lrow) * qsd + r) = v1;
       }
     }
   }
@@ -755,18 +777,28 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   constexpr int NCB = up_col_blocks<D>();  // 16-column blocks per wave
   const int ds = wave % NDS, cb0 = (wave / NDS) * NCB;
   f32x4 uacc[NCB];
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) uacc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
   {
+    // KV head (relative to g0) of this lane's output columns
+    int hu[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) hu[cb] = (c0 + min(16 * (cb0 + cb) + (lane & 15), cn - 1)) / N_g - g0;
     const int nk = bm.rv_pad >> 5;
     const __bf16* ob = olat + (16 * cb0 + (lane & 15)) * ols + 8 * (lane >> 4);
-    bf16x8 af = take();
-    for (int k = 0; k < nk; ++k) {
-      bf16x8 an = af;
-      if (k + 1 < nk) an = take();
+    for (int hh = 0; hh < nh; ++hh) {
+      f32x4 t[NCB];
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) uacc[cb] = mfma16(af, ld_bf16x8(ob + 16 * cb * ols + 32 * k), uacc[cb]);
-      af = an;
+      for (int cb = 0; cb < NCB; ++cb) t[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      bf16x8 af = take();
+      for (int k = 0; k < nk; ++k) {
+        bf16x8 an = af;
+        if (k + 1 < nk) an = take();
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) t[cb] = mfma16(af, ld_bf16x8(ob + 16 * cb * ols + 32 * k), t[cb]);
+        af = an;
+      }
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+        if (hh == 0 || hu[cb] == hh) uacc[cb] = t[cb];
     }
   }
   // the item's partial: per-column maximum m_run (score layout), sum (thread
@@ -779,19 +811,16 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   auto store = [&](const f32x4 (&o)[NCB], const float (&m)[2], float l) {
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
-      const int c = c0 + 16 * (cb0 + cb) + (lane & 15);
-      if (c < ncg) {
-        const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
+      const int cl = 16 * (cb0 + cb) + (lane & 15);
+      if (cl < cn) {
+        const int64_t colg = query_row(c0 + cl, N_g, G, a.H_q);
         *reinterpret_cast<float4*>(a.part_o + (colg * a.n_slots + slot) * D + 16 * ds + 4 * (lane >> 4)) =
             make_float4(o[cb][0], o[cb][1], o[cb][2], o[cb][3]);
       }
     }
-    if (tid < kCols) {
-      const int c = c0 + tid;
-      if (c < ncg) {
-        const int64_t colg = (int64_t)(c / G) * a.H_q + g * G + c % G;
-        a.part_ml[colg * a.n_slots + slot] = make_float2(tid < 32 ? m[0] : m[1], l);
-      }
+    if (tid < cn) {
+      const int64_t colg = query_row(c0 + tid, N_g, G, a.H_q);
+      a.part_ml[colg * a.n_slots + slot] = make_float2(tid < 32 ? m[0] : m[1], l);
     }
   };
   if constexpr (MAX_RT <= 2) {
@@ -871,8 +900,8 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
 
 // ---------------------------------------------------------------------------
 // Log-sum-exp merge: one workgroup per query column (i, h).  Its partials are
-// the block-group slots [0, nb) of its (KV head, column tile), then request i's
-// tail chunks at n_block_slots + chunk.  Thread t takes the
+// the block-group slots [0, nb) of its column tile, then request i's tail
+// chunks at n_block_slots + chunk.  Thread t takes the
 // 4 output dims 4 (t % (D/4)) of the slots s = t / (D/4) (mod slots per pass),
 // so every load is one 16-byte vector and a wave reads whole slots; the loads
 // of kMergeUnroll passes are issued before any is used, and each thread keeps
@@ -890,9 +919,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
   const int col = blockIdx.x, tid = threadIdx.x;
   const int dq = tid % TPS, sl = tid / TPS;
   const int i = col / a.H_q, h = col % a.H_q;
-  const int ct = (i * a.G + h % a.G) / kCols;                   // the column's tile within its KV head
-  const int nb = a.slot_count[(h / a.G) * a.n_ct + ct];        // block-group slots of that (head, tile)
-  const int n_valid = nb + (a.tail_len[i] + kTailChunk - 1) / kTailChunk;
+  const int cf = (h / a.G) * a.tiles.N_g + i * a.G + h % a.G;  // head-major column
+  const int nb = a.slot_count[tile_of(a.tiles, cf)];         // block-group slots of its column tile
+  const int n_valid = nb + (tail_len_of(a.tl, i) + kTailChunk - 1) / kTailChunk;
   const float2* ml = a.part_ml + (int64_t)col * a.n_slots;
   const float4* po = reinterpret_cast<const float4*>(a.part_o + (int64_t)col * a.n_slots * D) + dq;
   float m = -INFINITY, l = 0.f;
@@ -967,23 +996,6 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t attend_lds_base_bytes(int head_dim, int rk_pad_max, int rv_pad_max, bool half_w) {
-  const size_t qsd = (size_t)rk_pad_max + 8;
-  const size_t ws = half_w ? kTile / 2 + 8 : kWStride;
-  const size_t loop = kCols * qsd * 2 + (size_t)kCols * ws * 2 + (size_t)kWaves * kCols * 4;
-  // up-projection: the latent accumulator as bf16 [col][rank], or the segment
-  // partials being combined (at most 4 slots x 3 rank tiles x 8 KiB), then the
-  // per-wave column sums at the end of the region
-  const size_t olat = (size_t)kCols * (rv_pad_max + 8) * 2;
-  const size_t segs = (size_t)4 * 3 * 2 * 16 * 64 * 4;
-  const size_t epi = (olat > segs ? olat : segs) + (size_t)kWaves * kCols * 4;
-  const size_t tail = ((size_t)2 * kWaves * 32 + (size_t)kTailChunk * 32 + (size_t)kWaves * kMaxGroup * head_dim) * 4;
-  size_t m = loop > epi ? loop : epi;
-  m = m > tail ? m : tail;
-  return (m + 1023) / 1024 * 1024;  // the fragment rings start here
-}
-
-size_t attend_ring_bytes(int nslot) { return (size_t)kWaves * nslot * kFragElems * 2; }
 
 template <int D, int MAX_RT, int NSLOT, bool WH>
 static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,

@@ -1,0 +1,48 @@
+// Work plan of one attention call (host only): how the query columns are cut
+// into column tiles, and which work items every persistent workgroup of the
+// attention kernel runs (programs in the kernel's WorkItem format).
+#pragma once
+
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "milo_internal.h"
+
+namespace milo {
+
+// What the planner needs to know about a cache.
+struct PlanInput {
+  const BlockMeta* meta;  // [n_blocks]
+  int n_kv, d;
+};
+
+struct Tiling {
+  TileGeom geom{};
+  int n_ct = 0;
+  std::vector<int> c0, cn, g0, nh;  // per tile: first column, columns, first KV head, KV heads
+};
+
+int gang_size(int n_ct);
+Tiling make_tiling(int n_kv, int N_g);
+
+struct Schedule {
+  std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs, then slot counts
+  int n_launch = 0, n_parts = 0, prog_bytes = 0, rk_pad_max = 32, rv_pad_max = 32, max_own = 1;
+  int n_block_slots = 0;  // block-group slots of the busiest column tile
+  int gang = 1;           // workgroups per gang
+  bool half_w = false;    // the weight tile in 128-token halves (LDS is short)
+  int64_t count_off = 0;  // byte offset of the int32 [n_ct] slot counts in `bytes`
+};
+
+int max_owned(const BlockMeta& m);
+
+// Build the plan for the selected blocks table[0 .. n_sel), n_q requests with
+// n_chunks planned tail chunks each, over the column tiles `til`.  program_cap
+// (< 0: none) caps the LDS bytes of a workgroup program.  Returns false with a
+// message in *err when no plan fits.
+bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q, int n_chunks, const Tiling& til,
+                    int64_t program_cap, Schedule* out, std::string* err);
+
+}  // namespace milo

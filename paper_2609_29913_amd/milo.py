@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.milo_last_error.restype = ctypes.c_char_p
         L.milo_cache_device_bytes.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
         L.milo_cache_device_bytes.restype = ctypes.c_int
+        L.milo_cache_plan_builds.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
+        L.milo_cache_plan_builds.restype = ctypes.c_int
         L.milo_cache_read_factor.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, vp]
         L.milo_cache_read_factor.restype = ctypes.c_int
         L.milo_timing_enable.argtypes = [ctypes.c_int]
@@ -104,15 +106,50 @@ def _addr(x) -> int:
     return int(x.data_ptr())
 
 
+# shapes of the caches this process created: handle -> (n_blocks, n_kv_heads, head_dim)
+_CACHES: dict = {}
+_BF16_DTYPES = ("torch.bfloat16", "torch.int16", "torch.uint16")  # bf16 values or their bit patterns
+
+
+def _dev_tensor(x, name: str, dtypes, ndim: int | None = None):
+    """Require a contiguous tensor on the current GPU with one of `dtypes`
+    (names), so that no host pointer, wrong element type or strided view ever
+    reaches a kernel."""
+    import torch
+    if not isinstance(x, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor on the GPU, got {type(x).__name__}")
+    if not x.is_cuda:
+        raise ValueError(f"{name} must be on the GPU (got device {x.device})")
+    if x.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name} is on {x.device}, the current device is cuda:{torch.cuda.current_device()}")
+    if str(x.dtype) not in dtypes:
+        raise ValueError(f"{name} must have dtype {' or '.join(dtypes)}, got {x.dtype}")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and x.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got shape {tuple(x.shape)}")
+    return x
+
+
 def _is_device(x) -> bool:
     return not isinstance(x, np.ndarray) and getattr(x, "is_cuda", False)
 
 
-def _i32(seq) -> ctypes.Array | None:
+class _I32Arg:
+    """An int32 host array passed by pointer (no element-wise copy); keeps the
+    numpy buffer alive for the duration of the call."""
+
+    def __init__(self, seq):
+        self.a = np.ascontiguousarray(np.asarray(seq, dtype=np.int32).reshape(-1))
+        if self.a.size == 0:
+            self.a = np.zeros(1, dtype=np.int32)
+        self._as_parameter_ = self.a.ctypes.data_as(_c_i32p)
+
+
+def _i32(seq) -> _I32Arg | None:
     if seq is None:
         return None
-    a = np.ascontiguousarray(np.asarray(seq, dtype=np.int32))
-    return (ctypes.c_int32 * max(1, a.size))(*a.tolist())
+    return _I32Arg(seq)
 
 
 def _stream(stream) -> int:
@@ -134,24 +171,62 @@ def milo_cache_create(block_tokens: Sequence[int], rank_k: Sequence[int], rank_v
     if len(on_dev) > 1:
         raise ValueError("factors must all be host arrays or all device tensors")
     src_on_device = 1 if on_dev == {True} else 0
+    if not (len(block_tokens) == len(rank_k) == len(rank_v) == nb):
+        raise ValueError("block_tokens / rank_k / rank_v must hold one entry per block")
+    D = int(n_kv_heads) * int(head_dim)
     keep = []
     arrays = []
-    for s in srcs:
+    for kind, s in zip(("P^K", "R^K", "P^V", "R^V"), srcs):
         ptrs = (ctypes.c_void_p * nb)()
         for b, x in enumerate(s):
+            r = int(rank_k[b] if kind[-1] == "K" else rank_v[b])
+            want = (int(block_tokens[b]), r) if kind[0] == "P" else (r, D)
+            if tuple(x.shape) != want:
+                raise ValueError(f"block {b}: {kind} has shape {tuple(x.shape)}, expected {want}")
             if isinstance(x, np.ndarray):
-                x = np.ascontiguousarray(x, dtype=np.uint16)
+                if x.dtype not in (np.uint16, np.int16):
+                    raise ValueError(f"block {b}: host {kind} must hold bf16 bit patterns (uint16), got {x.dtype}")
+                x = np.ascontiguousarray(x).view(np.uint16)
                 keep.append(x)
-            elif not x.is_contiguous():
-                raise ValueError("device factors must be contiguous")
+            else:
+                _dev_tensor(x, f"block {b} {kind}", _BF16_DTYPES)
             ptrs[b] = _addr(x)
         arrays.append(ptrs)
     bt, rks, rvs = _i32(block_tokens), _i32(rank_k), _i32(rank_v)
-    desc = milo_cache_desc(nb, n_kv_heads, head_dim, bt, rks, rvs)
+    desc = milo_cache_desc(nb, n_kv_heads, head_dim, bt._as_parameter_, rks._as_parameter_, rvs._as_parameter_)
     out = ctypes.c_void_p()
     s = _stream(stream) if src_on_device else (0 if stream is None else _stream(stream))
     _check(lib().milo_cache_create(ctypes.byref(desc), *arrays, src_on_device, s, ctypes.byref(out)))
+    _CACHES[out.value] = (nb, int(n_kv_heads), int(head_dim))
     return out.value
+
+
+def _check_attend_args(cache, q, tail_k, tail_v, out, tail_rank: int):
+    """Shapes and element types of an attention call against the cache's
+    (n_kv_heads, head_dim); tail_rank is 4 for per-request tails, 3 for one
+    shared tail."""
+    _dev_tensor(q, "q", _BF16_DTYPES, 3)
+    _dev_tensor(out, "out", ("torch.float32",), 3)
+    if tuple(out.shape) != tuple(q.shape):
+        raise ValueError(f"out shape {tuple(out.shape)} differs from q shape {tuple(q.shape)}")
+    shape = _CACHES.get(cache)
+    if shape is None:
+        raise ValueError("unknown cache handle (not created by milo_cache_create, or already freed)")
+    _, n_kv, d = shape
+    if q.shape[2] != d:
+        raise ValueError(f"q head dim {q.shape[2]} differs from the cache's {d}")
+    if tail_k is None and tail_v is None:
+        return
+    for name, t in (("tail_k", tail_k), ("tail_v", tail_v)):
+        if t is None:
+            raise ValueError(f"{name} is None while the other tail is given")
+        _dev_tensor(t, name, _BF16_DTYPES, tail_rank)
+        if tuple(t.shape[-2:]) != (n_kv, d):
+            raise ValueError(f"{name} rows must be [H_kv={n_kv}][d={d}], got {tuple(t.shape)}")
+    if tuple(tail_k.shape) != tuple(tail_v.shape):
+        raise ValueError("tail_k and tail_v differ in shape")
+    if tail_rank == 4 and tail_k.shape[0] != q.shape[0]:
+        raise ValueError(f"tails hold {tail_k.shape[0]} requests, q holds {q.shape[0]}")
 
 
 def milo_attend_decode(cache: int, block_table, q, tail_k, tail_v, tail_len, scale: float, out,
@@ -159,12 +234,20 @@ def milo_attend_decode(cache: int, block_table, q, tail_k, tail_v, tail_len, sca
                        tail_cap: int | None = None) -> None:
     """Queue one decode step.  q: bf16 [n_q][H_q][d], tail_k/v: bf16
     [n_q][tail_cap][H_kv][d], out: fp32 [n_q][H_q][d] (device tensors)."""
+    _check_attend_args(cache, q, tail_k, tail_v, out, 4)
     if n_q is None:
         n_q, n_q_heads = int(q.shape[0]), int(q.shape[1])
+    elif n_q * n_q_heads * q.shape[2] != q.numel():
+        raise ValueError(f"n_q={n_q}, n_q_heads={n_q_heads} do not match q of shape {tuple(q.shape)}")
     if tail_cap is None:
         tail_cap = 0 if tail_k is None else int(tail_k.shape[1])
-    table = None if block_table is None else list(block_table)
-    n_sel = 0 if table is None else len(table)
+    elif tail_k is not None and tail_cap != tail_k.shape[1]:
+        raise ValueError(f"tail_cap={tail_cap} differs from the tails' {tail_k.shape[1]} rows")
+    if tail_cap > 0:
+        if tail_len is None or len(tail_len) != n_q:
+            raise ValueError(f"tail_len must hold {n_q} lengths")
+    table = None if block_table is None else np.asarray(block_table, dtype=np.int32).reshape(-1)
+    n_sel = 0 if table is None else int(table.size)
     _check(lib().milo_attend_decode(
         ctypes.c_void_p(cache), _i32(table) if n_sel else None, n_sel, n_q, n_q_heads,
         _addr(q), _addr(tail_k), _addr(tail_v), _i32(tail_len), tail_cap, float(scale), _addr(out),
@@ -177,10 +260,13 @@ def milo_attend_prefill(cache: int, block_table, q, tail_k, tail_v, tail_base: i
     [n_tok][H_q][d], tail_k/v: bf16 [tail_cap][H_kv][d] (one shared tail whose rows
     tail_base .. tail_base + n_tok - 1 are the chunk's own keys / values), out: fp32
     [n_tok][H_q][d] (device tensors)."""
+    _check_attend_args(cache, q, tail_k, tail_v, out, 3)
+    if tail_k is None:
+        raise ValueError("prefill needs the request's tail (its chunk's own keys and values)")
     n_tok, n_q_heads = int(q.shape[0]), int(q.shape[1])
     tail_cap = int(tail_k.shape[0])
-    table = None if block_table is None else list(block_table)
-    n_sel = 0 if table is None else len(table)
+    table = None if block_table is None else np.asarray(block_table, dtype=np.int32).reshape(-1)
+    n_sel = 0 if table is None else int(table.size)
     _check(lib().milo_attend_prefill(
         ctypes.c_void_p(cache), _i32(table) if n_sel else None, n_sel, n_tok, n_q_heads,
         _addr(q), _addr(tail_k), _addr(tail_v), int(tail_base), tail_cap, float(scale), _addr(out),
@@ -191,7 +277,17 @@ def milo_allocate_ranks(sigma, n_sv, r_total: int, r_min: int, r_max: int, strea
     """Per-block ranks (Sec. 4.3 allocation).  sigma: device fp32 [n_blocks][ld]
     tensor of non-increasing singular values, n_sv: host [n_blocks] counts.
     Returns int32 [n_blocks]; synchronous."""
-    n_blocks, ld = int(sigma.shape[0]), int(sigma.shape[1])
+    import torch
+    if not isinstance(sigma, torch.Tensor) or not sigma.is_cuda or sigma.dtype != torch.float32 \
+            or sigma.dim() != 2 or sigma.stride(1) != 1:
+        raise ValueError("sigma must be a float32 GPU tensor [n_blocks][ld] with unit column stride")
+    if sigma.device.index != torch.cuda.current_device():
+        raise ValueError(f"sigma is on {sigma.device}, the current device is cuda:{torch.cuda.current_device()}")
+    n_blocks, ld = int(sigma.shape[0]), int(sigma.stride(0)) if sigma.shape[0] > 1 else int(sigma.shape[1])
+    if len(n_sv) != n_blocks:
+        raise ValueError(f"n_sv must hold {n_blocks} counts")
+    if n_blocks > 0 and max(int(v) for v in n_sv) > sigma.shape[1]:
+        raise ValueError("a block's singular-value count exceeds the row length")
     out = (ctypes.c_int32 * max(1, n_blocks))()
     _check(lib().milo_allocate_ranks(_addr(sigma), ld, n_blocks, _i32(n_sv), int(r_total), int(r_min),
                                      int(r_max), out, _stream(stream)))
@@ -199,12 +295,20 @@ def milo_allocate_ranks(sigma, n_sv, r_total: int, r_min: int, r_max: int, strea
 
 
 def milo_cache_free(cache: int | None) -> None:
+    _CACHES.pop(cache, None)
     lib().milo_cache_free(ctypes.c_void_p(cache) if cache else None)
 
 
 def milo_cache_device_bytes(cache: int) -> int:
     v = ctypes.c_int64()
     _check(lib().milo_cache_device_bytes(ctypes.c_void_p(cache), ctypes.byref(v)))
+    return v.value
+
+
+def milo_cache_plan_builds(cache: int) -> int:
+    """Work plans built for this cache so far."""
+    v = ctypes.c_int64()
+    _check(lib().milo_cache_plan_builds(ctypes.c_void_p(cache), ctypes.byref(v)))
     return v.value
 
 

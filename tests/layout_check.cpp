@@ -54,9 +54,10 @@ static int check(int kind, int T, int r, int n_kv, int d) {
   return 0;
 }
 
-// The fragment runs every wave derives for one whole block (block_runs):
-// over the eight waves, each fragment of P^K, P^V and of head g's slices of
-// R^K and R^V is read the expected number of times (once; R^V once per wave
+// The fragment runs every wave derives for one whole block (block_runs), for a
+// column tile of one KV head and for tiles spanning several heads: over the
+// eight waves, each fragment of P^K, P^V and of the tile's heads' slices of R^K
+// and R^V is read the expected number of times (once; R^V once per wave
 // sharing a 16-dim slice), and each wave's run lengths match what the kernel
 // consumes per phase.
 static int check_runs(int T, int rk, int rv, int n_kv, int d) {
@@ -75,11 +76,15 @@ static int check_runs(int T, int rk, int rv, int n_kv, int d) {
   const long long total = n_pk + n_rk + n_pv + n_rv;
   const int ntile = T_pad / kTile, nds = d / 16;
   const int lg_ng = lg_rank_groups(bm.rv_pad / 32);
-  for (int g = 0; g < n_kv; ++g) {
+  // every head alone, and tiles spanning the heads g .. g + nh - 1
+  const int nh_multi = n_kv < kMaxTileHeads ? n_kv : kMaxTileHeads;
+  for (int pass = 0; pass < 2; ++pass)
+  for (int g = 0; g + (pass ? nh_multi : 1) <= n_kv; ++g) {
+    const int nh = pass ? nh_multi : 1;
     std::vector<int> seen((size_t)total, 0);
     for (int w = 0; w < kWaves; ++w) {
       std::vector<std::pair<int, int>> runs;
-      block_runs(bm, g, 0, ntile, w, d, lg_ng, [&](int x, int n) { runs.push_back({x, n}); });
+      block_runs(bm, g, nh, 0, ntile, w, d, lg_ng, [&](int x, int n) { runs.push_back({x, n}); });
       for (auto& r : runs)
         for (int k = 0; k < r.second; ++k) {
           if (r.first + k < 0 || r.first + k >= total) {
@@ -92,20 +97,29 @@ static int check_runs(int T, int rk, int rv, int n_kv, int d) {
       const int nrt_k = bm.rk_pad / 32, nrt_v = bm.rv_pad / 32, nseg = v_segments(nrt_v), ng = kWaves / nseg;
       const int own_k = owned_tiles(nrt_k, w, kWaves), own_v = owned_tiles(nrt_v, w % ng, ng);
       size_t i = 0;
-      if (own_k > 0 && (runs[i++].second != d / 16 * own_k)) { std::printf("runs: R^K length\n"); return 1; }
+      for (int h = 0; h < nh; ++h)
+        if (own_k > 0 && (runs[i++].second != d / 16 * own_k)) { std::printf("runs: R^K length\n"); return 1; }
       for (int t = 0; t < ntile; ++t) {
         if (runs[i++].second != bm.rk_pad / 16) { std::printf("runs: P^K length\n"); return 1; }
         if (own_v > 0 && runs[i++].second != kTile / 16 / nseg * own_v) { std::printf("runs: P^V length\n"); return 1; }
       }
-      if (runs[i++].second != bm.rv_pad / 32 || i != runs.size()) { std::printf("runs: R^V / count\n"); return 1; }
+      for (int h = 0; h < nh; ++h)
+        if (runs[i++].second != bm.rv_pad / 32) { std::printf("runs: R^V length\n"); return 1; }
+      if (i != runs.size()) { std::printf("runs: count\n"); return 1; }
       if ((int)runs.size() > kRunCap - 1) { std::printf("runs: more than the run buffer holds\n"); return 1; }
     }
     for (long long f = 0; f < total; ++f) {
       int want = 0;
       if (f < n_pk) want = 1;
-      else if (f < n_pk + n_rk) want = (f - n_pk) / (n_rk / n_kv) == g;
-      else if (f < n_pk + n_rk + n_pv) want = 1;
-      else want = (f - n_pk - n_rk - n_pv) / (n_rv / n_kv) == g ? kWaves / nds : 0;
+      else if (f < n_pk + n_rk) {
+        const long long h = (f - n_pk) / (n_rk / n_kv);
+        want = h >= g && h < g + nh;
+      } else if (f < n_pk + n_rk + n_pv) {
+        want = 1;
+      } else {
+        const long long h = (f - n_pk - n_rk - n_pv) / (n_rv / n_kv);
+        want = h >= g && h < g + nh ? kWaves / nds : 0;
+      }
       if (seen[(size_t)f] != want) {
         std::printf("runs: head %d fragment %lld read %d times, want %d\n", g, f, seen[(size_t)f], want);
         return 1;

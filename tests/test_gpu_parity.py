@@ -4,6 +4,7 @@ Bar: max over (query, head) of the relative L2 error <= 1e-2 (bf16 factors,
 fp32 accumulation).  Shapes span several token tiles, several rank tiles,
 ragged block sizes, odd ranks, K/V ranks that differ, ragged and empty tails,
 several column tiles, and 1..16 query heads per KV head."""
+import ctypes
 import zlib
 
 import numpy as np
@@ -59,6 +60,23 @@ SHAPES = {
                     head_dim=128, n_q=2, n_q_heads=40, tail_cap=64),
     "rank896": dict(block_tokens=[1000], rank_k=[896], rank_v=[840], n_kv_heads=8, head_dim=128, n_q=1,
                     n_q_heads=16, tail_cap=0),
+    # 32B-shaped heads (80 columns per KV head): ten 64-column tiles spanning two
+    # heads each on a gang of ten, two solo workgroups per XCD on tail chunks
+    "flat_tiles_32b_heads": dict(block_tokens=[2048, 512, 1024], rank_k=[320, 128, 512], n_kv_heads=8,
+                                 head_dim=128, n_q=16, n_q_heads=40, tail_cap=600),
+    # the same tiling at ranks above 512 (half weight tile, three latent rank tiles)
+    "flat_tiles_rank768": dict(block_tokens=[1024, 800], rank_k=[768, 640], rank_v=[704, 768], n_kv_heads=8,
+                               head_dim=128, n_q=16, n_q_heads=40, tail_cap=40),
+    # 7B 28-layer heads (224 columns per KV head): four tiles per head, a gang of 16
+    "gang16_7b_heads": dict(block_tokens=[1024, 300, 700], rank_k=[448, 96, 160], n_kv_heads=4, head_dim=128,
+                            n_q=32, n_q_heads=28, tail_cap=300),
+    # six columns per KV head: four heads packed into one tile
+    "packed_four_heads": dict(block_tokens=[512, 77], rank_k=[96, 40], n_kv_heads=4, head_dim=64, n_q=3,
+                              n_q_heads=8, tail_cap=20, tail_len=[20, 0, 7]),
+    # more requests than the kernel arguments carry: tail lengths from device memory
+    "batch_300_device_tail_lengths": dict(block_tokens=[256, 100], rank_k=[32, 64], n_kv_heads=1, head_dim=64,
+                                          n_q=300, n_q_heads=2, tail_cap=5,
+                                          tail_len=[i % 6 for i in range(300)]),
 }
 
 
@@ -75,25 +93,50 @@ def test_parity_q7b_single_layer():
     _check(synth.gen_layer("q7b_1l"), label="q7b_1l")
 
 
-@pytest.mark.parametrize("cfg,layer", [("q7b_28l", 27), ("q14b_48l", 0), ("q32b_64l", 0)])
-def test_parity_full_size_layers_sampled(cfg, layer):
-    """One whole layer of each large workload (all selected blocks, full decode
-    batch, full tails) on the GPU; the oracle checks a seeded sample of columns
-    (every KV head group is represented)."""
+def _head_major(c, N_g, G):
+    """(request, query head) of head-major column c = g * N_g + i * G + (h mod G)."""
+    g, rem = divmod(int(c), N_g)
+    return rem // G, g * G + rem % G
+
+
+def _full_size_columns(inp, cfg):
+    """Columns checked against the oracle at full size: every column of the 7B
+    28-layer batch; for the 14B and 32B batches the first and last query of the
+    batch with all their heads, plus the first and last column of every
+    64-column stretch and of every KV head in head-major order (so every column
+    tile of either tiling is hit at both ends)."""
+    G = inp.n_q_heads // inp.n_kv_heads
+    N_g = inp.n_q * G
+    if cfg == "q7b_28l":
+        return [(i, h) for i in range(inp.n_q) for h in range(inp.n_q_heads)]
+    cols = {(i, h) for i in (0, inp.n_q - 1) for h in range(inp.n_q_heads)}
+    N = N_g * inp.n_kv_heads
+    for c in range(N):
+        if c % 64 in (0, 63) or c % N_g in (0, N_g - 1) or c == N - 1:
+            cols.add(_head_major(c, N_g, G))
+    return sorted(cols)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("cfg,layer", [("q7b_28l", 0), ("q7b_28l", 27), ("q14b_48l", 0), ("q14b_48l", 47),
+                                       ("q32b_64l", 0), ("q32b_64l", 63)])
+def test_parity_full_size_layers(cfg, layer):
+    """The first and last layer of each large workload, whole (all selected
+    blocks, full decode batch, full tails) on the GPU; the oracle checks the
+    columns of _full_size_columns."""
     inp = synth.gen_layer(cfg, layer)
+    print(f"[parity] {cfg} layer {layer}: generated", flush=True)
     gl = GpuLayer(inp)
     try:
         got = gl.attend().cpu().numpy()
     finally:
         gl.free()
     assert np.all(np.isfinite(got)), "unwritten or non-finite outputs"
-    rng = np.random.default_rng(zlib.crc32(cfg.encode()) + layer)
-    G = inp.n_q_heads // inp.n_kv_heads
-    cols = [(int(rng.integers(inp.n_q)), g * G + int(rng.integers(G))) for g in range(inp.n_kv_heads)]
-    cols += [(int(rng.integers(inp.n_q)), int(rng.integers(inp.n_q_heads))) for _ in range(4)]
+    cols = _full_size_columns(inp, cfg)
+    print(f"[parity] {cfg} layer {layer}: GPU done, oracle on {len(cols)} columns", flush=True)
     ref = oracle.attend_latent(**oracle_args(inp), columns=cols)
     err = col_rel_l2(np.stack([got[i, h] for i, h in cols]), ref)
-    print(f"[parity] {cfg} layer {layer}: {len(cols)} sampled columns, max rel-L2 = {err.max():.3e}", flush=True)
+    print(f"[parity] {cfg} layer {layer}: {len(cols)} columns, max rel-L2 = {err.max():.3e}", flush=True)
     assert err.max() <= TOL_REL_L2
 
 
@@ -149,11 +192,12 @@ def test_plan_changes_between_calls():
 
 def test_work_split_over_several_launches(monkeypatch):
     """When the workgroup programs do not fit in LDS the step runs as several
-    attention launches.  A cap of 5376 program bytes holds the run buffers and
-    at most three 80-byte items per workgroup; 1200 one-tile blocks on one KV
-    head give some workgroup at least five items in a single launch, so the
-    plan needs two or more launches."""
-    monkeypatch.setenv("MILO_MAX_PROGRAM_BYTES", "5376")
+    attention launches.  A cap of 6912 program bytes holds the run buffers
+    (8 waves x 4 buffers x 26 runs x 8 bytes = 6656) and at most three 80-byte
+    items per workgroup; 1200 one-tile blocks on one KV head give some workgroup
+    at least five items in a single launch, so the plan needs two or more
+    launches."""
+    monkeypatch.setenv("MILO_MAX_PROGRAM_BYTES", "6912")
     n = 1200
     inp = synth.make_problem(31, [32] * n, [16] * n, rank_v=[8] * n, n_kv_heads=1, head_dim=64, n_q=2,
                              n_q_heads=2, tail_cap=40, tail_len=[40, 3])
@@ -166,6 +210,36 @@ def test_work_split_over_several_launches(monkeypatch):
     err = max_rel_l2(got, ref)
     print(f"[parity] several launches max rel-L2 = {err:.3e}", flush=True)
     assert err <= TOL_REL_L2
+
+
+def test_tails_growing_across_calls():
+    """A decode loop: the same cache and block table, every request's tail one
+    token longer at each call, crossing the 256-token chunk boundaries and the
+    planned chunk capacity (1 -> 2 chunks, then 3: four rounded up, capped by the
+    700-row buffer).  Every call matches the oracle, and the plan is rebuilt only
+    when the capacity grows."""
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(40, [1024, 300], [256, 64], n_kv_heads=2, head_dim=128, n_q=3, n_q_heads=14,
+                             tail_cap=700, tail_len=[0, 0, 0])
+    gl = GpuLayer(inp)
+    try:
+        builds0 = milo.milo_cache_plan_builds(gl.cache)
+        lens = np.array([254, 250, 100])
+        steps = 0
+        for start in (0, 258):
+            for k in range(5):
+                tl = lens + start + k
+                got = gl.attend(None, tl).cpu().numpy()
+                ref = oracle.attend_latent(**oracle_args(inp, None, tl))
+                err = max_rel_l2(got, ref)
+                assert err <= TOL_REL_L2, (tl, err)
+                steps += 1
+        builds = milo.milo_cache_plan_builds(gl.cache) - builds0
+        print(f"[parity] growing tails: {steps} calls, {builds} plan builds", flush=True)
+        # capacities seen: 1 chunk (longest tail 254..256), 2 chunks (257..512), 3 chunks (513..516)
+        assert builds == 3
+    finally:
+        gl.free()
 
 
 def test_deterministic_and_fully_written():
@@ -222,18 +296,23 @@ def test_attend_rejects_bad_arguments():
             dict(block_table=[], tail_len=[4, 0]),  # request 1 has no keys
             dict(tail_len=[5, 0]),                # longer than tail_cap
             dict(tail_len=[-1, 0]),
-            dict(n_q_heads=3),                    # not a multiple of H_kv
             dict(scale=float("inf")),
         ]
         for kw in bad:
             args = dict(block_table=[0, 1], q=gl.q, tail_k=gl.tk, tail_v=gl.tv, tail_len=[4, 0],
                         scale=inp.scale, out=out)
-            n_q_heads = kw.pop("n_q_heads", None)
             args.update(kw)
             with pytest.raises(milo.MiloError) as ei:
-                milo.milo_attend_decode(gl.cache, **args, n_q=2 if n_q_heads else None,
-                                        n_q_heads=n_q_heads)
+                milo.milo_attend_decode(gl.cache, **args)
             assert ei.value.code == milo.MILO_ERR_INVALID_ARG, kw
+        # query heads not a multiple of the KV heads: the library's own check
+        # (the binding would refuse the shape first), called through the C ABI
+        tl = (ctypes.c_int32 * 2)(4, 0)
+        table = (ctypes.c_int32 * 2)(0, 1)
+        rc = milo.lib().milo_attend_decode(ctypes.c_void_p(gl.cache), table, 2, 2, 3, gl.q.data_ptr(),
+                                           gl.tk.data_ptr(), gl.tv.data_ptr(), tl, 4, inp.scale, out.data_ptr(),
+                                           None)
+        assert rc == milo.MILO_ERR_INVALID_ARG and "multiple" in milo.milo_last_error()
     finally:
         gl.free()
 
