@@ -121,6 +121,26 @@ int milo_attend_decode(milo_cache* cache, const int32_t* block_table, int32_t n_
                        const int32_t* tail_len, int32_t tail_cap, float scale, float* out,
                        void* hip_stream);
 
+/* milo_attend_decode for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, kernels and results, but the call's workspace (work plan,
+ * partial results, tail lengths of batches above 256 requests) lives in a fixed
+ * 64 MiB scratch array of the library, one copy per GPU, held until the process
+ * ends; the call makes no device allocation and no hipFree (the plan is built in
+ * host memory and copied in stream order).  Limits: an 8 MiB plan, 55 MiB of
+ * partial results (n_q * H_q columns x slots x (4 d + 8) bytes; e.g. the
+ * 7B- and 32B-shaped layers fit, a 14B-shaped 64-query layer does not) and
+ * 262144 requests; larger calls return MILO_ERR_UNSUPPORTED before queuing
+ * anything.  Every call on a GPU shares that GPU's scratch and it keeps the
+ * last call's contents (nothing in it needs clearing): calls that overlap on one
+ * GPU race, so order them on one stream.  Kernel timing (milo_timing_*) does not
+ * record these calls.  Errors: as milo_attend_decode. */
+int milo_attend_decode_noalloc(milo_cache* cache, const int32_t* block_table, int32_t n_sel,
+                               int32_t n_q, int32_t n_q_heads, const uint16_t* q,
+                               const uint16_t* tail_k, const uint16_t* tail_v,
+                               const int32_t* tail_len, int32_t tail_cap, float scale,
+                               float* out, void* hip_stream);
+
 /* Prefill of one request: a chunk of n_tok consecutive query tokens attends to
  * the selected blocks plus the request's dense tail, causally among its own
  * tokens (Alg. 1 inference stage with a multi-token input query Q; Eq. 1).

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -17,6 +18,7 @@
 #include <vector>
 
 #include "milo.h"
+#include "milo_attend.h"
 #include "milo_internal.h"
 #include "milo_plan.h"
 
@@ -79,12 +81,13 @@ TimingState g_timing;
 
 struct milo_cache {
   int device = -1;
+  uint64_t serial = 0;  // distinct for every cache of the process (plan keys)
   int n_blocks = 0, n_kv = 0, d = 0;
   std::vector<int32_t> T, rk, rv;
   std::vector<BlockMeta> meta;
   uint16_t* data = nullptr;
   int64_t data_elems = 0;
-  // per-call workspace
+  // per-call workspace of milo_attend_decode / milo_attend_prefill
   float* part_o = nullptr;
   float2* part_ml = nullptr;
   int64_t part_cols_slots = 0;  // capacity in (column, slot) pairs
@@ -95,14 +98,7 @@ struct milo_cache {
   bool plan_evt_live = false;
   int32_t* tail_len_d = nullptr;         // tail lengths of batches above kInlineTails requests
   int64_t tail_len_cap = 0;
-  // the plan of the previous call
-  std::vector<int32_t> plan_key;
-  int64_t plan_builds = 0;
-  int n_launch = 0, n_slots = 0, n_block_slots = 0, max_rt = 0, nslot = 0, rk_pad_max = 0, n_chunks = 0;
-  TileGeom tiles{};
-  int64_t count_off = 0;  // byte offset of the plan's slot counts
-  int prog_bytes = 0, ring_offset = 0;
-  size_t lds = 0;
+  PlanState plan;                        // the plan of the previous call
 };
 
 namespace {
@@ -192,7 +188,9 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     if (!pk[b] || !rk[b] || !pv[b] || !rv[b]) return fail(MILO_ERR_INVALID_ARG, "block %d: NULL factor", b);
   }
 
+  static std::atomic<uint64_t> next_serial{1};
   milo_cache* c = new milo_cache();
+  c->serial = next_serial.fetch_add(1);
   c->n_blocks = desc->n_blocks;
   c->n_kv = desc->n_kv_heads;
   c->d = desc->head_dim;
@@ -274,7 +272,7 @@ int milo_cache_device_bytes(const milo_cache* cache, int64_t* bytes) {
 int milo_cache_plan_builds(const milo_cache* cache, int64_t* builds) {
   g_err.clear();
   if (!cache || !builds) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
-  *builds = cache->plan_builds;
+  *builds = cache->plan.builds;
   return MILO_OK;
 }
 
@@ -298,15 +296,92 @@ int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which
   return MILO_OK;
 }
 
-// Attention of n_q query tokens over the selected blocks plus their dense tails:
-// query i reads tail rows [i * tail_stride, i * tail_stride + len_i) of tail_k /
-// tail_v (tail_stride = tail_cap: one tail per request; 0: one shared tail),
-// with len_i = tail_len[i] (host array), or tail_base + i + 1 when tail_len is
-// NULL (the causal lengths of a prefill chunk).
-static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_q, int32_t n_q_heads,
-                  const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
-                  int32_t tail_base, int32_t tail_cap, int64_t tail_stride, float scale, float* out,
-                  void* hip_stream) {
+}  // extern "C"
+
+namespace {
+
+// The workspace a cache owns: device buffers grown on demand (growth waits for
+// the stream, since queued calls may still read the old buffers) and a pinned
+// staging buffer for plan uploads, rewritten once its previous upload was consumed.
+class CacheWorkspace : public Workspace {
+ public:
+  explicit CacheWorkspace(milo_cache* c) : c_(c) {}
+  int upload_plan(const std::vector<unsigned char>& bytes, hipStream_t s, const unsigned char** dev) override {
+    milo_cache* c = c_;
+    const int64_t plan_bytes = (int64_t)bytes.size();
+    if (plan_bytes > c->plan_cap) {
+      MILO_HIP(hipStreamSynchronize(s));
+      (void)hipFree(c->plan_d);
+      (void)hipHostFree(c->plan_pinned);
+      c->plan_d = nullptr;
+      c->plan_pinned = nullptr;
+      c->plan_cap = 0;
+      c->plan_evt_live = false;
+      const int64_t cap = plan_bytes + plan_bytes / 4;
+      MILO_HIP(hipMalloc(&c->plan_d, (size_t)cap));
+      MILO_HIP(hipHostMalloc(&c->plan_pinned, (size_t)cap, hipHostMallocDefault));
+      c->plan_cap = cap;
+    }
+    if (!c->plan_evt) MILO_HIP(hipEventCreateWithFlags(&c->plan_evt, hipEventDisableTiming));
+    if (c->plan_evt_live) MILO_HIP(hipEventSynchronize(c->plan_evt));
+    c->plan_evt_live = false;
+    std::memcpy(c->plan_pinned, bytes.data(), (size_t)plan_bytes);
+    MILO_HIP(hipMemcpyAsync(c->plan_d, c->plan_pinned, (size_t)plan_bytes, hipMemcpyHostToDevice, s));
+    MILO_HIP(hipEventRecord(c->plan_evt, s));
+    c->plan_evt_live = true;
+    *dev = c->plan_d;
+    return MILO_OK;
+  }
+  int partials(int64_t need, int d, hipStream_t s, float** o, float2** ml) override {
+    milo_cache* c = c_;
+    if (need > c->part_cols_slots) {
+      MILO_HIP(hipStreamSynchronize(s));
+      (void)hipFree(c->part_o);
+      (void)hipFree(c->part_ml);
+      c->part_o = nullptr;
+      c->part_ml = nullptr;
+      c->part_cols_slots = 0;
+      const int64_t cap = env_byte_cap();
+      const int64_t bytes = need * ((int64_t)d * 4 + 8);
+      if (cap >= 0 && c->data_elems * 2 + bytes > cap)
+        return fail(MILO_ERR_OUT_OF_MEMORY, "workspace of %lld bytes exceeds MILO_MAX_DEVICE_BYTES",
+                    (long long)bytes);
+      MILO_HIP(hipMalloc(&c->part_o, (size_t)need * d * 4));
+      MILO_HIP(hipMalloc(&c->part_ml, (size_t)need * sizeof(float2)));
+      c->part_cols_slots = need;
+    }
+    *o = c->part_o;
+    *ml = c->part_ml;
+    return MILO_OK;
+  }
+  int tail_lengths(const int32_t* host, int n_q, hipStream_t s, const int32_t** dev) override {
+    milo_cache* c = c_;
+    if (n_q > c->tail_len_cap) {
+      MILO_HIP(hipStreamSynchronize(s));
+      (void)hipFree(c->tail_len_d);
+      c->tail_len_d = nullptr;
+      c->tail_len_cap = 0;
+      MILO_HIP(hipMalloc(&c->tail_len_d, sizeof(int32_t) * n_q));
+      c->tail_len_cap = n_q;
+    }
+    MILO_HIP(hipMemcpyAsync(c->tail_len_d, host, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
+    *dev = c->tail_len_d;
+    return MILO_OK;
+  }
+  bool may_time() const override { return true; }
+
+ private:
+  milo_cache* c_;
+};
+
+}  // namespace
+
+namespace milo {
+
+int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* block_table, int32_t n_sel, int32_t n_q,
+                int32_t n_q_heads, const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v,
+                const int32_t* tail_len, int32_t tail_base, int32_t tail_cap, int64_t tail_stride, float scale,
+                float* out, void* hip_stream) {
   // ---- validation (host only, nothing queued yet) ----
   if (!c) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
   if (n_sel < 0) return fail(MILO_ERR_INVALID_ARG, "n_sel must be >= 0");
@@ -358,18 +433,20 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
     n_chunks = std::min(n_chunks, (tail_cap + kTailChunk - 1) / kTailChunk);
   }
   std::vector<int32_t> key;
-  key.reserve(4 + n_sel);
+  key.reserve(6 + n_sel);
+  key.push_back((int32_t)(c->serial & 0xffffffffu));  // the cache (plans of a shared workspace)
+  key.push_back((int32_t)(c->serial >> 32));
   key.push_back(n_sel);
   key.push_back(n_q);
   key.push_back(n_q_heads);
   key.push_back(n_chunks);
   key.insert(key.end(), block_table, block_table + n_sel);
   const int n_cols = n_q * n_q_heads;
-  if (key != c->plan_key) {
+  if (key != ps.key) {
     // no plan is valid until this one is complete: a failure below (an
     // allocation, an upload) must not leave the old key pointing at buffers
     // that were freed or half rewritten
-    c->plan_key.clear();
+    ps.key.clear();
     const Tiling til = make_tiling(c->n_kv, n_q * G);
     Schedule sch;
     std::string why;
@@ -391,62 +468,37 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
       for (int cand : {8, 6})
         if (prog + base + attend_ring_bytes(cand) <= (size_t)kLdsBytes) { nslot = cand; break; }
     }
-    // upload in stream order: the kernels of earlier calls, queued before the
-    // copy, read the old plan first.  Only growth of the device buffer waits for
-    // the stream (the old buffer may still be read); the pinned staging buffer
-    // is rewritten once its previous upload has been consumed.
-    const int64_t plan_bytes = (int64_t)sch.bytes.size();
-    if (plan_bytes > c->plan_cap) {
-      MILO_HIP(hipStreamSynchronize(s));
-      (void)hipFree(c->plan_d);
-      (void)hipHostFree(c->plan_pinned);
-      c->plan_d = nullptr;
-      c->plan_pinned = nullptr;
-      c->plan_cap = 0;
-      c->plan_evt_live = false;
-      const int64_t cap = plan_bytes + plan_bytes / 4;
-      MILO_HIP(hipMalloc(&c->plan_d, (size_t)cap));
-      MILO_HIP(hipHostMalloc(&c->plan_pinned, (size_t)cap, hipHostMallocDefault));
-      c->plan_cap = cap;
-    }
-    if (!c->plan_evt) MILO_HIP(hipEventCreateWithFlags(&c->plan_evt, hipEventDisableTiming));
-    if (c->plan_evt_live) MILO_HIP(hipEventSynchronize(c->plan_evt));
-    c->plan_evt_live = false;
-    std::memcpy(c->plan_pinned, sch.bytes.data(), (size_t)plan_bytes);
-    MILO_HIP(hipMemcpyAsync(c->plan_d, c->plan_pinned, (size_t)plan_bytes, hipMemcpyHostToDevice, s));
-    MILO_HIP(hipEventRecord(c->plan_evt, s));
-    c->plan_evt_live = true;
-    c->n_launch = sch.n_launch;
-    c->n_chunks = n_chunks;
-    c->n_slots = sch.n_block_slots + n_chunks;
-    c->n_block_slots = sch.n_block_slots;
-    c->count_off = sch.count_off;
-    c->tiles = til.geom;
-    c->max_rt = max_rt;
-    c->nslot = nslot;
-    c->rk_pad_max = sch.rk_pad_max;
-    c->prog_bytes = sch.prog_bytes;
-    c->ring_offset = (int)base;
-    c->lds = prog + base + attend_ring_bytes(nslot);
-    c->plan_key.swap(key);
-    ++c->plan_builds;
+    // the workspace for the new plan's partials first (a workspace that cannot
+    // hold them fails here, before anything is queued), then the upload, in
+    // stream order: the kernels of earlier calls, queued before the copy, read
+    // the old plan first
+    float* po = nullptr;
+    float2* pml = nullptr;
+    if (const int err = ws.partials((int64_t)n_cols * (sch.n_block_slots + n_chunks), c->d, s, &po, &pml);
+        err != MILO_OK)
+      return err;
+    const unsigned char* plan_d = nullptr;
+    if (const int err = ws.upload_plan(sch.bytes, s, &plan_d); err != MILO_OK) return err;
+    ps.plan_d = plan_d;
+    ps.n_launch = sch.n_launch;
+    ps.n_chunks = n_chunks;
+    ps.n_slots = sch.n_block_slots + n_chunks;
+    ps.n_block_slots = sch.n_block_slots;
+    ps.count_off = sch.count_off;
+    ps.tiles = til.geom;
+    ps.max_rt = max_rt;
+    ps.nslot = nslot;
+    ps.rk_pad_max = sch.rk_pad_max;
+    ps.prog_bytes = sch.prog_bytes;
+    ps.ring_offset = (int)base;
+    ps.lds = prog + base + attend_ring_bytes(nslot);
+    ps.key.swap(key);
+    ++ps.builds;
   }
-  const int64_t need = (int64_t)n_cols * c->n_slots;
-  if (need > c->part_cols_slots) {
-    MILO_HIP(hipStreamSynchronize(s));
-    (void)hipFree(c->part_o);
-    (void)hipFree(c->part_ml);
-    c->part_o = nullptr;
-    c->part_ml = nullptr;
-    c->part_cols_slots = 0;
-    const int64_t cap = env_byte_cap();
-    const int64_t bytes = need * ((int64_t)c->d * 4 + 8);
-    if (cap >= 0 && c->data_elems * 2 + bytes > cap)
-      return fail(MILO_ERR_OUT_OF_MEMORY, "workspace of %lld bytes exceeds MILO_MAX_DEVICE_BYTES", (long long)bytes);
-    MILO_HIP(hipMalloc(&c->part_o, (size_t)need * c->d * 4));
-    MILO_HIP(hipMalloc(&c->part_ml, (size_t)need * sizeof(float2)));
-    c->part_cols_slots = need;
-  }
+  float* part_o = nullptr;
+  float2* part_ml = nullptr;
+  if (const int err = ws.partials((int64_t)n_cols * ps.n_slots, c->d, s, &part_o, &part_ml); err != MILO_OK)
+    return err;
   // this call's tail lengths travel in the kernel arguments; a batch above
   // kInlineTails requests copies them to the device in stream order
   TailLens tls{};
@@ -459,50 +511,41 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
     for (int i = 0; i < n_q; ++i) tls.v[i] = tail_len[i];
   } else {
     tls.mode = kTailDevice;
-    if (n_q > c->tail_len_cap) {
-      MILO_HIP(hipStreamSynchronize(s));
-      (void)hipFree(c->tail_len_d);
-      c->tail_len_d = nullptr;
-      c->tail_len_cap = 0;
-      MILO_HIP(hipMalloc(&c->tail_len_d, sizeof(int32_t) * n_q));
-      c->tail_len_cap = n_q;
-    }
-    MILO_HIP(hipMemcpyAsync(c->tail_len_d, tail_len, sizeof(int32_t) * n_q, hipMemcpyHostToDevice, s));
-    tls.dev = c->tail_len_d;
+    if (const int err = ws.tail_lengths(tail_len, n_q, s, &tls.dev); err != MILO_OK) return err;
   }
 
   // ---- launches ----
   AttendArgs aa{};
   aa.data = c->data;
-  aa.prog = c->plan_d;
+  aa.prog = ps.plan_d;
   aa.q = q;
   aa.tail_k = tail_k;
   aa.tail_v = tail_v;
-  aa.part_o = c->part_o;
-  aa.part_ml = c->part_ml;
+  aa.part_o = part_o;
+  aa.part_ml = part_ml;
   aa.qscale = scale * 1.4426950408889634f;
   aa.n_q = n_q;
   aa.H_q = n_q_heads;
   aa.H_kv = c->n_kv;
   aa.G = G;
   aa.tail_stride = tail_stride;
-  aa.n_slots = c->n_slots;
-  aa.n_block_slots = c->n_block_slots;
-  aa.qt_stride = c->rk_pad_max + 8;
-  aa.prog_bytes = c->prog_bytes;
-  aa.ring_offset = c->ring_offset;
+  aa.n_slots = ps.n_slots;
+  aa.n_block_slots = ps.n_block_slots;
+  aa.qt_stride = ps.rk_pad_max + 8;
+  aa.prog_bytes = ps.prog_bytes;
+  aa.ring_offset = ps.ring_offset;
   aa.N_g = n_q * G;
   aa.tl = tls;
   MergeArgs ma{};
-  ma.part_o = c->part_o;
-  ma.part_ml = c->part_ml;
+  ma.part_o = part_o;
+  ma.part_ml = part_ml;
   ma.out = out;
-  ma.slot_count = reinterpret_cast<const int32_t*>(c->plan_d + c->count_off);
+  ma.slot_count = reinterpret_cast<const int32_t*>(ps.plan_d + ps.count_off);
   ma.H_q = n_q_heads;
   ma.G = G;
-  ma.n_block_slots = c->n_block_slots;
-  ma.n_slots = c->n_slots;
-  ma.tiles = c->tiles;
+  ma.n_block_slots = ps.n_block_slots;
+  ma.n_slots = ps.n_slots;
+  ma.tiles = ps.tiles;
   ma.tl = tls;
 
   // timing: events recorded by the launches themselves at kernel start and end
@@ -510,7 +553,7 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
   bool timed = false;
   {
     std::lock_guard<std::mutex> lk(g_timing.mu);
-    if (g_timing.enabled) {
+    if (g_timing.enabled && ws.may_time()) {
       for (int k = 0; k < 4; ++k) {
         if (g_timing.pool.empty()) {
           hipEvent_t e;
@@ -536,10 +579,10 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
     return hip_fail(err, what);
   };
   hipError_t e = hipSuccess;
-  for (int l = 0; l < c->n_launch; ++l) {
-    aa.wg = reinterpret_cast<const WgProgram*>(c->plan_d) + (size_t)l * kCUs;
-    e = launch_attend(aa, c->d, c->max_rt, c->nslot, kCUs, c->lds, s, l == 0 ? ev[0] : nullptr,
-                      l == c->n_launch - 1 ? ev[1] : nullptr);
+  for (int l = 0; l < ps.n_launch; ++l) {
+    aa.wg = reinterpret_cast<const WgProgram*>(ps.plan_d) + (size_t)l * kCUs;
+    e = launch_attend(aa, c->d, ps.max_rt, ps.nslot, kCUs, ps.lds, s, l == 0 ? ev[0] : nullptr,
+                      l == ps.n_launch - 1 ? ev[1] : nullptr);
     if (e != hipSuccess) return launch_fail(e, "attend kernel launch");
   }
   e = launch_merge(ma, c->d, n_cols, s, ev[2], ev[3]);
@@ -551,13 +594,19 @@ static int attend(milo_cache* c, const int32_t* block_table, int32_t n_sel, int3
   return MILO_OK;
 }
 
+}  // namespace milo
+
+extern "C" {
+
 int milo_attend_decode(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_q, int32_t n_q_heads,
                        const uint16_t* q, const uint16_t* tail_k, const uint16_t* tail_v, const int32_t* tail_len,
                        int32_t tail_cap, float scale, float* out, void* hip_stream) {
   g_err.clear();
+  if (!c) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
   if (tail_cap > 0 && !tail_len) return fail(MILO_ERR_INVALID_ARG, "tail_len must be non-NULL when tail_cap > 0");
-  return attend(c, block_table, n_sel, n_q, n_q_heads, q, tail_k, tail_v, tail_len, -1, tail_cap, tail_cap, scale,
-                out, hip_stream);
+  CacheWorkspace ws(c);
+  return attend_call(c, c->plan, ws, block_table, n_sel, n_q, n_q_heads, q, tail_k, tail_v, tail_len, -1, tail_cap,
+                     tail_cap, scale, out, hip_stream);
 }
 
 int milo_attend_prefill(milo_cache* c, const int32_t* block_table, int32_t n_sel, int32_t n_tok, int32_t n_q_heads,
@@ -570,9 +619,11 @@ int milo_attend_prefill(milo_cache* c, const int32_t* block_table, int32_t n_sel
     return fail(MILO_ERR_INVALID_ARG, "tail_cap (%d) must hold tail_base + n_tok = %lld rows", tail_cap,
                 (long long)tail_base + n_tok);
   if (!tail_k || !tail_v) return fail(MILO_ERR_INVALID_ARG, "tail_k / tail_v must be non-NULL");
+  if (!c) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
   // token j sees the tail_base rows before the chunk and the chunk's first j + 1 tokens
-  return attend(c, block_table, n_sel, n_tok, n_q_heads, q, tail_k, tail_v, nullptr, tail_base, tail_cap, 0, scale,
-                out, hip_stream);
+  CacheWorkspace ws(c);
+  return attend_call(c, c->plan, ws, block_table, n_sel, n_tok, n_q_heads, q, tail_k, tail_v, nullptr, tail_base,
+                     tail_cap, 0, scale, out, hip_stream);
 }
 
 int milo_timing_enable(int enable) {

@@ -58,6 +58,9 @@ def lib() -> ctypes.CDLL:
         L.milo_attend_decode.argtypes = [vp, _c_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                          vp, vp, vp, _c_i32p, ctypes.c_int32, ctypes.c_float, vp, vp]
         L.milo_attend_decode.restype = ctypes.c_int
+        L.milo_attend_decode_noalloc.argtypes = [vp, _c_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                 vp, vp, vp, _c_i32p, ctypes.c_int32, ctypes.c_float, vp, vp]
+        L.milo_attend_decode_noalloc.restype = ctypes.c_int
         L.milo_attend_prefill.argtypes = [vp, _c_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                           vp, vp, vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, vp, vp]
         L.milo_attend_prefill.restype = ctypes.c_int
@@ -249,6 +252,23 @@ def milo_attend_decode(cache: int, block_table, q, tail_k, tail_v, tail_len, sca
     table = None if block_table is None else np.asarray(block_table, dtype=np.int32).reshape(-1)
     n_sel = 0 if table is None else int(table.size)
     _check(lib().milo_attend_decode(
+        ctypes.c_void_p(cache), _i32(table) if n_sel else None, n_sel, n_q, n_q_heads,
+        _addr(q), _addr(tail_k), _addr(tail_v), _i32(tail_len), tail_cap, float(scale), _addr(out),
+        _stream(stream)))
+
+
+def milo_attend_decode_noalloc(cache: int, block_table, q, tail_k, tail_v, tail_len, scale: float, out,
+                               stream=None) -> None:
+    """milo_attend_decode with its workspace in the library's fixed scratch
+    (no device allocation; see include/milo.h for the limits)."""
+    _check_attend_args(cache, q, tail_k, tail_v, out, 4)
+    n_q, n_q_heads = int(q.shape[0]), int(q.shape[1])
+    tail_cap = 0 if tail_k is None else int(tail_k.shape[1])
+    if tail_cap > 0 and (tail_len is None or len(tail_len) != n_q):
+        raise ValueError(f"tail_len must hold {n_q} lengths")
+    table = None if block_table is None else np.asarray(block_table, dtype=np.int32).reshape(-1)
+    n_sel = 0 if table is None else int(table.size)
+    _check(lib().milo_attend_decode_noalloc(
         ctypes.c_void_p(cache), _i32(table) if n_sel else None, n_sel, n_q, n_q_heads,
         _addr(q), _addr(tail_k), _addr(tail_v), _i32(tail_len), tail_cap, float(scale), _addr(out),
         _stream(stream)))
