@@ -60,19 +60,20 @@ def counter_summary(workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"attend_kernel_{workload}_counters.md")
 
 
-def counter_traffic(workload: str):
-    """HBM bytes per attention-kernel launch from the committed rocprofv3 counter
-    summary of this workload, or None when absent or taken on different kernel
-    sources."""
+def counter_values(workload: str):
+    """(HBM bytes per attention-kernel launch, MFMA busy fraction) from the
+    committed rocprofv3 counter summary of this workload, or (None, None) when
+    absent or taken on different kernel sources."""
     path = counter_summary(workload)
     if not os.path.exists(path):
-        return None
+        return None, None
     txt = open(path).read()
     m = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    busy = re.search(r"mfma_busy_frac:\s*([0-9.eE+]+)", txt)
     hsh = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", txt)
     if not m or not hsh or hsh.group(1) != kernel_source_hash():
-        return None
-    return float(m.group(1))
+        return None, None
+    return float(m.group(1)), (float(busy.group(1)) if busy else None)
 
 
 def to_device(a, dev):
@@ -318,24 +319,20 @@ def device_env(dev, n_bytes=1 << 30, reps=5):
 
 
 def gpu_clocks():
-    """Graphics clock levels the driver supports (rocm-smi --showclkfrq, MHz) and the
-    level active when read (between runs the GPU idles at its lowest), or None."""
-    import shutil
-    import subprocess
-    exe = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
-    try:
-        out = subprocess.run([exe, "--showclkfrq"], capture_output=True, text=True, timeout=30).stdout
-    except (OSError, subprocess.SubprocessError):
-        return None
-    sec = out.split("Supported sclk frequencies", 1)
-    if len(sec) < 2:
-        return None
-    body = sec[1].split("Supported", 1)[0]
-    levels = [(int(m.group(1)), "*" in m.group(0)) for m in re.finditer(r"(\d+)\s*Mhz\s*\*?", body, re.I)]
-    if not levels:
-        return None
-    return {"sclk_levels_mhz": [v for v, _ in levels], "sclk_max_mhz": max(v for v, _ in levels),
-            "sclk_active_when_read_mhz": next((v for v, cur in levels if cur), None)}
+    """Graphics clock levels the driver offers (sysfs pp_dpm_sclk of the first
+    card that has one, MHz) and the level active when read (between runs the
+    GPU idles at its lowest), or None.  Read from sysfs: no child process."""
+    import glob
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            body = open(path).read()
+        except OSError:
+            continue
+        levels = [(int(m.group(1)), "*" in m.group(0)) for m in re.finditer(r"(\d+)\s*Mhz\s*\*?", body, re.I)]
+        if levels:
+            return {"sclk_levels_mhz": [v for v, _ in levels], "sclk_max_mhz": max(v for v, _ in levels),
+                    "sclk_active_when_read_mhz": next((v for v, cur in levels if cur), None), "source": path}
+    return None
 
 
 def calibrate_copy(dev, n_bytes=1 << 30, reps=5):
@@ -411,16 +408,19 @@ def main():
     mean_ranks = []
     groups = [[]]
     t_gen = time.perf_counter()
+    t_make = 0.0
     for l in range(cfg.n_layers):
         x = synth.gen_layer(cfg, l)
-        if cfg.n_layers > 1:
-            print(f"bench: layer {l + 1}/{cfg.n_layers} generated ({time.perf_counter() - t_gen:.0f} s)",
-                  file=sys.stderr, flush=True)
         per_step += synth.algorithmic_bytes(x)
         flops_step += synth.latent_flops(x)
         out_bytes += 4 * x.n_q * x.n_q_heads * x.head_dim
         mean_ranks.append(float(x.rank_k.mean()))
+        t1 = time.perf_counter()
         groups[0].append(Layer(x, dev))
+        t_make += time.perf_counter() - t1
+        if cfg.n_layers > 1:
+            print(f"bench: layer {l + 1}/{cfg.n_layers} ready ({time.perf_counter() - t_gen:.0f} s, "
+                  f"{t_make:.1f} s of it in milo_cache_create)", file=sys.stderr, flush=True)
         if l == 0:
             x0 = x
     copies = max(1, int(np.ceil(args.rotate_bytes / per_step)))
@@ -499,7 +499,7 @@ def main():
     mfma_tflops = flops / att_avg_s / 1e12
     # the bound is the roof the kernel's arithmetic intensity meets first
     bound = "hbm" if flops / kern_bytes < MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
-    traffic = counter_traffic(args.config)
+    traffic, mfma_busy = counter_values(args.config)
     t_roof = max(kern_bytes / (HBM_PEAK_GBS * 1e9), flops / (MFMA_BF16_PEAK_TFLOPS * 1e12))
 
     ctx_tokens = int(x0.block_tokens.sum()) + (mean_tail if args.grow_tails else int(x0.tail_len.max()))
@@ -558,6 +558,9 @@ def main():
             "hbm_gbs": achieved,
             "mfma_tflops": mfma_tflops,
             "mfma_frac": mfma_tflops / MFMA_BF16_PEAK_TFLOPS,
+            "hbm_frac": achieved / HBM_PEAK_GBS,
+            "mfma_busy_counter": mfma_busy,
+            "counters": os.path.relpath(counter_summary(args.config), ROOT) if traffic is not None else None,
             "attainable_frac": t_roof / att_avg_s,
             "kernel_source_sha256_16": kernel_source_hash(),
         },
