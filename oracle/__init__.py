@@ -36,15 +36,48 @@ ascending, then the tail.
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 
 __all__ = ["allocate_ranks", "attend_dense", "attend_latent", "attend_prefill", "reconstruct",
            "spectral_information"]
 
 
-def reconstruct(p: np.ndarray, r: np.ndarray) -> np.ndarray:
+def _mm(a: np.ndarray, b: np.ndarray, ordered: bool) -> np.ndarray:
+    """a @ b for a 2-D a and a 1-D or 2-D b.  With ordered=True the sum over the
+    shared index runs strictly left to right (one rounded product and one rounded
+    addition per term, starting from 0), so the result does not depend on how a
+    library blocks the sum; otherwise BLAS."""
+    if not ordered:
+        return a @ b
+    out = np.zeros((a.shape[0],) + b.shape[1:], dtype=np.result_type(a, b))
+    for k in range(a.shape[1]):
+        out += np.multiply.outer(a[:, k], b[k])
+    return out
+
+
+def _colsum(w: np.ndarray, ordered: bool):
+    """Sum over the first axis (tokens); left to right when ordered."""
+    if not ordered:
+        return w.sum(axis=0)
+    out = np.zeros(w.shape[1:], dtype=w.dtype)
+    for t in range(w.shape[0]):
+        out += w[t]
+    return out
+
+
+def _exp(x: np.ndarray, ordered: bool) -> np.ndarray:
+    """Elementwise exp; with ordered=True one math.exp call per element, so two
+    arrays holding the same value get the same result whatever their shapes."""
+    if not ordered:
+        return np.exp(x)
+    return np.vectorize(math.exp, otypes=[np.float64])(x) if x.size else np.exp(x)
+
+
+def reconstruct(p: np.ndarray, r: np.ndarray, ordered: bool = False) -> np.ndarray:
     """Eq. 3 with the singular values folded into P: the dense block P R."""
-    return p @ r
+    return _mm(p, r, ordered)
 
 
 def _shapes(q, rk_list, tail_k):
@@ -58,10 +91,14 @@ def _shapes(q, rk_list, tail_k):
     return n_q, n_q_heads, d, n_kv, n_q_heads // n_kv
 
 
-def attend_dense(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale):
+def attend_dense(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale, ordered=False):
     """Definition: Eq. 1 over the keys/values that the factors of the selected
-    blocks define (Eq. 3), concatenated in table order, followed by request i's
-    first tail_len[i] uncompressed tail tokens.
+    blocks define (Eq. 3), in table order, followed by request i's first
+    tail_len[i] uncompressed tail tokens:
+        o = sum_t e^{s_t - M} v_t / sum_t e^{s_t - M},  s_t = scale q . k_t,  M = max_t s_t,
+    both sums taken block by block (tokens ascending) in table order, then over
+    the tail.  ordered=True makes every dot product and sum run left to right
+    (see _mm), which fixes the result to the last bit.
 
     pk, rk, pv, rv: lists (indexed by block id) of float64 arrays
         P^K_b [T_b, rk_b], R^K_b [rk_b, H_kv*d], P^V_b [T_b, rv_b], R^V_b [rv_b, H_kv*d]
@@ -70,28 +107,31 @@ def attend_dense(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale):
     returns o: [n_q, H_q, d] float64
     """
     n_q, n_q_heads, d, n_kv, G = _shapes(q, [rk[b] for b in table], tail_k)
-    D = n_kv * d
-    keys = [reconstruct(pk[b], rk[b]) for b in table]
-    vals = [reconstruct(pv[b], rv[b]) for b in table]
-    k_ctx = np.concatenate(keys) if keys else np.zeros((0, D))
-    v_ctx = np.concatenate(vals) if vals else np.zeros((0, D))
+    keys = [reconstruct(pk[b], rk[b], ordered) for b in table]
+    vals = [reconstruct(pv[b], rv[b], ordered) for b in table]
     out = np.empty((n_q, n_q_heads, d))
     for i in range(n_q):
         n_t = int(tail_len[i])
         for h in range(n_q_heads):
             g = h // G
-            k_all = np.concatenate([k_ctx[:, g * d:(g + 1) * d], tail_k[i, :n_t, g, :]])
-            v_all = np.concatenate([v_ctx[:, g * d:(g + 1) * d], tail_v[i, :n_t, g, :]])
-            if k_all.shape[0] == 0:
+            cols = slice(g * d, (g + 1) * d)       # KV head g's columns of K and V
+            k_parts = [k[:, cols] for k in keys] + [tail_k[i, :n_t, g, :]]
+            v_parts = [v[:, cols] for v in vals] + [tail_v[i, :n_t, g, :]]
+            s_parts = [scale * _mm(kp, q[i, h], ordered) for kp in k_parts]
+            if sum(len(sp) for sp in s_parts) == 0:
                 raise ValueError("no keys to attend to")
-            s = scale * (k_all @ q[i, h])
-            w = np.exp(s - s.max())
-            out[i, h] = (w / w.sum()) @ v_all
+            m = max(sp.max() for sp in s_parts if len(sp))
+            num, den = np.zeros(d), 0.0
+            for sp, vp in zip(s_parts, v_parts):
+                w = _exp(sp - m, ordered)
+                den += _colsum(w, ordered)
+                num += _mm(vp.T, w, ordered)
+            out[i, h] = num / den
     return out
 
 
 def attend_latent(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale,
-                  columns=None, return_weights=False):
+                  columns=None, return_weights=False, ordered=False):
     """Same result as attend_dense, computed in each block's rank space.
 
     For query column (i, h) with KV head g and selected block b:
@@ -107,7 +147,9 @@ def attend_latent(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale,
     columns: optional list of (i, h) pairs to evaluate (default: all).
     Returns o [len(columns), d] when columns is given, else [n_q, H_q, d].
     With return_weights, also returns the normalised weights of every column
-    (blocks in table order, tokens ascending, then the tail).
+    (blocks in table order, tokens ascending, then the tail).  Sums over keys
+    run block by block in table order, then over the tail, as in attend_dense;
+    ordered=True makes every dot product and sum run left to right.
     """
     n_q, n_q_heads, d, n_kv, G = _shapes(q, [rk[b] for b in table], tail_k)
     all_cols = columns is None
@@ -125,13 +167,13 @@ def attend_latent(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale,
         gs = slice(g * d, (g + 1) * d)
         qg = np.stack([q[columns[c][0], columns[c][1]] for c in cidx], axis=1)  # [d, n]
         # scores of every selected block: [T_b, n]
-        s_blk = [scale * (pk[b] @ (rk[b][:, gs] @ qg)) for b in table]
+        s_blk = [scale * _mm(pk[b], _mm(rk[b][:, gs], qg, ordered), ordered) for b in table]
         # tail scores per column (each request has its own tail)
         s_tail = []
         for c in cidx:
             i, h = columns[c]
             n_t = int(tail_len[i])
-            s_tail.append(scale * (tail_k[i, :n_t, g, :] @ q[i, h]))
+            s_tail.append(scale * _mm(tail_k[i, :n_t, g, :], q[i, h], ordered))
         m = np.full(len(cidx), -np.inf)
         for s in s_blk:
             if s.shape[0]:
@@ -141,21 +183,21 @@ def attend_latent(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale,
                 m[k] = max(m[k], s.max())
         if not np.all(np.isfinite(m)):
             raise ValueError("no keys to attend to")
-        w_blk = [np.exp(s - m) for s in s_blk]
-        w_tail = [np.exp(s - m[k]) for k, s in enumerate(s_tail)]
+        w_blk = [_exp(s - m, ordered) for s in s_blk]
+        w_tail = [_exp(s - m[k], ordered) for k, s in enumerate(s_tail)]
         l = np.zeros(len(cidx))
         for w in w_blk:
-            l += w.sum(axis=0)
+            l += _colsum(w, ordered)
         for k, w in enumerate(w_tail):
-            l[k] += w.sum()
+            l[k] += _colsum(w, ordered)
         u = np.zeros((d, len(cidx)))
         for b, w in zip(table, w_blk):
-            ot = pv[b].T @ w                      # [rv_b, n]
-            u += rv[b][:, gs].T @ ot              # [d, n]
+            ot = _mm(pv[b].T, w, ordered)              # [rv_b, n]
+            u += _mm(rv[b][:, gs].T, ot, ordered)      # [d, n]
         for k, c in enumerate(cidx):
             i, h = columns[c]
             n_t = int(tail_len[i])
-            u_tail = w_tail[k] @ tail_v[i, :n_t, g, :]
+            u_tail = _mm(tail_v[i, :n_t, g, :].T, w_tail[k], ordered)
             out[c] = (u[:, k] + u_tail) / l[k]
             if return_weights:
                 weights[c] = np.concatenate([w[:, k] for w in w_blk] + [w_tail[k]]) / l[k]

@@ -87,6 +87,29 @@ def pin_identity_factors_sdpa(dense, latent):
             assert np.allclose(ol[i, h], ref, rtol=1e-12, atol=1e-13)
 
 
+def test_identity_factors_routes_agree_bitwise():
+    """P = K, R = I at full rank (r = H_kv*d), with every sum taken left to right
+    (ordered=True): the latent route's projection multiplies by 1 and adds exact
+    zeros, its up-projection selects the head's rows of the latent sums, and both
+    routes group the softmax sums block by block in table order, then the tail.
+    So the two routes are not merely close: they agree to the last bit, and the
+    latent route equals plain attention over K and V exactly."""
+    rng = np.random.default_rng(31)
+    for n_kv, d, G, T, tl in ((2, 4, 2, [3, 5], [2, 1]), (1, 8, 3, [7], [0, 4]), (3, 2, 1, [1, 6, 2], [3, 3])):
+        D, n_q = n_kv * d, len(tl)
+        K = [rng.standard_normal((t, D)) for t in T]
+        V = [rng.standard_normal((t, D)) for t in T]
+        eye = np.eye(D)
+        args = dict(pk=K, rk=[eye] * len(T), pv=V, rv=[eye] * len(T), table=list(range(len(T)))[::-1],
+                    q=rng.standard_normal((n_q, n_kv * G, d)), tail_k=rng.standard_normal((n_q, 4, n_kv, d)),
+                    tail_v=rng.standard_normal((n_q, 4, n_kv, d)), tail_len=np.array(tl), scale=0.45)
+        od = oracle.attend_dense(**args, ordered=True)
+        ol = oracle.attend_latent(**args, ordered=True)
+        assert np.array_equal(od.view(np.uint64), ol.view(np.uint64))
+        # and the BLAS route agrees with the ordered one within rounding
+        assert _col_rel(oracle.attend_latent(**args), ol) < 1e-13
+
+
 def pin_bruteforce_tiny(dense, latent):
     """Scalar Python loops: rebuild every key/value element, softmax with math.exp."""
     a = _case(3, [2, 3], [2, 1], [1, 2], n_kv_heads=2, head_dim=2, n_q=2, n_q_heads=4,
@@ -319,20 +342,20 @@ def test_no_keys_is_an_error():
 # ----------------------------------------------------------------------------------
 MUTATIONS = [
     ("latent: wrong GQA group", "by_group.setdefault(h // G", "by_group.setdefault(h % G"),
-    ("dense: wrong GQA group", "g = h // G\n            k_all", "g = h % G\n            k_all"),
+    ("dense: wrong GQA group", "g = h // G\n            cols = slice", "g = h % G\n            cols = slice"),
     ("latent: wrong head slice", "gs = slice(g * d, (g + 1) * d)", "gs = slice(g, g + d)"),
-    ("dense: wrong head slice", "k_ctx[:, g * d:(g + 1) * d]", "k_ctx[:, g:g + d]"),
-    ("latent: scale dropped", "s_blk = [scale * (pk[b]", "s_blk = [(pk[b]"),
-    ("dense: scale dropped", "s = scale * (k_all @ q[i, h])", "s = (k_all @ q[i, h])"),
+    ("dense: wrong head slice", "k_parts = [k[:, cols] for k in keys]", "k_parts = [k[:, g:g + d] for k in keys]"),
+    ("latent: scale dropped", "s_blk = [scale * _mm(pk[b]", "s_blk = [_mm(pk[b]"),
+    ("dense: scale dropped", "s_parts = [scale * _mm(kp,", "s_parts = [_mm(kp,"),
     ("latent: tail values dropped", "out[c] = (u[:, k] + u_tail) / l[k]", "out[c] = u[:, k] / l[k]"),
-    ("latent: tail missing from normaliser", "l[k] += w.sum()", "l[k] += 0.0"),
-    ("latent: scores from P^V", "scale * (pk[b] @", "scale * (pv[b] @"),
-    ("latent: latent V from P^K", "ot = pv[b].T @ w", "ot = pk[b].T @ w"),
-    ("latent: up-projection through R^K", "u += rv[b][:, gs].T @ ot", "u += rk[b][:, gs].T @ ot"),
-    ("dense: tail of the wrong request", "tail_k[i, :n_t, g, :]])", "tail_k[0, :n_t, g, :]])"),
-    ("dense: values rebuilt with R^K", "vals = [reconstruct(pv[b], rv[b])", "vals = [reconstruct(pv[b], rk[b])"),
-    ("latent: tail scores unscaled", "s_tail.append(scale * (", "s_tail.append(1.0 * ("),
-    ("reconstruct: dropped factor", "return p @ r", "return p @ (0.5 * r)"),
+    ("latent: tail missing from normaliser", "l[k] += _colsum(w, ordered)", "l[k] += 0.0"),
+    ("latent: scores from P^V", "scale * _mm(pk[b],", "scale * _mm(pv[b],"),
+    ("latent: latent V from P^K", "ot = _mm(pv[b].T, w, ordered)", "ot = _mm(pk[b].T, w, ordered)"),
+    ("latent: up-projection through R^K", "u += _mm(rv[b][:, gs].T, ot, ordered)", "u += _mm(rk[b][:, gs].T, ot, ordered)"),
+    ("dense: tail of the wrong request", "+ [tail_k[i, :n_t, g, :]]", "+ [tail_k[0, :n_t, g, :]]"),
+    ("dense: values rebuilt with R^K", "vals = [reconstruct(pv[b], rv[b]", "vals = [reconstruct(pv[b], rk[b]"),
+    ("latent: tail scores unscaled", "s_tail.append(scale * _mm(", "s_tail.append(1.0 * _mm("),
+    ("reconstruct: dropped factor", "return _mm(p, r, ordered)", "return _mm(p, 0.5 * r, ordered)"),
 ]
 
 
