@@ -60,6 +60,11 @@ def counter_summary(workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"attend_kernel_{workload}_counters.md")
 
 
+def workload_name(cfg, args) -> str:
+    """The workload as the JSON line and the profile summaries name it."""
+    return cfg.name + ("_int8" if getattr(args, "int8", False) else "")
+
+
 def counter_values(workload: str):
     """(HBM bytes per attention-kernel launch, MFMA busy fraction) from the
     committed rocprofv3 counter summary of this workload, or (None, None) when
@@ -85,11 +90,11 @@ class Layer:
     """One layer's device state: its cache, queries, tails and output (the host
     copies of the factors are not kept)."""
 
-    def __init__(self, inp: synth.LayerInputs, dev):
+    def __init__(self, inp: synth.LayerInputs, dev, p_int8: bool = False):
         import torch
         from paper_2609_29913_amd import milo
         self.cache = milo.milo_cache_create(inp.block_tokens, inp.rank_k, inp.rank_v, inp.n_kv_heads,
-                                            inp.head_dim, inp.pk, inp.rk, inp.pv, inp.rv)
+                                            inp.head_dim, inp.pk, inp.rk, inp.pv, inp.rv, p_int8=p_int8)
         self.q = to_device(inp.q, dev)
         self.tk = to_device(inp.tail_k, dev)
         self.tv = to_device(inp.tail_v, dev)
@@ -356,6 +361,8 @@ def main():
                          "kernels reach their steady-state speed after ~100 back-to-back steps")
     ap.add_argument("--config", default="q32b_64l", choices=sorted(synth.CONFIGS),
                     help="workload (default: the largest that fits one GPU, the 32B-shaped 64-layer step)")
+    ap.add_argument("--int8", action="store_true",
+                    help="store P^K and P^V as INT8 codes with per-token scales (MILO_P_INT8)")
     ap.add_argument("--grow-tails", action="store_true",
                     help="decode loop: every request's tail grows by one token per step (warm-up and timed "
                          "steps), ending at the workload's tail length")
@@ -411,12 +418,12 @@ def main():
     t_make = 0.0
     for l in range(cfg.n_layers):
         x = synth.gen_layer(cfg, l)
-        per_step += synth.algorithmic_bytes(x)
+        per_step += synth.algorithmic_bytes(x, p_int8=args.int8)
         flops_step += synth.latent_flops(x)
         out_bytes += 4 * x.n_q * x.n_q_heads * x.head_dim
         mean_ranks.append(float(x.rank_k.mean()))
         t1 = time.perf_counter()
-        groups[0].append(Layer(x, dev))
+        groups[0].append(Layer(x, dev, args.int8))
         t_make += time.perf_counter() - t1
         if cfg.n_layers > 1:
             print(f"bench: layer {l + 1}/{cfg.n_layers} ready ({time.perf_counter() - t_gen:.0f} s, "
@@ -425,7 +432,7 @@ def main():
             x0 = x
     copies = max(1, int(np.ceil(args.rotate_bytes / per_step)))
     for _ in range(1, copies):
-        groups.append([Layer(synth.gen_layer(cfg, l), dev) for l in range(cfg.n_layers)])
+        groups.append([Layer(synth.gen_layer(cfg, l), dev, args.int8) for l in range(cfg.n_layers)])
     stream = torch.cuda.current_stream()
     if args.grow_tails:
         for grp in groups:
@@ -499,7 +506,7 @@ def main():
     mfma_tflops = flops / att_avg_s / 1e12
     # the bound is the roof the kernel's arithmetic intensity meets first
     bound = "hbm" if flops / kern_bytes < MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
-    traffic, mfma_busy = counter_values(args.config)
+    traffic, mfma_busy = counter_values(workload_name(cfg, args))
     t_roof = max(kern_bytes / (HBM_PEAK_GBS * 1e9), flops / (MFMA_BF16_PEAK_TFLOPS * 1e12))
 
     ctx_tokens = int(x0.block_tokens.sum()) + (mean_tail if args.grow_tails else int(x0.tail_len.max()))
@@ -518,7 +525,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) factors / N(0,1/r) R, bf16)",
         "config": {
-            "workload": cfg.name,
+            "workload": workload_name(cfg, args),
+            "p_factors": "int8 codes + per-token fp32 scales" if args.int8 else "bf16",
             "description": cfg.description,
             "layers": cfg.n_layers,
             "decode_batch": x0.n_q,
@@ -560,7 +568,8 @@ def main():
             "mfma_frac": mfma_tflops / MFMA_BF16_PEAK_TFLOPS,
             "hbm_frac": achieved / HBM_PEAK_GBS,
             "mfma_busy_counter": mfma_busy,
-            "counters": os.path.relpath(counter_summary(args.config), ROOT) if traffic is not None else None,
+            "counters": (os.path.relpath(counter_summary(workload_name(cfg, args)), ROOT)
+                         if traffic is not None else None),
             "attainable_frac": t_roof / att_avg_s,
             "kernel_source_sha256_16": kernel_source_hash(),
         },

@@ -63,7 +63,20 @@ typedef struct milo_cache_desc {
   const int32_t* block_tokens;
   const int32_t* rank_k;
   const int32_t* rank_v;
+  int32_t p_format;  /* MILO_P_BF16 (0) or MILO_P_INT8 (1), see below */
 } milo_cache_desc;
+
+/* Storage of the P factors (p_format).  MILO_P_INT8 combines the low-rank cache
+ * with INT8 quantisation (Sec. 5.3, Table 2): P^K and P^V are stored as int8
+ * codes with one fp32 scale per token row, s_t = max_k |P[t][k]| / 127 and
+ * c[t][k] = round-to-nearest-even(P[t][k] / s_t) (fp32, correctly rounded
+ * division), so P[t][k] is replaced by s_t c[t][k]; the R factors stay bf16.
+ * This halves the bytes of P (1 byte per element plus 8 bytes per token).
+ * Attention then computes exactly with the dequantised factors s_t c[t][k]
+ * (codes exact in bf16, scales applied in fp32).  Creation refuses a P factor
+ * with a non-finite value (INVALID_ARG). */
+#define MILO_P_BF16 0
+#define MILO_P_INT8 1
 
 /* Build a cache from per-block factors (LC.Store of Alg. 1, encoding stage, with
  * the singular values folded into P).
@@ -206,6 +219,13 @@ const char* milo_last_error(void);
  * INVALID_ARG for NULL arguments. */
 int milo_cache_device_bytes(const milo_cache* cache, int64_t* bytes);
 
+/* INT8 P factors: copy block `block`'s stored codes and scales of P^K (which = 0)
+ * or P^V (which = 2) to host memory: codes [T_b][rank] row-major, scales [T_b].
+ * Synchronous.  Errors: INVALID_ARG (NULL argument, a cache with bf16 P factors,
+ * bad block or which), HIP_ERROR. */
+int milo_cache_read_int8(const milo_cache* cache, int32_t block, int32_t which, int8_t* codes,
+                         float* scales);
+
 /* Number of work plans milo_attend_decode / milo_attend_prefill have built for
  * this cache so far (a plan is rebuilt when the block table, the batch shape or
  * the planned tail-chunk capacity changes; see milo_attend_decode).  Returns
@@ -215,7 +235,8 @@ int milo_cache_plan_builds(const milo_cache* cache, int64_t* builds);
 /* Copy one stored factor of one block back to host memory in the caller's
  * row-major layout (for checking the packed layout).  which: 0 = P^K, 1 = R^K,
  * 2 = P^V, 3 = R^V.  dst: host buffer of the factor's size in uint16_t.
- * Synchronous.  Errors: INVALID_ARG, HIP_ERROR. */
+ * Synchronous.  Errors: INVALID_ARG (also for P factors stored as INT8),
+ * HIP_ERROR. */
 int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which,
                            uint16_t* dst);
 

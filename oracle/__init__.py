@@ -21,6 +21,8 @@ What it computes (the method's result, written out plainly in fp64):
 `attend_prefill` is the same definition for a multi-token input query of one
 request whose tokens attend causally among themselves (a chunk of new tokens
 sharing one tail).
+`quantize_rows_int8` is the INT8 storage of a P factor (Sec. 5.3 combines the
+low-rank cache with INT8 quantisation): one scale per token row.
 `allocate_ranks` is the encoder's rank allocation (Sec. 4.3): per-block ranks
 that maximise the retained spectral information (Eq. 5) under a total rank
 budget and per-block bounds (Eq. 6), found by the greedy over marginal gains
@@ -40,8 +42,8 @@ import math
 
 import numpy as np
 
-__all__ = ["allocate_ranks", "attend_dense", "attend_latent", "attend_prefill", "reconstruct",
-           "spectral_information"]
+__all__ = ["allocate_ranks", "attend_dense", "attend_latent", "attend_prefill", "dequantize_rows_int8",
+           "quantize_rows_int8", "reconstruct", "spectral_information"]
 
 
 def _mm(a: np.ndarray, b: np.ndarray, ordered: bool) -> np.ndarray:
@@ -274,3 +276,32 @@ def allocate_ranks(sigmas, r_total: int, r_min: int, r_max: int, eps: float = 1e
         left -= 1
         nxt[i] = gain(i)
     return r
+
+
+# --------------------------------------------------------------------------
+# INT8 P factors (Sec. 5.3, Table 2: the low-rank cache combined with INT8)
+# --------------------------------------------------------------------------
+def quantize_rows_int8(p):
+    """Symmetric INT8 quantisation of a P factor with one scale per token row:
+    s_t = max_k |P[t][k]| / 127 and c[t][k] = P[t][k] / s_t rounded to the
+    nearest integer, ties to even, both computed in fp32 (P holds bf16 values,
+    exact in fp32; fp32 division is correctly rounded); a row of zeros gets
+    s = 0 and codes 0.  Returns (codes int8 [T][r], scales float32 [T]); the
+    factor the attention then uses is dequantize_rows_int8(codes, scales)."""
+    p = np.asarray(p, dtype=np.float32)
+    if p.ndim != 2:
+        raise ValueError("P must be 2-D")
+    amax = np.abs(p).max(axis=1) if p.shape[1] else np.zeros(p.shape[0], np.float32)
+    if not np.all(np.isfinite(amax)):
+        raise ValueError("P must be finite")
+    scales = (amax / np.float32(127.0)).astype(np.float32)
+    codes = np.zeros(p.shape, dtype=np.int8)
+    nz = scales > 0
+    q = np.rint(p[nz] / scales[nz, None])          # fp32 / fp32 -> fp32, then ties to even
+    codes[nz] = np.clip(q, -127, 127).astype(np.int8)
+    return codes, scales
+
+
+def dequantize_rows_int8(codes, scales):
+    """The factor INT8 storage stands for: P[t][k] = s_t c[t][k] (float64, exact)."""
+    return np.asarray(scales, dtype=np.float64)[:, None] * np.asarray(codes, dtype=np.float64)

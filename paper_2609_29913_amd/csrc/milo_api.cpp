@@ -82,6 +82,7 @@ TimingState g_timing;
 struct milo_cache {
   int device = -1;
   uint64_t serial = 0;  // distinct for every cache of the process (plan keys)
+  bool p_int8 = false;  // P^K / P^V stored as INT8 codes with per-token scales
   int n_blocks = 0, n_kv = 0, d = 0;
   std::vector<int32_t> T, rk, rv;
   std::vector<BlockMeta> meta;
@@ -176,6 +177,9 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     return fail(MILO_ERR_INVALID_ARG, "block_tokens / rank_k / rank_v must be non-NULL");
   if (!pk || !rk || !pv || !rv) return fail(MILO_ERR_INVALID_ARG, "factor pointer arrays must be non-NULL");
   if (src_on_device != 0 && src_on_device != 1) return fail(MILO_ERR_INVALID_ARG, "src_on_device must be 0 or 1");
+  if (desc->p_format != MILO_P_BF16 && desc->p_format != MILO_P_INT8)
+    return fail(MILO_ERR_INVALID_ARG, "p_format must be MILO_P_BF16 or MILO_P_INT8 (got %d)", desc->p_format);
+  const bool i8 = desc->p_format == MILO_P_INT8;
   const int64_t D = (int64_t)desc->n_kv_heads * desc->head_dim;
   for (int b = 0; b < desc->n_blocks; ++b) {
     const int T = desc->block_tokens[b], a = desc->rank_k[b], v = desc->rank_v[b];
@@ -192,13 +196,14 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
   milo_cache* c = new milo_cache();
   c->serial = next_serial.fetch_add(1);
   c->n_blocks = desc->n_blocks;
+  c->p_int8 = i8;
   c->n_kv = desc->n_kv_heads;
   c->d = desc->head_dim;
   c->T.assign(desc->block_tokens, desc->block_tokens + c->n_blocks);
   c->rk.assign(desc->rank_k, desc->rank_k + c->n_blocks);
   c->rv.assign(desc->rank_v, desc->rank_v + c->n_blocks);
   c->meta.resize(c->n_blocks);
-  int64_t off = 0, max_src = 0;
+  int64_t off = 0, max_src = 0, max_tpad = 0;
   for (int b = 0; b < c->n_blocks; ++b) {
     BlockMeta& m = c->meta[b];
     m.T = c->T[b];
@@ -209,9 +214,14 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     for (int w = 0; w < 4; ++w) {
       const FactorGeom f = geom_of(*c, b, w);
       *offs[w] = off;
-      off = round_up(off + frag_count(f) * kFragElems, kAlignElems);
+      // INT8 P factors: one byte per code, and after P^V the block's scale units
+      int64_t elems = frag_count(f) * kFragElems;
+      if (i8 && w == kPK) elems = i8_factor_bytes(m.T_pad, m.rk_pad) / 2;
+      if (i8 && w == kPV) elems = i8_factor_bytes(m.T_pad, m.rv_pad) / 2 + i8_scale_bytes(m.T_pad) / 2;
+      off = round_up(off + elems, kAlignElems);
       max_src = std::max<int64_t>(max_src, (int64_t)f.rows * f.cols);
     }
+    max_tpad = std::max<int64_t>(max_tpad, m.T_pad);
   }
   c->data_elems = off;
   if (off / kFragElems >= ((int64_t)1 << 31)) {
@@ -228,8 +238,10 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
 
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
   uint16_t* staging = nullptr;
+  float* i8_tmp = nullptr;  // INT8: K and V row scales of the block being packed, then a flag
   auto cleanup_fail = [&](int code) {
     if (staging) (void)hipFree(staging);
+    if (i8_tmp) (void)hipFree(i8_tmp);
     destroy(c);
     return code;
   };
@@ -239,8 +251,19 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     return cleanup_fail(hip_fail(e, "hipMalloc(packed factors)"));
   if (!src_on_device && (e = hipMalloc(&staging, (size_t)max_src * 2)) != hipSuccess)
     return cleanup_fail(hip_fail(e, "hipMalloc(staging)"));
+  float *ks = nullptr, *vs = nullptr;
+  int* bad = nullptr;
+  if (i8) {
+    if ((e = hipMalloc(&i8_tmp, (size_t)(2 * max_tpad + 64) * sizeof(float))) != hipSuccess)
+      return cleanup_fail(hip_fail(e, "hipMalloc(row scales)"));
+    ks = i8_tmp;
+    vs = i8_tmp + max_tpad;
+    bad = reinterpret_cast<int*>(i8_tmp + 2 * max_tpad);
+    if ((e = hipMemsetAsync(bad, 0, sizeof(int), s)) != hipSuccess) return cleanup_fail(hip_fail(e, "hipMemsetAsync"));
+  }
   const uint16_t* const* srcs[4] = {pk, rk, pv, rv};
   for (int b = 0; b < c->n_blocks; ++b) {
+    const BlockMeta& m = c->meta[b];
     for (int w = 0; w < 4; ++w) {
       const FactorGeom f = geom_of(*c, b, w);
       const uint16_t* src = srcs[w][b];
@@ -249,11 +272,30 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
           return cleanup_fail(hip_fail(e, "hipMemcpyAsync(factor)"));
         src = staging;
       }
-      PackArgs pa{src, c->data + factor_offset(c->meta[b], w), f, frag_count(f)};
+      PackArgs pa{src, c->data + factor_offset(m, w), f, frag_count(f), nullptr};
+      if (i8 && (w == kPK || w == kPV)) {
+        float* rs = w == kPK ? ks : vs;
+        if ((e = launch_row_scales(src, f.rows, f.cols, m.T_pad, rs, bad, s)) != hipSuccess)
+          return cleanup_fail(hip_fail(e, "row scale kernel"));
+        pa.row_scale = rs;
+      }
       if ((e = launch_pack(pa, s)) != hipSuccess) return cleanup_fail(hip_fail(e, "pack kernel"));
+    }
+    if (i8) {
+      float* units = reinterpret_cast<float*>(c->data + i8_scale_offset(m.off_pv, m.T_pad, m.rv_pad));
+      if ((e = launch_scale_units(ks, vs, m.T_pad, units, s)) != hipSuccess)
+        return cleanup_fail(hip_fail(e, "scale unit kernel"));
     }
   }
   if ((e = hipStreamSynchronize(s)) != hipSuccess) return cleanup_fail(hip_fail(e, "hipStreamSynchronize"));
+  if (i8) {
+    int flag = 0;
+    if ((e = hipMemcpy(&flag, bad, sizeof(int), hipMemcpyDeviceToHost)) != hipSuccess)
+      return cleanup_fail(hip_fail(e, "hipMemcpy(flag)"));
+    if (flag) return cleanup_fail(fail(MILO_ERR_INVALID_ARG, "a P factor holds a non-finite value (INT8 scales)"));
+    (void)hipFree(i8_tmp);
+    i8_tmp = nullptr;
+  }
   if (staging) (void)hipFree(staging);
   staging = nullptr;
   *out = c;
@@ -269,6 +311,32 @@ int milo_cache_device_bytes(const milo_cache* cache, int64_t* bytes) {
   return MILO_OK;
 }
 
+int milo_cache_read_int8(const milo_cache* cache, int32_t block, int32_t which, int8_t* codes, float* scales) {
+  g_err.clear();
+  if (!cache || !codes || !scales) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
+  if (!cache->p_int8) return fail(MILO_ERR_INVALID_ARG, "this cache stores bf16 P factors");
+  if (block < 0 || block >= cache->n_blocks) return fail(MILO_ERR_INVALID_ARG, "block %d out of range", block);
+  if (which != kPK && which != kPV) return fail(MILO_ERR_INVALID_ARG, "which must be 0 (P^K) or 2 (P^V)");
+  const BlockMeta& m = cache->meta[block];
+  const FactorGeom f = geom_of(*cache, block, which);
+  const int64_t nb = i8_factor_bytes(m.T_pad, f.r_pad);
+  std::vector<int8_t> packed((size_t)nb);
+  MILO_HIP(hipMemcpy(packed.data(), cache->data + factor_offset(m, which), (size_t)nb, hipMemcpyDeviceToHost));
+  for (int64_t fr = 0; fr < frag_count(f); ++fr)
+    for (int lane = 0; lane < 64; ++lane)
+      for (int e = 0; e < 8; ++e) {
+        int row, col;
+        frag_source(f, fr, lane, e, &row, &col);
+        if (row < f.rows && col < f.cols)
+          codes[(int64_t)row * f.cols + col] = packed[(size_t)(fr * kFragElems + lane * 8 + e)];
+      }
+  std::vector<float> units((size_t)i8_scale_bytes(m.T_pad) / 4);
+  MILO_HIP(hipMemcpy(units.data(), cache->data + i8_scale_offset(m.off_pv, m.T_pad, m.rv_pad), units.size() * 4,
+                     hipMemcpyDeviceToHost));
+  for (int t = 0; t < m.T; ++t) scales[t] = units[(size_t)(t / 32) * 64 + (which == kPK ? 0 : 32) + t % 32];
+  return MILO_OK;
+}
+
 int milo_cache_plan_builds(const milo_cache* cache, int64_t* builds) {
   g_err.clear();
   if (!cache || !builds) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
@@ -281,6 +349,8 @@ int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which
   if (!cache || !dst) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
   if (block < 0 || block >= cache->n_blocks) return fail(MILO_ERR_INVALID_ARG, "block %d out of range", block);
   if (which < 0 || which > 3) return fail(MILO_ERR_INVALID_ARG, "which must be 0..3");
+  if (cache->p_int8 && (which == kPK || which == kPV))
+    return fail(MILO_ERR_INVALID_ARG, "P factors of this cache are stored as INT8 (milo_cache_read_int8)");
   const FactorGeom f = geom_of(*cache, block, which);
   const int64_t n = frag_count(f) * kFragElems;
   std::vector<uint16_t> packed((size_t)n);
@@ -450,7 +520,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     const Tiling til = make_tiling(c->n_kv, n_q * G);
     Schedule sch;
     std::string why;
-    if (!build_schedule(PlanInput{c->meta.data(), c->n_kv, c->d}, block_table, n_sel, n_q, n_chunks, til,
+    if (!build_schedule(PlanInput{c->meta.data(), c->n_kv, c->d, c->p_int8}, block_table, n_sel, n_q, n_chunks, til,
                         env_program_cap(), &sch, &why))
       return fail(MILO_ERR_UNSUPPORTED, "%s", why.c_str());
     const int max_rt = sch.max_own <= 2 ? 2 : sch.max_own == 3 ? 3 : 4;
@@ -581,7 +651,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   hipError_t e = hipSuccess;
   for (int l = 0; l < ps.n_launch; ++l) {
     aa.wg = reinterpret_cast<const WgProgram*>(ps.plan_d) + (size_t)l * kCUs;
-    e = launch_attend(aa, c->d, ps.max_rt, ps.nslot, kCUs, ps.lds, s, l == 0 ? ev[0] : nullptr,
+    e = launch_attend(aa, c->d, ps.max_rt, ps.nslot, c->p_int8, kCUs, ps.lds, s, l == 0 ? ev[0] : nullptr,
                       l == ps.n_launch - 1 ? ev[1] : nullptr);
     if (e != hipSuccess) return launch_fail(e, "attend kernel launch");
   }

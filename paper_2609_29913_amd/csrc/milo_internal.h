@@ -82,13 +82,39 @@ struct BlockMeta {
   int32_t T, T_pad, rk_pad, rv_pad;
 };
 
+// INT8 P factors (a cache option; Sec. 5.3 combines the low-rank cache with
+// INT8 quantisation): P^K and P^V are stored as int8 codes c with one fp32
+// scale per token row, P[t][k] = s_t c[t][k] (s_t = max_k |P[t][k]| / 127,
+// c = round-to-nearest-even(P / s_t), both in fp32).  Codes keep the fragment
+// order above at one byte per element (a fragment is 512 bytes: lane l's 8
+// codes at bytes 8l..8l+7), so one 1 KiB unit of the fragment stream holds two
+// consecutive fragments of a run.  Each block's scales follow its P^V codes
+// as 256-byte units, one per (256-token tile t, wave w): the K scales of the
+// wave's 32 score tokens 256t + 32w + m (m = 0..31), then their V scales.
+constexpr int kScaleUnitBytes = 256;
+// bytes of the int8 codes of a P factor with T_pad tokens and rank r_pad, and
+// the offset (in bf16 elements of the cache buffer) of a block's scale units
+__host__ __device__ inline int64_t i8_factor_bytes(int T_pad, int r_pad) { return (int64_t)T_pad * r_pad; }
+__host__ __device__ inline int64_t i8_scale_offset(int64_t off_pv, int T_pad, int rv_pad) {
+  return off_pv + i8_factor_bytes(T_pad, rv_pad) / 2;
+}
+__host__ __device__ inline int64_t i8_scale_bytes(int T_pad) { return (int64_t)(T_pad / kTile) * kWaves * kScaleUnitBytes; }
+
 // Most 256-token tiles in one block item (parts of larger blocks are split),
 // most KV heads one 64-column tile may span, and so the most fragment runs
-// one item gives a wave (plus an end marker).
+// one item gives a wave (plus an end marker): the R^K and R^V runs of every
+// head, per tile the P^K run, the scale unit (INT8) and the P^V run.
 constexpr int kMaxPartTiles = 8;
 constexpr int kMaxTileHeads = 4;
-constexpr int kRunCap = 2 * kMaxTileHeads + 2 * kMaxPartTiles + 2;
+constexpr int kRunCap = 2 * kMaxTileHeads + 3 * kMaxPartTiles + 2;
 constexpr int kRunBufs = 4;  // run buffers per wave in the attention kernel
+// A run (x, n) names n units of one kind, encoded in bits 28-29 of n:
+//   kRunBf16   bf16 fragments x .. x+n-1 (1 KiB each)
+//   kRunI8     int8 fragments x .. x+n-1 (512 bytes each, n even: n/2 units of two)
+//   kRunScale  n scale units from byte 256 x
+constexpr int kRunKindShift = 28;
+constexpr int kRunCountMask = (1 << kRunKindShift) - 1;
+enum RunKind : int { kRunBf16 = 0, kRunI8 = 1, kRunScale = 2 };
 
 // log2 of the rank groups (kWaves / nseg) of a block with nrt V rank tiles
 __host__ __device__ inline int lg_rank_groups(int nrt) {
@@ -103,12 +129,13 @@ __host__ __device__ inline int lg_rank_groups(int nrt) {
 // its P^K sub-tile and the P^V rank tiles of its rank group over its token
 // segment; then R^V for its 16-dim output slice over all ranks, every head in
 // turn (up-projection).  lg_ng = lg_rank_groups(rv_pad / 32) (passed in, so
-// the kernel derives runs with shifts only).  emit(first fragment index,
-// count) is called for every non-empty run; offsets follow the packed layout
-// above.
+// the kernel derives runs with shifts only).  With INT8 P factors (i8) each
+// tile's P^K and P^V runs are int8 runs and the wave's scale unit comes
+// between them.  emit(first unit index, count | kind) is called for every
+// non-empty run; offsets follow the packed layout above.
 template <typename Emit>
 __host__ __device__ inline void block_runs(const BlockMeta& bm, int g0, int nh, int tile0, int ntile, int w, int d,
-                                           int lg_ng, Emit&& emit) {
+                                           int lg_ng, bool i8, Emit&& emit) {
   static_assert(kWaves == 8, "rank tiles are dealt over 8 waves");
   const int NK = d / 16;
   const int nrt_k = bm.rk_pad >> 5, nks = bm.rk_pad >> 4, nrt_v = bm.rv_pad >> 5;
@@ -127,9 +154,20 @@ __host__ __device__ inline void block_runs(const BlockMeta& bm, int g0, int nh, 
   if (own_k > 0)
     for (int h = 0; h < nh; ++h) emit(rk0 + (g0 + h) * nrt_k * NK + NK * before_k, NK * own_k);
   const int pv_first = (bm.T_pad / 16) * before_v;
-  for (int t = tile0; t < tile0 + ntile; ++t) {
-    emit(pk0 + (w * tiles_all + t) * nks, nks);
-    if (own_v > 0) emit(pv0 + pv_first + (16 * t + nst * sg) * own_v, nst * own_v);
+  if (i8) {
+    // int8 fragment indices count 512-byte units from the buffer start
+    const int pk8 = (int)(bm.off_pk / 256), pv8 = (int)(bm.off_pv / 256);
+    const int sc0 = (int)(i8_scale_offset(bm.off_pv, bm.T_pad, bm.rv_pad) * 2 / kScaleUnitBytes);
+    for (int t = tile0; t < tile0 + ntile; ++t) {
+      emit(pk8 + (w * tiles_all + t) * nks, nks | (kRunI8 << kRunKindShift));
+      emit(sc0 + t * kWaves + w, 1 | (kRunScale << kRunKindShift));
+      if (own_v > 0) emit(pv8 + pv_first + (16 * t + nst * sg) * own_v, (nst * own_v) | (kRunI8 << kRunKindShift));
+    }
+  } else {
+    for (int t = tile0; t < tile0 + ntile; ++t) {
+      emit(pk0 + (w * tiles_all + t) * nks, nks);
+      if (own_v > 0) emit(pv0 + pv_first + (16 * t + nst * sg) * own_v, nst * own_v);
+    }
   }
   const int nds = d / 16, nkr = bm.rv_pad >> 5;
   for (int h = 0; h < nh; ++h) emit(rv0 + ((g0 + h) * nds + w % nds) * nkr, nkr);
@@ -245,7 +283,7 @@ static_assert(sizeof(WorkItem) == 80, "work item layout");
 // partial into it (log-sum-exp), and the last one writes it out.  Slots of a
 // (head, column tile) are numbered densely from 0; tail items write slot
 // n_block_slots + their chunk index.
-enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2 };
+enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2, kItemInt8 = 4 };  // kItemInt8: INT8 P factors
 // packed fields of a block item's flags: bits 8-9 lg_rank_groups of its block,
 // bits 16-21 the tile's column count - 1, bits 24-26 its KV head count - 1
 constexpr int kItemLgNgShift = 8;
@@ -266,7 +304,7 @@ struct WgProgram {
   int32_t pad[2];
 };
 static_assert(sizeof(WgProgram) == 24, "program entry layout");
-constexpr int kSentinelRun = 1 << 30;
+constexpr int kSentinelRun = 1 << 27;  // a bf16 run long enough for any look-ahead
 
 // Attention kernel geometry.
 constexpr int kThreads = 64 * kWaves;
@@ -367,6 +405,7 @@ struct PackArgs {
   uint16_t* dst;
   FactorGeom geom;
   int64_t n_frags;
+  const float* row_scale;  // INT8 P factors: per-token scales [T_pad] (NULL: bf16)
 };
 
 // Launchers (defined in milo_kernels.hip).
@@ -377,10 +416,16 @@ int report_error(int code, const char* msg);  // stores msg, returns code
 bool timing_enabled();
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+// INT8 P factors: per-row scales of a row-major bf16 factor [rows][cols] into
+// scale[0 .. rows_pad) (rows past `rows` get 0); a row that is not finite sets *bad.
+hipError_t launch_row_scales(const uint16_t* src, int rows, int cols, int rows_pad, float* scale, int* bad,
+                             hipStream_t s);
+// INT8 P factors: the scale units of a block from its K and V row scales
+hipError_t launch_scale_units(const float* ks, const float* vs, int T_pad, float* dst, hipStream_t s);
 // e0 / e1 (may be null): events recorded when the kernel starts and ends
 // (hipExtLaunchKernelGGL), so they time the kernel itself.
-hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, int grid, size_t lds_bytes,
-                         hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, bool p_int8, int grid,
+                         size_t lds_bytes, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s, hipEvent_t e0 = nullptr,
                         hipEvent_t e1 = nullptr);
 // LDS of the attention kernel: a base region (projected query, weight tile and

@@ -38,6 +38,17 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8 ld_bf16x8(const void* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
+// eight int8 codes (little-endian in two dwords) as bf16, exactly
+__device__ __forceinline__ bf16x8 i8_to_bf16x8(uint2 raw) {
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = (__bf16)(float)(int8_t)(raw.x >> (8 * e));
+    v[4 + e] = (__bf16)(float)(int8_t)(raw.y >> (8 * e));
+  }
+  return v;
+}
+
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -125,6 +136,29 @@ __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
   const int64_t frag = gid >> 6;
   const int lane = (int)(gid & 63);
   if (frag >= a.n_frags) return;
+  if (a.row_scale) {
+    // INT8 P factor: code = round-to-nearest-even(P / s_row) in fp32 (correctly
+    // rounded division), |code| <= 127; 8 codes per lane at byte 8 lane of the
+    // fragment's 512 bytes
+    uint32_t w[2] = {0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      int row, col;
+      frag_source(a.geom, frag, lane, e, &row, &col);
+      int code = 0;
+      if (row < a.geom.rows && col < a.geom.cols) {
+        const float sc = a.row_scale[row];
+        if (sc > 0.f) {
+          const float x = bf16_to_f32(a.src[(int64_t)row * a.geom.cols + col]);
+          code = (int)fminf(127.f, fmaxf(-127.f, rintf(__fdiv_rn(x, sc))));
+        }
+      }
+      w[e >> 2] |= (uint32_t)(code & 0xff) << (8 * (e & 3));
+    }
+    *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(a.dst) + frag * kFragElems + lane * 8) =
+        make_uint2(w[0], w[1]);
+    return;
+  }
   uint16_t v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -138,6 +172,35 @@ __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
   out.z = v[4] | ((uint32_t)v[5] << 16);
   out.w = v[6] | ((uint32_t)v[7] << 16);
   *reinterpret_cast<uint4*>(a.dst + frag * kFragElems + lane * 8) = out;
+}
+
+// INT8 P factors: per-row scale s = max |P[row][:]| / 127 (fp32, correctly
+// rounded division); rows past `rows` up to rows_pad get 0; a non-finite row sets *bad.
+__global__ __launch_bounds__(256) void row_scale_kernel(const uint16_t* src, int rows, int cols, int rows_pad,
+                                                        float* scale, int* bad) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows_pad) return;
+  float m = 0.f;
+  if (r < rows) {
+    for (int c = 0; c < cols; ++c) m = fmaxf(m, fabsf(bf16_to_f32(src[(int64_t)r * cols + c])));
+    bool finite = true;
+    for (int c = 0; c < cols; ++c) finite = finite && isfinite(bf16_to_f32(src[(int64_t)r * cols + c]));
+    if (!finite) {
+      atomicOr(bad, 1);
+      m = 0.f;
+    }
+  }
+  scale[r] = __fdiv_rn(m, 127.f);
+}
+
+// INT8 P factors: the 256-byte scale unit of (tile t, wave w) holds the K then
+// the V scales of tokens 256 t + 32 w + m, m = 0..31
+__global__ __launch_bounds__(256) void scale_units_kernel(const float* ks, const float* vs, int T_pad, float* dst) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;  // float index in the units
+  if (i >= T_pad * 2) return;
+  const int unit = i / 64, m = i % 64;                  // unit = t * kWaves + w
+  const int tok = 32 * unit + (m & 31);
+  dst[i] = m < 32 ? ks[tok] : vs[tok];
 }
 
 // ---------------------------------------------------------------------------
@@ -317,20 +380,24 @@ __device__ __forceinline__ WorkItem lds_item(const unsigned char* p) {
 // use, so every wait is a constant vmcnt; the look-ahead crosses item
 // boundaries, so the next item's first fragments load while the current one
 // finishes.  With NSLOT == 0 fragments are loaded straight into registers.
-template <int D, int NSLOT>
+template <int D, int NSLOT, bool I8>
 struct FragRing {
-  static constexpr int kDepth = NSLOT > 2 ? NSLOT - 2 : 1;  // fragments in flight
-  static_assert(kDepth <= 6, "run buffers are derived two block items (>= 6 fragments) ahead");
-  const uint16_t* data_lane;  // packed factor buffer + this lane's 8-element offset
-  int lane8;                  // this lane's element offset inside a fragment
+  static constexpr int kDepth = NSLOT > 2 ? NSLOT - 2 : 1;  // units in flight
+  static_assert(kDepth <= 6, "run buffers are derived two block items (>= 6 units) ahead");
+  const unsigned char* data;  // packed factor buffer
+  int lane;                   // this lane
   __bf16* ring;               // this wave's NSLOT slots
   uint32_t ring_lds;          // LDS byte address of slot 0 (wave-uniform)
   const int2* run;            // current entry of the run buffers (LDS)
   int2* rbuf;                 // this wave's kRunBufs run buffers of kRunCap entries
   int rb;                     // buffer the stream reads
-  int64_t off;                // element offset of the next fragment
-  int left;                   // fragments left in the current run
+  int64_t off;                // byte offset of the next unit
+  int left;                   // units left in the current run
+  int step;                   // bytes per unit of the current run (1 KiB, or 256 for scale units)
+  int lane_off;               // this lane's byte offset in a unit of the current run
   int rs, ws;                 // ring slots: next to read, next to fill
+  bf16x8 held;                // the second fragment of the last int8 unit taken
+  bool have_held;
 
   __device__ __forceinline__ void load_run() {
     int2 v = prog_read_b64(run);
@@ -339,19 +406,46 @@ struct FragRing {
       run = rbuf + rb * kRunCap;
       v = prog_read_b64(run);
     }
-    off = (int64_t)__builtin_amdgcn_readfirstlane(v.x) * kFragElems;
-    left = __builtin_amdgcn_readfirstlane(v.y);
+    const int x = __builtin_amdgcn_readfirstlane(v.x), n = __builtin_amdgcn_readfirstlane(v.y);
+    if constexpr (!I8) {  // every run holds bf16 fragments
+      off = (int64_t)x * (kFragElems * 2);
+      left = n;
+      return;
+    }
+    const int kind = (n >> kRunKindShift) & 3, count = n & kRunCountMask;
+    if (kind == kRunBf16) {
+      off = (int64_t)x * (kFragElems * 2);
+      left = count;
+      step = kFragElems * 2;
+      lane_off = 16 * lane;
+    } else if (kind == kRunI8) {  // two 512-byte fragments per unit
+      off = (int64_t)x * (kFragElems);
+      left = count >> 1;
+      step = kFragElems * 2;
+      lane_off = 16 * lane;
+    } else {  // scale unit: 256 bytes, every group of 16 lanes loads all of it
+      off = (int64_t)x * kScaleUnitBytes;
+      left = count;
+      step = kScaleUnitBytes;
+      lane_off = 16 * (lane & 15);
+    }
   }
-  // address of this lane's part of the next fragment; advances the stream
-  __device__ __forceinline__ const uint16_t* next() {
+  // the unit's start, and this lane's address in the next unit; advances the stream
+  __device__ __forceinline__ const unsigned char* next(const unsigned char** unit = nullptr) {
     if (left == 0) {
       ++run;
       load_run();
     }
-    const uint16_t* o = data_lane + off;
-    off += kFragElems;
+    const unsigned char* u = data + off;
+    if (unit) *unit = u;
     --left;
-    return o;
+    if constexpr (!I8) {
+      off += kFragElems * 2;
+      return u + 16 * lane;
+    } else {
+      off += step;
+      return u + lane_off;
+    }
   }
   __device__ __forceinline__ void start() {
     rb = 0;
@@ -359,24 +453,51 @@ struct FragRing {
     load_run();
     rs = 0;
     ws = 0;
+    have_held = false;
     if constexpr (NSLOT > 0) {
 #pragma unroll
       for (int k = 0; k < kDepth; ++k) lds_dma16(next(), ring_lds + k * kFragElems * 2);
       ws = kDepth;
     }
   }
-  // the next fragment, in this lane's operand layout
-  __device__ __forceinline__ bf16x8 take() {
+  // the slot (LDS) or unit (global memory) of the next unit, and advance
+  __device__ __forceinline__ const unsigned char* next_unit() {
     if constexpr (NSLOT > 0) {
       wait_vmcnt<kDepth - 1>();
-      const bf16x8 v = ld_bf16x8(ring + rs * kFragElems + lane8);
+      const unsigned char* slot = reinterpret_cast<const unsigned char*>(ring + rs * kFragElems);
       lds_dma16(next(), ring_lds + ws * kFragElems * 2);
       rs = rs + 1 == NSLOT ? 0 : rs + 1;
       ws = ws + 1 == NSLOT ? 0 : ws + 1;
-      return v;
+      return slot;
     } else {
-      return ld_bf16x8(next());
+      const unsigned char* u;
+      next(&u);
+      return u;
     }
+  }
+  // the next bf16 fragment, in this lane's operand layout
+  __device__ __forceinline__ bf16x8 take() {
+    return ld_bf16x8(next_unit() + 16 * lane);
+  }
+  // the next fragment of an int8 run, converted to bf16 (exact: |code| <= 127);
+  // a unit holds two fragments, the second is kept for the following call
+  __device__ __forceinline__ bf16x8 take_i8() {
+    static_assert(I8, "int8 fragments only in the INT8 instantiation");
+    if (have_held) {
+      have_held = false;
+      return held;
+    }
+    const unsigned char* u = next_unit();
+    const uint2 lo = *reinterpret_cast<const uint2*>(u + 8 * lane);
+    const uint2 hi = *reinterpret_cast<const uint2*>(u + kFragElems + 8 * lane);
+    held = i8_to_bf16x8(hi);
+    have_held = true;
+    return i8_to_bf16x8(lo);
+  }
+  // the next scale unit: 32 K then 32 V scales (fp32); the pointer stays valid
+  // until the next take
+  __device__ __forceinline__ const float* take_scales() {
+    return reinterpret_cast<const float*>(next_unit());
   }
 };
 
@@ -413,7 +534,7 @@ struct RunDeriver {
       };
       if (found)
         block_runs(it.blk, it.g, ((it.flags >> kItemHeadsShift) & 7) + 1, it.tile0, it.ntile, lane, D,
-                   (it.flags >> kItemLgNgShift) & 3, put);
+                   (it.flags >> kItemLgNgShift) & 3, (it.flags & kItemInt8) != 0, put);
       else put(0, kSentinelRun);
       put(0, 0);
     }
@@ -457,9 +578,9 @@ constexpr int up_col_blocks() {
 // LDS at its start.  Every loop is software-pipelined: the operands of step
 // k+1 are read while the MFMAs of step k run.
 // ---------------------------------------------------------------------------
-template <int D, int MAX_RT, int NSLOT, bool WH>
+template <int D, int MAX_RT, int NSLOT, bool WH, bool I8>
 __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
-                                           FragRing<D, NSLOT>& fr, RunDeriver<D>& rd,
+                                           FragRing<D, NSLOT, I8>& fr, RunDeriver<D>& rd,
                                            GroupAcc<up_col_blocks<D>()>& acc, const int tid) {
   constexpr int NK = D / 16;
   constexpr int kORed = 4;  // partial-output slots of the up-projection reduction
@@ -491,6 +612,11 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   // the wave's runs: R^K (waves that own projection rank tiles), then per tile
   // P^K and P^V, then R^V
   auto take = [&]() -> bf16x8 { return fr.take(); };
+  // P^K / P^V fragments: bf16, or int8 codes converted exactly (INT8 P factors)
+  auto take_p = [&]() -> bf16x8 {
+    if constexpr (I8) return fr.take_i8();
+    else return fr.take();
+  };
 
   // ---- the item's 64 query rows -> LDS (in the weight tile's area, idle until
   // the first tile).  Row-major [column][D]; the 16-byte chunk j of column c is
@@ -572,16 +698,16 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
     {
       // operands of rank step k: ak (P^K sub-tile), b0/b1 (Qt column tiles);
       // nks is even (ranks are padded to 32), so the loop runs over step pairs
-      bf16x8 ak = take();
+      bf16x8 ak = take_p();
       bf16x8 b0 = ld_bf16x8(qr0), b1 = ld_bf16x8(qr1);
       for (int k = 0; k < nks; k += 2) {
-        const bf16x8 ck = take();
+        const bf16x8 ck = take_p();
         const bf16x8 d0 = ld_bf16x8(qr0 + 16 * (k + 1));
         const bf16x8 d1 = ld_bf16x8(qr1 + 16 * (k + 1));
         s0 = mfma32(ak, b0, s0);
         s1 = mfma32(ak, b1, s1);
         if (k + 2 < nks) {
-          ak = take();
+          ak = take_p();
           b0 = ld_bf16x8(qr0 + 16 * (k + 2));
           b1 = ld_bf16x8(qr1 + 16 * (k + 2));
         }
@@ -590,6 +716,25 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       }
     }
     f32x16 sc[2] = {s0, s1};
+    // INT8 P factors: the scores of int8 codes times each token's K scale; the
+    // V scales fold into the weights below (lane: tokens 8 j + 4 lhi + u of the
+    // wave's 32, j, u = 0..3)
+    float vsc[16];
+    if constexpr (I8) {
+      const float* su = fr.take_scales();
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 k4 = *reinterpret_cast<const float4*>(su + 8 * j + 4 * lhi);
+        const float4 v4 = *reinterpret_cast<const float4*>(su + 32 + 8 * j + 4 * lhi);
+        const float kk[4] = {k4.x, k4.y, k4.z, k4.w}, vv[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          sc[0][4 * j + u] *= kk[u];
+          sc[1][4 * j + u] *= kk[u];
+          vsc[4 * j + u] = vv[u];
+        }
+      }
+    }
     // mask tokens past the end of the block (only the block's last tile can
     // hold any; the test is wave-uniform), wave-local column max
     float mx[2] = {-INFINITY, -INFINITY};
@@ -633,7 +778,8 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
         for (int u = 0; u < 4; ++u) {
           const float w = fast_exp2(sc[ch][4 * j + u] - m_run[ch]);
           lsum += w;
-          wv[ch][j][u] = (__bf16)w;
+          if constexpr (I8) wv[ch][j][u] = (__bf16)(w * vsc[4 * j + u]);
+          else wv[ch][j][u] = (__bf16)w;
         }
       l_run[ch] = l_run[ch] * alpha[ch] + lsum;
     }
@@ -655,13 +801,13 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       bf16x8 w0 = ld_bf16x8(w0p + 16 * lo), w1 = ld_bf16x8(w1p + 16 * lo);
 #pragma unroll
       for (int r = 0; r < MAX_RT; ++r)
-        if (r < own_v) pa[r] = take();
+        if (r < own_v) pa[r] = take_p();
       for (int st = lo; st < hi; st += 2) {
         const bf16x8 x0 = ld_bf16x8(w0p + 16 * (st + 1));
         const bf16x8 x1 = ld_bf16x8(w1p + 16 * (st + 1));
 #pragma unroll
         for (int r = 0; r < MAX_RT; ++r)
-          if (r < own_v) pc[r] = take();
+          if (r < own_v) pc[r] = take_p();
 #pragma unroll
         for (int r = 0; r < MAX_RT; ++r)
           if (r < own_v) {
@@ -673,7 +819,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
           w1 = ld_bf16x8(w1p + 16 * (st + 2));
 #pragma unroll
           for (int r = 0; r < MAX_RT; ++r)
-            if (r < own_v) pa[r] = take();
+            if (r < own_v) pa[r] = take_p();
         }
 #pragma unroll
         for (int r = 0; r < MAX_RT; ++r)
@@ -853,7 +999,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   }
 }
 
-template <int D, int MAX_RT, int NSLOT, bool WH>
+template <int D, int MAX_RT, int NSLOT, bool WH, bool I8>
 __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const WgProgram p = a.wg[blockIdx.x];
@@ -866,10 +1012,10 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   lds_barrier();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   unsigned char* work = smem + a.prog_bytes;
-  FragRing<D, NSLOT> fr;
+  FragRing<D, NSLOT, I8> fr;
   GroupAcc<up_col_blocks<D>()> acc;
-  fr.data_lane = a.data + (threadIdx.x & 63) * 8;
-  fr.lane8 = (threadIdx.x & 63) * 8;
+  fr.data = reinterpret_cast<const unsigned char*>(a.data);
+  fr.lane = threadIdx.x & 63;
   fr.ring = reinterpret_cast<__bf16*>(work + a.ring_offset) + (size_t)wave * NSLOT * kFragElems;
   fr.ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(fr.ring));
   RunDeriver<D> rd;
@@ -892,7 +1038,7 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
     // lane-dependent address of one item kind stays live across the other
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
-    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT, WH>(a, it, work, fr, rd, acc, tid);
+    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT, WH, I8>(a, it, work, fr, rd, acc, tid);
     else if (it.kind == kItemTail) tail_item<D>(a, it, work, tid);
   }
   if constexpr (NSLOT > 0) wait_vmcnt<0>();  // no LDS write may land after the workgroup ends
@@ -996,51 +1142,69 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_row_scales(const uint16_t* src, int rows, int cols, int rows_pad, float* scale, int* bad,
+                             hipStream_t s) {
+  if (rows_pad == 0) return hipSuccess;
+  hipLaunchKernelGGL(row_scale_kernel, dim3((rows_pad + 255) / 256), dim3(256), 0, s, src, rows, cols, rows_pad,
+                     scale, bad);
+  return hipGetLastError();
+}
 
-template <int D, int MAX_RT, int NSLOT, bool WH>
+hipError_t launch_scale_units(const float* ks, const float* vs, int T_pad, float* dst, hipStream_t s) {
+  if (T_pad == 0) return hipSuccess;
+  hipLaunchKernelGGL(scale_units_kernel, dim3((2 * T_pad + 255) / 256), dim3(256), 0, s, ks, vs, T_pad, dst);
+  return hipGetLastError();
+}
+
+
+template <int D, int MAX_RT, int NSLOT, bool WH, bool I8>
 static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                                   hipEvent_t e1) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_kernel<D, MAX_RT, NSLOT, WH>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_kernel<D, MAX_RT, NSLOT, WH, I8>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipExtLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT, WH>), dim3(grid), dim3(kThreads), (uint32_t)lds, s, e0, e1, 0,
-                        a);
+  hipExtLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT, WH, I8>), dim3(grid), dim3(kThreads), (uint32_t)lds, s, e0,
+                        e1, 0, a);
   return hipGetLastError();
 }
 
 // ring slots 8 / 6 / none with the whole weight tile; 4 with the half tile
-template <int D, int MAX_RT>
+template <int D, int MAX_RT, bool I8>
 static hipError_t launch_attend_r(const AttendArgs& a, int nslot, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                                   hipEvent_t e1) {
   switch (nslot) {
-    case 8: return launch_attend_t<D, MAX_RT, 8, false>(a, grid, lds, s, e0, e1);
-    case 6: return launch_attend_t<D, MAX_RT, 6, false>(a, grid, lds, s, e0, e1);
-    case 4: return launch_attend_t<D, MAX_RT, 4, true>(a, grid, lds, s, e0, e1);
-    case 0: return launch_attend_t<D, MAX_RT, 0, false>(a, grid, lds, s, e0, e1);
+    case 8: return launch_attend_t<D, MAX_RT, 8, false, I8>(a, grid, lds, s, e0, e1);
+    case 6: return launch_attend_t<D, MAX_RT, 6, false, I8>(a, grid, lds, s, e0, e1);
+    case 4: return launch_attend_t<D, MAX_RT, 4, true, I8>(a, grid, lds, s, e0, e1);
+    case 0: return launch_attend_t<D, MAX_RT, 0, false, I8>(a, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <int D>
+template <int D, bool I8>
 static hipError_t launch_attend_d(const AttendArgs& a, int max_rt, int nslot, int grid, size_t lds,
                                   hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   switch (max_rt) {
-    case 2: return launch_attend_r<D, 2>(a, nslot, grid, lds, s, e0, e1);
-    case 3: return launch_attend_r<D, 3>(a, nslot, grid, lds, s, e0, e1);
-    case 4: return launch_attend_r<D, 4>(a, nslot, grid, lds, s, e0, e1);
+    case 2: return launch_attend_r<D, 2, I8>(a, nslot, grid, lds, s, e0, e1);
+    case 3: return launch_attend_r<D, 3, I8>(a, nslot, grid, lds, s, e0, e1);
+    case 4: return launch_attend_r<D, 4, I8>(a, nslot, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, int grid, size_t lds_bytes,
-                         hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, bool p_int8, int grid,
+                         size_t lds_bytes, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (grid == 0) return hipSuccess;
-  if (head_dim == 64) return launch_attend_d<64>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
-  if (head_dim == 128) return launch_attend_d<128>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
+  if (head_dim == 64)
+    return p_int8 ? launch_attend_d<64, true>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1)
+                  : launch_attend_d<64, false>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
+  if (head_dim == 128)
+    return p_int8 ? launch_attend_d<128, true>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1)
+                  : launch_attend_d<128, false>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
   return hipErrorInvalidValue;
 }
 

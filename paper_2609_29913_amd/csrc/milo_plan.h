@@ -16,6 +16,7 @@ namespace milo {
 struct PlanInput {
   const BlockMeta* meta;  // [n_blocks]
   int n_kv, d;
+  bool p_int8;            // P factors stored as INT8 codes (block items carry kItemInt8)
 };
 
 struct Tiling {

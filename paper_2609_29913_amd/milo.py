@@ -24,10 +24,14 @@ _c_i32p = ctypes.POINTER(ctypes.c_int32)
 _c_u16p = ctypes.POINTER(ctypes.c_uint16)
 
 
+MILO_P_BF16 = 0
+MILO_P_INT8 = 1
+
+
 class milo_cache_desc(ctypes.Structure):
     _fields_ = [("n_blocks", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("block_tokens", _c_i32p),
-                ("rank_k", _c_i32p), ("rank_v", _c_i32p)]
+                ("rank_k", _c_i32p), ("rank_v", _c_i32p), ("p_format", ctypes.c_int32)]
 
 
 class MiloError(RuntimeError):
@@ -76,6 +80,8 @@ def lib() -> ctypes.CDLL:
         L.milo_last_error.restype = ctypes.c_char_p
         L.milo_cache_device_bytes.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
         L.milo_cache_device_bytes.restype = ctypes.c_int
+        L.milo_cache_read_int8.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, vp, vp]
+        L.milo_cache_read_int8.restype = ctypes.c_int
         L.milo_cache_plan_builds.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
         L.milo_cache_plan_builds.restype = ctypes.c_int
         L.milo_cache_read_factor.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, vp]
@@ -163,9 +169,10 @@ def _stream(stream) -> int:
 
 
 def milo_cache_create(block_tokens: Sequence[int], rank_k: Sequence[int], rank_v: Sequence[int],
-                      n_kv_heads: int, head_dim: int, pk, rk, pv, rv, stream=None) -> int:
+                      n_kv_heads: int, head_dim: int, pk, rk, pv, rv, stream=None, p_int8: bool = False) -> int:
     """Build a cache from per-block bf16 factors (numpy uint16 arrays in host memory,
-    or device tensors); returns the opaque handle as an int."""
+    or device tensors); returns the opaque handle as an int.  p_int8 stores P^K and
+    P^V as int8 codes with per-token scales (MILO_P_INT8)."""
     nb = len(pk)
     if not (len(rk) == len(pv) == len(rv) == nb):
         raise ValueError("factor lists differ in length")
@@ -196,7 +203,8 @@ def milo_cache_create(block_tokens: Sequence[int], rank_k: Sequence[int], rank_v
             ptrs[b] = _addr(x)
         arrays.append(ptrs)
     bt, rks, rvs = _i32(block_tokens), _i32(rank_k), _i32(rank_v)
-    desc = milo_cache_desc(nb, n_kv_heads, head_dim, bt._as_parameter_, rks._as_parameter_, rvs._as_parameter_)
+    desc = milo_cache_desc(nb, n_kv_heads, head_dim, bt._as_parameter_, rks._as_parameter_, rvs._as_parameter_,
+                           MILO_P_INT8 if p_int8 else MILO_P_BF16)
     out = ctypes.c_void_p()
     s = _stream(stream) if src_on_device else (0 if stream is None else _stream(stream))
     _check(lib().milo_cache_create(ctypes.byref(desc), *arrays, src_on_device, s, ctypes.byref(out)))
@@ -323,6 +331,14 @@ def milo_cache_device_bytes(cache: int) -> int:
     v = ctypes.c_int64()
     _check(lib().milo_cache_device_bytes(ctypes.c_void_p(cache), ctypes.byref(v)))
     return v.value
+
+
+def milo_cache_read_int8(cache: int, block: int, which: int, shape):
+    """INT8 P factors: (codes int8 [T][rank], scales float32 [T]) of P^K (which=0) or P^V (2)."""
+    codes = np.zeros(shape, dtype=np.int8)
+    scales = np.zeros(shape[0], dtype=np.float32)
+    _check(lib().milo_cache_read_int8(ctypes.c_void_p(cache), block, which, codes.ctypes.data, scales.ctypes.data))
+    return codes, scales
 
 
 def milo_cache_plan_builds(cache: int) -> int:

@@ -249,13 +249,18 @@ def make_problem(seed: int, block_tokens, rank_k, rank_v=None, *, n_kv_heads=2, 
 # --------------------------------------------------------------------------
 # Accounting (what one decode step over one layer must move / compute)
 # --------------------------------------------------------------------------
-def algorithmic_bytes(inp: LayerInputs, table=None) -> int:
-    """Bytes a step must touch once: every selected factor (bf16), each request's
-    valid tail K/V (bf16), the queries (bf16) and the fp32 output."""
+def algorithmic_bytes(inp: LayerInputs, table=None, p_int8: bool = False) -> int:
+    """Bytes a step must touch once: every selected factor (bf16; with INT8 P
+    factors one byte per P element plus two fp32 scales per token), each
+    request's valid tail K/V (bf16), the queries (bf16) and the fp32 output."""
     table = range(inp.n_blocks) if table is None else table
     D = inp.n_kv_heads * inp.head_dim
-    fac = sum(2 * (int(inp.block_tokens[b]) + D) * (int(inp.rank_k[b]) + int(inp.rank_v[b]))
-              for b in table)
+    if p_int8:
+        fac = sum((int(inp.block_tokens[b]) + 2 * D) * (int(inp.rank_k[b]) + int(inp.rank_v[b]))
+                  + 8 * int(inp.block_tokens[b]) for b in table)
+    else:
+        fac = sum(2 * (int(inp.block_tokens[b]) + D) * (int(inp.rank_k[b]) + int(inp.rank_v[b]))
+                  for b in table)
     tail = 2 * 2 * int(np.sum(inp.tail_len)) * D
     ncol = inp.n_q * inp.n_q_heads
     return fac + tail + 2 * ncol * inp.head_dim + 4 * ncol * inp.head_dim

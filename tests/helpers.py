@@ -24,6 +24,20 @@ def oracle_args(inp: LayerInputs, table=None, tail_len=None):
         tail_len=inp.tail_len if tail_len is None else np.asarray(tail_len), scale=inp.scale)
 
 
+def oracle_args_int8(inp: LayerInputs, table=None, tail_len=None):
+    """The oracle's arguments for a cache that stores P^K and P^V as INT8: the
+    dequantised P factors (oracle.quantize_rows_int8 of the bf16 values), the
+    bf16 R factors, queries and tails."""
+    import oracle
+    from synth import bf16_to_f32
+    a = oracle_args(inp, table, tail_len)
+    deq = lambda x: oracle.dequantize_rows_int8(*oracle.quantize_rows_int8(bf16_to_f32(x)))
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        a["pk"] = list(ex.map(deq, inp.pk))
+        a["pv"] = list(ex.map(deq, inp.pv))
+    return a
+
+
 def col_rel_l2(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
     d = ref.shape[-1]
     got = np.asarray(got, dtype=np.float64).reshape(-1, d)
@@ -47,7 +61,7 @@ def to_device(a: np.ndarray):
 class GpuLayer:
     """A cache built from one LayerInputs plus device copies of q and the tails."""
 
-    def __init__(self, inp: LayerInputs, src_on_device=False):
+    def __init__(self, inp: LayerInputs, src_on_device=False, p_int8=False):
         from paper_2609_29913_amd import milo
         self.inp = inp
         if src_on_device:
@@ -55,7 +69,7 @@ class GpuLayer:
         else:
             facs = [inp.pk, inp.rk, inp.pv, inp.rv]
         self.cache = milo.milo_cache_create(inp.block_tokens, inp.rank_k, inp.rank_v, inp.n_kv_heads,
-                                            inp.head_dim, *facs)
+                                            inp.head_dim, *facs, p_int8=p_int8)
         self.q = to_device(inp.q)
         self.tk = to_device(inp.tail_k)
         self.tv = to_device(inp.tail_v)

@@ -84,7 +84,7 @@ static int check_runs(int T, int rk, int rv, int n_kv, int d) {
     std::vector<int> seen((size_t)total, 0);
     for (int w = 0; w < kWaves; ++w) {
       std::vector<std::pair<int, int>> runs;
-      block_runs(bm, g, nh, 0, ntile, w, d, lg_ng, [&](int x, int n) { runs.push_back({x, n}); });
+      block_runs(bm, g, nh, 0, ntile, w, d, lg_ng, false, [&](int x, int n) { runs.push_back({x, n}); });
       for (auto& r : runs)
         for (int k = 0; k < r.second; ++k) {
           if (r.first + k < 0 || r.first + k >= total) {
@@ -129,13 +129,73 @@ static int check_runs(int T, int rk, int rv, int n_kv, int d) {
   return 0;
 }
 
+// The same for INT8 P factors: over the eight waves every int8 fragment
+// (512-byte unit) of P^K and P^V is read exactly once, every (tile, wave)
+// scale unit exactly once and by that wave, between its P^K and P^V runs, and
+// every int8 run has an even length (whole 1 KiB units of two fragments).
+static int check_runs_i8(int T, int rk, int rv, int n_kv, int d) {
+  const int T_pad = (T + kTile - 1) / kTile * kTile;
+  BlockMeta bm{};
+  bm.T = T;
+  bm.T_pad = T_pad;
+  bm.rk_pad = (rk + 31) / 32 * 32;
+  bm.rv_pad = (rv + 31) / 32 * 32;
+  const long long D = (long long)n_kv * d;
+  // element offsets as the cache lays them out (each region on a 512-element boundary)
+  auto up = [](long long x) { return (x + kFragElems - 1) / kFragElems * kFragElems; };
+  bm.off_pk = 0;
+  bm.off_rk = up(i8_factor_bytes(T_pad, bm.rk_pad) / 2);
+  bm.off_pv = up(bm.off_rk + (long long)bm.rk_pad * D);
+  bm.off_rv = up(bm.off_pv + i8_factor_bytes(T_pad, bm.rv_pad) / 2 + i8_scale_bytes(T_pad) / 2);
+  const long long pk8_0 = bm.off_pk / 256, pk8_n = i8_factor_bytes(T_pad, bm.rk_pad) / 512;
+  const long long pv8_0 = bm.off_pv / 256, pv8_n = i8_factor_bytes(T_pad, bm.rv_pad) / 512;
+  const long long sc_0 = i8_scale_offset(bm.off_pv, T_pad, bm.rv_pad) * 2 / kScaleUnitBytes;
+  const int ntile = T_pad / kTile, lg_ng = lg_rank_groups(bm.rv_pad / 32);
+  std::vector<int> seen_pk(pk8_n, 0), seen_pv(pv8_n, 0), seen_sc(ntile * kWaves, 0);
+  for (int w = 0; w < kWaves; ++w) {
+    int last_kind = -1, tile = 0;
+    bool bad = false;
+    block_runs(bm, 0, 1, 0, ntile, w, d, lg_ng, true, [&](int x, int n) {
+      const int kind = (n >> kRunKindShift) & 3, cnt = n & kRunCountMask;
+      if (kind == kRunI8) {
+        if (cnt % 2) bad = true;
+        for (int k = 0; k < cnt; ++k) {
+          const long long f = x + k;
+          if (f >= pk8_0 && f < pk8_0 + pk8_n) seen_pk[f - pk8_0]++;
+          else if (f >= pv8_0 && f < pv8_0 + pv8_n) seen_pv[f - pv8_0]++;
+          else bad = true;
+        }
+      } else if (kind == kRunScale) {
+        const long long u = x - sc_0;
+        if (cnt != 1 || last_kind != kRunI8 || u != (long long)tile * kWaves + w) bad = true;
+        else seen_sc[u]++;
+        ++tile;
+      }
+      last_kind = kind;
+    });
+    if (bad) {
+      std::printf("int8 runs: wave %d has a malformed run\n", w);
+      return 1;
+    }
+  }
+  for (auto* v : {&seen_pk, &seen_pv, &seen_sc})
+    for (size_t k = 0; k < v->size(); ++k)
+      if ((*v)[k] != 1) {
+        std::printf("int8 runs: unit %zu read %d times\n", k, (*v)[k]);
+        return 1;
+      }
+  return 0;
+}
+
 int main(int argc, char** argv) {
   // argv: groups of (T, r, n_kv, d); with --runs first: groups of (T, rk, rv, n_kv, d)
-  if (argc > 1 && std::string(argv[1]) == "--runs") {
+  if (argc > 1 && (std::string(argv[1]) == "--runs" || std::string(argv[1]) == "--runs-int8")) {
+    const bool i8 = std::string(argv[1]) == "--runs-int8";
     int bad = 0, n = 0;
     for (int i = 2; i + 4 < argc; i += 5) {
-      bad |= check_runs(std::atoi(argv[i]), std::atoi(argv[i + 1]), std::atoi(argv[i + 2]), std::atoi(argv[i + 3]),
-                        std::atoi(argv[i + 4]));
+      const int T = std::atoi(argv[i]), rk = std::atoi(argv[i + 1]), rv = std::atoi(argv[i + 2]),
+                nkv = std::atoi(argv[i + 3]), d = std::atoi(argv[i + 4]);
+      bad |= i8 ? check_runs_i8(T, rk, rv, nkv, d) : check_runs(T, rk, rv, nkv, d);
       ++n;
     }
     std::printf("%s (%d geometries)\n", bad ? "FAIL" : "OK", n);

@@ -14,7 +14,7 @@
 //    of every tile says how many (folding only where the kernel folds);
 //  - every program fits the LDS region the plan reserves for it.
 // Case format (whitespace separated):
-//   n_kv d G n_q n_chunks program_cap n_blocks  (T rk rv) x n_blocks  n_sel  table...
+//   n_kv d G n_q n_chunks program_cap int8 n_blocks  (T rk rv) x n_blocks  n_sel  table...
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -38,7 +38,7 @@ static int fails = 0;
     }                                            \
   } while (0)
 
-static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks, long long program_cap,
+static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks, long long program_cap, int i8,
                      const std::vector<int>& T, const std::vector<int>& rk, const std::vector<int>& rv,
                      const std::vector<int>& table) {
   const int nb = (int)T.size();
@@ -77,7 +77,7 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
   }
   Schedule sch;
   std::string err;
-  if (!build_schedule(PlanInput{meta.data(), n_kv, d}, table.data(), (int)table.size(), n_q, n_chunks, til,
+  if (!build_schedule(PlanInput{meta.data(), n_kv, d, i8 != 0}, table.data(), (int)table.size(), n_q, n_chunks, til,
                       program_cap, &sch, &err)) {
     CHECK(false, "plan failed: %s", err.c_str());
   }
@@ -122,6 +122,7 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
         if (meta[x].off_pk == w.blk.off_pk) b = x;
       CHECK(b >= 0 && std::memcmp(&meta[b], &w.blk, sizeof(BlockMeta)) == 0, "block item metadata");
       CHECK(((w.flags >> kItemLgNgShift) & 3) == lg_rank_groups(meta[b].rv_pad / 32), "rank groups field");
+      CHECK(((w.flags & kItemInt8) != 0) == (i8 != 0), "INT8 flag");
       CHECK(w.ntile >= 1 && w.ntile <= kMaxPartTiles && w.tile0 >= 0 && w.tile0 + w.ntile <= meta[b].T_pad / kTile,
             "block item tile range");
       auto it = cover.find({b, k});
@@ -130,7 +131,7 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
       for (int wave = 0; wave < kWaves; ++wave) {
         int runs = 0;
         block_runs(w.blk, w.g, til.nh[k], w.tile0, w.ntile, wave, d, lg_rank_groups(meta[b].rv_pad / 32),
-                   [&](int, int) { ++runs; });
+                   (w.flags & kItemInt8) != 0, [&](int, int) { ++runs; });
         CHECK(runs <= kRunCap - 1, "%d runs exceed the run buffer", runs);
       }
       // slot groups
@@ -173,9 +174,9 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
 
 int main() {
   int case_no = 0;
-  int n_kv, d, G, n_q, n_chunks, nb;
+  int n_kv, d, G, n_q, n_chunks, nb, i8;
   long long cap;
-  while (std::scanf("%d %d %d %d %d %lld %d", &n_kv, &d, &G, &n_q, &n_chunks, &cap, &nb) == 7) {
+  while (std::scanf("%d %d %d %d %d %lld %d %d", &n_kv, &d, &G, &n_q, &n_chunks, &cap, &i8, &nb) == 8) {
     std::vector<int> T(nb), rk(nb), rv(nb);
     for (int b = 0; b < nb; ++b)
       if (std::scanf("%d %d %d", &T[b], &rk[b], &rv[b]) != 3) return 2;
@@ -184,7 +185,7 @@ int main() {
     std::vector<int> table(n_sel);
     for (int j = 0; j < n_sel; ++j)
       if (std::scanf("%d", &table[j]) != 1) return 2;
-    run_case(case_no++, n_kv, d, G, n_q, n_chunks, cap, T, rk, rv, table);
+    run_case(case_no++, n_kv, d, G, n_q, n_chunks, cap, i8, T, rk, rv, table);
   }
   std::printf("%s (%d cases)\n", fails ? "FAIL" : "OK", case_no);
   return fails ? 1 : 0;

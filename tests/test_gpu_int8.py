@@ -1,0 +1,123 @@
+"""INT8 P factors on the GPU (MILO_P_INT8, through the C ABI): the stored codes
+and scales equal the oracle's quantisation bit for bit, and attention over the
+INT8 cache matches the oracle evaluated on the dequantised factors within the
+same bar as the bf16 path (max per-head rel-L2 <= 1e-2: the codes are exact in
+bf16 and the scales enter in fp32, so the GPU keeps the bf16 path's roundings)."""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from helpers import TOL_REL_L2, GpuLayer, col_rel_l2, max_rel_l2, oracle_args_int8
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_29913_amd import milo
+    milo.lib()
+
+
+SHAPES = {
+    "ragged_d128_g4": dict(block_tokens=[1, 31, 33, 300, 1024, 257], rank_k=[1, 16, 33, 100, 512, 200],
+                           rank_v=[1, 8, 31, 128, 480, 257], n_kv_heads=4, head_dim=128, n_q=3,
+                           n_q_heads=16, tail_cap=130, tail_len=[0, 5, 130]),
+    "d64_g7": dict(block_tokens=[513, 64, 700], rank_k=[64, 64, 64], rank_v=[32, 64, 96], n_kv_heads=2,
+                   head_dim=64, n_q=10, n_q_heads=14, tail_cap=200,
+                   tail_len=[200, 129, 1, 0, 128, 127, 50, 3, 200, 77]),
+    "q7b_shape_5_blocks": dict(block_tokens=[1024] * 5, rank_k=[64, 288, 512, 96, 352], n_kv_heads=4,
+                               head_dim=128, n_q=8, n_q_heads=28, tail_cap=256),
+    "flat_tiles_32b_heads": dict(block_tokens=[2048, 512, 1024], rank_k=[320, 128, 512], n_kv_heads=8,
+                                 head_dim=128, n_q=16, n_q_heads=40, tail_cap=600),
+    "rank768_half_weight_tile": dict(block_tokens=[1024, 800], rank_k=[768, 640], rank_v=[704, 768],
+                                     n_kv_heads=8, head_dim=128, n_q=2, n_q_heads=40, tail_cap=64),
+    "rank896_no_ring": dict(block_tokens=[1000], rank_k=[896], rank_v=[840], n_kv_heads=8, head_dim=128,
+                            n_q=1, n_q_heads=16, tail_cap=0),
+    "g16_segments": dict(block_tokens=[256, 128, 300], rank_k=[64, 32, 48], n_kv_heads=1, head_dim=64, n_q=5,
+                         n_q_heads=16, tail_cap=9, tail_len=[9, 0, 4, 9, 1]),
+}
+
+
+def _check(inp, label, table=None, columns=None):
+    gl = GpuLayer(inp, p_int8=True)
+    try:
+        got = gl.attend(table).cpu().numpy()
+    finally:
+        gl.free()
+    assert np.all(np.isfinite(got)), "unwritten or non-finite outputs"
+    a = oracle_args_int8(inp, table)
+    if columns is None:
+        err = max_rel_l2(got, oracle.attend_latent(**a))
+    else:
+        ref = oracle.attend_latent(**a, columns=columns)
+        err = float(col_rel_l2(np.stack([got[i, h] for i, h in columns]), ref).max())
+    print(f"[int8] {label}: max rel-L2 vs the oracle on dequantised factors = {err:.3e}", flush=True)
+    assert err <= TOL_REL_L2
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_int8_parity_shapes(name):
+    _check(synth.make_problem(zlib.crc32(name.encode()) % 1000, **SHAPES[name]), name)
+
+
+def test_int8_parity_q7b_single_layer():
+    _check(synth.gen_layer("q7b_1l"), "q7b_1l")
+
+
+def test_int8_parity_32b_layer_sampled():
+    inp = synth.gen_layer("q32b_64l", 0)
+    G = inp.n_q_heads // inp.n_kv_heads
+    cols = [(i, h) for i in (0, inp.n_q - 1) for h in range(inp.n_q_heads)]
+    cols += [((c % (inp.n_q * G)) // G, (c // (inp.n_q * G)) * G + c % G)
+             for c in range(0, inp.n_q * inp.n_q_heads, 64)]
+    _check(inp, "q32b_64l layer 0, sampled columns", columns=sorted(set(cols)))
+
+
+def test_int8_subset_table_and_tails():
+    inp = synth.make_problem(41, [300, 512, 64, 1000, 7], [32, 64, 16, 256, 7], n_kv_heads=2, head_dim=128,
+                             n_q=2, n_q_heads=6, tail_cap=40, tail_len=[40, 13])
+    _check(inp, "subset [3, 0, 4]", table=[3, 0, 4])
+
+
+def test_int8_codes_and_scales_match_the_oracle():
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(42, [1, 45, 300, 1024], [1, 33, 100, 512], [1, 20, 190, 288], n_kv_heads=4,
+                             head_dim=128, n_q=1, n_q_heads=4, tail_cap=0)
+    gl = GpuLayer(inp, p_int8=True)
+    try:
+        for b in range(inp.n_blocks):
+            for which, p in ((0, inp.pk[b]), (2, inp.pv[b])):
+                codes, scales = milo.milo_cache_read_int8(gl.cache, b, which, p.shape)
+                rc, rs = oracle.quantize_rows_int8(synth.bf16_to_f32(p))
+                assert np.array_equal(scales.view(np.uint32), rs.view(np.uint32)), (b, which)
+                assert np.array_equal(codes, rc), (b, which)
+            # the R factors stay bf16 and read back unchanged
+            assert np.array_equal(milo.milo_cache_read_factor(gl.cache, b, 1, inp.rk[b].shape), inp.rk[b])
+        with pytest.raises(milo.MiloError):
+            milo.milo_cache_read_factor(gl.cache, 0, 0, inp.pk[0].shape)
+    finally:
+        gl.free()
+
+
+def test_int8_rejects_a_non_finite_factor():
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(43, [64, 64], [16, 16], n_kv_heads=2, head_dim=64, n_q=1, n_q_heads=2)
+    pv1 = inp.pv[1].copy()
+    pv1[5, 3] = 0x7F80  # +inf in bf16
+    with pytest.raises(milo.MiloError) as ei:
+        milo.milo_cache_create(inp.block_tokens, inp.rank_k, inp.rank_v, 2, 64, inp.pk, inp.rk,
+                               [inp.pv[0], pv1], inp.rv, p_int8=True)
+    assert ei.value.code == milo.MILO_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_int8_parity_random_shapes(seed):
+    from test_gpu_parity import _random_case
+    inp, table = _random_case(seed)
+    _check(inp, f"random seed {seed}", table=table)

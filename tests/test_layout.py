@@ -53,3 +53,13 @@ def test_derived_fragment_runs_cover_each_block_once(checker):
     res = subprocess.run([checker, "--runs", *args], capture_output=True, text=True)
     assert res.returncode == 0, res.stdout + res.stderr
     assert res.stdout.startswith("OK")
+
+
+def test_int8_runs_cover_codes_and_scales_once(checker):
+    """INT8 P factors: the runs of the eight waves read every int8 fragment of
+    P^K and P^V once, in whole 1 KiB units of two, and every (tile, wave) scale
+    unit once, by its own wave, between its P^K and P^V runs."""
+    args = [str(x) for g in RUN_GEOMS for x in g]
+    res = subprocess.run([checker, "--runs-int8", *args], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert res.stdout.startswith("OK")

@@ -26,10 +26,10 @@ def checker(tmp_path_factory):
     return exe
 
 
-def _case(n_kv, d, G, n_q, n_chunks, T, rk, rv=None, table=None, cap=-1):
+def _case(n_kv, d, G, n_q, n_chunks, T, rk, rv=None, table=None, cap=-1, i8=False):
     rv = rk if rv is None else rv
     table = list(range(len(T))) if table is None else table
-    head = f"{n_kv} {d} {G} {n_q} {n_chunks} {cap} {len(T)}"
+    head = f"{n_kv} {d} {G} {n_q} {n_chunks} {cap} {int(i8)} {len(T)}"
     blocks = " ".join(f"{t} {a} {b}" for t, a, b in zip(T, rk, rv))
     return f"{head} {blocks} {len(table)} {' '.join(map(str, table))}\n"
 
@@ -79,7 +79,7 @@ def test_plans_of_random_shapes(checker):
         rv = [int(rng.integers(1, min(int(t), D, 896) + 1)) for t in T]
         k = int(rng.integers(1, nb + 1))
         table = [int(b) for b in rng.permutation(nb)[:k]]
-        cases.append(_case(n_kv, d, G, n_q, int(rng.integers(0, 5)), T, rk, rv, table))
+        cases.append(_case(n_kv, d, G, n_q, int(rng.integers(0, 5)), T, rk, rv, table, i8=bool(rng.integers(2))))
     _run(checker, cases)
 
 
@@ -87,7 +87,7 @@ def test_plan_split_over_launches(checker):
     """A program cap small enough to need several launches (1200 one-tile
     blocks on one KV head), and tail chunks with leftover solo workgroups."""
     n = 1200
-    cases = [_case(1, 64, 2, 2, 1, [32] * n, [16] * n, [8] * n, cap=6912),
+    cases = [_case(1, 64, 2, 2, 1, [32] * n, [16] * n, [8] * n, cap=8960),
              _case(8, 128, 5, 16, 8, [1024] * 30, [320] * 30, cap=12000)]
     out = _run(checker, cases)
     assert "launches 1 " not in out.splitlines()[0]
