@@ -23,6 +23,9 @@ request whose tokens attend causally among themselves (a chunk of new tokens
 sharing one tail).
 `quantize_rows_int8` is the INT8 storage of a P factor (Sec. 5.3 combines the
 low-rank cache with INT8 quantisation): one scale per token row.
+`block_svd` / `block_factors` are the encoder's per-block truncated SVD (Sec.
+4.2 Eq. 3, Alg. 1 encoding stage): the singular values and right singular
+vectors of a block's keys (or values), then P = U_r Sigma_r = K V_r, R = V_r^T.
 `allocate_ranks` is the encoder's rank allocation (Sec. 4.3): per-block ranks
 that maximise the retained spectral information (Eq. 5) under a total rank
 budget and per-block bounds (Eq. 6), found by the greedy over marginal gains
@@ -42,8 +45,8 @@ import math
 
 import numpy as np
 
-__all__ = ["allocate_ranks", "attend_dense", "attend_latent", "attend_prefill", "dequantize_rows_int8",
-           "quantize_rows_int8", "reconstruct", "spectral_information"]
+__all__ = ["allocate_ranks", "attend_dense", "attend_latent", "attend_prefill", "block_factors", "block_svd",
+           "dequantize_rows_int8", "quantize_rows_int8", "reconstruct", "spectral_information"]
 
 
 def _mm(a: np.ndarray, b: np.ndarray, ordered: bool) -> np.ndarray:
@@ -305,3 +308,51 @@ def quantize_rows_int8(p):
 def dequantize_rows_int8(codes, scales):
     """The factor INT8 storage stands for: P[t][k] = s_t c[t][k] (float64, exact)."""
     return np.asarray(scales, dtype=np.float64)[:, None] * np.asarray(codes, dtype=np.float64)
+
+
+# --------------------------------------------------------------------------
+# Per-block truncated SVD of the encoder (Sec. 4.2 Eq. 3, Alg. 1 encoding stage)
+# --------------------------------------------------------------------------
+def block_svd(k, tol: float = 1e-13, max_sweeps: int = 60):
+    """Singular values and right singular vectors of one block's K (T x D), by
+    one-sided Jacobi (Hestenes): rotate pairs of columns of A = K until every
+    pair is orthogonal; the rotations accumulate into V, the column norms of
+    the final A are the singular values.  Textbook cyclic order (p < q, row by
+    row), fp64.  Returns (sigma [D] non-increasing, V [D, D] with column j the
+    right singular vector of sigma_j), so K = U diag(sigma) V^T with
+    U = A / sigma.  Only the first min(T, D) values can be non-zero."""
+    a = np.array(k, dtype=np.float64)
+    n = a.shape[1]
+    v = np.eye(n)
+    for _ in range(max_sweeps):
+        rotated = False
+        for p in range(n - 1):
+            for q in range(p + 1, n):
+                alpha = a[:, p] @ a[:, p]
+                beta = a[:, q] @ a[:, q]
+                gamma = a[:, p] @ a[:, q]
+                if gamma == 0.0 or abs(gamma) <= tol * math.sqrt(alpha * beta):
+                    continue
+                rotated = True
+                # the rotation that makes columns p and q orthogonal
+                zeta = (beta - alpha) / (2.0 * gamma)
+                t = math.copysign(1.0, zeta) / (abs(zeta) + math.sqrt(1.0 + zeta * zeta))
+                c = 1.0 / math.sqrt(1.0 + t * t)
+                s_ = c * t
+                ap, aq = a[:, p].copy(), a[:, q].copy()
+                a[:, p], a[:, q] = c * ap - s_ * aq, s_ * ap + c * aq
+                vp, vq = v[:, p].copy(), v[:, q].copy()
+                v[:, p], v[:, q] = c * vp - s_ * vq, s_ * vp + c * vq
+        if not rotated:
+            break
+    sigma = np.sqrt(np.sum(a * a, axis=0))
+    order = np.argsort(-sigma, kind="stable")
+    return sigma[order], v[:, order]
+
+
+def block_factors(k, v, r: int):
+    """Eq. 3 truncated at rank r with the singular values folded into P:
+    P = U_r Sigma_r = K V_r (T x r) and R = V_r^T (r x D), so P R is the best
+    rank-r approximation of K."""
+    vr = np.asarray(v, dtype=np.float64)[:, :r]
+    return np.asarray(k, dtype=np.float64) @ vr, vr.T.copy()

@@ -11,7 +11,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmilo.so")
 SOURCES = [os.path.join(CSRC, f)
-           for f in ("milo_api.cpp", "milo_plan.cpp", "milo_kernels.hip", "milo_alloc.hip", "milo_noalloc.hip")]
+           for f in ("milo_api.cpp", "milo_plan.cpp", "milo_kernels.hip", "milo_alloc.hip", "milo_noalloc.hip",
+                     "milo_encode.hip")]
 
 # Packed fp32 VALU ops are kept out of the device code (the compiler would form
 # them from ordinary float code); the host pass ignores the feature with a warning.

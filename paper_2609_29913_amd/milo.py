@@ -80,6 +80,13 @@ def lib() -> ctypes.CDLL:
         L.milo_last_error.restype = ctypes.c_char_p
         L.milo_cache_device_bytes.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
         L.milo_cache_device_bytes.restype = ctypes.c_int
+        L.milo_block_svd.argtypes = [ctypes.POINTER(vp), _c_i32p, ctypes.c_int32, ctypes.c_int32, vp, vp, vp]
+        L.milo_block_svd.restype = ctypes.c_int
+        L.milo_block_factors.argtypes = [ctypes.POINTER(vp), _c_i32p, ctypes.c_int32, ctypes.c_int32, vp, _c_i32p,
+                                         ctypes.POINTER(vp), ctypes.POINTER(vp), vp]
+        L.milo_block_factors.restype = ctypes.c_int
+        L.milo_block_svd_sweeps.argtypes = [_c_i32p]
+        L.milo_block_svd_sweeps.restype = ctypes.c_int
         L.milo_cache_read_int8.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, vp, vp]
         L.milo_cache_read_int8.restype = ctypes.c_int
         L.milo_cache_plan_builds.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
@@ -320,6 +327,64 @@ def milo_allocate_ranks(sigma, n_sv, r_total: int, r_min: int, r_max: int, strea
     _check(lib().milo_allocate_ranks(_addr(sigma), ld, n_blocks, _i32(n_sv), int(r_total), int(r_min),
                                      int(r_max), out, _stream(stream)))
     return np.frombuffer(out, dtype=np.int32, count=n_blocks).copy()
+
+
+def _dev_ptrs(tensors, name, cols=None):
+    ptrs = (ctypes.c_void_p * max(1, len(tensors)))()
+    for b, x in enumerate(tensors):
+        _dev_tensor(x, f"{name}[{b}]", _BF16_DTYPES, 2)
+        if cols is not None and x.shape[1] != cols:
+            raise ValueError(f"{name}[{b}] has {x.shape[1]} columns, expected {cols}")
+        ptrs[b] = x.data_ptr()
+    return ptrs
+
+
+def milo_block_svd(blocks, stream=None):
+    """Encoder (Sec. 4.2 Eq. 3): singular values and right singular vectors of
+    every block.  blocks: list of device bf16 tensors [T_b][D] (one shared D).
+    Returns (sigma float32 [n_blocks][D], vt float32 [n_blocks][D][D]) on the
+    GPU; synchronous."""
+    import torch
+    if not blocks:
+        raise ValueError("no blocks")
+    D = int(blocks[0].shape[1])
+    ptrs = _dev_ptrs(blocks, "blocks", D)
+    dev = blocks[0].device
+    sigma = torch.empty((len(blocks), D), dtype=torch.float32, device=dev)
+    vt = torch.empty((len(blocks), D, D), dtype=torch.float32, device=dev)
+    tokens = [int(x.shape[0]) for x in blocks]
+    _check(lib().milo_block_svd(ptrs, _i32(tokens), len(blocks), D, sigma.data_ptr(), vt.data_ptr(),
+                                _stream(stream)))
+    return sigma, vt
+
+
+def milo_block_svd_sweeps() -> int:
+    v = ctypes.c_int32()
+    _check(lib().milo_block_svd_sweeps(ctypes.byref(v)))
+    return v.value
+
+
+def milo_block_factors(blocks, vt, ranks, stream=None):
+    """The truncated factors P_b = K_b V_r (bf16 [T_b][r_b]) and R_b = V_r^T
+    (bf16 [r_b][D]) of every block, as device int16 tensors of bf16 bits."""
+    import torch
+    D = int(blocks[0].shape[1])
+    ptrs = _dev_ptrs(blocks, "blocks", D)
+    if tuple(vt.shape) != (len(blocks), D, D) or vt.dtype != torch.float32 or not vt.is_cuda or \
+            not vt.is_contiguous():
+        raise ValueError("vt must be the float32 [n_blocks][D][D] GPU tensor milo_block_svd returned")
+    ranks = [int(r) for r in ranks]
+    if len(ranks) != len(blocks):
+        raise ValueError("one rank per block")
+    dev = blocks[0].device
+    ps = [torch.empty((int(x.shape[0]), r), dtype=torch.int16, device=dev) for x, r in zip(blocks, ranks)]
+    rs = [torch.empty((r, D), dtype=torch.int16, device=dev) for r in ranks]
+    pp = (ctypes.c_void_p * len(ps))(*[p.data_ptr() for p in ps])
+    rp = (ctypes.c_void_p * len(rs))(*[r.data_ptr() for r in rs])
+    tokens = [int(x.shape[0]) for x in blocks]
+    _check(lib().milo_block_factors(ptrs, _i32(tokens), len(blocks), D, vt.data_ptr(), _i32(ranks), pp, rp,
+                                    _stream(stream)))
+    return ps, rs
 
 
 def milo_cache_free(cache: int | None) -> None:

@@ -26,7 +26,7 @@ import numpy as np
 __all__ = [
     "Config", "CONFIGS", "LayerInputs", "f32_to_bf16", "bf16_to_f32",
     "bf16_to_f64", "gen_layer", "make_problem", "draw_block_tokens",
-    "draw_ranks", "algorithmic_bytes", "latent_flops", "gen_spectra", "Spectra",
+    "draw_ranks", "algorithmic_bytes", "latent_flops", "gen_spectra", "Spectra", "gen_kv_block",
 ]
 
 _MAGIC = 0x4D494C4F  # "MILO"
@@ -322,3 +322,20 @@ def gen_spectra(cfg: Config | str, layer: int = 0, rho: float = 0.5, r_min: int 
     B = float(T.mean())
     r_total = int(np.floor(rho * len(T) * D * B / (B + D)))
     return Spectra(sigma, n_sv, r_total, r_min, r_max)
+
+
+# --------------------------------------------------------------------------
+# Uncompressed key / value blocks for the encoder (input of the per-block SVD)
+# --------------------------------------------------------------------------
+def gen_kv_block(seed: int, T: int, D: int, decay: float = 0.8, scale: float = 8.0) -> np.ndarray:
+    """A T x D block of keys (or values) with a power-law spectrum:
+    K = U diag(sigma) V^T with U, V random orthonormal (QR of Gaussian
+    matrices, seeded) and sigma_j = scale (j + 1)^(-decay), j < min(T, D),
+    rounded to bf16 (uint16 bit patterns).  Real key blocks are strongly
+    low-rank (Sec. 3); the decay sets how much."""
+    rng = np.random.Generator(np.random.Philox(key=[_MAGIC, 0x5356 + seed]))
+    n = min(T, D)
+    u, _ = np.linalg.qr(rng.standard_normal((T, n)))
+    v, _ = np.linalg.qr(rng.standard_normal((D, n)))
+    sig = scale * np.arange(1, n + 1, dtype=np.float64) ** -decay
+    return f32_to_bf16(((u * sig) @ v.T).astype(np.float32))

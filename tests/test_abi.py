@@ -125,3 +125,20 @@ def test_allocate_rejects_on_the_host():
         assert word in milo.milo_last_error(), (word, milo.milo_last_error())
     assert list(out) == [-7, -7]
     assert milo.milo_timing_read_alloc() == (0.0, 0.0, 0)
+
+
+def test_encoder_rejects_on_the_host():
+    """milo_block_svd / milo_block_factors check their arguments before any GPU work."""
+    L = milo.lib()
+    vp = ctypes.c_void_p
+    fake = (vp * 2)(4096, 8192)              # never dereferenced
+    toks = (ctypes.c_int32 * 2)(64, 0)
+    ranks = (ctypes.c_int32 * 2)(8, 8)
+    assert L.milo_block_svd(None, toks, 2, 128, 4096, 4096, None) == milo.MILO_ERR_INVALID_ARG
+    assert L.milo_block_svd(fake, toks, 2, 128, 4096, 4096, None) == milo.MILO_ERR_INVALID_ARG   # T_1 = 0
+    assert "T_b" in milo.milo_last_error()
+    assert L.milo_block_svd(fake, (ctypes.c_int32 * 2)(64, 64), 2, 2048, 4096, 4096, None) == \
+        milo.MILO_ERR_UNSUPPORTED
+    assert L.milo_block_factors(fake, (ctypes.c_int32 * 2)(64, 64), 2, 128, 4096, (ctypes.c_int32 * 2)(8, 65),
+                                fake, fake, None) == milo.MILO_ERR_INVALID_ARG                    # rank > T
+    assert "rank" in milo.milo_last_error()
