@@ -148,7 +148,7 @@ def test_encoder_pipeline_feeds_the_decode_step():
     # compression error: dense attention over the original blocks (P = K, R = I)
     dense = dict(a, pk=[_f64(x) for x in K], rk=[np.eye(D)] * 4, pv=[_f64(x) for x in V], rv=[np.eye(D)] * 4)
     comp = max_rel_l2(got, oracle.attend_dense(**dense))
-    print(f"[svd] pipeline: ranks K {ranks["k"].tolist()} V {ranks["v"].tolist()}; decode vs oracle on the GPU factors "
+    print(f"[svd] pipeline: ranks K {ranks['k'].tolist()} V {ranks['v'].tolist()}; decode vs oracle on the GPU factors "
           f"{err:.3e}; vs dense attention on the original blocks {comp:.3e}", flush=True)
     assert err <= TOL_REL_L2
     assert sum(ranks["k"]) <= budget and sum(ranks["v"]) <= budget
