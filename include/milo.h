@@ -175,6 +175,37 @@ int milo_attend_prefill(milo_cache* cache, const int32_t* block_table, int32_t n
                         int32_t tail_base, int32_t tail_cap, float scale, float* out,
                         void* hip_stream);
 
+/* How a cache's blocks are attended (Sec. 4.5 inference path).
+ *   MILO_PATH_LATENT       (default) every block in its rank space (Eq. 1 with
+ *                          q.k = (R^K q).p): the query is projected through R^K,
+ *                          scored against P^K, the weights pass through P^V and
+ *                          the result is lifted through R^V.
+ *   MILO_PATH_RECONSTRUCT  every selected block is first rebuilt at full rank,
+ *                          K_b = P^K_b R^K_b and V_b = P^V_b R^V_b (Alg. 1
+ *                          full-rank reconstruction; bf16 with fp32
+ *                          accumulation), into a per-call buffer of the cache
+ *                          (4 T_pad H_kv d bytes per selected block, kept and
+ *                          grown like the rest of the workspace), and then
+ *                          attended as uncompressed keys and values.
+ *   MILO_PATH_AUTO         per block and call, whichever an MI355X cost model
+ *                          expects to be faster: reconstruction pays for blocks
+ *                          of high rank attended by many query columns
+ *                          (roughly r N > r H_kv d + d N, N = n_q H_q).
+ * Both routes compute the same attention up to rounding.  A plan with any
+ * reconstructed block cuts the query columns per KV head.  INT8 caches attend
+ * latent only (UNSUPPORTED for the other paths), and so does
+ * milo_attend_decode_noalloc (AUTO attends latent there; RECONSTRUCT returns
+ * UNSUPPORTED).  The setting applies from the next call on; calls queued
+ * earlier are not affected.  Errors: INVALID_ARG (NULL cache, unknown path),
+ * UNSUPPORTED.
+ * milo_cache_recon_blocks: how many blocks the plan of the cache's last
+ * milo_attend_decode / milo_attend_prefill call reconstructs. */
+#define MILO_PATH_LATENT 0
+#define MILO_PATH_RECONSTRUCT 1
+#define MILO_PATH_AUTO 2
+int milo_cache_set_path(milo_cache* cache, int32_t path);
+int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n);
+
 /* Entropy-based rank allocation of the encoder (Sec. 4.3): the per-block ranks
  * r_b that maximise the retained spectral information sum_b H_b(r_b), with
  * H_b(r) = sum_{j<=r} log(1 + sigma_{b,j}^2 / eps^2) (Eq. 5), subject to
@@ -284,6 +315,10 @@ int milo_cache_read_factor(const milo_cache* cache, int32_t block, int32_t which
  * Any argument of milo_timing_read may be NULL. */
 int milo_timing_enable(int enable);
 int milo_timing_read(double* attend_kernel_ms, double* merge_kernel_ms, int64_t* n_calls);
+/* The same for the reconstruction kernel of calls that reconstruct blocks:
+ * summed milliseconds and the number of such calls since the last read (then
+ * cleared); independent of milo_timing_read. */
+int milo_timing_read_recon(double* recon_kernel_ms, int64_t* n_calls);
 /* The same for milo_allocate_ranks calls made while timing is enabled: summed
  * milliseconds of the whole kernel chain and of its histogram passes, and the
  * number of calls, since the last read (then cleared). */

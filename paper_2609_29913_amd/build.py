@@ -12,7 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmilo.so")
 SOURCES = [os.path.join(CSRC, f)
            for f in ("milo_api.cpp", "milo_plan.cpp", "milo_kernels.hip", "milo_alloc.hip", "milo_noalloc.hip",
-                     "milo_encode.hip")]
+                     "milo_encode.hip", "milo_recon.hip")]
 
 # Packed fp32 VALU ops are kept out of the device code (the compiler would form
 # them from ordinary float code); the host pass ignores the feature with a warning.

@@ -74,6 +74,7 @@ struct TimingState {
   bool enabled = false;
   std::vector<hipEvent_t> pool;
   std::vector<hipEvent_t> recorded;  // groups of 4: attend kernel start / end, merge kernel start / end
+  std::vector<hipEvent_t> recon_recorded;  // pairs: reconstruction kernel start / end
 };
 TimingState g_timing;
 
@@ -99,6 +100,10 @@ struct milo_cache {
   bool plan_evt_live = false;
   int32_t* tail_len_d = nullptr;         // tail lengths of batches above kInlineTails requests
   int64_t tail_len_cap = 0;
+  int32_t path = MILO_PATH_LATENT;       // milo_cache_set_path
+  unsigned char* recon_raw = nullptr;    // reconstruction buffer (allocation)
+  uint16_t* recon_d = nullptr;           // its start, a whole number of fragments from `data`
+  int64_t recon_cap = 0;                 // capacity in bf16 elements
   PlanState plan;                        // the plan of the previous call
 };
 
@@ -140,6 +145,7 @@ void destroy(milo_cache* c) {
     (void)hipFree(c->part_ml);
     (void)hipFree(c->plan_d);
     (void)hipFree(c->tail_len_d);
+    (void)hipFree(c->recon_raw);
     (void)hipHostFree(c->plan_pinned);
     if (c->plan_evt) (void)hipEventDestroy(c->plan_evt);
     if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
@@ -337,6 +343,25 @@ int milo_cache_read_int8(const milo_cache* cache, int32_t block, int32_t which, 
   return MILO_OK;
 }
 
+int milo_cache_set_path(milo_cache* cache, int32_t path) {
+  g_err.clear();
+  if (!cache) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
+  if (path != MILO_PATH_LATENT && path != MILO_PATH_RECONSTRUCT && path != MILO_PATH_AUTO)
+    return fail(MILO_ERR_INVALID_ARG, "path must be MILO_PATH_LATENT, MILO_PATH_RECONSTRUCT or MILO_PATH_AUTO (got %d)",
+                path);
+  if (cache->p_int8 && path != MILO_PATH_LATENT)
+    return fail(MILO_ERR_UNSUPPORTED, "caches with INT8 P factors attend latent only");
+  cache->path = path;
+  return MILO_OK;
+}
+
+int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n) {
+  g_err.clear();
+  if (!cache || !n) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
+  *n = cache->plan.n_recon_blocks;
+  return MILO_OK;
+}
+
 int milo_cache_plan_builds(const milo_cache* cache, int64_t* builds) {
   g_err.clear();
   if (!cache || !builds) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
@@ -439,10 +464,53 @@ class CacheWorkspace : public Workspace {
     return MILO_OK;
   }
   bool may_time() const override { return true; }
+  bool can_recon() const override { return true; }
+  int recon_buffer(int64_t elems, const uint16_t* data, hipStream_t s, uint16_t** buf) override {
+    milo_cache* c = c_;
+    if (elems > c->recon_cap) {
+      MILO_HIP(hipStreamSynchronize(s));
+      (void)hipFree(c->recon_raw);
+      c->recon_raw = nullptr;
+      c->recon_d = nullptr;
+      c->recon_cap = 0;
+      const int64_t cap = env_byte_cap();
+      const int64_t bytes = elems * 2 + 1024;
+      if (cap >= 0 && c->data_elems * 2 + bytes > cap)
+        return fail(MILO_ERR_OUT_OF_MEMORY, "reconstruction buffer of %lld bytes exceeds MILO_MAX_DEVICE_BYTES",
+                    (long long)bytes);
+      MILO_HIP(hipMalloc(&c->recon_raw, (size_t)bytes));
+      // start a whole number of 1 KiB fragments from the factor buffer
+      const uintptr_t raw = reinterpret_cast<uintptr_t>(c->recon_raw), base = reinterpret_cast<uintptr_t>(data);
+      const uintptr_t adj = (base - raw) & 1023u;
+      c->recon_d = reinterpret_cast<uint16_t*>(c->recon_raw + adj);
+      c->recon_cap = elems;
+    }
+    *buf = c->recon_d;
+    return MILO_OK;
+  }
 
  private:
   milo_cache* c_;
 };
+
+// Reconstruct-then-attend pays for a block when rebuilding its keys and values
+// and attending them densely costs less than the latent route.  Both are timed
+// by an MI355X cost model: MFMA work at the efficiency each kernel reaches
+// (latent block items ~20% of the bf16 peak, the reconstruction GEMM ~35%, the
+// dense items like the latent ones) plus, for reconstruction, writing and
+// re-reading the full-rank blocks through HBM (~5 TB/s).  Per block of T
+// tokens, ranks rk / rv, N query columns, D = H_kv d:
+//   latent        2 N (rk + rv)(T + d)            flops (scores, value pass, projections)
+//   reconstruct   2 T D (rk + rv)                 flops (K = P^K R^K, V = P^V R^V)
+//               + 4 N T d                         flops (dense scores and value pass)
+//               + 8 T D                           bytes (bf16 K and V written, then read)
+bool recon_pays(int T, int rk, int rv, int64_t N, int D, int d) {
+  constexpr double kPeak = 2.5e15, kLat = 0.20, kGemm = 0.35, kDense = 0.20, kBw = 5.0e12;
+  const double lat = 2.0 * N * (rk + rv) * (double)(T + d) / (kLat * kPeak);
+  const double rec = 2.0 * T * (double)D * (rk + rv) / (kGemm * kPeak) + 4.0 * N * (double)T * d / (kDense * kPeak) +
+                     8.0 * T * (double)D / kBw;
+  return rec < lat;
+}
 
 }  // namespace
 
@@ -492,6 +560,20 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   if (dev != c->device) return fail(MILO_ERR_INVALID_ARG, "cache lives on device %d, current device is %d", c->device, dev);
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
 
+  // ---- which blocks are reconstructed (milo_cache_set_path) ----
+  if (c->path == MILO_PATH_RECONSTRUCT && !ws.can_recon())
+    return fail(MILO_ERR_UNSUPPORTED, "this entry point attends latent only (reconstruction needs a workspace)");
+  std::vector<char> recon((size_t)std::max(n_sel, 1), 0);
+  int n_recon = 0;
+  if (c->path != MILO_PATH_LATENT && ws.can_recon()) {
+    for (int j = 0; j < n_sel; ++j) {
+      const int b = block_table[j];
+      recon[j] = c->path == MILO_PATH_RECONSTRUCT ||
+                 recon_pays(c->T[b], c->rk[b], c->rv[b], (int64_t)n_q * n_q_heads, c->n_kv * c->d, c->d);
+      n_recon += recon[j];
+    }
+  }
+
   // ---- plan: rebuilt only when the block table, the batch shape or the tail
   // chunk capacity changes (the longest tail rounded up to a power of two of
   // chunks, at most tail_cap), not when tails merely grow ----
@@ -510,6 +592,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   key.push_back(n_q);
   key.push_back(n_q_heads);
   key.push_back(n_chunks);
+  key.push_back(n_recon > 0 ? c->path : MILO_PATH_LATENT);
   key.insert(key.end(), block_table, block_table + n_sel);
   const int n_cols = n_q * n_q_heads;
   if (key != ps.key) {
@@ -517,12 +600,28 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     // allocation, an upload) must not leave the old key pointing at buffers
     // that were freed or half rewritten
     ps.key.clear();
-    const Tiling til = make_tiling(c->n_kv, n_q * G);
+    std::vector<int64_t> region;
+    ReconPlan rp;
+    if (n_recon > 0) {
+      region.assign(c->n_blocks, -1);
+      build_recon_plan(c->meta.data(), block_table, n_sel, recon.data(), c->n_kv, c->d, &region, &rp);
+    }
+    const Tiling til = make_tiling(c->n_kv, n_q * G, n_recon > 0);
     Schedule sch;
     std::string why;
-    if (!build_schedule(PlanInput{c->meta.data(), c->n_kv, c->d, c->p_int8}, block_table, n_sel, n_q, n_chunks, til,
-                        env_program_cap(), &sch, &why))
+    PlanInput pin{c->meta.data(), c->n_kv, c->d, c->p_int8};
+    pin.recon_region = n_recon > 0 ? region.data() : nullptr;
+    if (!build_schedule(pin, block_table, n_sel, n_q, n_chunks, til, env_program_cap(), &sch, &why))
       return fail(MILO_ERR_UNSUPPORTED, "%s", why.c_str());
+    // the reconstruction table and tasks follow the schedule in the plan
+    int64_t rb_off = 0, rt_off = 0;
+    if (n_recon > 0) {
+      rb_off = (int64_t)round_up((int64_t)sch.bytes.size(), 64);
+      rt_off = rb_off + (int64_t)(rp.blocks.size() * sizeof(ReconBlock));
+      sch.bytes.resize((size_t)(rt_off + (int64_t)(rp.tasks.size() * sizeof(int2))));
+      std::memcpy(sch.bytes.data() + rb_off, rp.blocks.data(), rp.blocks.size() * sizeof(ReconBlock));
+      std::memcpy(sch.bytes.data() + rt_off, rp.tasks.data(), rp.tasks.size() * sizeof(int2));
+    }
     const int max_rt = sch.max_own <= 2 ? 2 : sch.max_own == 3 ? 3 : 4;
     // deepest fragment ring that fits next to the program, projected query and
     // weight tile (4 slots go with the half weight tile)
@@ -562,6 +661,11 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ps.prog_bytes = sch.prog_bytes;
     ps.ring_offset = (int)base;
     ps.lds = prog + base + attend_ring_bytes(nslot);
+    ps.n_recon_blocks = (int)rp.blocks.size();
+    ps.n_recon_tasks = (int)rp.tasks.size();
+    ps.recon_blocks_off = rb_off;
+    ps.recon_tasks_off = rt_off;
+    ps.recon_elems = rp.elems;
     ps.key.swap(key);
     ++ps.builds;
   }
@@ -584,9 +688,22 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     if (const int err = ws.tail_lengths(tail_len, n_q, s, &tls.dev); err != MILO_OK) return err;
   }
 
+  // reconstruction buffer of this call
+  uint16_t* rbuf = nullptr;
+  int recon_delta = 0;
+  if (ps.n_recon_tasks > 0) {
+    if (const int err = ws.recon_buffer(ps.recon_elems, c->data, s, &rbuf); err != MILO_OK) return err;
+    const int64_t dbytes = (reinterpret_cast<const unsigned char*>(rbuf) - reinterpret_cast<const unsigned char*>(c->data));
+    const int64_t dfr = dbytes / (kFragElems * 2);
+    if (dbytes % (kFragElems * 2) != 0 || dfr < -((int64_t)1 << 30) || dfr + ps.recon_elems / kFragElems > ((int64_t)1 << 30))
+      return fail(MILO_ERR_UNSUPPORTED, "reconstruction buffer out of the fragment index range of the factor buffer");
+    recon_delta = (int)dfr;
+  }
+
   // ---- launches ----
   AttendArgs aa{};
   aa.data = c->data;
+  aa.recon_delta = recon_delta;
   aa.prog = ps.plan_d;
   aa.q = q;
   aa.tail_k = tail_k;
@@ -619,12 +736,14 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   ma.tl = tls;
 
   // timing: events recorded by the launches themselves at kernel start and end
-  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};  // attend start / end, merge start / end
+  // attend start / end, merge start / end, reconstruction start / end
+  hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  const int n_ev = ps.n_recon_tasks > 0 ? 6 : 4;
   bool timed = false;
   {
     std::lock_guard<std::mutex> lk(g_timing.mu);
     if (g_timing.enabled && ws.may_time()) {
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < n_ev; ++k) {
         if (g_timing.pool.empty()) {
           hipEvent_t e;
           const hipError_t ce = hipEventCreate(&e);
@@ -644,11 +763,20 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   auto launch_fail = [&](hipError_t err, const char* what) {
     if (timed) {
       std::lock_guard<std::mutex> lk(g_timing.mu);
-      g_timing.pool.insert(g_timing.pool.end(), ev, ev + 4);
+      g_timing.pool.insert(g_timing.pool.end(), ev, ev + n_ev);
     }
     return hip_fail(err, what);
   };
   hipError_t e = hipSuccess;
+  if (ps.n_recon_tasks > 0) {
+    ReconArgs ra{};
+    ra.data = c->data;
+    ra.recon = rbuf;
+    ra.blocks = reinterpret_cast<const ReconBlock*>(ps.plan_d + ps.recon_blocks_off);
+    ra.tasks = reinterpret_cast<const int2*>(ps.plan_d + ps.recon_tasks_off);
+    e = launch_recon(ra, c->d, ps.n_recon_tasks, s, ev[4], ev[5]);
+    if (e != hipSuccess) return launch_fail(e, "reconstruction kernel launch");
+  }
   for (int l = 0; l < ps.n_launch; ++l) {
     aa.wg = reinterpret_cast<const WgProgram*>(ps.plan_d) + (size_t)l * kCUs;
     e = launch_attend(aa, c->d, ps.max_rt, ps.nslot, c->p_int8, kCUs, ps.lds, s, l == 0 ? ev[0] : nullptr,
@@ -660,6 +788,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   if (timed) {
     std::lock_guard<std::mutex> lk(g_timing.mu);
     g_timing.recorded.insert(g_timing.recorded.end(), ev, ev + 4);
+    if (n_ev == 6) g_timing.recon_recorded.insert(g_timing.recon_recorded.end(), ev + 4, ev + 6);
   }
   return MILO_OK;
 }
@@ -700,6 +829,25 @@ int milo_timing_enable(int enable) {
   g_err.clear();
   std::lock_guard<std::mutex> lk(g_timing.mu);
   g_timing.enabled = enable != 0;
+  return MILO_OK;
+}
+
+int milo_timing_read_recon(double* recon_kernel_ms, int64_t* n_calls) {
+  g_err.clear();
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  double t = 0.0;
+  const size_t n = g_timing.recon_recorded.size() / 2;
+  for (size_t k = 0; k < n; ++k) {
+    hipEvent_t* e = &g_timing.recon_recorded[2 * k];
+    MILO_HIP(hipEventSynchronize(e[1]));
+    float ms = 0.f;
+    MILO_HIP(hipEventElapsedTime(&ms, e[0], e[1]));
+    t += ms;
+  }
+  g_timing.pool.insert(g_timing.pool.end(), g_timing.recon_recorded.begin(), g_timing.recon_recorded.end());
+  g_timing.recon_recorded.clear();
+  if (recon_kernel_ms) *recon_kernel_ms = t;
+  if (n_calls) *n_calls = (int64_t)n;
   return MILO_OK;
 }
 

@@ -8,6 +8,7 @@
 
 #include <vector>
 
+#include "milo.h"
 #include "milo_internal.h"
 
 struct milo_cache;
@@ -25,6 +26,10 @@ struct PlanState {
   int64_t count_off = 0;  // byte offset of the plan's slot counts
   int prog_bytes = 0, ring_offset = 0;
   size_t lds = 0;
+  // reconstruct-then-attend: reconstructed blocks, their table and tasks in the plan
+  int n_recon_blocks = 0, n_recon_tasks = 0;
+  int64_t recon_blocks_off = 0, recon_tasks_off = 0;  // byte offsets in the plan
+  int64_t recon_elems = 0;                            // reconstruction buffer (bf16 elements)
 };
 
 // Device memory one attention call uses beyond its inputs and outputs.  Each
@@ -40,6 +45,14 @@ class Workspace {
   virtual int tail_lengths(const int32_t* host, int n_q, hipStream_t s, const int32_t** dev) = 0;
   // whether the call may take timing events from the library's pool (creating some when it is empty)
   virtual bool may_time() const = 0;
+  // reconstruct-then-attend: a buffer of `elems` bf16 elements whose distance
+  // from `data` is a whole number of 1 KiB fragments; workspaces that cannot
+  // hold one return false from can_recon (their calls attend every block latent)
+  virtual bool can_recon() const { return false; }
+  virtual int recon_buffer(int64_t elems, const uint16_t* data, hipStream_t s, uint16_t** buf) {
+    (void)elems; (void)data; (void)s; (void)buf;
+    return MILO_ERR_UNSUPPORTED;
+  }
 };
 
 // Attention of n_q query tokens over the selected blocks plus their dense tails

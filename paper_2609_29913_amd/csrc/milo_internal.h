@@ -133,9 +133,12 @@ __host__ __device__ inline int lg_rank_groups(int nrt) {
 // tile's P^K and P^V runs are int8 runs and the wave's scale unit comes
 // between them.  emit(first unit index, count | kind) is called for every
 // non-empty run; offsets follow the packed layout above.
+// A dense item (dense: a reconstructed block; bm = dense_meta of its head,
+// offsets relative to the reconstruction buffer, frag_base fragments from the
+// factor buffer) has no R^K or R^V runs.
 template <typename Emit>
 __host__ __device__ inline void block_runs(const BlockMeta& bm, int g0, int nh, int tile0, int ntile, int w, int d,
-                                           int lg_ng, bool i8, Emit&& emit) {
+                                           int lg_ng, bool i8, Emit&& emit, bool dense = false, int frag_base = 0) {
   static_assert(kWaves == 8, "rank tiles are dealt over 8 waves");
   const int NK = d / 16;
   const int nrt_k = bm.rk_pad >> 5, nks = bm.rk_pad >> 4, nrt_v = bm.rv_pad >> 5;
@@ -149,9 +152,12 @@ __host__ __device__ inline void block_runs(const BlockMeta& bm, int g0, int nh, 
   const int before_v = rg * (nrt_v >> lg_ng) + (rg < rem_v ? rg : rem_v);
   const int nst = 2 << lg_ng;  // 16-token steps of a segment per tile (16 / nseg)
   const int tiles_all = bm.T_pad / kTile;
-  const int rk0 = (int)(bm.off_rk / kFragElems), pk0 = (int)(bm.off_pk / kFragElems);
-  const int pv0 = (int)(bm.off_pv / kFragElems), rv0 = (int)(bm.off_rv / kFragElems);
-  if (own_k > 0)
+  // a dense item's offsets count from the reconstruction buffer; every other
+  // item's from the factor buffer itself
+  const int fb = dense ? frag_base : 0;
+  const int rk0 = (int)(bm.off_rk / kFragElems), pk0 = (int)(bm.off_pk / kFragElems) + fb;
+  const int pv0 = (int)(bm.off_pv / kFragElems) + fb, rv0 = (int)(bm.off_rv / kFragElems);
+  if (own_k > 0 && !dense)
     for (int h = 0; h < nh; ++h) emit(rk0 + (g0 + h) * nrt_k * NK + NK * before_k, NK * own_k);
   const int pv_first = (bm.T_pad / 16) * before_v;
   if (i8) {
@@ -169,6 +175,7 @@ __host__ __device__ inline void block_runs(const BlockMeta& bm, int g0, int nh, 
       if (own_v > 0) emit(pv0 + pv_first + (16 * t + nst * sg) * own_v, nst * own_v);
     }
   }
+  if (dense) return;
   const int nds = d / 16, nkr = bm.rv_pad >> 5;
   for (int h = 0; h < nh; ++h) emit(rv0 + ((g0 + h) * nds + w % nds) * nkr, nkr);
 }
@@ -253,6 +260,72 @@ __host__ __device__ inline void frag_source(const FactorGeom& f, int64_t frag, i
   }
 }
 
+// Fragment index (in 1 KiB units from the buffer start) of a given fragment of
+// each factor of block bm, the inverse of frag_source for that factor:
+//   P^K (token sub-tile tau, 16-rank step kap)     P^V (16-token step sig, rank tile rho)
+//   R^K (KV head g, rank tile rho, 16-dim step kap) R^V (KV head g, 16-dim slice ds, 32-rank step kap)
+__host__ __device__ inline int64_t pk_frag(const BlockMeta& bm, int tau, int kap) {
+  const int nks = bm.rk_pad / 16, tiles_all = bm.T_pad / kTile;
+  return bm.off_pk / kFragElems + ((int64_t)(tau % kWaves) * tiles_all + tau / kWaves) * nks + kap;
+}
+__host__ __device__ inline int64_t pv_frag(const BlockMeta& bm, int sig, int rho) {
+  const int nrt = bm.rv_pad / 32, ng = kWaves / v_segments(nrt);
+  const int rg = rho % ng, j = rho / ng;
+  return bm.off_pv / kFragElems + (int64_t)(bm.T_pad / 16) * owned_before(nrt, rg, ng) +
+         (int64_t)sig * owned_tiles(nrt, rg, ng) + j;
+}
+__host__ __device__ inline int64_t rk_frag(const BlockMeta& bm, int d, int g, int rho, int kap) {
+  const int nk = d / 16, nrt = bm.rk_pad / 32;
+  return bm.off_rk / kFragElems + (int64_t)g * nrt * nk + (int64_t)nk * (owned_before(nrt, rho % kWaves, kWaves) + rho / kWaves) +
+         kap;
+}
+__host__ __device__ inline int64_t rv_frag(const BlockMeta& bm, int d, int g, int ds, int kap) {
+  const int nds = d / 16, nkr = bm.rv_pad / 32;
+  return bm.off_rv / kFragElems + ((int64_t)g * nds + ds) * nkr + kap;
+}
+
+// ---------------------------------------------------------------------------
+// Reconstruct-then-attend (Sec. 4.5 inference path, Alg. 1 full-rank
+// reconstruction): a selected block may instead be rebuilt as its full-rank keys
+// and values, K_b = P^K R^K and V_b = P^V R^V (bf16, fp32 accumulation), into a
+// per-call buffer, and then attended like an uncompressed block.  For KV head g
+// the buffer holds K_{b,g} (T_pad x d) in the P^K fragment layout and V_{b,g}
+// in the P^V fragment layout, both with "rank" d, so the attention kernel reads
+// them with its latent loops unchanged: the scores of a column are K_{b,g} q
+// (the query itself, scaled, takes the place of the projected query) and the
+// value pass yields the output directly (no up-projection).  Such "dense"
+// block items need one KV head per column tile.
+//   region of reconstructed block i: 2 T_pad D elements; head g at 2 g T_pad d,
+//   its V at + T_pad d.
+// The reconstruction kernel takes one task per (block, K or V, KV head, 256-token tile).
+struct ReconBlock {
+  BlockMeta src;    // the block's factors in the cache buffer
+  int64_t dst;      // element offset of its region in the reconstruction buffer
+  int32_t pad[2];
+};
+static_assert(sizeof(ReconBlock) == 64, "reconstruction block layout");
+// task: x = reconstruction block (-1: none), y = tile << 8 | g << 1 | side (0: K, 1: V)
+struct ReconArgs {
+  const uint16_t* data;       // packed factors
+  uint16_t* recon;            // reconstruction buffer
+  const ReconBlock* blocks;   // [n_recon]
+  const int2* tasks;          // [grid]
+};
+// the BlockMeta of head g of a reconstructed block whose region starts at
+// element `region` (offsets relative to the reconstruction buffer)
+__host__ __device__ inline BlockMeta dense_meta(const BlockMeta& src, int64_t region, int g, int d) {
+  BlockMeta m{};
+  m.T = src.T;
+  m.T_pad = src.T_pad;
+  m.rk_pad = d;
+  m.rv_pad = d;
+  m.off_pk = region + (int64_t)g * 2 * src.T_pad * d;
+  m.off_pv = m.off_pk + (int64_t)src.T_pad * d;
+  m.off_rk = 0;
+  m.off_rv = 0;
+  return m;
+}
+
 // Per-block metadata in device memory; offsets are in bf16 elements from the
 // start of the cache's packed buffer.
 
@@ -283,7 +356,9 @@ static_assert(sizeof(WorkItem) == 80, "work item layout");
 // partial into it (log-sum-exp), and the last one writes it out.  Slots of a
 // (head, column tile) are numbered densely from 0; tail items write slot
 // n_block_slots + their chunk index.
-enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2, kItemInt8 = 4 };  // kItemInt8: INT8 P factors
+// kItemInt8: INT8 P factors; kItemDense: a reconstructed block (its metadata
+// names one KV head's K and V in the reconstruction buffer)
+enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2, kItemInt8 = 4, kItemDense = 8 };
 // packed fields of a block item's flags: bits 8-9 lg_rank_groups of its block,
 // bits 16-21 the tile's column count - 1, bits 24-26 its KV head count - 1
 constexpr int kItemLgNgShift = 8;
@@ -387,6 +462,7 @@ struct AttendArgs {
   int prog_bytes;            // LDS bytes reserved for the program (the work area follows)
   int ring_offset;           // byte offset of the per-wave fragment rings in the work area
   int N_g;                   // query columns per KV head, n_q * G
+  int recon_delta;           // fragments from `data` to the reconstruction buffer (dense items)
   TailLens tl;               // tail lengths of this call
 };
 
@@ -427,6 +503,9 @@ hipError_t launch_scale_units(const float* ks, const float* vs, int T_pad, float
 hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, bool p_int8, int grid,
                          size_t lds_bytes, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s, hipEvent_t e0 = nullptr,
+                        hipEvent_t e1 = nullptr);
+// Reconstruction of the dense blocks of a call: one workgroup per task.
+hipError_t launch_recon(const ReconArgs& a, int head_dim, int n_tasks, hipStream_t s, hipEvent_t e0 = nullptr,
                         hipEvent_t e1 = nullptr);
 // LDS of the attention kernel: a base region (projected query, weight tile and
 // reductions, or the tail item's buffers) followed by kWaves rings of nslot fragments.

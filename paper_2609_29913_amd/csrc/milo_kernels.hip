@@ -513,6 +513,7 @@ struct RunDeriver {
   int gk;                      // next item to look at
   int gb;                      // buffer the next derivation fills
   int2* rbuf;                  // all waves' run buffers: [wave][kRunBufs][kRunCap]
+  int recon_delta;             // fragments from the factor buffer to the reconstruction buffer
 
   __device__ void derive(int lane) {
     WorkItem it{};
@@ -534,7 +535,8 @@ struct RunDeriver {
       };
       if (found)
         block_runs(it.blk, it.g, ((it.flags >> kItemHeadsShift) & 7) + 1, it.tile0, it.ntile, lane, D,
-                   (it.flags >> kItemLgNgShift) & 3, (it.flags & kItemInt8) != 0, put);
+                   (it.flags >> kItemLgNgShift) & 3, (it.flags & kItemInt8) != 0, put, (it.flags & kItemDense) != 0,
+                   recon_delta);
       else put(0, kSentinelRun);
       put(0, 0);
     }
@@ -588,6 +590,10 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   const int slot = it.slot, g0 = it.g, c0 = it.req;
   const int cn = ((it.flags >> kItemColsShift) & 63) + 1;  // columns of the tile
   const int nh = ((it.flags >> kItemHeadsShift) & 7) + 1;  // KV heads of the tile
+  // a reconstructed block: bm names K_{b,g} / V_{b,g} of the tile's one KV head
+  // (rank d); the query takes the projection's place and the value pass gives
+  // the output
+  const bool dense = (it.flags & kItemDense) != 0;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lrow = lane & 31, lhi = lane >> 5;
@@ -641,8 +647,18 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   }
 
   // ---- projection: Qt[rank][col] (stored [col][rank]), once per KV head of
-  // the tile; each column stores its own head's result ----
-  if (own_k > 0) {
+  // the tile; each column stores its own head's result.  Dense items: Qt is
+  // the scaled query itself ----
+  if (dense) {
+    for (int x = tid; x < kCols * kRowChunks; x += kThreads) {
+      const int cl = x / kRowChunks, j = x % kRowChunks;
+      const bf16x8 v = ld_bf16x8(qimg + cl * D + 8 * (j ^ (cl % kRowChunks)));
+      bf16x8 o;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (__bf16)((float)v[e] * a.qscale);
+      *reinterpret_cast<bf16x8*>(qt + cl * qsd + 8 * j) = o;
+    }
+  } else if (own_k > 0) {
     bf16x8 qf[NK][2];
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch)
@@ -897,56 +913,84 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       lds_barrier();
     }
   }
-  // the latent accumulator of every rank tile -> LDS as bf16 [col][rank]
-  __bf16* olat = reinterpret_cast<__bf16*>(smem);
-  const int ols = bm.rv_pad + 8;
-  if (sg == 0) {
-#pragma unroll
-    for (int r = 0; r < MAX_RT; ++r)
-      if (r < own_v) {
-        const int rt = rg + ng * r;
-#pragma unroll
-        for (int ch = 0; ch < 2; ++ch)
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            bf16x4 v;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = (__bf16)oacc[r][ch][4 * jj + u];
-            *reinterpret_cast<bf16x4*>(olat + (32 * ch + lrow) * ols + 32 * rt + 8 * jj + 4 * lhi) = v;
-          }
-      }
-  }
-  lds_barrier();
-  // every wave: output dims [16 ds, 16 ds + 16) of its 16-column blocks, over
-  // all ranks (16x16x32 MFMAs: R^V fragment x latent columns from LDS)
   constexpr int NDS = D / 16;              // 16-dim slices
   constexpr int NCB = up_col_blocks<D>();  // 16-column blocks per wave
   const int ds = wave % NDS, cb0 = (wave / NDS) * NCB;
   f32x4 uacc[NCB];
-  {
-    // KV head (relative to g0) of this lane's output columns
-    int hu[NCB];
+  if (dense) {
+    // the value pass already produced the output: its accumulators (fp32,
+    // [col][dim]) through LDS into the up-projection's lane layout
+    float* of = reinterpret_cast<float*>(smem);
+    constexpr int ofs = D + 4;
+    if (sg == 0) {
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) hu[cb] = (c0 + min(16 * (cb0 + cb) + (lane & 15), cn - 1)) / N_g - g0;
-    const int nk = bm.rv_pad >> 5;
-    const __bf16* ob = olat + (16 * cb0 + (lane & 15)) * ols + 8 * (lane >> 4);
-    for (int hh = 0; hh < nh; ++hh) {
-      f32x4 t[NCB];
+      for (int r = 0; r < MAX_RT; ++r)
+        if (r < own_v) {
+          const int rt = rg + ng * r;
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) t[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      bf16x8 af = take();
-      for (int k = 0; k < nk; ++k) {
-        bf16x8 an = af;
-        if (k + 1 < nk) an = take();
+          for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) t[cb] = mfma16(af, ld_bf16x8(ob + 16 * cb * ols + 32 * k), t[cb]);
-        af = an;
-      }
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-        if (hh == 0 || hu[cb] == hh) uacc[cb] = t[cb];
+            for (int jj = 0; jj < 4; ++jj)
+              *reinterpret_cast<float4*>(of + (32 * ch + lrow) * ofs + 32 * rt + 8 * jj + 4 * lhi) =
+                  make_float4(oacc[r][ch][4 * jj], oacc[r][ch][4 * jj + 1], oacc[r][ch][4 * jj + 2],
+                              oacc[r][ch][4 * jj + 3]);
+        }
     }
-  }
+    lds_barrier();
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const float4 v = *reinterpret_cast<const float4*>(of + (16 * (cb0 + cb) + (lane & 15)) * ofs + 16 * ds +
+                                                        4 * (lane >> 4));
+      uacc[cb] = f32x4{v.x, v.y, v.z, v.w};
+    }
+  } else {
+    // the latent accumulator of every rank tile -> LDS as bf16 [col][rank]
+    __bf16* olat = reinterpret_cast<__bf16*>(smem);
+    const int ols = bm.rv_pad + 8;
+    if (sg == 0) {
+#pragma unroll
+      for (int r = 0; r < MAX_RT; ++r)
+        if (r < own_v) {
+          const int rt = rg + ng * r;
+#pragma unroll
+          for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              bf16x4 v;
+#pragma unroll
+              for (int u = 0; u < 4; ++u) v[u] = (__bf16)oacc[r][ch][4 * jj + u];
+              *reinterpret_cast<bf16x4*>(olat + (32 * ch + lrow) * ols + 32 * rt + 8 * jj + 4 * lhi) = v;
+            }
+        }
+    }
+    lds_barrier();
+    // every wave: output dims [16 ds, 16 ds + 16) of its 16-column blocks, over
+    // all ranks (16x16x32 MFMAs: R^V fragment x latent columns from LDS)
+    {
+      // KV head (relative to g0) of this lane's output columns
+      int hu[NCB];
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) hu[cb] = (c0 + min(16 * (cb0 + cb) + (lane & 15), cn - 1)) / N_g - g0;
+      const int nk = bm.rv_pad >> 5;
+      const __bf16* ob = olat + (16 * cb0 + (lane & 15)) * ols + 8 * (lane >> 4);
+      for (int hh = 0; hh < nh; ++hh) {
+        f32x4 t[NCB];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) t[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        bf16x8 af = take();
+        for (int k = 0; k < nk; ++k) {
+          bf16x8 an = af;
+          if (k + 1 < nk) an = take();
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) t[cb] = mfma16(af, ld_bf16x8(ob + 16 * cb * ols + 32 * k), t[cb]);
+          af = an;
+        }
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+          if (hh == 0 || hu[cb] == hh) uacc[cb] = t[cb];
+      }
+    }
+  }  // latent up-projection
   // the item's partial: per-column maximum m_run (score layout), sum (thread
   // tid < kCols: column tid), output uacc (up-projection layout)
   float l_item = 0.f;
@@ -1024,6 +1068,7 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   rd.gk = 0;
   rd.gb = 0;
   rd.rbuf = reinterpret_cast<int2*>(smem + (size_t)p.n_items * sizeof(WorkItem));
+  rd.recon_delta = a.recon_delta;
   if (wave == 0) {
     rd.derive(threadIdx.x & 63);
     rd.derive(threadIdx.x & 63);

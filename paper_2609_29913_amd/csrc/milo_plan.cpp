@@ -86,10 +86,14 @@ int gang_size(int n_ct) {
   return best >= 2 * pow2 ? best : pow2;
 }
 
-Tiling make_tiling(int n_kv, int N_g) {
+Tiling make_tiling(int n_kv, int N_g, bool head_tiles) {
   Tiling t;
   const int N = n_kv * N_g;
-  if (N_g < kCols) {
+  if (head_tiles) {
+    const int a = (N_g + kCols - 1) / kCols;
+    t.geom = TileGeom{kTileHead, a, N_g, N};
+    t.n_ct = n_kv * a;
+  } else if (N_g < kCols) {
     const int a = std::max(1, std::min(kMaxTileHeads, kCols / N_g));
     t.geom = TileGeom{kTilePacked, a, N_g, N};
     t.n_ct = (n_kv + a - 1) / a;
@@ -125,13 +129,22 @@ int max_owned(const BlockMeta& m) {
 bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q, int n_chunks, const Tiling& til,
                     int64_t program_cap, Schedule* out, std::string* err) {
   const int NK = c.d / 16;
-  auto item_cost = [&](const BlockMeta& m, int nt, int nh) {
+  const bool any_recon = c.recon_region && std::any_of(table, table + n_sel, [&](int b) { return c.recon_region[b] >= 0; });
+  if (any_recon && til.geom.mode != kTileHead) {
+    *err = "reconstructed blocks need one KV head per column tile";
+    return false;
+  }
+  auto is_dense = [&](int b) { return c.recon_region && c.recon_region[b] >= 0; };
+  // the metadata the kernel sees for block b (for a reconstructed block: its
+  // KV head 0; the other heads differ only in offsets)
+  auto item_meta = [&](int b) { return is_dense(b) ? dense_meta(c.meta[b], c.recon_region[b], 0, c.d) : c.meta[b]; };
+  auto item_cost = [&](const BlockMeta& m, int nt, int nh, bool dense) {
     const int nrt_k = m.rk_pad / 32, nks = m.rk_pad / 16, nrt_v = m.rv_pad / 32;
     const int nseg = v_segments(nrt_v), ng = kWaves / nseg;
     const int mk = (nrt_k + kWaves - 1) / kWaves, mv = (nrt_v + ng - 1) / ng;
     int rounds = 0;
     for (int h = nseg; h > 1; h /= 2) ++rounds;
-    const double item_frags = nh * ((double)NK * mk + m.rv_pad / 32.0);
+    const double item_frags = dense ? 0.0 : nh * ((double)NK * mk + m.rv_pad / 32.0);
     const double tile_frags = nt * ((double)nks + 16.0 / nseg * mv);
     return kCostFragItem * item_frags + kCostFragTile * tile_frags + kCostTile * nt + kCostItem +
            kCostSegRound * rounds;
@@ -146,8 +159,8 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
   out->gang = C;
   double total_blk = 0.0;
   for (int j = 0; j < n_sel; ++j) {
-    const BlockMeta& m = c.meta[table[j]];
-    for (int cg = 0; cg < n_cg; ++cg) total_blk += item_cost(m, m.T_pad / kTile, grp_nh[cg]);
+    const BlockMeta m = item_meta(table[j]);
+    for (int cg = 0; cg < n_cg; ++cg) total_blk += item_cost(m, m.T_pad / kTile, grp_nh[cg], is_dense(table[j]));
   }
   // tail items, numbered (request, KV head, chunk); solo workgroups take the
   // first n_solo_items, the rest run in bundles of C on the gangs
@@ -177,9 +190,10 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
     jobs.clear();
     for (int j = 0; j < n_sel; ++j) {
       const int b = table[j];
-      const BlockMeta& m = c.meta[b];
+      const BlockMeta m = item_meta(b);
       const int nt = m.T_pad / kTile;
-      const int np_cost = (int)std::min<double>(nt, std::max(1.0, std::ceil(item_cost(m, nt, 1) / target)));
+      const int np_cost =
+          (int)std::min<double>(nt, std::max(1.0, std::ceil(item_cost(m, nt, 1, is_dense(b)) / target)));
       const int np = std::max(np_cost, (nt + kMaxPartTiles - 1) / kMaxPartTiles);
       for (int p = 0; p < np; ++p) {
         const int t_a = (int)((int64_t)nt * p / np), t_b = (int)((int64_t)nt * (p + 1) / np);
@@ -188,7 +202,8 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
     }
     for (int p = 0; p < (int)parts.size(); ++p)
       for (int cg = 0; cg < n_cg; ++cg)
-        jobs.push_back({p, cg, 0, 0, item_cost(c.meta[parts[p].b], parts[p].ntile, grp_nh[cg])});
+        jobs.push_back(
+            {p, cg, 0, 0, item_cost(item_meta(parts[p].b), parts[p].ntile, grp_nh[cg], is_dense(parts[p].b))});
     for (int t0 = n_solo_items; t0 < n_tail; t0 += C) jobs.push_back({-1, 0, t0, std::min(C, n_tail - t0), kCostTail});
     std::stable_sort(jobs.begin(), jobs.end(), [](const Job& x, const Job& y) { return x.cost > y.cost; });
   };
@@ -260,9 +275,10 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
   const int n_parts = (int)parts.size();
   out->n_parts = n_parts;
   for (const Part& pt : parts) {
-    out->rk_pad_max = std::max(out->rk_pad_max, c.meta[pt.b].rk_pad);
-    out->rv_pad_max = std::max(out->rv_pad_max, c.meta[pt.b].rv_pad);
-    out->max_own = std::max(out->max_own, max_owned(c.meta[pt.b]));
+    const BlockMeta m = item_meta(pt.b);
+    out->rk_pad_max = std::max(out->rk_pad_max, m.rk_pad);
+    out->rv_pad_max = std::max(out->rv_pad_max, m.rv_pad);
+    out->max_own = std::max(out->max_own, max_owned(m));
   }
 
   // a workgroup folds consecutive block items of one column tile into one
@@ -345,7 +361,8 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
             const int tile = jb.cg * C + j;
             const Part& pt = parts[jb.part];
             WorkItem w{};
-            w.blk = c.meta[pt.b];
+            const bool dense = is_dense(pt.b);
+            w.blk = dense ? dense_meta(c.meta[pt.b], c.recon_region[pt.b], til.g0[tile], c.d) : c.meta[pt.b];
             w.kind = kItemBlock;
             w.g = til.g0[tile];
             w.sub = tile;
@@ -353,7 +370,8 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
             w.tile0 = pt.tile0;
             w.ntile = pt.ntile;
             w.flags = (lg_rank_groups(w.blk.rv_pad / 32) << kItemLgNgShift) | ((til.cn[tile] - 1) << kItemColsShift) |
-                      ((til.nh[tile] - 1) << kItemHeadsShift) | (c.p_int8 ? kItemInt8 : 0);
+                      ((til.nh[tile] - 1) << kItemHeadsShift) | (c.p_int8 ? kItemInt8 : 0) |
+                      (dense ? kItemDense : 0);
             items.push_back(w);
           }
           emit(l, wg, items);
@@ -393,6 +411,41 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
   }
   *err = "work schedule does not fit in LDS";
   return false;
+}
+
+void build_recon_plan(const BlockMeta* meta, const int32_t* table, int n_sel, const char* recon, int n_kv, int d,
+                      std::vector<int64_t>* region, ReconPlan* out) {
+  out->blocks.clear();
+  out->tasks.clear();
+  out->elems = 0;
+  const int D = n_kv * d;
+  std::vector<std::vector<int2>> queue(kXcds);
+  std::vector<double> load(kXcds, 0.0);
+  for (int j = 0; j < n_sel; ++j) {
+    const int b = table[j];
+    if (!recon[j]) continue;
+    const BlockMeta& m = meta[b];
+    ReconBlock rb{};
+    rb.src = m;
+    rb.dst = out->elems;
+    (*region)[b] = out->elems;
+    out->elems += 2 * (int64_t)m.T_pad * D;
+    const int i = (int)out->blocks.size();
+    out->blocks.push_back(rb);
+    // K, then V: each side's tasks (heads x tiles) on the least loaded XCD
+    for (int side = 0; side < 2; ++side) {
+      const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+      const int r_pad = side ? m.rv_pad : m.rk_pad;
+      for (int t = 0; t < m.T_pad / kTile; ++t)
+        for (int g = 0; g < n_kv; ++g) queue[x].push_back(make_int2(i, (t << 8) | (g << 1) | side));
+      load[x] += (double)(m.T_pad / kTile) * n_kv * (r_pad / 32 + 2);  // rank steps + epilogue
+    }
+  }
+  size_t longest = 0;
+  for (const auto& q : queue) longest = std::max(longest, q.size());
+  out->tasks.assign(longest * kXcds, make_int2(-1, 0));
+  for (int x = 0; x < kXcds; ++x)
+    for (size_t k = 0; k < queue[x].size(); ++k) out->tasks[k * kXcds + x] = queue[x][k];
 }
 
 }  // namespace milo

@@ -17,6 +17,10 @@ struct PlanInput {
   const BlockMeta* meta;  // [n_blocks]
   int n_kv, d;
   bool p_int8;            // P factors stored as INT8 codes (block items carry kItemInt8)
+  // reconstruct-then-attend: per block id, the element offset of its region in
+  // the reconstruction buffer, or -1 (latent); NULL: every block latent.  A plan
+  // with reconstructed blocks needs one KV head per column tile.
+  const int64_t* recon_region = nullptr;
 };
 
 struct Tiling {
@@ -26,7 +30,8 @@ struct Tiling {
 };
 
 int gang_size(int n_ct);
-Tiling make_tiling(int n_kv, int N_g);
+// head_tiles: one KV head per column tile (kTileHead), as dense items need
+Tiling make_tiling(int n_kv, int N_g, bool head_tiles = false);
 
 struct Schedule {
   std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs, then slot counts
@@ -38,6 +43,22 @@ struct Schedule {
 };
 
 int max_owned(const BlockMeta& m);
+
+// The reconstruction work of a plan: the reconstructed blocks of the table (in
+// table order) with their regions, and one task per (block, K or V, KV head,
+// 256-token tile), ordered so that all tasks of one block's K (or V) run on one
+// XCD (workgroup i runs on XCD i % 8; blocks dealt to the least loaded XCD),
+// where they share the block's P and R factors in that XCD's L2.  Padding
+// tasks (x = -1) fill the XCD queues to equal length.
+struct ReconPlan {
+  std::vector<ReconBlock> blocks;
+  std::vector<int2> tasks;
+  int64_t elems = 0;  // reconstruction buffer size (bf16 elements)
+};
+// Regions of the blocks table[0 .. n_sel) chosen by recon[j] != 0, laid out
+// consecutively; fills region[block id] (others -1) and the tasks.
+void build_recon_plan(const BlockMeta* meta, const int32_t* table, int n_sel, const char* recon, int n_kv, int d,
+                      std::vector<int64_t>* region, ReconPlan* out);
 
 // Build the plan for the selected blocks table[0 .. n_sel), n_q requests with
 // n_chunks planned tail chunks each, over the column tiles `til`.  program_cap

@@ -1,0 +1,217 @@
+// Full-rank reconstruction of selected blocks (Sec. 4.5 inference path, Alg. 1
+// full-rank reconstruction): K_b = P^K_b R^K_b and V_b = P^V_b R^V_b, one KV
+// head's d columns and one 256-token tile per workgroup, written as bf16 into
+// the reconstruction buffer in the fragment layouts the attention kernel reads
+// (P^K layout for K_{b,g}, P^V layout for V_{b,g}, both with rank d).
+//
+// A workgroup (8 waves) accumulates its 256 x d output tile over the block's
+// rank in steps of 32 with v_mfma_f32_32x32x16_bf16, fp32 accumulation: every
+// step stages the 256 x 32 slice of P and the 32 x d slice of R_g in LDS with
+// the rank index contiguous (the MFMA contraction runs over the rank).  The
+// cache stores P^K and R^V rank-contiguous already; P^V (token-contiguous, for
+// the latent value pass) and R^K (dim-contiguous, for the query projection)
+// are transposed on their way into LDS.  The next step's slices are loaded
+// into registers while the current step's MFMAs run (two LDS buffers).  Wave w
+// computes tokens 64 (w % 4) .. +63 times dims (d / 2)(w / 4) .. +d/2; for K
+// it forms K^T = R^T P^T, so a lane's accumulators hold consecutive dims of
+// one token and the tile goes to LDS as [token][dim], for V it forms P R,
+// giving consecutive tokens of one dim and an LDS tile [dim][token]; the
+// packed fragments are then stored with one 16-byte store per lane.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include "milo_internal.h"
+
+namespace milo {
+namespace {
+
+typedef __bf16 bf16x8r __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4r __attribute__((ext_vector_type(4)));
+typedef float f32x16r __attribute__((ext_vector_type(16)));
+
+constexpr int kReconThreads = 512;
+constexpr int kStageStride = 40;  // bf16 row stride of a staged 32-rank slice (+8: conflict-free reads)
+
+__device__ __forceinline__ f32x16r mfma32r(bf16x8r a, bf16x8r b, f32x16r c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// bytes of LDS the kernel uses for head dimension D
+constexpr size_t recon_lds_bytes(int D) {
+  const size_t stage = (size_t)2 * (kTile + D) * kStageStride * 2;
+  const size_t out_k = (size_t)kTile * (D + 8) * 2, out_v = (size_t)D * (kTile + 8) * 2;
+  const size_t out = out_k > out_v ? out_k : out_v;
+  return stage > out ? stage : out;
+}
+
+template <int D>
+__global__ __launch_bounds__(kReconThreads) void recon_kernel(ReconArgs a) {
+  static_assert(D == 64 || D == 128, "head dimension");
+  constexpr int NJ = D / 64;  // 32-column blocks of a wave's d / 2 dims
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int2 task = a.tasks[blockIdx.x];
+  if (task.x < 0) return;
+  const ReconBlock rb = a.blocks[task.x];
+  const BlockMeta& bm = rb.src;
+  const int side = task.y & 1, g = (task.y >> 1) & 127, t = task.y >> 8;
+  const int nrt = (side ? bm.rv_pad : bm.rk_pad) >> 5;  // 32-rank steps
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lrow = lane & 31, lhi = lane >> 5;
+  const unsigned char* data = reinterpret_cast<const unsigned char*>(a.data);
+  __bf16* sA = reinterpret_cast<__bf16*>(smem);      // [2][kTile][kStageStride]: P slice [token][rank]
+  __bf16* sB = sA + 2 * kTile * kStageStride;         // [2][D][kStageStride]: R_g slice [dim][rank]
+
+  // global -> registers for 32-rank step kc: two P chunks and (threads < 4 D) one R chunk
+  uint4 pa[2], rbv;
+  auto load = [&](int kc) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = tid + kReconThreads * h, f = q >> 6, ln = q & 63;
+      const int64_t frag = side ? pv_frag(bm, 16 * t + f, kc) : pk_frag(bm, kWaves * t + (f >> 1), 2 * kc + (f & 1));
+      pa[h] = *reinterpret_cast<const uint4*>(data + frag * (kFragElems * 2) + 16 * ln);
+    }
+    if (tid < 4 * D) {
+      const int f = tid >> 6, ln = tid & 63;
+      const int64_t frag = side ? rv_frag(bm, D, g, f, kc) : rk_frag(bm, D, g, kc, f);
+      rbv = *reinterpret_cast<const uint4*>(data + frag * (kFragElems * 2) + 16 * ln);
+    }
+  };
+  // registers -> LDS buffer `buf` (rank contiguous)
+  auto stage = [&](int buf) {
+    __bf16* A = sA + buf * kTile * kStageStride;
+    __bf16* B = sB + buf * D * kStageStride;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = tid + kReconThreads * h, f = q >> 6, ln = q & 63, m = ln & 31, c = ln >> 5;
+      if (side == 0) {
+        // P^K: lane (c, m) holds ranks 16 kap + 8 c .. +7 of token 32 tau + m
+        *reinterpret_cast<uint4*>(A + (32 * (f >> 1) + m) * kStageStride + 16 * (f & 1) + 8 * c) = pa[h];
+      } else {
+        // P^V: lane (c, m) holds tokens 16 sig + 8 c .. +7 of rank 32 rho + m
+        const __bf16* v = reinterpret_cast<const __bf16*>(&pa[h]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) A[(16 * f + 8 * c + e) * kStageStride + m] = v[e];
+      }
+    }
+    if (tid < 4 * D) {
+      const int f = tid >> 6, ln = tid & 63;
+      if (side == 0) {
+        // R^K: lane (c, m) holds dims 16 kap + 8 c .. +7 (of head g) at rank 32 rho + m
+        const int m = ln & 31, c = ln >> 5;
+        const __bf16* v = reinterpret_cast<const __bf16*>(&rbv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) B[(16 * f + 8 * c + e) * kStageStride + m] = v[e];
+      } else {
+        // R^V: lane 16 qq + n holds ranks 32 kap + 8 qq .. +7 at dim 16 ds + n
+        const int n = ln & 15, qq = ln >> 4;
+        *reinterpret_cast<uint4*>(B + (16 * f + n) * kStageStride + 8 * qq) = rbv;
+      }
+    }
+  };
+
+  const int wt = wave & 3, wd = wave >> 2;
+  f32x16r acc[2][NJ];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16r{};
+  load(0);
+  stage(0);
+  __syncthreads();
+  for (int kc = 0; kc < nrt; ++kc) {
+    const int buf = kc & 1;
+    if (kc + 1 < nrt) load(kc + 1);
+    const __bf16* A = sA + buf * kTile * kStageStride;
+    const __bf16* B = sB + buf * D * kStageStride;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8r af[2], bfr[NJ];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const bf16x8r*>(A + (32 * (2 * wt + i) + lrow) * kStageStride + 16 * kk + 8 * lhi);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8r*>(B + ((D / 2) * wd + 32 * j + lrow) * kStageStride + 16 * kk +
+                                                   8 * lhi);
+      if (side == 0) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32r(bfr[j], af[i], acc[i][j]);  // K^T: [dim][token]
+      } else {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32r(af[i], bfr[j], acc[i][j]);  // V: [token][dim]
+      }
+    }
+    if (kc + 1 < nrt) stage(buf ^ 1);  // the other buffer: its last readers passed the previous barrier
+    __syncthreads();
+  }
+
+  // the tile as bf16 in LDS (all staging reads are done: the loop ended on a barrier)
+  __bf16* O = reinterpret_cast<__bf16*>(smem);
+  constexpr int kOK = D + 8, kOV = kTile + 8;  // row strides: K [token][dim], V [dim][token]
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        bf16x4r v;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = (__bf16)acc[i][j][4 * jj + u];
+        const int tok_blk = 32 * (2 * wt + i), dim_blk = (D / 2) * wd + 32 * j;
+        if (side == 0)  // rows: dims 8 jj + 4 lhi + u of the block, column: token lrow
+          *reinterpret_cast<bf16x4r*>(O + (tok_blk + lrow) * kOK + dim_blk + 8 * jj + 4 * lhi) = v;
+        else  // rows: tokens 8 jj + 4 lhi + u, column: dim lrow
+          *reinterpret_cast<bf16x4r*>(O + (dim_blk + lrow) * kOV + tok_blk + 8 * jj + 4 * lhi) = v;
+      }
+  __syncthreads();
+
+  // packed stores: 32 D chunks of 16 bytes (8 D / 16 ... fragments of 64 lanes)
+  const BlockMeta dm = dense_meta(bm, rb.dst, g, D);
+  unsigned char* out = reinterpret_cast<unsigned char*>(a.recon);
+  for (int q = tid; q < 32 * D; q += kReconThreads) {
+    const int f = q >> 6, ln = q & 63, m = ln & 31, c = ln >> 5;
+    int64_t frag;
+    uint4 v;
+    if (side == 0) {
+      // K_{b,g} in the P^K layout: fragment (tau = 8 t + w, kap), lane (c, m) = dims 16 kap + 8 c .. +7 of token 32 w + m
+      const int w = f / (D / 16), kap = f % (D / 16);
+      frag = pk_frag(dm, kWaves * t + w, kap);
+      v = *reinterpret_cast<const uint4*>(O + (32 * w + m) * kOK + 16 * kap + 8 * c);
+    } else {
+      // V_{b,g} in the P^V layout: fragment (sig = 16 t + s, rho), lane (c, m) = tokens 16 s + 8 c .. +7 of dim 32 rho + m
+      const int s = f / (D / 32), rho = f % (D / 32);
+      frag = pv_frag(dm, 16 * t + s, rho);
+      v = *reinterpret_cast<const uint4*>(O + (32 * rho + m) * kOV + 16 * s + 8 * c);
+    }
+    *reinterpret_cast<uint4*>(out + frag * (kFragElems * 2) + 16 * ln) = v;
+  }
+}
+
+template <int D>
+hipError_t launch_recon_t(const ReconArgs& a, int n_tasks, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const size_t lds = recon_lds_bytes(D);
+  static bool attr_set = false;
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&recon_kernel<D>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipExtLaunchKernelGGL(recon_kernel<D>, dim3(n_tasks), dim3(kReconThreads), (uint32_t)lds, s, e0, e1, 0, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_recon(const ReconArgs& a, int head_dim, int n_tasks, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (n_tasks <= 0) return hipSuccess;
+  if (head_dim == 64) return launch_recon_t<64>(a, n_tasks, s, e0, e1);
+  if (head_dim == 128) return launch_recon_t<128>(a, n_tasks, s, e0, e1);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace milo

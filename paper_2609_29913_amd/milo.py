@@ -26,6 +26,9 @@ _c_u16p = ctypes.POINTER(ctypes.c_uint16)
 
 MILO_P_BF16 = 0
 MILO_P_INT8 = 1
+MILO_PATH_LATENT = 0
+MILO_PATH_RECONSTRUCT = 1
+MILO_PATH_AUTO = 2
 
 
 class milo_cache_desc(ctypes.Structure):
@@ -98,6 +101,12 @@ def lib() -> ctypes.CDLL:
         L.milo_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(ctypes.c_int64)]
         L.milo_timing_read.restype = ctypes.c_int
+        L.milo_timing_read_recon.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
+        L.milo_timing_read_recon.restype = ctypes.c_int
+        L.milo_cache_set_path.argtypes = [vp, ctypes.c_int32]
+        L.milo_cache_set_path.restype = ctypes.c_int
+        L.milo_cache_recon_blocks.argtypes = [vp, _c_i32p]
+        L.milo_cache_recon_blocks.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -404,6 +413,25 @@ def milo_cache_read_int8(cache: int, block: int, which: int, shape):
     scales = np.zeros(shape[0], dtype=np.float32)
     _check(lib().milo_cache_read_int8(ctypes.c_void_p(cache), block, which, codes.ctypes.data, scales.ctypes.data))
     return codes, scales
+
+
+def milo_cache_set_path(cache: int, path: int) -> None:
+    """MILO_PATH_LATENT, MILO_PATH_RECONSTRUCT or MILO_PATH_AUTO (Sec. 4.5 inference path)."""
+    _check(lib().milo_cache_set_path(ctypes.c_void_p(cache), int(path)))
+
+
+def milo_cache_recon_blocks(cache: int) -> int:
+    """Blocks the plan of the cache's last attention call reconstructs."""
+    v = ctypes.c_int32()
+    _check(lib().milo_cache_recon_blocks(ctypes.c_void_p(cache), ctypes.byref(v)))
+    return v.value
+
+
+def milo_timing_read_recon():
+    """(reconstruction kernel ms, number of calls) since the last read."""
+    t, n = ctypes.c_double(), ctypes.c_int64()
+    _check(lib().milo_timing_read_recon(ctypes.byref(t), ctypes.byref(n)))
+    return t.value, n.value
 
 
 def milo_cache_plan_builds(cache: int) -> int:

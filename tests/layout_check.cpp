@@ -51,6 +51,29 @@ static int check(int kind, int T, int r, int n_kv, int d) {
       std::printf("kind %d: element (%zu, %zu) produced %d times\n", kind, k / pcol, k % pcol, seen[k]);
       return 1;
     }
+  // the fragment index helpers (pk_frag, pv_frag, rk_frag, rv_frag) invert
+  // frag_source: the coordinates of a fragment's lane 0, element 0 lead back to it
+  BlockMeta bm{};
+  bm.T = T;
+  bm.T_pad = T_pad;
+  bm.rk_pad = r_pad;
+  bm.rv_pad = r_pad;
+  for (long long fr = 0; fr < nf; ++fr) {
+    int row, col;
+    frag_source(f, fr, 0, 0, &row, &col);
+    long long back;
+    switch (kind) {
+      case kPK: back = pk_frag(bm, row / 32, col / 16); break;
+      case kPV: back = pv_frag(bm, row / 16, col / 32); break;
+      case kRK: back = rk_frag(bm, d, col / d, row / 32, (col % d) / 16); break;
+      default: back = rv_frag(bm, d, col / d, (col % d) / 16, row / 32); break;
+    }
+    if (back != fr) {
+      std::printf("kind %d: fragment %lld starts at (%d, %d), whose index helper gives %lld\n", kind, fr, row, col,
+                  back);
+      return 1;
+    }
+  }
   return 0;
 }
 
@@ -187,7 +210,116 @@ static int check_runs_i8(int T, int rk, int rv, int n_kv, int d) {
   return 0;
 }
 
+// Reconstructed blocks (dense items): for every KV head, the reconstruction
+// kernel's stores (K_{b,g} as fragments (tau = 8 t + w, kap) holding dims
+// 16 kap + 8 c + e of token 32 tau + m, V_{b,g} as fragments (sig = 16 t + s,
+// rho) holding tokens 16 sig + 8 c + e of dim 32 rho + m) put every element of
+// the head's region where frag_source says the P^K / P^V layouts of rank d
+// keep it, each fragment exactly once; and the runs the eight waves derive for
+// a dense item (offset by frag_base fragments) read each of those fragments
+// once and nothing else (no R^K or R^V runs).
+static int check_dense(int T, int n_kv, int d) {
+  const int T_pad = (T + kTile - 1) / kTile * kTile, ntile = T_pad / kTile;
+  BlockMeta src{};
+  src.T = T;
+  src.T_pad = T_pad;
+  const int64_t region = 3 * (int64_t)kFragElems * 7;  // some region start (whole fragments)
+  const int frag_base = -5;                            // buffer distance, in fragments
+  const long long per_side = (long long)T_pad * d / kFragElems;
+  for (int g = 0; g < n_kv; ++g) {
+    const BlockMeta dm = dense_meta(src, region, g, d);
+    const long long k0 = dm.off_pk / kFragElems, v0 = dm.off_pv / kFragElems;
+    if (dm.off_pk % kFragElems || dm.off_pv != dm.off_pk + per_side * kFragElems ||
+        dm.off_pk != region + 2LL * g * per_side * kFragElems) {
+      std::printf("dense: head %d region offsets\n", g);
+      return 1;
+    }
+    FactorGeom fk{}, fv{};
+    fk.kind = kPK;
+    fk.T_pad = T_pad;
+    fk.r_pad = d;
+    fv.kind = kPV;
+    fv.T_pad = T_pad;
+    fv.r_pad = d;
+    std::vector<int> wk(per_side, 0), wv(per_side, 0);
+    for (int t = 0; t < ntile; ++t)
+      for (int f = 0; f < d / 2; ++f) {
+        // K side store f: w = f / (d / 16), kap = f % (d / 16)
+        {
+          const int w = f / (d / 16), kap = f % (d / 16);
+          const long long fr = pk_frag(dm, kWaves * t + w, kap) - k0;
+          if (fr < 0 || fr >= per_side) { std::printf("dense: K store outside the region\n"); return 1; }
+          wk[fr]++;
+          for (int lane = 0; lane < 64; lane += 37)
+            for (int e = 0; e < 8; e += 7) {
+              int row, col;
+              frag_source(fk, fr, lane, e, &row, &col);
+              if (row != 32 * (kWaves * t + w) + (lane & 31) || col != 16 * kap + 8 * (lane >> 5) + e) {
+                std::printf("dense: K fragment %lld lane %d e %d holds (%d, %d)\n", fr, lane, e, row, col);
+                return 1;
+              }
+            }
+        }
+        // V side store f: s = f / (d / 32), rho = f % (d / 32)
+        {
+          const int sx = f / (d / 32), rho = f % (d / 32);
+          const long long fr = pv_frag(dm, 16 * t + sx, rho) - v0;
+          if (fr < 0 || fr >= per_side) { std::printf("dense: V store outside the region\n"); return 1; }
+          wv[fr]++;
+          for (int lane = 0; lane < 64; lane += 37)
+            for (int e = 0; e < 8; e += 7) {
+              int row, col;
+              frag_source(fv, fr, lane, e, &row, &col);
+              if (row != 16 * (16 * t + sx) + 8 * (lane >> 5) + e || col != 32 * rho + (lane & 31)) {
+                std::printf("dense: V fragment %lld lane %d e %d holds (%d, %d)\n", fr, lane, e, row, col);
+                return 1;
+              }
+            }
+        }
+      }
+    for (long long k = 0; k < per_side; ++k)
+      if (wk[k] != 1 || wv[k] != 1) {
+        std::printf("dense: head %d fragment %lld stored %d / %d times\n", g, k, wk[k], wv[k]);
+        return 1;
+      }
+    // the runs of a dense item over the whole block
+    std::vector<int> rk_seen(per_side, 0), rv_seen(per_side, 0);
+    for (int w = 0; w < kWaves; ++w) {
+      int n_runs = 0;
+      bool bad = false;
+      block_runs(dm, g, 1, 0, ntile, w, d, lg_rank_groups(d / 32), false, [&](int x, int n) {
+        ++n_runs;
+        for (int k = 0; k < n; ++k) {
+          const long long fr = (long long)x + k - frag_base;
+          if (fr >= k0 && fr < k0 + per_side) rk_seen[fr - k0]++;
+          else if (fr >= v0 && fr < v0 + per_side) rv_seen[fr - v0]++;
+          else bad = true;
+        }
+      }, true, frag_base);
+      if (bad || n_runs > 2 * ntile) {
+        std::printf("dense: wave %d runs leave the head's region (%d runs)\n", w, n_runs);
+        return 1;
+      }
+    }
+    for (long long k = 0; k < per_side; ++k)
+      if (rk_seen[k] != 1 || rv_seen[k] != 1) {
+        std::printf("dense: head %d fragment %lld read %d / %d times\n", g, k, rk_seen[k], rv_seen[k]);
+        return 1;
+      }
+  }
+  return 0;
+}
+
 int main(int argc, char** argv) {
+  if (argc > 1 && std::string(argv[1]) == "--dense") {
+    int bad = 0, n = 0;
+    for (int i = 2; i + 2 < argc; i += 3) {
+      bad |= check_dense(std::atoi(argv[i]), std::atoi(argv[i + 1]), std::atoi(argv[i + 2]));
+      ++n;
+    }
+    std::printf("%s (%d geometries)\n", bad ? "FAIL" : "OK", n);
+    return bad;
+  }
   // argv: groups of (T, r, n_kv, d); with --runs first: groups of (T, rk, rv, n_kv, d)
   if (argc > 1 && (std::string(argv[1]) == "--runs" || std::string(argv[1]) == "--runs-int8")) {
     const bool i8 = std::string(argv[1]) == "--runs-int8";

@@ -13,13 +13,20 @@
 //    slot; slots of a tile are numbered densely from 0 and the plan's slot count
 //    of every tile says how many (folding only where the kernel folds);
 //  - every program fits the LDS region the plan reserves for it.
+//  - reconstructed blocks (recon 1: every selected block, 2: every other one):
+//    their items are dense items naming the tile's KV head in the block's
+//    region, per-head column tiles; the reconstruction tasks cover every
+//    (block, K or V, KV head, 256-token tile) exactly once, each block side's
+//    tasks on one XCD, and the regions lie back to back.
 // Case format (whitespace separated):
-//   n_kv d G n_q n_chunks program_cap int8 n_blocks  (T rk rv) x n_blocks  n_sel  table...
+//   n_kv d G n_q n_chunks program_cap int8 recon n_blocks  (T rk rv) x n_blocks  n_sel  table...
 #include <cstdio>
 #include <cstring>
 #include <map>
 #include <set>
 #include <string>
+#include <tuple>
+#include <algorithm>
 #include <vector>
 
 #include "milo_plan.h"
@@ -39,7 +46,7 @@ static int fails = 0;
   } while (0)
 
 static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks, long long program_cap, int i8,
-                     const std::vector<int>& T, const std::vector<int>& rk, const std::vector<int>& rv,
+                     int recon_mode, const std::vector<int>& T, const std::vector<int>& rk, const std::vector<int>& rv,
                      const std::vector<int>& table) {
   const int nb = (int)T.size();
   std::vector<BlockMeta> meta(nb);
@@ -61,7 +68,51 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
     off += (int64_t)m.rv_pad * D;
   }
   const int N_g = n_q * G, N = n_kv * N_g;
-  const Tiling til = make_tiling(n_kv, N_g);
+  // reconstructed blocks
+  std::vector<char> recon(table.size(), 0);
+  for (size_t j = 0; j < table.size(); ++j) recon[j] = recon_mode == 1 || (recon_mode == 2 && j % 2 == 0);
+  const bool any_recon = std::any_of(recon.begin(), recon.end(), [](char x) { return x != 0; });
+  std::vector<int64_t> region(nb, -1);
+  ReconPlan rp;
+  if (any_recon) build_recon_plan(meta.data(), table.data(), (int)table.size(), recon.data(), n_kv, d, &region, &rp);
+  {
+    const int D = n_kv * d;
+    int64_t next = 0;
+    std::map<std::tuple<int, int, int, int>, int> task_seen;
+    std::map<std::pair<int, int>, int> xcd_of;  // (recon block, side) -> XCD
+    int i = 0;
+    for (size_t j = 0; j < table.size(); ++j) {
+      const int b = table[j];
+      if (!recon[j]) {
+        CHECK(region[b] == -1, "latent block %d has a region", b);
+        continue;
+      }
+      CHECK(region[b] == next && rp.blocks[i].dst == next, "block %d region %lld, expected %lld", b,
+            (long long)region[b], (long long)next);
+      CHECK(std::memcmp(&rp.blocks[i].src, &meta[b], sizeof(BlockMeta)) == 0, "reconstruction block %d metadata", i);
+      next += 2LL * meta[b].T_pad * D;
+      ++i;
+    }
+    CHECK(i == (int)rp.blocks.size() && rp.elems == next, "reconstruction blocks / buffer size");
+    CHECK(rp.tasks.size() % kXcds == 0, "task count not a multiple of the XCDs");
+    for (size_t k = 0; k < rp.tasks.size(); ++k) {
+      const int2 tk = rp.tasks[k];
+      if (tk.x < 0) continue;
+      CHECK(tk.x < (int)rp.blocks.size(), "task %zu block %d", k, tk.x);
+      const int side = tk.y & 1, g = (tk.y >> 1) & 127, t = tk.y >> 8;
+      CHECK(g < n_kv && t < rp.blocks[tk.x].src.T_pad / kTile, "task %zu out of range", k);
+      const int seen_now = ++task_seen[std::make_tuple(tk.x, side, g, t)];
+      CHECK(seen_now == 1, "task %zu repeated", k);
+      auto it = xcd_of.find({tk.x, side});
+      if (it == xcd_of.end()) xcd_of[{tk.x, side}] = (int)(k % kXcds);
+      else CHECK(it->second == (int)(k % kXcds), "block %d side %d spread over XCDs", tk.x, side);
+    }
+    size_t want = 0;
+    for (const ReconBlock& r : rp.blocks) want += 2 * (size_t)n_kv * (r.src.T_pad / kTile);
+    CHECK(task_seen.size() == want, "%zu tasks, want %zu", task_seen.size(), want);
+  }
+  const Tiling til = make_tiling(n_kv, N_g, any_recon);
+  if (any_recon) CHECK(til.geom.mode == kTileHead, "reconstructed blocks without per-head tiles");
   // tiles partition the columns; tile_of agrees with tile_range
   {
     int next = 0;
@@ -77,8 +128,9 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
   }
   Schedule sch;
   std::string err;
-  if (!build_schedule(PlanInput{meta.data(), n_kv, d, i8 != 0}, table.data(), (int)table.size(), n_q, n_chunks, til,
-                      program_cap, &sch, &err)) {
+  PlanInput pin{meta.data(), n_kv, d, i8 != 0};
+  pin.recon_region = any_recon ? region.data() : nullptr;
+  if (!build_schedule(pin, table.data(), (int)table.size(), n_q, n_chunks, til, program_cap, &sch, &err)) {
     CHECK(false, "plan failed: %s", err.c_str());
   }
   const bool fold = sch.max_own <= 2;
@@ -117,22 +169,55 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
       CHECK(w.req == til.c0[k] && w.g == til.g0[k], "block item tile fields");
       CHECK(((w.flags >> kItemColsShift) & 63) + 1 == til.cn[k], "block item column count");
       CHECK(((w.flags >> kItemHeadsShift) & 7) + 1 == til.nh[k], "block item head count");
+      const bool dense = (w.flags & kItemDense) != 0;
       int b = -1;
-      for (int x = 0; x < nb; ++x)
-        if (meta[x].off_pk == w.blk.off_pk) b = x;
-      CHECK(b >= 0 && std::memcmp(&meta[b], &w.blk, sizeof(BlockMeta)) == 0, "block item metadata");
-      CHECK(((w.flags >> kItemLgNgShift) & 3) == lg_rank_groups(meta[b].rv_pad / 32), "rank groups field");
+      if (dense) {
+        for (int x = 0; x < nb; ++x)
+          if (region[x] >= 0 && w.blk.off_pk >= region[x] && w.blk.off_pk < region[x] + 2LL * meta[x].T_pad * n_kv * d)
+            b = x;
+        CHECK(b >= 0, "dense item outside every region");
+        const BlockMeta want = dense_meta(meta[b], region[b], til.g0[k], d);
+        CHECK(std::memcmp(&want, &w.blk, sizeof(BlockMeta)) == 0 && til.nh[k] == 1, "dense item metadata");
+      } else {
+        for (int x = 0; x < nb; ++x)
+          if (meta[x].off_pk == w.blk.off_pk) b = x;
+        CHECK(b >= 0 && std::memcmp(&meta[b], &w.blk, sizeof(BlockMeta)) == 0, "block item metadata");
+        CHECK(region[b] < 0, "block %d is reconstructed but has a latent item", b);
+      }
+      CHECK(((w.flags >> kItemLgNgShift) & 3) == lg_rank_groups(w.blk.rv_pad / 32), "rank groups field");
       CHECK(((w.flags & kItemInt8) != 0) == (i8 != 0), "INT8 flag");
       CHECK(w.ntile >= 1 && w.ntile <= kMaxPartTiles && w.tile0 >= 0 && w.tile0 + w.ntile <= meta[b].T_pad / kTile,
             "block item tile range");
+      CHECK(!dense || !i8, "dense item in an INT8 plan");
       auto it = cover.find({b, k});
       CHECK(it != cover.end(), "block %d is not selected", b);
       for (int t = w.tile0; t < w.tile0 + w.ntile; ++t) it->second[t]++;
+      // the runs of every wave, derived as the kernel does with a distance to
+      // the reconstruction buffer: a dense item's fragments lie in its head's
+      // region (shifted by that distance), any other item's in its own block's
+      // factors (bf16 fragments; INT8 runs count 512-byte units)
+      const int kDelta = 1 << 24;
+      int64_t lo, hi;  // element range of the item's fragments
+      if (dense) {
+        lo = w.blk.off_pk + (int64_t)kDelta * kFragElems;
+        hi = lo + 2LL * w.blk.T_pad * d;
+      } else {
+        lo = std::min({meta[b].off_pk, meta[b].off_rk, meta[b].off_pv, meta[b].off_rv});
+        hi = meta[b].off_rv + (int64_t)meta[b].rv_pad * n_kv * d;
+      }
       for (int wave = 0; wave < kWaves; ++wave) {
         int runs = 0;
-        block_runs(w.blk, w.g, til.nh[k], w.tile0, w.ntile, wave, d, lg_rank_groups(meta[b].rv_pad / 32),
-                   (w.flags & kItemInt8) != 0, [&](int, int) { ++runs; });
+        bool outside = false;
+        block_runs(w.blk, w.g, til.nh[k], w.tile0, w.ntile, wave, d, lg_rank_groups(w.blk.rv_pad / 32),
+                   (w.flags & kItemInt8) != 0, [&](int x, int n) {
+                     ++runs;
+                     const int kind = (n >> kRunKindShift) & 3, cnt = n & kRunCountMask;
+                     if (kind == kRunScale) return;  // scale units: checked by the layout tests
+                     const int64_t unit = kind == kRunI8 ? kFragElems / 2 : kFragElems;  // elements per unit index
+                     if ((int64_t)x * unit < lo || ((int64_t)x + cnt) * unit > hi) outside = true;
+                   }, dense, kDelta);
         CHECK(runs <= kRunCap - 1, "%d runs exceed the run buffer", runs);
+        CHECK(!outside, "%s item: wave %d reads outside its block", dense ? "dense" : "latent", wave);
       }
       // slot groups
       const bool first = (w.flags & kItemFirst) != 0, flush = (w.flags & kItemFlush) != 0;
@@ -174,9 +259,9 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
 
 int main() {
   int case_no = 0;
-  int n_kv, d, G, n_q, n_chunks, nb, i8;
+  int n_kv, d, G, n_q, n_chunks, nb, i8, rc;
   long long cap;
-  while (std::scanf("%d %d %d %d %d %lld %d %d", &n_kv, &d, &G, &n_q, &n_chunks, &cap, &i8, &nb) == 8) {
+  while (std::scanf("%d %d %d %d %d %lld %d %d %d", &n_kv, &d, &G, &n_q, &n_chunks, &cap, &i8, &rc, &nb) == 9) {
     std::vector<int> T(nb), rk(nb), rv(nb);
     for (int b = 0; b < nb; ++b)
       if (std::scanf("%d %d %d", &T[b], &rk[b], &rv[b]) != 3) return 2;
@@ -185,7 +270,7 @@ int main() {
     std::vector<int> table(n_sel);
     for (int j = 0; j < n_sel; ++j)
       if (std::scanf("%d", &table[j]) != 1) return 2;
-    run_case(case_no++, n_kv, d, G, n_q, n_chunks, cap, i8, T, rk, rv, table);
+    run_case(case_no++, n_kv, d, G, n_q, n_chunks, cap, i8, rc, T, rk, rv, table);
   }
   std::printf("%s (%d cases)\n", fails ? "FAIL" : "OK", case_no);
   return fails ? 1 : 0;

@@ -1,0 +1,216 @@
+"""Reconstruct-then-attend (milo_cache_set_path) on the GPU, through the C ABI,
+against the CPU oracle on the same seeded inputs.  The route differs, the
+attention does not: every check uses the latent parity bar (max over (query,
+head) of the relative L2 error <= 1e-2); the rebuilt K and V are rounded to
+bf16 once, as the latent route rounds the projected query and latent output.
+
+Covered: every selected block rebuilt (the shapes of the latent parity suite:
+ragged blocks, ranks up to 896, d = 64 / 128, 1..16 query heads per KV head,
+tails ragged and empty, column counts per KV head below and above 64), the
+cost model mixing both routes in one plan, switching routes on one cache,
+growing tails, prefill, a full 14B-shaped layer, and the entry points that
+cannot rebuild (no-allocation decode, INT8 caches)."""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from helpers import TOL_REL_L2, GpuLayer, col_rel_l2, max_rel_l2, oracle_args, to_device
+from test_gpu_parity import PREFILL, SHAPES, _full_size_columns, _random_case
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_29913_amd import milo
+    milo.lib()
+
+
+def _run(inp, path, table=None, tail_len=None, label=""):
+    from paper_2609_29913_amd import milo
+    gl = GpuLayer(inp)
+    try:
+        milo.milo_cache_set_path(gl.cache, path)
+        got = gl.attend(table, tail_len).cpu().numpy()
+        n_rec = milo.milo_cache_recon_blocks(gl.cache)
+    finally:
+        gl.free()
+    assert np.all(np.isfinite(got)), "unwritten or non-finite outputs"
+    ref = oracle.attend_latent(**oracle_args(inp, table, tail_len))
+    err = max_rel_l2(got, ref)
+    print(f"[recon] {label}: {n_rec} blocks rebuilt, max rel-L2 = {err:.3e}", flush=True)
+    assert err <= TOL_REL_L2
+    return got, n_rec
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_reconstruct_every_block(name):
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(zlib.crc32(name.encode()) % 1000, **SHAPES[name])
+    _, n_rec = _run(inp, milo.MILO_PATH_RECONSTRUCT, label=name)
+    assert n_rec == inp.n_blocks
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_reconstruct_random_shapes(seed):
+    from paper_2609_29913_amd import milo
+    inp, table = _random_case(seed)
+    if max(max(inp.rank_k), max(inp.rank_v)) > 896:
+        pytest.skip("rank above the supported maximum")
+    _, n_rec = _run(inp, milo.MILO_PATH_RECONSTRUCT, table=table, label=f"random seed {seed}")
+    assert n_rec == len(table)
+
+
+def _mixed_problem():
+    # 7B-shaped heads (896 columns): high-rank blocks pay for reconstruction, low-rank ones do not
+    return synth.make_problem(77, [1024, 1024, 700, 1024, 300, 1024], [512, 64, 448, 96, 160, 480],
+                              [512, 64, 448, 128, 96, 512], n_kv_heads=4, head_dim=128, n_q=32, n_q_heads=28,
+                              tail_cap=300)
+
+
+def test_auto_mixes_both_routes_in_one_plan():
+    from paper_2609_29913_amd import milo
+    inp = _mixed_problem()
+    _, n_rec = _run(inp, milo.MILO_PATH_AUTO, label="auto, 7B heads, mixed ranks")
+    assert 0 < n_rec < inp.n_blocks
+
+
+def test_routes_switch_on_one_cache():
+    """LATENT, RECONSTRUCT, AUTO and LATENT again on one cache: each call
+    rebuilds its plan, and all agree with the oracle."""
+    from paper_2609_29913_amd import milo
+    inp = _mixed_problem()
+    ref = oracle.attend_latent(**oracle_args(inp))
+    gl = GpuLayer(inp)
+    try:
+        outs, recs = [], []
+        for path in (milo.MILO_PATH_LATENT, milo.MILO_PATH_RECONSTRUCT, milo.MILO_PATH_AUTO, milo.MILO_PATH_LATENT):
+            milo.milo_cache_set_path(gl.cache, path)
+            outs.append(gl.attend().cpu().numpy())
+            recs.append(milo.milo_cache_recon_blocks(gl.cache))
+        builds = milo.milo_cache_plan_builds(gl.cache)
+    finally:
+        gl.free()
+    print(f"[recon] route switch: rebuilt blocks per call {recs}, {builds} plans", flush=True)
+    assert recs[0] == 0 and recs[1] == inp.n_blocks and 0 < recs[2] < inp.n_blocks and recs[3] == 0
+    assert builds == 4
+    for o in outs:
+        assert max_rel_l2(o, ref) <= TOL_REL_L2
+    assert np.array_equal(outs[0], outs[3])
+
+
+def test_reconstruct_with_growing_tails_and_subsets():
+    """Tails growing by a token per call reuse the plan; a block subset in
+    another order rebuilds it; results stay at the bar and repeat bitwise."""
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(31, [1024, 512, 300], [256, 128, 200], n_kv_heads=2, head_dim=128, n_q=4,
+                             n_q_heads=14, tail_cap=300, tail_len=[100, 0, 255, 257])
+    gl = GpuLayer(inp)
+    try:
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_RECONSTRUCT)
+        lens = np.array([100, 0, 255, 257], dtype=np.int32)
+        for step in range(3):
+            got = gl.attend(tail_len=lens).cpu().numpy()
+            err = max_rel_l2(got, oracle.attend_latent(**oracle_args(inp, tail_len=lens)))
+            assert err <= TOL_REL_L2, (step, err)
+            lens = np.minimum(lens + 1, 300)
+        assert milo.milo_cache_plan_builds(gl.cache) == 1
+        table = [2, 0]
+        a = gl.attend(table=table, tail_len=lens).cpu().numpy()
+        b = gl.attend(table=table, tail_len=lens).cpu().numpy()
+        assert np.array_equal(a, b)
+        assert max_rel_l2(a, oracle.attend_latent(**oracle_args(inp, table, lens))) <= TOL_REL_L2
+        assert milo.milo_cache_recon_blocks(gl.cache) == 2
+    finally:
+        gl.free()
+
+
+@pytest.mark.parametrize("name", list(PREFILL))
+def test_reconstruct_prefill(name):
+    import torch
+    from paper_2609_29913_amd import milo
+    c = dict(PREFILL[name])
+    n_tok, tail_base, extra = c.pop("n_tok"), c.pop("tail_base"), c.pop("extra_rows")
+    blocks = c.pop("block_tokens")
+    ranks = c.pop("rank_k")
+    inp = synth.make_problem(zlib.crc32(name.encode()) % 1000, blocks or [1], ranks or [1], n_q=n_tok,
+                             tail_cap=tail_base + n_tok + extra, **c)
+    table = list(range(len(blocks)))
+    gl = GpuLayer(inp)
+    try:
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_RECONSTRUCT)
+        tk, tv = to_device(inp.tail_k[0]), to_device(inp.tail_v[0])
+        out = torch.full(inp.q.shape, float("nan"), dtype=torch.float32, device="cuda")
+        milo.milo_attend_prefill(gl.cache, table, gl.q, tk, tv, tail_base, inp.scale, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert milo.milo_cache_recon_blocks(gl.cache) == len(blocks)
+    finally:
+        gl.free()
+    a = oracle_args(inp, table)
+    ref = oracle.attend_prefill(a["pk"], a["rk"], a["pv"], a["rv"], table, a["q"], a["tail_k"][0],
+                                a["tail_v"][0], tail_base, inp.scale)
+    err = max_rel_l2(got, ref)
+    print(f"[recon] prefill {name}: max rel-L2 = {err:.3e}", flush=True)
+    assert err <= TOL_REL_L2
+
+
+@pytest.mark.timeout(900)
+def test_reconstruct_full_size_14b_layer():
+    """A whole 14B-shaped layer (256 blocks of 1024 tokens, ranks 128..768, 64
+    queries x 40 heads, 1024-token tails) with every block rebuilt; the oracle
+    checks the sampled columns of the latent full-size test."""
+    from paper_2609_29913_amd import milo
+    inp = synth.gen_layer("q14b_48l", 0)
+    print("[recon] q14b layer 0: generated", flush=True)
+    gl = GpuLayer(inp)
+    try:
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_RECONSTRUCT)
+        got = gl.attend().cpu().numpy()
+    finally:
+        gl.free()
+    assert np.all(np.isfinite(got))
+    cols = _full_size_columns(inp, "q14b_48l")
+    ref = oracle.attend_latent(**oracle_args(inp), columns=cols)
+    err = col_rel_l2(np.stack([got[i, h] for i, h in cols]), ref)
+    print(f"[recon] q14b layer 0: {len(cols)} columns, max rel-L2 = {err.max():.3e}", flush=True)
+    assert err.max() <= TOL_REL_L2
+
+
+def test_entry_points_that_cannot_rebuild():
+    """milo_attend_decode_noalloc attends AUTO caches latent and refuses
+    RECONSTRUCT; INT8 caches refuse both rebuilding paths."""
+    import torch
+    from paper_2609_29913_amd import milo
+    inp = _mixed_problem()
+    gl = GpuLayer(inp)
+    try:
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_AUTO)
+        out = torch.full(inp.q.shape, float("nan"), dtype=torch.float32, device="cuda")
+        milo.milo_attend_decode_noalloc(gl.cache, list(range(inp.n_blocks)), gl.q, gl.tk, gl.tv, inp.tail_len,
+                                        inp.scale, out)
+        torch.cuda.synchronize()
+        assert max_rel_l2(out.cpu().numpy(), oracle.attend_latent(**oracle_args(inp))) <= TOL_REL_L2
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_RECONSTRUCT)
+        with pytest.raises(milo.MiloError, match="latent only"):
+            milo.milo_attend_decode_noalloc(gl.cache, list(range(inp.n_blocks)), gl.q, gl.tk, gl.tv,
+                                            inp.tail_len, inp.scale, out)
+        with pytest.raises(milo.MiloError):
+            milo.milo_cache_set_path(gl.cache, 7)
+    finally:
+        gl.free()
+    small = synth.make_problem(5, [256, 100], [32, 64], n_kv_heads=1, head_dim=64, n_q=2, n_q_heads=2, tail_cap=4)
+    g8 = GpuLayer(small, p_int8=True)
+    try:
+        for path in (milo.MILO_PATH_RECONSTRUCT, milo.MILO_PATH_AUTO):
+            with pytest.raises(milo.MiloError, match="INT8"):
+                milo.milo_cache_set_path(g8.cache, path)
+        milo.milo_cache_set_path(g8.cache, milo.MILO_PATH_LATENT)
+    finally:
+        g8.free()

@@ -1,5 +1,6 @@
 """Packed factor layout (host logic, no GPU): the fragment order the kernels
-stream must be a bijection onto the padded source block for every factor."""
+stream must be a bijection onto the padded source block for every factor, and
+the fragment index helpers (used by the reconstruction kernel) its inverse."""
 import os
 import subprocess
 
@@ -61,5 +62,16 @@ def test_int8_runs_cover_codes_and_scales_once(checker):
     unit once, by its own wave, between its P^K and P^V runs."""
     args = [str(x) for g in RUN_GEOMS for x in g]
     res = subprocess.run([checker, "--runs-int8", *args], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert res.stdout.startswith("OK")
+
+
+def test_reconstructed_blocks_are_stored_and_read_once(checker):
+    """Reconstruct-then-attend: the reconstruction kernel's packed stores put
+    K_{b,g} and V_{b,g} exactly where the P^K / P^V layouts of rank d keep
+    them, every fragment once, and a dense item's derived runs read each of
+    them once (no R runs), for ragged token counts, 1..8 KV heads, d = 64 / 128."""
+    geoms = [(1, 1, 64), (256, 2, 128), (300, 4, 128), (1000, 8, 128), (513, 3, 64), (2048, 8, 128), (45, 1, 128)]
+    res = subprocess.run([checker, "--dense", *[str(x) for g in geoms for x in g]], capture_output=True, text=True)
     assert res.returncode == 0, res.stdout + res.stderr
     assert res.stdout.startswith("OK")

@@ -26,10 +26,11 @@ def checker(tmp_path_factory):
     return exe
 
 
-def _case(n_kv, d, G, n_q, n_chunks, T, rk, rv=None, table=None, cap=-1, i8=False):
+def _case(n_kv, d, G, n_q, n_chunks, T, rk, rv=None, table=None, cap=-1, i8=False, recon=0):
+    """recon: 0 every block latent, 1 every selected block reconstructed, 2 every other one."""
     rv = rk if rv is None else rv
     table = list(range(len(T))) if table is None else table
-    head = f"{n_kv} {d} {G} {n_q} {n_chunks} {cap} {int(i8)} {len(T)}"
+    head = f"{n_kv} {d} {G} {n_q} {n_chunks} {cap} {int(i8)} {recon} {len(T)}"
     blocks = " ".join(f"{t} {a} {b}" for t, a, b in zip(T, rk, rv))
     return f"{head} {blocks} {len(table)} {' '.join(map(str, table))}\n"
 
@@ -106,3 +107,32 @@ def test_column_tiling_choices(checker):
     assert "tiles 10 (mode 2) gang 10" in lines[1]
     assert "tiles 16 (mode 1) gang 16" in lines[2]
     assert "tiles 40 (mode 1) gang 8" in lines[3]
+
+
+def test_plans_with_reconstructed_blocks(checker):
+    """Reconstruct-then-attend plans: every block or every other block rebuilt,
+    on the workloads and on random shapes (few and many columns per KV head):
+    dense items per head tile, reconstruction tasks covering each (block, side,
+    head, tile) once with each block side on one XCD."""
+    cases = []
+    for name, cfg in synth.CONFIGS.items():
+        T = synth.draw_block_tokens(cfg)
+        r = synth.draw_ranks(cfg, 0, len(T))
+        for mode in (1, 2):
+            cases.append(_case(cfg.n_kv_heads, cfg.head_dim, cfg.group, cfg.n_q, _chunks(cfg.tail, cfg.tail), T, r,
+                               recon=mode))
+    rng = np.random.default_rng(11)
+    for _ in range(40):
+        d = int(rng.choice([64, 128]))
+        n_kv = int(rng.choice([1, 2, 3, 4, 8]))
+        G = int(rng.choice([1, 2, 5, 7, 16]))
+        n_q = int(rng.integers(1, 70))
+        nb = int(rng.integers(1, 30))
+        T = rng.integers(1, 5000, nb)
+        D = n_kv * d
+        rk = [int(rng.integers(1, min(int(t), D, 896) + 1)) for t in T]
+        rv = [int(rng.integers(1, min(int(t), D, 896) + 1)) for t in T]
+        k = int(rng.integers(1, nb + 1))
+        table = [int(b) for b in rng.permutation(nb)[:k]]
+        cases.append(_case(n_kv, d, G, n_q, int(rng.integers(0, 5)), T, rk, rv, table, recon=int(rng.integers(1, 3))))
+    _run(checker, cases)
