@@ -62,7 +62,11 @@ def counter_summary(workload: str) -> str:
 
 def workload_name(cfg, args) -> str:
     """The workload as the JSON line and the profile summaries name it."""
-    return cfg.name + ("_int8" if getattr(args, "int8", False) else "")
+    path = getattr(args, "path", "latent")
+    return cfg.name + ("_int8" if getattr(args, "int8", False) else "") + ("" if path == "latent" else f"_{path}")
+
+
+PATHS = {"latent": 0, "reconstruct": 1, "auto": 2}  # MILO_PATH_* of milo_cache_set_path
 
 
 def counter_values(workload: str):
@@ -90,11 +94,13 @@ class Layer:
     """One layer's device state: its cache, queries, tails and output (the host
     copies of the factors are not kept)."""
 
-    def __init__(self, inp: synth.LayerInputs, dev, p_int8: bool = False):
+    def __init__(self, inp: synth.LayerInputs, dev, p_int8: bool = False, path: str = "latent"):
         import torch
         from paper_2609_29913_amd import milo
         self.cache = milo.milo_cache_create(inp.block_tokens, inp.rank_k, inp.rank_v, inp.n_kv_heads,
                                             inp.head_dim, inp.pk, inp.rk, inp.pv, inp.rv, p_int8=p_int8)
+        if path != "latent":
+            milo.milo_cache_set_path(self.cache, PATHS[path])
         self.q = to_device(inp.q, dev)
         self.tk = to_device(inp.tail_k, dev)
         self.tv = to_device(inp.tail_v, dev)
@@ -168,7 +174,9 @@ def run_prefill(args, cfg, dev):
         layers[k % copies].step(stream)
     torch.cuda.synchronize()
     att_ms, merge_ms, n_calls = milo.milo_timing_read()
+    recon_ms, _ = milo.milo_timing_read_recon()
     milo.milo_timing_enable(False)
+    recon_blocks = sum(milo.milo_cache_recon_blocks(layer.cache) for layer in groups[0])
     att_s = att_ms / n_calls * 1e-3
     kern_bytes = first.bytes  # the attention kernel reads every factor, the tail and the queries once
     flops = first.flops
@@ -365,6 +373,9 @@ def main():
                     help="workload (default: the largest that fits one GPU, the 32B-shaped 64-layer step)")
     ap.add_argument("--int8", action="store_true",
                     help="store P^K and P^V as INT8 codes with per-token scales (MILO_P_INT8)")
+    ap.add_argument("--path", choices=sorted(PATHS), default="latent",
+                    help="how blocks are attended: latent (rank space), reconstruct (full-rank K/V rebuilt "
+                         "per step, Sec. 4.5) or auto (per block, by the library's cost model)")
     ap.add_argument("--grow-tails", action="store_true",
                     help="decode loop: every request's tail grows by one token per step (warm-up and timed "
                          "steps), ending at the workload's tail length")
@@ -413,7 +424,7 @@ def main():
     if args.grow_tails:
         grow_from = max(1, cfg.tail - (args.warmup + args.steps) + 1)
     x0 = None
-    per_step = flops_step = out_bytes = 0
+    per_step = flops_step = recon_flops_step = out_bytes = 0
     mean_ranks = []
     groups = [[]]
     t_gen = time.perf_counter()
@@ -422,10 +433,11 @@ def main():
         x = synth.gen_layer(cfg, l)
         per_step += synth.algorithmic_bytes(x, p_int8=args.int8)
         flops_step += synth.latent_flops(x)
+        recon_flops_step += synth.recon_flops(x)
         out_bytes += 4 * x.n_q * x.n_q_heads * x.head_dim
         mean_ranks.append(float(x.rank_k.mean()))
         t1 = time.perf_counter()
-        groups[0].append(Layer(x, dev, args.int8))
+        groups[0].append(Layer(x, dev, args.int8, args.path))
         t_make += time.perf_counter() - t1
         if cfg.n_layers > 1:
             print(f"bench: layer {l + 1}/{cfg.n_layers} ready ({time.perf_counter() - t_gen:.0f} s, "
@@ -434,7 +446,7 @@ def main():
             x0 = x
     copies = max(1, int(np.ceil(args.rotate_bytes / per_step)))
     for _ in range(1, copies):
-        groups.append([Layer(synth.gen_layer(cfg, l), dev, args.int8) for l in range(cfg.n_layers)])
+        groups.append([Layer(synth.gen_layer(cfg, l), dev, args.int8, args.path) for l in range(cfg.n_layers)])
     stream = torch.cuda.current_stream()
     if args.grow_tails:
         for grp in groups:
@@ -492,7 +504,9 @@ def main():
         run_step(k)
     torch.cuda.synchronize()
     att_ms, merge_ms, n_calls = milo.milo_timing_read()
+    recon_ms, _ = milo.milo_timing_read_recon()
     milo.milo_timing_enable(False)
+    recon_blocks = sum(milo.milo_cache_recon_blocks(layer.cache) for layer in groups[0])
     att_avg_s = att_ms / n_calls * 1e-3
     merge_avg_s = merge_ms / n_calls * 1e-3
 
@@ -582,6 +596,23 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if args.path != "latent":
+        # the route's own work: rebuilt blocks do 2 T D (rk + rv) flops of
+        # reconstruction and 4 N T d of dense attention instead of the latent
+        # 2 N (rk + rv)(T + d); the roofline above prices the latent work
+        recon_avg_s = recon_ms / n_calls * 1e-3
+        result["route"] = {
+            "path": args.path,
+            "reconstructed_blocks_per_step": recon_blocks,
+            "blocks_per_step": x0.n_blocks * cfg.n_layers,
+            "recon_kernel_avg_us": recon_avg_s * 1e6,
+            "attend_plus_recon_us": (att_avg_s + recon_avg_s) * 1e6,
+        }
+        if args.path == "reconstruct":
+            rflops = recon_flops_step / cfg.n_layers
+            result["route"]["route_flops_per_layer"] = rflops
+            result["route"]["route_tflops"] = rflops / (att_avg_s + recon_avg_s) / 1e12
+            result["route"]["route_mfma_frac"] = rflops / (att_avg_s + recon_avg_s) / 1e12 / MFMA_BF16_PEAK_TFLOPS
     for grp in groups:
         for layer in grp:
             milo.milo_cache_free(layer.cache)

@@ -188,9 +188,12 @@ int milo_attend_prefill(milo_cache* cache, const int32_t* block_table, int32_t n
  *                          grown like the rest of the workspace), and then
  *                          attended as uncompressed keys and values.
  *   MILO_PATH_AUTO         per block and call, whichever an MI355X cost model
- *                          expects to be faster: reconstruction pays for blocks
- *                          of high rank attended by many query columns
- *                          (roughly r N > r H_kv d + d N, N = n_q H_q).
+ *                          (fitted to measured kernel times) expects to be
+ *                          clearly faster: reconstruction pays for blocks of
+ *                          high rank attended by many query columns (the
+ *                          latent route costs ~ r N (T + d), reconstruction
+ *                          ~ r T H_kv d + T H_kv d + N T d; N = n_q H_q), e.g.
+ *                          the ranks above ~400 of a 14B-shaped 64-query step.
  * Both routes compute the same attention up to rounding.  A plan with any
  * reconstructed block cuts the query columns per KV head.  INT8 caches attend
  * latent only (UNSUPPORTED for the other paths), and so does

@@ -494,22 +494,21 @@ class CacheWorkspace : public Workspace {
 };
 
 // Reconstruct-then-attend pays for a block when rebuilding its keys and values
-// and attending them densely costs less than the latent route.  Both are timed
-// by an MI355X cost model: MFMA work at the efficiency each kernel reaches
-// (latent block items ~20% of the bf16 peak, the reconstruction GEMM ~35%, the
-// dense items like the latent ones) plus, for reconstruction, writing and
-// re-reading the full-rank blocks through HBM (~5 TB/s).  Per block of T
-// tokens, ranks rk / rv, N query columns, D = H_kv d:
-//   latent        2 N (rk + rv)(T + d)            flops (scores, value pass, projections)
-//   reconstruct   2 T D (rk + rv)                 flops (K = P^K R^K, V = P^V R^V)
-//               + 4 N T d                         flops (dense scores and value pass)
-//               + 8 T D                           bytes (bf16 K and V written, then read)
+// and attending them densely is clearly faster than the latent route.  Per-block
+// times (microseconds) fitted to MI355X kernel timings of the 7B- (28-layer) and
+// 14B-shaped steps, for a block of T tokens, ranks rk / rv, N query columns,
+// D = H_kv d:
+//   latent        4.24e-9 N (rk + rv)(T + d)        (latent block items)
+//   reconstruct   4.17e-9 T D (rk + rv)             (reconstruction GEMMs)
+//               + 1.99e-6 T D                       (writing, then reading, the bf16 K and V)
+//               + 7.06e-9 N T d                     (dense block items)
+// and reconstruction is chosen below 0.85 of the latent time (mixed plans
+// measured slower than the sum of their parts near the tie).
 bool recon_pays(int T, int rk, int rv, int64_t N, int D, int d) {
-  constexpr double kPeak = 2.5e15, kLat = 0.20, kGemm = 0.35, kDense = 0.20, kBw = 5.0e12;
-  const double lat = 2.0 * N * (rk + rv) * (double)(T + d) / (kLat * kPeak);
-  const double rec = 2.0 * T * (double)D * (rk + rv) / (kGemm * kPeak) + 4.0 * N * (double)T * d / (kDense * kPeak) +
-                     8.0 * T * (double)D / kBw;
-  return rec < lat;
+  const double r = (double)rk + rv;
+  const double lat = 4.24e-9 * (double)N * r * (T + d);
+  const double rec = 4.17e-9 * (double)T * D * r + 1.99e-6 * (double)T * D + 7.06e-9 * (double)N * T * d;
+  return rec < 0.85 * lat;
 }
 
 }  // namespace

@@ -62,7 +62,7 @@ __host__ __device__ inline int owned_before(int nrt, int w, int n) {
 // wave, ties going to fewer segments (fewer partial sums to combine), with no wave
 // owning more than kMaxOwn rank tiles; past 8 * kMaxOwn rank tiles no split
 // qualifies and the block uses one segment (every wave owns nrt / 8 tiles).
-__host__ __device__ inline int v_segments(int nrt) {
+__host__ __device__ constexpr int v_segments(int nrt) {
   int best = 1, best_work = 1 << 30;
   for (int nseg = 1; nseg <= kWaves; nseg *= 2) {
     const int ng = kWaves / nseg;
@@ -282,6 +282,22 @@ __host__ __device__ inline int64_t rk_frag(const BlockMeta& bm, int d, int g, in
 __host__ __device__ inline int64_t rv_frag(const BlockMeta& bm, int d, int g, int ds, int kap) {
   const int nds = d / 16, nkr = bm.rv_pad / 32;
   return bm.off_rv / kFragElems + ((int64_t)g * nds + ds) * nkr + kap;
+}
+
+// The same indices with the per-block splits precomputed, for inner loops:
+// P^V with lg = lg_rank_groups(nrt) (rank groups ng = 2^lg) and T16 = T_pad / 16,
+// R^K with nrt its 32-rank tiles and nk = d / 16 (pv0 / rk0: the factor's
+// first fragment; rk_head: nrt * nk fragments per KV head).
+__host__ __device__ inline int pv_frag_split(int pv0, int T16, int nrt, int lg, int sig, int rho) {
+  const int ng = 1 << lg, rg = rho & (ng - 1), j = rho >> lg;
+  const int q = nrt >> lg, rem = nrt & (ng - 1);
+  const int before = rg * q + (rg < rem ? rg : rem), own = q + (rg < rem ? 1 : 0);
+  return pv0 + T16 * before + sig * own + j;
+}
+__host__ __device__ inline int rk_frag_split(int rk0, int nrt, int nk, int g, int rho, int kap) {
+  const int w = rho & (kWaves - 1), j = rho >> 3, q = nrt >> 3, rem = nrt & (kWaves - 1);
+  static_assert(kWaves == 8, "rank tiles are dealt over 8 waves");
+  return rk0 + g * nrt * nk + nk * (w * q + (w < rem ? w : rem) + j) + kap;
 }
 
 // ---------------------------------------------------------------------------

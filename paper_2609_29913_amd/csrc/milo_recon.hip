@@ -44,16 +44,13 @@ constexpr size_t recon_lds_bytes(int D) {
   return stage > out ? stage : out;
 }
 
-template <int D>
-__global__ __launch_bounds__(kReconThreads) void recon_kernel(ReconArgs a) {
-  static_assert(D == 64 || D == 128, "head dimension");
+// one task of side SIDE (0: K, 1: V)
+template <int D, int SIDE>
+__device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock& rb, int g, int t,
+                                           unsigned char* smem) {
   constexpr int NJ = D / 64;  // 32-column blocks of a wave's d / 2 dims
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int2 task = a.tasks[blockIdx.x];
-  if (task.x < 0) return;
-  const ReconBlock rb = a.blocks[task.x];
+  constexpr int side = SIDE;
   const BlockMeta& bm = rb.src;
-  const int side = task.y & 1, g = (task.y >> 1) & 127, t = task.y >> 8;
   const int nrt = (side ? bm.rv_pad : bm.rk_pad) >> 5;  // 32-rank steps
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lhi = lane >> 5;
@@ -61,19 +58,48 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(ReconArgs a) {
   __bf16* sA = reinterpret_cast<__bf16*>(smem);      // [2][kTile][kStageStride]: P slice [token][rank]
   __bf16* sB = sA + 2 * kTile * kStageStride;         // [2][D][kStageStride]: R_g slice [dim][rank]
 
-  // global -> registers for 32-rank step kc: two P chunks and (threads < 4 D) one R chunk
+  // global -> registers for 32-rank step kc: two P chunks and (threads < 4 D) one
+  // R chunk.  The fragment indices are split into per-task constants (set up
+  // once) and a cheap per-step part: P^K and R^V advance by whole fragments per
+  // step, P^V and R^K follow their rank-group / wave dealing (shifts only).
+  const int f0 = tid >> 6, ln = tid & 63;  // chunk h covers fragment f0 + 8 h
+  const unsigned char* pa_ptr[2];
+  int pv_sig[2];
+  const unsigned char* rb_ptr = data + 16 * ln;
+  int pv0 = 0, T16 = 0, lgv = 0, rk0 = 0;
+  if constexpr (side == 0) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int f = f0 + 8 * h;
+      pa_ptr[h] = data + pk_frag(bm, kWaves * t + (f >> 1), f & 1) * (kFragElems * 2) + 16 * ln;
+    }
+    rk0 = (int)(bm.off_rk / kFragElems);
+  } else {
+    pv0 = (int)(bm.off_pv / kFragElems);
+    T16 = bm.T_pad / 16;
+    lgv = lg_rank_groups(nrt);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) pv_sig[h] = 16 * t + f0 + 8 * h;
+    if (tid < 4 * D) rb_ptr = data + rv_frag(bm, D, g, f0, 0) * (kFragElems * 2) + 16 * ln;
+  }
   uint4 pa[2], rbv;
   auto load = [&](int kc) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int q = tid + kReconThreads * h, f = q >> 6, ln = q & 63;
-      const int64_t frag = side ? pv_frag(bm, 16 * t + f, kc) : pk_frag(bm, kWaves * t + (f >> 1), 2 * kc + (f & 1));
-      pa[h] = *reinterpret_cast<const uint4*>(data + frag * (kFragElems * 2) + 16 * ln);
+      if constexpr (side == 0) {
+        pa[h] = *reinterpret_cast<const uint4*>(pa_ptr[h] + (size_t)kc * 2 * (kFragElems * 2));
+      } else {
+        const int fr = pv_frag_split(pv0, T16, nrt, lgv, pv_sig[h], kc);
+        pa[h] = *reinterpret_cast<const uint4*>(data + (int64_t)fr * (kFragElems * 2) + 16 * ln);
+      }
     }
     if (tid < 4 * D) {
-      const int f = tid >> 6, ln = tid & 63;
-      const int64_t frag = side ? rv_frag(bm, D, g, f, kc) : rk_frag(bm, D, g, kc, f);
-      rbv = *reinterpret_cast<const uint4*>(data + frag * (kFragElems * 2) + 16 * ln);
+      if constexpr (side == 0) {
+        const int fr = rk_frag_split(rk0, nrt, D / 16, g, kc, f0);
+        rbv = *reinterpret_cast<const uint4*>(data + (int64_t)fr * (kFragElems * 2) + 16 * ln);
+      } else {
+        rbv = *reinterpret_cast<const uint4*>(rb_ptr + (size_t)kc * (kFragElems * 2));
+      }
     }
   };
   // registers -> LDS buffer `buf` (rank contiguous)
@@ -169,26 +195,43 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(ReconArgs a) {
       }
   __syncthreads();
 
-  // packed stores: 32 D chunks of 16 bytes (8 D / 16 ... fragments of 64 lanes)
+  // packed stores: 32 D chunks of 16 bytes (D / 2 fragments of 64 lanes).  With
+  // rank d every rank group of the P^V layout owns one rank tile (v_segments:
+  // 2 token segments for d = 128, 4 for d = 64), so fragment (sig, rho) sits at
+  // rho T_pad / 16 + sig.
+  static_assert(kWaves / v_segments(D / 32) == D / 32, "one rank tile per rank group at rank d");
   const BlockMeta dm = dense_meta(bm, rb.dst, g, D);
+  const int tiles_all = bm.T_pad / kTile;
   unsigned char* out = reinterpret_cast<unsigned char*>(a.recon);
   for (int q = tid; q < 32 * D; q += kReconThreads) {
     const int f = q >> 6, ln = q & 63, m = ln & 31, c = ln >> 5;
     int64_t frag;
     uint4 v;
-    if (side == 0) {
+    if constexpr (side == 0) {
       // K_{b,g} in the P^K layout: fragment (tau = 8 t + w, kap), lane (c, m) = dims 16 kap + 8 c .. +7 of token 32 w + m
       const int w = f / (D / 16), kap = f % (D / 16);
-      frag = pk_frag(dm, kWaves * t + w, kap);
+      frag = dm.off_pk / kFragElems + ((int64_t)w * tiles_all + t) * (D / 16) + kap;
       v = *reinterpret_cast<const uint4*>(O + (32 * w + m) * kOK + 16 * kap + 8 * c);
     } else {
       // V_{b,g} in the P^V layout: fragment (sig = 16 t + s, rho), lane (c, m) = tokens 16 s + 8 c .. +7 of dim 32 rho + m
       const int s = f / (D / 32), rho = f % (D / 32);
-      frag = pv_frag(dm, 16 * t + s, rho);
+      frag = dm.off_pv / kFragElems + (int64_t)rho * (bm.T_pad / 16) + 16 * t + s;
       v = *reinterpret_cast<const uint4*>(O + (32 * rho + m) * kOV + 16 * s + 8 * c);
     }
     *reinterpret_cast<uint4*>(out + frag * (kFragElems * 2) + 16 * ln) = v;
   }
+}
+
+template <int D>
+__global__ __launch_bounds__(kReconThreads) void recon_kernel(ReconArgs a) {
+  static_assert(D == 64 || D == 128, "head dimension");
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int2 task = a.tasks[blockIdx.x];
+  if (task.x < 0) return;
+  const ReconBlock rb = a.blocks[task.x];
+  const int g = (task.y >> 1) & 127, t = task.y >> 8;
+  if (task.y & 1) recon_task<D, 1>(a, rb, g, t, smem);
+  else recon_task<D, 0>(a, rb, g, t, smem);
 }
 
 template <int D>

@@ -26,7 +26,7 @@ import numpy as np
 __all__ = [
     "Config", "CONFIGS", "LayerInputs", "f32_to_bf16", "bf16_to_f32",
     "bf16_to_f64", "gen_layer", "make_problem", "draw_block_tokens",
-    "draw_ranks", "algorithmic_bytes", "latent_flops", "gen_spectra", "Spectra", "gen_kv_block",
+    "draw_ranks", "algorithmic_bytes", "latent_flops", "recon_flops", "gen_spectra", "Spectra", "gen_kv_block",
 ]
 
 _MAGIC = 0x4D494C4F  # "MILO"
@@ -274,6 +274,21 @@ def latent_flops(inp: LayerInputs, table=None) -> int:
     d = inp.head_dim
     blk = sum(2 * ncol * (int(inp.rank_k[b]) + int(inp.rank_v[b])) * (int(inp.block_tokens[b]) + d)
               for b in table)
+    G = inp.n_q_heads // inp.n_kv_heads
+    tail = 4 * int(np.sum(inp.tail_len)) * G * inp.n_kv_heads * d
+    return blk + tail
+
+
+def recon_flops(inp: LayerInputs, table=None) -> int:
+    """Multiply-add flops of the reconstruct-then-attend route with every block
+    rebuilt: K_b = P^K R^K and V_b = P^V R^V (2 T D r each), then dense scores
+    and value pass (4 N T d), and the tail."""
+    table = range(inp.n_blocks) if table is None else table
+    ncol = inp.n_q * inp.n_q_heads
+    d = inp.head_dim
+    D = inp.n_kv_heads * d
+    blk = sum(2 * int(inp.block_tokens[b]) * D * (int(inp.rank_k[b]) + int(inp.rank_v[b])) +
+              4 * ncol * int(inp.block_tokens[b]) * d for b in table)
     G = inp.n_q_heads // inp.n_kv_heads
     tail = 4 * int(np.sum(inp.tail_len)) * G * inp.n_kv_heads * d
     return blk + tail

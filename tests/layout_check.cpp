@@ -73,6 +73,14 @@ static int check(int kind, int T, int r, int n_kv, int d) {
                   back);
       return 1;
     }
+    // the split forms of the reconstruction kernel's inner loop agree
+    long long split = back;
+    if (kind == kPV) split = pv_frag_split(0, T_pad / 16, r_pad / 32, lg_rank_groups(r_pad / 32), row / 16, col / 32);
+    if (kind == kRK) split = rk_frag_split(0, r_pad / 32, d / 16, col / d, row / 32, (col % d) / 16);
+    if (split != fr) {
+      std::printf("kind %d: fragment %lld, split index form gives %lld\n", kind, fr, split);
+      return 1;
+    }
   }
   return 0;
 }

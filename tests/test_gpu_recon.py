@@ -68,16 +68,16 @@ def test_reconstruct_random_shapes(seed):
 
 
 def _mixed_problem():
-    # 7B-shaped heads (896 columns): high-rank blocks pay for reconstruction, low-rank ones do not
-    return synth.make_problem(77, [1024, 1024, 700, 1024, 300, 1024], [512, 64, 448, 96, 160, 480],
-                              [512, 64, 448, 128, 96, 512], n_kv_heads=4, head_dim=128, n_q=32, n_q_heads=28,
-                              tail_cap=300)
+    # 14B-shaped heads (2560 columns): high-rank blocks pay for reconstruction, low-rank ones do not
+    return synth.make_problem(77, [1024, 1024, 700, 1024, 300, 1024], [768, 128, 640, 128, 160, 512],
+                              [768, 96, 640, 128, 128, 576], n_kv_heads=8, head_dim=128, n_q=64, n_q_heads=40,
+                              tail_cap=100)
 
 
 def test_auto_mixes_both_routes_in_one_plan():
     from paper_2609_29913_amd import milo
     inp = _mixed_problem()
-    _, n_rec = _run(inp, milo.MILO_PATH_AUTO, label="auto, 7B heads, mixed ranks")
+    _, n_rec = _run(inp, milo.MILO_PATH_AUTO, label="auto, 14B heads, mixed ranks")
     assert 0 < n_rec < inp.n_blocks
 
 
@@ -188,7 +188,7 @@ def test_entry_points_that_cannot_rebuild():
     RECONSTRUCT; INT8 caches refuse both rebuilding paths."""
     import torch
     from paper_2609_29913_amd import milo
-    inp = _mixed_problem()
+    inp = synth.make_problem(zlib.crc32(b"q7b_shape_5_blocks") % 1000, **SHAPES["q7b_shape_5_blocks"])
     gl = GpuLayer(inp)
     try:
         milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_AUTO)
