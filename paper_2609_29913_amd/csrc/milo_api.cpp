@@ -573,6 +573,24 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     }
   }
 
+  // ---- the latent projection: MFMA (measured faster on gfx950 at every batch,
+  // 7 columns per KV head included), or a wavefront GEMV kernel variant for
+  // small batches (at most kGemvCols query columns per KV head, bf16 P factors)
+  // when the MILO_PROJECTION environment variable says "gemv" ----
+  const int N_g = n_q * G;
+  bool gemv = false;
+  if (const char* pe = std::getenv("MILO_PROJECTION"); pe && *pe) {
+    if (std::strcmp(pe, "gemv") == 0) {
+      if (N_g > kGemvCols || c->p_int8)
+        return fail(MILO_ERR_UNSUPPORTED,
+                    "the GEMV projection needs bf16 P factors and at most %d query columns per KV head (got %d)",
+                    kGemvCols, N_g);
+      gemv = true;
+    } else if (std::strcmp(pe, "mfma") != 0) {
+      return fail(MILO_ERR_INVALID_ARG, "MILO_PROJECTION must be mfma or gemv (got %s)", pe);
+    }
+  }
+
   // ---- plan: rebuilt only when the block table, the batch shape or the tail
   // chunk capacity changes (the longest tail rounded up to a power of two of
   // chunks, at most tail_cap), not when tails merely grow ----
@@ -592,6 +610,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   key.push_back(n_q_heads);
   key.push_back(n_chunks);
   key.push_back(n_recon > 0 ? c->path : MILO_PATH_LATENT);
+  key.push_back(gemv ? 1 : 0);
   key.insert(key.end(), block_table, block_table + n_sel);
   const int n_cols = n_q * n_q_heads;
   if (key != ps.key) {
@@ -605,7 +624,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
       region.assign(c->n_blocks, -1);
       build_recon_plan(c->meta.data(), block_table, n_sel, recon.data(), c->n_kv, c->d, &region, &rp);
     }
-    const Tiling til = make_tiling(c->n_kv, n_q * G, n_recon > 0);
+    const Tiling til = make_tiling(c->n_kv, n_q * G, n_recon > 0, gemv ? kGemvCols : kCols);
     Schedule sch;
     std::string why;
     PlanInput pin{c->meta.data(), c->n_kv, c->d, c->p_int8};
@@ -665,6 +684,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ps.recon_blocks_off = rb_off;
     ps.recon_tasks_off = rt_off;
     ps.recon_elems = rp.elems;
+    ps.gemv = gemv;
     ps.key.swap(key);
     ++ps.builds;
   }
@@ -778,7 +798,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   }
   for (int l = 0; l < ps.n_launch; ++l) {
     aa.wg = reinterpret_cast<const WgProgram*>(ps.plan_d) + (size_t)l * kCUs;
-    e = launch_attend(aa, c->d, ps.max_rt, ps.nslot, c->p_int8, kCUs, ps.lds, s, l == 0 ? ev[0] : nullptr,
+    e = launch_attend(aa, c->d, ps.max_rt, ps.nslot, c->p_int8, ps.gemv, kCUs, ps.lds, s, l == 0 ? ev[0] : nullptr,
                       l == ps.n_launch - 1 ? ev[1] : nullptr);
     if (e != hipSuccess) return launch_fail(e, "attend kernel launch");
   }

@@ -30,6 +30,7 @@ struct PlanState {
   int n_recon_blocks = 0, n_recon_tasks = 0;
   int64_t recon_blocks_off = 0, recon_tasks_off = 0;  // byte offsets in the plan
   int64_t recon_elems = 0;                            // reconstruction buffer (bf16 elements)
+  bool gemv = false;                                  // latent projection as a wavefront GEMV
 };
 
 // Device memory one attention call uses beyond its inputs and outputs.  Each

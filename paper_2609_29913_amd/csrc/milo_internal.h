@@ -400,6 +400,7 @@ constexpr int kSentinelRun = 1 << 27;  // a bf16 run long enough for any look-ah
 // Attention kernel geometry.
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCols = 64;                      // query columns per workgroup
+constexpr int kGemvCols = 16;                  // most columns of a tile whose projection may run as a GEMV
 constexpr int kTokWave = kTile / kWaves;       // tokens per wave per tile (one MFMA row block)
 static_assert(kTokWave == 32, "the score pass gives every wave one 32-token sub-tile");
 constexpr int kWStride = kTile + 8;            // bf16 row stride of the weight tile in LDS
@@ -516,7 +517,9 @@ hipError_t launch_row_scales(const uint16_t* src, int rows, int cols, int rows_p
 hipError_t launch_scale_units(const float* ks, const float* vs, int T_pad, float* dst, hipStream_t s);
 // e0 / e1 (may be null): events recorded when the kernel starts and ends
 // (hipExtLaunchKernelGGL), so they time the kernel itself.
-hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, bool p_int8, int grid,
+// gemv: the kernel variant whose latent projection is a wavefront GEMV (tiles
+// of at most kGemvCols columns; bf16 P factors only)
+hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, bool p_int8, bool gemv, int grid,
                          size_t lds_bytes, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s, hipEvent_t e0 = nullptr,
                         hipEvent_t e1 = nullptr);

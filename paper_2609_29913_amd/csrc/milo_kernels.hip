@@ -580,10 +580,14 @@ constexpr int up_col_blocks() {
 // LDS at its start.  Every loop is software-pipelined: the operands of step
 // k+1 are read while the MFMAs of step k run.
 // ---------------------------------------------------------------------------
-template <int D, int MAX_RT, int NSLOT, bool WH, bool I8>
+// MODE: 0 bf16 P factors, 1 INT8 P factors, 2 bf16 P factors with the
+// projection as a wavefront GEMV (kernel variants, so no branch of one costs
+// the others registers)
+template <int D, int MAX_RT, int NSLOT, bool WH, int MODE>
 __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& it, unsigned char* smem,
-                                           FragRing<D, NSLOT, I8>& fr, RunDeriver<D>& rd,
+                                           FragRing<D, NSLOT, MODE == 1>& fr, RunDeriver<D>& rd,
                                            GroupAcc<up_col_blocks<D>()>& acc, const int tid) {
+  constexpr bool I8 = MODE == 1, GV = MODE == 2;
   constexpr int NK = D / 16;
   constexpr int kORed = 4;  // partial-output slots of the up-projection reduction
   const BlockMeta& bm = it.blk;
@@ -657,6 +661,42 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = (__bf16)((float)v[e] * a.qscale);
       *reinterpret_cast<bf16x8*>(qt + cl * qsd + 8 * j) = o;
+    }
+  } else if (GV && own_k > 0) {
+    // small batches (a tile of at most kGemvCols columns): the projection as a
+    // wavefront GEMV.  Lane (c, m) of an R^K fragment holds rank 32 rt + m, dims
+    // 16 k + 8 c .. +7; it dots them with the same dims of every column of the
+    // current head (the query row chunk is one LDS broadcast), the two lane
+    // halves are summed, and lanes m < 32 store their rank of the head's columns.
+    // Columns past the tile's last one get zeros.
+    for (int x = 0; x < nh * own_k; ++x) {
+      const int hh = x / own_k, rt = wave + kWaves * (x - hh * own_k);
+      // the head's columns are the consecutive range [lo, hi) of the tile
+      const int lo = max(0, (g0 + hh) * N_g - c0), hi = min(cn, (g0 + hh + 1) * N_g - c0);
+      float acc[kGemvCols];
+#pragma unroll
+      for (int cl = 0; cl < kGemvCols; ++cl) acc[cl] = 0.f;
+      for (int k = 0; k < NK; ++k) {
+        const bf16x8 af = take();
+        float rf[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) rf[e] = (float)af[e];
+        // every one of the kGemvCols query rows (rows past the tile's columns
+        // hold a copy of its last one); only the head's columns are stored
+#pragma unroll
+        for (int cl = 0; cl < kGemvCols; ++cl) {
+          const bf16x8 qv = ld_bf16x8(qimg + cl * D + 8 * ((2 * k + lhi) ^ (cl % kRowChunks)));
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[cl] = fmaf(rf[e], (float)qv[e], acc[cl]);
+        }
+      }
+#pragma unroll
+      for (int cl = 0; cl < kGemvCols; ++cl) {
+        acc[cl] += __shfl_xor(acc[cl], 32);
+        if (lhi == 0 && cl >= lo && cl < hi) qt[cl * qsd + 32 * rt + lrow] = (__bf16)(acc[cl] * a.qscale);
+      }
+      if (hh == 0)
+        for (int cl = cn + lhi; cl < kCols; cl += 2) qt[cl * qsd + 32 * rt + lrow] = (__bf16)0.f;
     }
   } else if (own_k > 0) {
     bf16x8 qf[NK][2];
@@ -1043,8 +1083,9 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   }
 }
 
-template <int D, int MAX_RT, int NSLOT, bool WH, bool I8>
+template <int D, int MAX_RT, int NSLOT, bool WH, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
+  constexpr bool I8 = MODE == 1;
   extern __shared__ __align__(16) unsigned char smem[];
   const WgProgram p = a.wg[blockIdx.x];
   if (p.n_items == 0) return;
@@ -1083,7 +1124,7 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
     // lane-dependent address of one item kind stays live across the other
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
-    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT, WH, I8>(a, it, work, fr, rd, acc, tid);
+    if (it.kind == kItemBlock) block_item<D, MAX_RT, NSLOT, WH, MODE>(a, it, work, fr, rd, acc, tid);
     else if (it.kind == kItemTail) tail_item<D>(a, it, work, tid);
   }
   if constexpr (NSLOT > 0) wait_vmcnt<0>();  // no LDS write may land after the workgroup ends
@@ -1202,54 +1243,58 @@ hipError_t launch_scale_units(const float* ks, const float* vs, int T_pad, float
 }
 
 
-template <int D, int MAX_RT, int NSLOT, bool WH, bool I8>
+template <int D, int MAX_RT, int NSLOT, bool WH, int MODE>
 static hipError_t launch_attend_t(const AttendArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                                   hipEvent_t e1) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_kernel<D, MAX_RT, NSLOT, WH, I8>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_kernel<D, MAX_RT, NSLOT, WH, MODE>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipExtLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT, WH, I8>), dim3(grid), dim3(kThreads), (uint32_t)lds, s, e0,
-                        e1, 0, a);
+  hipExtLaunchKernelGGL((attend_kernel<D, MAX_RT, NSLOT, WH, MODE>), dim3(grid), dim3(kThreads), (uint32_t)lds, s,
+                        e0, e1, 0, a);
   return hipGetLastError();
 }
 
 // ring slots 8 / 6 / none with the whole weight tile; 4 with the half tile
-template <int D, int MAX_RT, bool I8>
+template <int D, int MAX_RT, int MODE>
 static hipError_t launch_attend_r(const AttendArgs& a, int nslot, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                                   hipEvent_t e1) {
   switch (nslot) {
-    case 8: return launch_attend_t<D, MAX_RT, 8, false, I8>(a, grid, lds, s, e0, e1);
-    case 6: return launch_attend_t<D, MAX_RT, 6, false, I8>(a, grid, lds, s, e0, e1);
-    case 4: return launch_attend_t<D, MAX_RT, 4, true, I8>(a, grid, lds, s, e0, e1);
-    case 0: return launch_attend_t<D, MAX_RT, 0, false, I8>(a, grid, lds, s, e0, e1);
+    case 8: return launch_attend_t<D, MAX_RT, 8, false, MODE>(a, grid, lds, s, e0, e1);
+    case 6: return launch_attend_t<D, MAX_RT, 6, false, MODE>(a, grid, lds, s, e0, e1);
+    case 4: return launch_attend_t<D, MAX_RT, 4, true, MODE>(a, grid, lds, s, e0, e1);
+    case 0: return launch_attend_t<D, MAX_RT, 0, false, MODE>(a, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <int D, bool I8>
+template <int D, int MODE>
 static hipError_t launch_attend_d(const AttendArgs& a, int max_rt, int nslot, int grid, size_t lds,
                                   hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   switch (max_rt) {
-    case 2: return launch_attend_r<D, 2, I8>(a, nslot, grid, lds, s, e0, e1);
-    case 3: return launch_attend_r<D, 3, I8>(a, nslot, grid, lds, s, e0, e1);
-    case 4: return launch_attend_r<D, 4, I8>(a, nslot, grid, lds, s, e0, e1);
+    case 2: return launch_attend_r<D, 2, MODE>(a, nslot, grid, lds, s, e0, e1);
+    case 3: return launch_attend_r<D, 3, MODE>(a, nslot, grid, lds, s, e0, e1);
+    case 4: return launch_attend_r<D, 4, MODE>(a, nslot, grid, lds, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, bool p_int8, int grid,
+template <int D>
+static hipError_t launch_attend_m(const AttendArgs& a, int max_rt, int nslot, bool p_int8, bool gemv, int grid,
+                                  size_t lds, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (p_int8) return launch_attend_d<D, 1>(a, max_rt, nslot, grid, lds, s, e0, e1);
+  if (gemv) return launch_attend_d<D, 2>(a, max_rt, nslot, grid, lds, s, e0, e1);
+  return launch_attend_d<D, 0>(a, max_rt, nslot, grid, lds, s, e0, e1);
+}
+
+hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslot, bool p_int8, bool gemv, int grid,
                          size_t lds_bytes, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (grid == 0) return hipSuccess;
-  if (head_dim == 64)
-    return p_int8 ? launch_attend_d<64, true>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1)
-                  : launch_attend_d<64, false>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
-  if (head_dim == 128)
-    return p_int8 ? launch_attend_d<128, true>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1)
-                  : launch_attend_d<128, false>(a, max_rt, nslot, grid, lds_bytes, s, e0, e1);
+  if (head_dim == 64) return launch_attend_m<64>(a, max_rt, nslot, p_int8, gemv, grid, lds_bytes, s, e0, e1);
+  if (head_dim == 128) return launch_attend_m<128>(a, max_rt, nslot, p_int8, gemv, grid, lds_bytes, s, e0, e1);
   return hipErrorInvalidValue;
 }
 

@@ -86,7 +86,7 @@ int gang_size(int n_ct) {
   return best >= 2 * pow2 ? best : pow2;
 }
 
-Tiling make_tiling(int n_kv, int N_g, bool head_tiles) {
+Tiling make_tiling(int n_kv, int N_g, bool head_tiles, int max_cols) {
   Tiling t;
   const int N = n_kv * N_g;
   if (head_tiles) {
@@ -94,7 +94,7 @@ Tiling make_tiling(int n_kv, int N_g, bool head_tiles) {
     t.geom = TileGeom{kTileHead, a, N_g, N};
     t.n_ct = n_kv * a;
   } else if (N_g < kCols) {
-    const int a = std::max(1, std::min(kMaxTileHeads, kCols / N_g));
+    const int a = std::max(1, std::min(kMaxTileHeads, max_cols / N_g));
     t.geom = TileGeom{kTilePacked, a, N_g, N};
     t.n_ct = (n_kv + a - 1) / a;
   } else {

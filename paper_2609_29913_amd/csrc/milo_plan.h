@@ -30,8 +30,10 @@ struct Tiling {
 };
 
 int gang_size(int n_ct);
-// head_tiles: one KV head per column tile (kTileHead), as dense items need
-Tiling make_tiling(int n_kv, int N_g, bool head_tiles = false);
+// head_tiles: one KV head per column tile (kTileHead), as dense items need;
+// max_cols: most columns of a tile that packs whole KV heads (kGemvCols when
+// the projection runs as a GEMV)
+Tiling make_tiling(int n_kv, int N_g, bool head_tiles = false, int max_cols = kCols);
 
 struct Schedule {
   std::vector<unsigned char> bytes;  // WgProgram[n_launch * kCUs], then the programs, then slot counts

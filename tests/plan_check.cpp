@@ -19,7 +19,9 @@
 //    (block, K or V, KV head, 256-token tile) exactly once, each block side's
 //    tasks on one XCD, and the regions lie back to back.
 // Case format (whitespace separated):
-//   n_kv d G n_q n_chunks program_cap int8 recon n_blocks  (T rk rv) x n_blocks  n_sel  table...
+//   n_kv d G n_q n_chunks program_cap int8 recon gemv n_blocks  (T rk rv) x n_blocks  n_sel  table...
+// (gemv: the projection runs as a GEMV, so tiles that pack heads hold at most
+// kGemvCols columns)
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -46,7 +48,7 @@ static int fails = 0;
   } while (0)
 
 static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks, long long program_cap, int i8,
-                     int recon_mode, const std::vector<int>& T, const std::vector<int>& rk, const std::vector<int>& rv,
+                     int recon_mode, int gemv, const std::vector<int>& T, const std::vector<int>& rk, const std::vector<int>& rv,
                      const std::vector<int>& table) {
   const int nb = (int)T.size();
   std::vector<BlockMeta> meta(nb);
@@ -111,8 +113,10 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
     for (const ReconBlock& r : rp.blocks) want += 2 * (size_t)n_kv * (r.src.T_pad / kTile);
     CHECK(task_seen.size() == want, "%zu tasks, want %zu", task_seen.size(), want);
   }
-  const Tiling til = make_tiling(n_kv, N_g, any_recon);
+  const Tiling til = make_tiling(n_kv, N_g, any_recon, gemv ? kGemvCols : kCols);
   if (any_recon) CHECK(til.geom.mode == kTileHead, "reconstructed blocks without per-head tiles");
+  if (gemv && N_g <= kGemvCols)
+    for (int k = 0; k < til.n_ct; ++k) CHECK(til.cn[k] <= kGemvCols, "GEMV tile %d has %d columns", k, til.cn[k]);
   // tiles partition the columns; tile_of agrees with tile_range
   {
     int next = 0;
@@ -259,9 +263,10 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
 
 int main() {
   int case_no = 0;
-  int n_kv, d, G, n_q, n_chunks, nb, i8, rc;
+  int n_kv, d, G, n_q, n_chunks, nb, i8, rc, gv;
   long long cap;
-  while (std::scanf("%d %d %d %d %d %lld %d %d %d", &n_kv, &d, &G, &n_q, &n_chunks, &cap, &i8, &rc, &nb) == 9) {
+  while (std::scanf("%d %d %d %d %d %lld %d %d %d %d", &n_kv, &d, &G, &n_q, &n_chunks, &cap, &i8, &rc, &gv, &nb) ==
+         10) {
     std::vector<int> T(nb), rk(nb), rv(nb);
     for (int b = 0; b < nb; ++b)
       if (std::scanf("%d %d %d", &T[b], &rk[b], &rv[b]) != 3) return 2;
@@ -270,7 +275,7 @@ int main() {
     std::vector<int> table(n_sel);
     for (int j = 0; j < n_sel; ++j)
       if (std::scanf("%d", &table[j]) != 1) return 2;
-    run_case(case_no++, n_kv, d, G, n_q, n_chunks, cap, i8, rc, T, rk, rv, table);
+    run_case(case_no++, n_kv, d, G, n_q, n_chunks, cap, i8, rc, gv, T, rk, rv, table);
   }
   std::printf("%s (%d cases)\n", fails ? "FAIL" : "OK", case_no);
   return fails ? 1 : 0;

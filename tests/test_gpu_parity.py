@@ -429,3 +429,51 @@ def test_parity_random_shapes(seed):
     inp, table = _random_case(seed)
     _check(inp, table=table, label=f"random seed {seed} (d={inp.head_dim}, H_kv={inp.n_kv_heads}, "
                                    f"G={inp.n_q_heads // inp.n_kv_heads}, blocks {len(table)}/{inp.n_blocks})")
+
+
+# small decode batches: at most 16 query columns per KV head, where the latent
+# projection may run as a wavefront GEMV (kernel variant, MILO_PROJECTION=gemv)
+GEMV_SHAPES = {
+    "tiny_config": None,
+    "one_query_g7_ragged": dict(block_tokens=[513, 64, 300, 1], rank_k=[96, 64, 33, 1], rank_v=[64, 32, 100, 1],
+                                n_kv_heads=2, head_dim=64, n_q=1, n_q_heads=14, tail_cap=70, tail_len=[70]),
+    "two_queries_g8_16_columns": dict(block_tokens=[1024, 700], rank_k=[512, 288], n_kv_heads=4, head_dim=128,
+                                      n_q=2, n_q_heads=32, tail_cap=300, tail_len=[300, 5]),
+    "g2_four_heads_per_tile_rank896": dict(block_tokens=[1000, 256], rank_k=[896, 128], rank_v=[840, 64],
+                                           n_kv_heads=8, head_dim=128, n_q=1, n_q_heads=16, tail_cap=9),
+    "g16_one_query": dict(block_tokens=[256, 128], rank_k=[64, 32], n_kv_heads=1, head_dim=64, n_q=1,
+                          n_q_heads=16, tail_cap=0),
+}
+
+
+@pytest.mark.parametrize("name", list(GEMV_SHAPES))
+def test_projection_variants_agree(name, monkeypatch):
+    """The GEMV projection and the MFMA one (the default), chosen through
+    MILO_PROJECTION, each match the oracle and each other."""
+    inp = synth.gen_layer("tiny") if GEMV_SHAPES[name] is None else \
+        synth.make_problem(zlib.crc32(name.encode()) % 1000, **GEMV_SHAPES[name])
+    ref = oracle.attend_latent(**oracle_args(inp))
+    outs = {}
+    for variant in ("gemv", "mfma"):
+        monkeypatch.setenv("MILO_PROJECTION", variant)
+        gl = GpuLayer(inp)
+        try:
+            outs[variant] = gl.attend().cpu().numpy()
+        finally:
+            gl.free()
+        err = max_rel_l2(outs[variant], ref)
+        print(f"[parity] {name} {variant} projection: max rel-L2 = {err:.3e}", flush=True)
+        assert err <= TOL_REL_L2
+    assert max_rel_l2(outs["gemv"], outs["mfma"]) <= TOL_REL_L2
+
+
+def test_gemv_projection_refuses_wide_batches(monkeypatch):
+    from paper_2609_29913_amd import milo
+    monkeypatch.setenv("MILO_PROJECTION", "gemv")
+    inp = synth.make_problem(3, [256], [32], n_kv_heads=1, head_dim=64, n_q=3, n_q_heads=8, tail_cap=0)
+    gl = GpuLayer(inp)
+    try:
+        with pytest.raises(milo.MiloError, match="GEMV"):
+            gl.attend()
+    finally:
+        gl.free()

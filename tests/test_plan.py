@@ -26,11 +26,12 @@ def checker(tmp_path_factory):
     return exe
 
 
-def _case(n_kv, d, G, n_q, n_chunks, T, rk, rv=None, table=None, cap=-1, i8=False, recon=0):
-    """recon: 0 every block latent, 1 every selected block reconstructed, 2 every other one."""
+def _case(n_kv, d, G, n_q, n_chunks, T, rk, rv=None, table=None, cap=-1, i8=False, recon=0, gemv=False):
+    """recon: 0 every block latent, 1 every selected block reconstructed, 2 every
+    other one; gemv: the projection runs as a GEMV (tiles of at most 16 columns)."""
     rv = rk if rv is None else rv
     table = list(range(len(T))) if table is None else table
-    head = f"{n_kv} {d} {G} {n_q} {n_chunks} {cap} {int(i8)} {recon} {len(T)}"
+    head = f"{n_kv} {d} {G} {n_q} {n_chunks} {cap} {int(i8)} {recon} {int(gemv)} {len(T)}"
     blocks = " ".join(f"{t} {a} {b}" for t, a, b in zip(T, rk, rv))
     return f"{head} {blocks} {len(table)} {' '.join(map(str, table))}\n"
 
@@ -136,3 +137,18 @@ def test_plans_with_reconstructed_blocks(checker):
         table = [int(b) for b in rng.permutation(nb)[:k]]
         cases.append(_case(n_kv, d, G, n_q, int(rng.integers(0, 5)), T, rk, rv, table, recon=int(rng.integers(1, 3))))
     _run(checker, cases)
+
+
+def test_gemv_tiling(checker):
+    """With the GEMV projection, tiles that pack whole KV heads hold at most 16
+    columns: 7 columns per head -> two heads per tile, 2 -> four, 16 -> one; the
+    MFMA projection packs up to 64."""
+    cases = [_case(8, 128, 7, 1, 1, [512] * 4, [64] * 4, gemv=True),
+             _case(8, 64, 2, 1, 1, [512] * 4, [64] * 4, gemv=True),
+             _case(4, 128, 4, 4, 1, [512] * 4, [64] * 4, gemv=True),
+             _case(8, 128, 7, 1, 1, [512] * 4, [64] * 4, gemv=False)]
+    lines = _run(checker, cases).splitlines()
+    assert "tiles 4 (mode 0)" in lines[0]
+    assert "tiles 2 (mode 0)" in lines[1]
+    assert "tiles 4 (mode 0)" in lines[2]
+    assert "tiles 2 (mode 0)" in lines[3]
