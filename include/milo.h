@@ -54,8 +54,12 @@ typedef struct milo_cache milo_cache;
  *   n_kv_heads    H_kv >= 1
  *   head_dim      d, 64 or 128 (others return MILO_ERR_UNSUPPORTED)
  *   block_tokens  [n_blocks] T_b >= 1
- *   rank_k/v      [n_blocks] 1 <= r <= min(T_b, H_kv*d); this library supports
- *                 r <= 896 (larger ranks return MILO_ERR_UNSUPPORTED). */
+ *   rank_k/v      [n_blocks] 1 <= r <= min(T_b, H_kv*d), at most 1024 (larger
+ *                 ranks return MILO_ERR_UNSUPPORTED).  The latent route handles
+ *                 r <= 896; a selected block of higher rank (full rank at
+ *                 H_kv*d = 1024) is always attended by reconstruction
+ *                 (milo_cache_set_path), so INT8 caches stay at r <= 896 and
+ *                 milo_attend_decode_noalloc refuses such blocks. */
 typedef struct milo_cache_desc {
   int32_t n_blocks;
   int32_t n_kv_heads;

@@ -193,8 +193,9 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     if (a < 1 || a > T || a > D || v < 1 || v > T || v > D)
       return fail(MILO_ERR_INVALID_ARG, "block %d: ranks (%d, %d) must lie in [1, min(T_b=%d, H_kv*d=%lld)]",
                   b, a, v, T, (long long)D);
-    if (a > kMaxRank || v > kMaxRank)
-      return fail(MILO_ERR_UNSUPPORTED, "block %d: rank above the supported maximum %d", b, kMaxRank);
+    const int rmax = i8 ? kMaxRank : kMaxStoredRank;  // INT8 blocks attend latent only
+    if (a > rmax || v > rmax)
+      return fail(MILO_ERR_UNSUPPORTED, "block %d: rank above the supported maximum %d", b, rmax);
     if (!pk[b] || !rk[b] || !pv[b] || !rv[b]) return fail(MILO_ERR_INVALID_ARG, "block %d: NULL factor", b);
   }
 
@@ -564,13 +565,18 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     return fail(MILO_ERR_UNSUPPORTED, "this entry point attends latent only (reconstruction needs a workspace)");
   std::vector<char> recon((size_t)std::max(n_sel, 1), 0);
   int n_recon = 0;
-  if (c->path != MILO_PATH_LATENT && ws.can_recon()) {
-    for (int j = 0; j < n_sel; ++j) {
-      const int b = block_table[j];
+  for (int j = 0; j < n_sel; ++j) {
+    const int b = block_table[j];
+    // ranks beyond the latent route's reach are always reconstructed
+    const bool must = c->rk[b] > kMaxRank || c->rv[b] > kMaxRank;
+    if (must && !ws.can_recon())
+      return fail(MILO_ERR_UNSUPPORTED, "block %d has rank above %d and needs reconstruction, which this entry point "
+                  "does not do", b, kMaxRank);
+    if (must) recon[j] = 1;
+    else if (c->path != MILO_PATH_LATENT && ws.can_recon())
       recon[j] = c->path == MILO_PATH_RECONSTRUCT ||
                  recon_pays(c->T[b], c->rk[b], c->rv[b], (int64_t)n_q * n_q_heads, c->n_kv * c->d, c->d);
-      n_recon += recon[j];
-    }
+    n_recon += recon[j];
   }
 
   // ---- the latent projection: MFMA (measured faster on gfx950 at every batch,
@@ -610,6 +616,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   key.push_back(n_q_heads);
   key.push_back(n_chunks);
   key.push_back(n_recon > 0 ? c->path : MILO_PATH_LATENT);
+  key.push_back(n_recon);
   key.push_back(gemv ? 1 : 0);
   key.insert(key.end(), block_table, block_table + n_sel);
   const int n_cols = n_q * n_q_heads;

@@ -405,7 +405,8 @@ constexpr int kTokWave = kTile / kWaves;       // tokens per wave per tile (one 
 static_assert(kTokWave == 32, "the score pass gives every wave one 32-token sub-tile");
 constexpr int kWStride = kTile + 8;            // bf16 row stride of the weight tile in LDS
 constexpr int kMaxGroup = 16;                  // max query heads per KV head
-constexpr int kMaxRank = 896;                  // largest supported rank (LDS bound)
+constexpr int kMaxRank = 896;                  // largest rank of the latent route (LDS bound)
+constexpr int kMaxStoredRank = 1024;           // largest rank a cache stores (higher-rank blocks are reconstructed)
 constexpr int kLdsBytes = 160 * 1024;          // LDS per workgroup on gfx950
 constexpr int kTailChunk = kWaves * 32;        // dense-tail tokens per work item
 constexpr int kXcds = 8;                       // XCDs of an MI355X (workgroup b runs on XCD b % 8)

@@ -35,9 +35,9 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, n)
 
 
-def _desc(nb=1, nkv=1, d=64, T=(64,), rk=(8,), rv=(8,)):
+def _desc(nb=1, nkv=1, d=64, T=(64,), rk=(8,), rv=(8,), p_format=0):
     bt, a, b = (ctypes.c_int32 * nb)(*T), (ctypes.c_int32 * nb)(*rk), (ctypes.c_int32 * nb)(*rv)
-    return milo.milo_cache_desc(nb, nkv, d, bt, a, b), (bt, a, b)
+    return milo.milo_cache_desc(nb, nkv, d, bt, a, b, p_format), (bt, a, b)
 
 
 def _create(desc, nb=1, null_factor=False):
@@ -54,7 +54,9 @@ def _create(desc, nb=1, null_factor=False):
     (dict(nb=1, T=(300,), rk=(65,), rv=(8,)), milo.MILO_ERR_INVALID_ARG),     # rank > H_kv*d
     (dict(nb=1, T=(64,), rk=(8,), rv=(0,)), milo.MILO_ERR_INVALID_ARG),       # rank 0
     (dict(nb=1, d=96, T=(64,), rk=(8,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # head_dim
-    (dict(nb=1, nkv=8, d=128, T=(2048,), rk=(928,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # rank cap
+    (dict(nb=1, nkv=16, d=128, T=(2048,), rk=(1056,), rv=(8,)), milo.MILO_ERR_UNSUPPORTED),  # rank cap (1024)
+    (dict(nb=1, nkv=8, d=128, T=(2048,), rk=(928,), rv=(8,), p_format=1),
+     milo.MILO_ERR_UNSUPPORTED),                                                 # INT8 rank cap (896)
     (dict(nb=1, nkv=0, T=(64,), rk=(8,), rv=(8,)), milo.MILO_ERR_INVALID_ARG),
 ])
 def test_create_rejects(kw, code):

@@ -61,8 +61,6 @@ def test_reconstruct_every_block(name):
 def test_reconstruct_random_shapes(seed):
     from paper_2609_29913_amd import milo
     inp, table = _random_case(seed)
-    if max(max(inp.rank_k), max(inp.rank_v)) > 896:
-        pytest.skip("rank above the supported maximum")
     _, n_rec = _run(inp, milo.MILO_PATH_RECONSTRUCT, table=table, label=f"random seed {seed}")
     assert n_rec == len(table)
 
@@ -214,3 +212,49 @@ def test_entry_points_that_cannot_rebuild():
         milo.milo_cache_set_path(g8.cache, milo.MILO_PATH_LATENT)
     finally:
         g8.free()
+
+
+def test_ranks_above_the_latent_reach_are_rebuilt():
+    """Blocks of rank 897..1024 (full rank at H_kv d = 1024, the 14B / 32B head
+    shape) are stored and always attended by reconstruction, whatever the path
+    setting; lower-rank blocks of the same call stay latent under LATENT."""
+    import torch
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(41, [1024, 1300, 512, 1024], [1024, 960, 64, 900], [1024, 1000, 96, 896],
+                             n_kv_heads=8, head_dim=128, n_q=2, n_q_heads=40, tail_cap=50, tail_len=[50, 3])
+    got, n_rec = _run(inp, milo.MILO_PATH_LATENT, label="ranks up to 1024 under LATENT")
+    assert n_rec == 3
+    gl = GpuLayer(inp)
+    try:
+        out = torch.zeros(inp.q.shape, dtype=torch.float32, device="cuda")
+        with pytest.raises(milo.MiloError, match="needs reconstruction"):
+            milo.milo_attend_decode_noalloc(gl.cache, [0, 2], gl.q, gl.tk, gl.tv, inp.tail_len, inp.scale, out)
+        # a table of only latent-reach blocks still works there
+        milo.milo_attend_decode_noalloc(gl.cache, [2], gl.q, gl.tk, gl.tv, inp.tail_len, inp.scale, out)
+        torch.cuda.synchronize()
+        assert max_rel_l2(out.cpu().numpy(), oracle.attend_latent(**oracle_args(inp, [2]))) <= TOL_REL_L2
+    finally:
+        gl.free()
+    with pytest.raises(milo.MiloError, match="rank above"):
+        GpuLayer(inp, p_int8=True)
+
+
+def test_full_rank_identity_factors_give_dense_attention():
+    """P = K and R = I at full rank D = H_kv d = 1024: the factors hold the keys
+    and values themselves, so the call computes plain dense attention over
+    them (the oracle's definition), rebuilt exactly (bf16 products with one)."""
+    from paper_2609_29913_amd import milo
+    rng = np.random.default_rng(5)
+    n_kv, d, T = 8, 128, [1024, 1100]
+    D = n_kv * d
+    base = synth.make_problem(42, T, [64, 64], n_kv_heads=n_kv, head_dim=d, n_q=2, n_q_heads=16, tail_cap=20)
+    eye = synth.f32_to_bf16(np.eye(D, dtype=np.float32))
+    keys = [synth.f32_to_bf16(rng.standard_normal((t, D)).astype(np.float32)) for t in T]
+    vals = [synth.f32_to_bf16(rng.standard_normal((t, D)).astype(np.float32)) for t in T]
+    inp = synth.LayerInputs(n_kv_heads=n_kv, head_dim=d, n_q_heads=16, block_tokens=np.array(T, np.int32),
+                            rank_k=np.array([D, D], np.int32), rank_v=np.array([D, D], np.int32),
+                            pk=keys, rk=[eye, eye], pv=vals, rv=[eye, eye], q=base.q, tail_k=base.tail_k,
+                            tail_v=base.tail_v, tail_len=base.tail_len, scale=base.scale)
+    got, n_rec = _run(inp, milo.MILO_PATH_AUTO, label="P = K, R = I at rank 1024")
+    assert n_rec == 2
+    assert max_rel_l2(got, oracle.attend_dense(**oracle_args(inp))) <= TOL_REL_L2
