@@ -174,9 +174,7 @@ def run_prefill(args, cfg, dev):
         layers[k % copies].step(stream)
     torch.cuda.synchronize()
     att_ms, merge_ms, n_calls = milo.milo_timing_read()
-    recon_ms, _ = milo.milo_timing_read_recon()
     milo.milo_timing_enable(False)
-    recon_blocks = sum(milo.milo_cache_recon_blocks(layer.cache) for layer in groups[0])
     att_s = att_ms / n_calls * 1e-3
     kern_bytes = first.bytes  # the attention kernel reads every factor, the tail and the queries once
     flops = first.flops

@@ -597,10 +597,28 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     }
   }
 
+  // ---- a prefill chunk of kSharedTailMinTokens tokens or more attends its
+  // shared tail once per KV head: packed like a reconstructed block (rows up to
+  // a planned capacity, the longest tail rounded up to a power of two of
+  // 256-token tiles, at most tail_cap) and read by dense items whose columns
+  // mask tokens past their causal limit.  Smaller chunks (measured on the
+  // 7B-shaped layer after 256 tail rows: 16 tokens +16%, 64 tokens +3%, 256
+  // tokens -5% attention time with the packed tail), INT8 caches and
+  // workspaces without a reconstruction buffer use tail items per token ----
+  constexpr int kSharedTailMinTokens = 128;
+  const bool shared_tail =
+      causal && max_len > 0 && n_q >= kSharedTailMinTokens && !c->p_int8 && ws.can_recon();
+  int tail_tiles = 0;
+  if (shared_tail) {
+    tail_tiles = 1;
+    while (tail_tiles * kTile < max_len) tail_tiles *= 2;
+    tail_tiles = std::min(tail_tiles, (tail_cap + kTile - 1) / kTile);
+  }
+
   // ---- plan: rebuilt only when the block table, the batch shape or the tail
   // chunk capacity changes (the longest tail rounded up to a power of two of
   // chunks, at most tail_cap), not when tails merely grow ----
-  const int need_chunks = (max_len + kTailChunk - 1) / kTailChunk;
+  const int need_chunks = shared_tail ? 0 : (max_len + kTailChunk - 1) / kTailChunk;
   int n_chunks = 0;
   if (need_chunks > 0) {
     n_chunks = 1;
@@ -618,6 +636,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   key.push_back(n_recon > 0 ? c->path : MILO_PATH_LATENT);
   key.push_back(n_recon);
   key.push_back(gemv ? 1 : 0);
+  key.push_back(tail_tiles);
   key.insert(key.end(), block_table, block_table + n_sel);
   const int n_cols = n_q * n_q_heads;
   if (key != ps.key) {
@@ -627,16 +646,34 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ps.key.clear();
     std::vector<int64_t> region;
     ReconPlan rp;
-    if (n_recon > 0) {
-      region.assign(c->n_blocks, -1);
+    // the blocks the plan sees: the cache's, plus the packed shared tail as
+    // block n_blocks after the table's last entry
+    std::vector<BlockMeta> meta_x;
+    std::vector<int32_t> table_x(block_table, block_table + n_sel);
+    int64_t tail_region = -1;
+    if (n_recon > 0 || shared_tail) {
+      region.assign(c->n_blocks + 1, -1);
       build_recon_plan(c->meta.data(), block_table, n_sel, recon.data(), c->n_kv, c->d, &region, &rp);
     }
-    const Tiling til = make_tiling(c->n_kv, n_q * G, n_recon > 0, gemv ? kGemvCols : kCols);
+    if (shared_tail) {
+      meta_x = c->meta;
+      BlockMeta tm{};
+      tm.T = tail_tiles * kTile;
+      tm.T_pad = tail_tiles * kTile;
+      tm.rk_pad = tm.rv_pad = c->d;
+      meta_x.push_back(tm);
+      tail_region = rp.elems;
+      region[c->n_blocks] = tail_region;
+      rp.elems += 2LL * tm.T_pad * c->n_kv * c->d;
+      table_x.push_back(c->n_blocks);
+    }
+    const Tiling til = make_tiling(c->n_kv, n_q * G, n_recon > 0 || shared_tail, gemv ? kGemvCols : kCols);
     Schedule sch;
     std::string why;
-    PlanInput pin{c->meta.data(), c->n_kv, c->d, c->p_int8};
-    pin.recon_region = n_recon > 0 ? region.data() : nullptr;
-    if (!build_schedule(pin, block_table, n_sel, n_q, n_chunks, til, env_program_cap(), &sch, &why))
+    PlanInput pin{shared_tail ? meta_x.data() : c->meta.data(), c->n_kv, c->d, c->p_int8};
+    pin.recon_region = region.empty() ? nullptr : region.data();
+    pin.causal_block = shared_tail ? c->n_blocks : -1;
+    if (!build_schedule(pin, table_x.data(), (int)table_x.size(), n_q, n_chunks, til, env_program_cap(), &sch, &why))
       return fail(MILO_ERR_UNSUPPORTED, "%s", why.c_str());
     // the reconstruction table and tasks follow the schedule in the plan
     int64_t rb_off = 0, rt_off = 0;
@@ -691,6 +728,8 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ps.recon_blocks_off = rb_off;
     ps.recon_tasks_off = rt_off;
     ps.recon_elems = rp.elems;
+    ps.tail_region = tail_region;
+    ps.tail_T_pad = tail_tiles * kTile;
     ps.gemv = gemv;
     ps.key.swap(key);
     ++ps.builds;
@@ -717,7 +756,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   // reconstruction buffer of this call
   uint16_t* rbuf = nullptr;
   int recon_delta = 0;
-  if (ps.n_recon_tasks > 0) {
+  if (ps.recon_elems > 0) {
     if (const int err = ws.recon_buffer(ps.recon_elems, c->data, s, &rbuf); err != MILO_OK) return err;
     const int64_t dbytes = (reinterpret_cast<const unsigned char*>(rbuf) - reinterpret_cast<const unsigned char*>(c->data));
     const int64_t dfr = dbytes / (kFragElems * 2);
@@ -760,6 +799,10 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   ma.n_slots = ps.n_slots;
   ma.tiles = ps.tiles;
   ma.tl = tls;
+  if (ps.tail_region >= 0) {  // the shared tail's partials sit in block slots
+    ma.tl = TailLens{};
+    ma.tl.mode = kTailAffine;
+  }
 
   // timing: events recorded by the launches themselves at kernel start and end
   // attend start / end, merge start / end, reconstruction start / end
@@ -802,6 +845,18 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ra.tasks = reinterpret_cast<const int2*>(ps.plan_d + ps.recon_tasks_off);
     e = launch_recon(ra, c->d, ps.n_recon_tasks, s, ev[4], ev[5]);
     if (e != hipSuccess) return launch_fail(e, "reconstruction kernel launch");
+  }
+  if (ps.tail_region >= 0) {
+    TailPackArgs ta{};
+    ta.tail_k = tail_k;
+    ta.tail_v = tail_v;
+    ta.recon = rbuf;
+    ta.region = ps.tail_region;
+    ta.rows = max_len;
+    ta.T_pad = ps.tail_T_pad;
+    ta.n_kv = c->n_kv;
+    e = launch_pack_tail(ta, c->d, s);
+    if (e != hipSuccess) return launch_fail(e, "tail packing kernel launch");
   }
   for (int l = 0; l < ps.n_launch; ++l) {
     aa.wg = reinterpret_cast<const WgProgram*>(ps.plan_d) + (size_t)l * kCUs;

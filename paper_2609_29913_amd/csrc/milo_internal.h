@@ -374,7 +374,9 @@ static_assert(sizeof(WorkItem) == 80, "work item layout");
 // n_block_slots + their chunk index.
 // kItemInt8: INT8 P factors; kItemDense: a reconstructed block (its metadata
 // names one KV head's K and V in the reconstruction buffer)
-enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2, kItemInt8 = 4, kItemDense = 8 };
+// kItemCausal: a dense item over a prefill chunk's shared tail, whose column of
+// request i sees only its first tail_len_of(tl, i) tokens
+enum ItemFlags : int32_t { kItemFirst = 1, kItemFlush = 2, kItemInt8 = 4, kItemDense = 8, kItemCausal = 16 };
 // packed fields of a block item's flags: bits 8-9 lg_rank_groups of its block,
 // bits 16-21 the tile's column count - 1, bits 24-26 its KV head count - 1
 constexpr int kItemLgNgShift = 8;
@@ -524,6 +526,17 @@ hipError_t launch_attend(const AttendArgs& a, int head_dim, int max_rt, int nslo
                          size_t lds_bytes, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int n_cols, hipStream_t s, hipEvent_t e0 = nullptr,
                         hipEvent_t e1 = nullptr);
+// The shared tail of a prefill chunk (rows [0, rows) of tail_k / tail_v,
+// [tail_cap][n_kv][d]) packed like a reconstructed block of T_pad tokens (rows
+// past `rows` zero) at element `region` of the reconstruction buffer.
+struct TailPackArgs {
+  const uint16_t* tail_k;
+  const uint16_t* tail_v;
+  uint16_t* recon;
+  int64_t region;
+  int rows, T_pad, n_kv;
+};
+hipError_t launch_pack_tail(const TailPackArgs& a, int head_dim, hipStream_t s);
 // Reconstruction of the dense blocks of a call: one workgroup per task.
 hipError_t launch_recon(const ReconArgs& a, int head_dim, int n_tasks, hipStream_t s, hipEvent_t e0 = nullptr,
                         hipEvent_t e1 = nullptr);

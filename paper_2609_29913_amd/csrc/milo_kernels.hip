@@ -598,6 +598,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   // (rank d); the query takes the projection's place and the value pass gives
   // the output
   const bool dense = (it.flags & kItemDense) != 0;
+  const bool causal = (it.flags & kItemCausal) != 0;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lrow = lane & 31, lhi = lane >> 5;
@@ -612,6 +613,17 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   const int nst = 16 / nseg;                // 16-token steps of the wave's segment per tile
   const int T = bm.T;
   const int ntiles = it.ntile, tile0 = it.tile0;  // tiles this item covers
+  // causal limits of this lane's two columns (32 ch + lane % 32; request (c mod N_g) / G)
+  // and the smallest over the tile (wave-uniform), past which tokens need masking
+  int lim[2] = {T, T}, lim_min = T;
+  if (causal) {
+#pragma unroll
+    for (int ch = 0; ch < 2; ++ch)
+      lim[ch] = tail_len_of(a.tl, ((c0 + min(32 * ch + (lane & 31), cn - 1)) % N_g) / G);
+    lim_min = min(lim[0], lim[1]);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) lim_min = min(lim_min, __shfl_xor(lim_min, off));
+  }
   __bf16* qt = reinterpret_cast<__bf16*>(smem);              // [kCols][qsd]
   // the weight tile: [kCols][kWS] bf16, all 256 tokens of a tile, or (WH) one
   // 128-token half at a time when LDS is short (ranks above 512)
@@ -792,15 +804,16 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       }
     }
     // mask tokens past the end of the block (only the block's last tile can
-    // hold any; the test is wave-uniform), wave-local column max
+    // hold any; the test is wave-uniform), and for a prefill chunk's shared
+    // tail the tokens past each column's causal limit; wave-local column max
     float mx[2] = {-INFINITY, -INFINITY};
-    if (tw + kTokWave > T) {
+    if (tw + kTokWave > T || (causal && tw + kTokWave > lim_min)) {
 #pragma unroll
       for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int tok = tw + 8 * (v >> 2) + 4 * lhi + (v & 3);
-          if (tok >= T) sc[ch][v] = -INFINITY;
+          if (tok >= T || tok >= lim[ch]) sc[ch][v] = -INFINITY;
         }
     }
 #pragma unroll
@@ -820,7 +833,9 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 #pragma unroll
       for (int w = 1; w < kWaves; ++w) tm = fmaxf(tm, red[w * kCols + 32 * ch + lrow]);
       const float mn = fmaxf(m_run[ch], tm);
-      alpha[ch] = fast_exp2(m_run[ch] - mn);
+      // a column with no key so far (a causal column before its first token)
+      // keeps m = -inf and zero weights
+      alpha[ch] = mn == -INFINITY ? 1.f : fast_exp2(m_run[ch] - mn);
       m_run[ch] = mn;
     }
     // weights W = 2^(s - m) (bf16) in registers, then to LDS as [col][token]
@@ -828,11 +843,12 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
       float lsum = 0.f;
+      const float mref = m_run[ch] == -INFINITY ? 0.f : m_run[ch];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const float w = fast_exp2(sc[ch][4 * j + u] - m_run[ch]);
+          const float w = fast_exp2(sc[ch][4 * j + u] - mref);
           lsum += w;
           if constexpr (I8) wv[ch][j][u] = (__bf16)(w * vsc[4 * j + u]);
           else wv[ch][j][u] = (__bf16)w;
@@ -1061,8 +1077,8 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
       const float mn = first ? m_run[ch] : fmaxf(acc.m[ch], m_run[ch]);
-      fa[ch] = first ? 0.f : fast_exp2(acc.m[ch] - mn);
-      fb[ch] = fast_exp2(m_run[ch] - mn);
+      fa[ch] = first || mn == -INFINITY ? 0.f : fast_exp2(acc.m[ch] - mn);
+      fb[ch] = mn == -INFINITY ? 0.f : fast_exp2(m_run[ch] - mn);
       acc.m[ch] = mn;
     }
 #pragma unroll

@@ -371,7 +371,7 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
             w.ntile = pt.ntile;
             w.flags = (lg_rank_groups(w.blk.rv_pad / 32) << kItemLgNgShift) | ((til.cn[tile] - 1) << kItemColsShift) |
                       ((til.nh[tile] - 1) << kItemHeadsShift) | (c.p_int8 ? kItemInt8 : 0) |
-                      (dense ? kItemDense : 0);
+                      (dense ? kItemDense : 0) | (pt.b == c.causal_block ? kItemCausal : 0);
             items.push_back(w);
           }
           emit(l, wg, items);

@@ -21,6 +21,9 @@ struct PlanInput {
   // the reconstruction buffer, or -1 (latent); NULL: every block latent.  A plan
   // with reconstructed blocks needs one KV head per column tile.
   const int64_t* recon_region = nullptr;
+  // a prefill chunk's shared tail, attended as a packed dense block: its block
+  // id in meta / recon_region (its items carry kItemCausal), or -1
+  int causal_block = -1;
 };
 
 struct Tiling {

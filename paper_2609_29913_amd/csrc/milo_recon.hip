@@ -234,6 +234,45 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(ReconArgs a) {
   else recon_task<D, 0>(a, rb, g, t, smem);
 }
 
+// One wave per packed fragment of a prefill chunk's shared tail (K of every
+// head in the P^K layout of rank d, V in the P^V layout, as the reconstruction
+// kernel stores them); lane (c, m) gathers its 8 elements.
+template <int D>
+__global__ __launch_bounds__(256) void pack_tail_kernel(TailPackArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t per_side = (int64_t)a.T_pad * D / kFragElems;
+  const int64_t f = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (f >= 2 * a.n_kv * per_side) return;
+  const int g = (int)(f / (2 * per_side)), side = (int)((f / per_side) & 1);
+  const int64_t fr = f % per_side;
+  const int m = lane & 31, c = lane >> 5;
+  const int64_t rs = (int64_t)a.n_kv * D;  // tail row stride
+  uint4 v;
+  __bf16* ve = reinterpret_cast<__bf16*>(&v);
+  if (side == 0) {
+    // fragment (tau = 8 t + w, kap) of the P^K layout: dims 16 kap + 8 c .. +7 of token 32 tau + m
+    constexpr int nks = D / 16;
+    const int tiles = a.T_pad / kTile;
+    const int kap = (int)(fr % nks), t = (int)((fr / nks) % tiles), w = (int)(fr / ((int64_t)nks * tiles));
+    const int row = 32 * (kWaves * t + w) + m;
+    if (row < a.rows) v = *reinterpret_cast<const uint4*>(a.tail_k + row * rs + (int64_t)g * D + 16 * kap + 8 * c);
+    else v = make_uint4(0, 0, 0, 0);
+  } else {
+    // fragment rho T_pad / 16 + sig of the P^V layout at rank d: tokens 16 sig + 8 c .. +7 of dim 32 rho + m
+    const int T16 = a.T_pad / 16;
+    const int rho = (int)(fr / T16), sig = (int)(fr % T16);
+    const uint16_t* src = a.tail_v + (int64_t)g * D + 32 * rho + m;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int row = 16 * sig + 8 * c + e;
+      const uint16_t u = row < a.rows ? src[row * rs] : (uint16_t)0;
+      ve[e] = *reinterpret_cast<const __bf16*>(&u);
+    }
+  }
+  uint16_t* dst = a.recon + a.region + ((int64_t)g * 2 + side) * a.T_pad * D + fr * kFragElems;
+  *reinterpret_cast<uint4*>(dst + 8 * lane) = v;
+}
+
 template <int D>
 hipError_t launch_recon_t(const ReconArgs& a, int n_tasks, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const size_t lds = recon_lds_bytes(D);
@@ -249,6 +288,15 @@ hipError_t launch_recon_t(const ReconArgs& a, int n_tasks, hipStream_t s, hipEve
 }
 
 }  // namespace
+
+hipError_t launch_pack_tail(const TailPackArgs& a, int head_dim, hipStream_t s) {
+  const int64_t frags = 2LL * a.n_kv * a.T_pad * head_dim / kFragElems;
+  const dim3 grid((unsigned)((frags + 3) / 4));
+  if (head_dim == 64) hipLaunchKernelGGL(pack_tail_kernel<64>, grid, dim3(256), 0, s, a);
+  else if (head_dim == 128) hipLaunchKernelGGL(pack_tail_kernel<128>, grid, dim3(256), 0, s, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 hipError_t launch_recon(const ReconArgs& a, int head_dim, int n_tasks, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (n_tasks <= 0) return hipSuccess;

@@ -346,6 +346,13 @@ PREFILL = {
     # 7B-shaped heads, 64-token chunk after 192 tail rows
     "q7b_heads_chunk64": dict(block_tokens=[1024] * 4, rank_k=[64, 512, 288, 160], n_kv_heads=4,
                               head_dim=128, n_q_heads=28, n_tok=64, tail_base=192, extra_rows=0),
+    # chunks of 128 tokens and more attend the shared tail as one packed block per
+    # KV head with per-column causal limits: early columns see nothing in the
+    # tail's second tile, spare capacity rows past the chunk stay masked
+    "packed_tail_chunk160_after_300": dict(block_tokens=[700, 1024], rank_k=[96, 448], n_kv_heads=4,
+                                           head_dim=128, n_q_heads=28, n_tok=160, tail_base=300, extra_rows=40),
+    "packed_tail_d64_chunk128_from_0": dict(block_tokens=[256], rank_k=[64], n_kv_heads=8, head_dim=64,
+                                            n_q_heads=16, n_tok=128, tail_base=0, extra_rows=50),
 }
 
 
