@@ -729,6 +729,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ps.recon_tasks_off = rt_off;
     ps.recon_elems = rp.elems;
     ps.tail_region = tail_region;
+    ps.run_cap = sch.run_cap;
     ps.tail_T_pad = tail_tiles * kTile;
     ps.gemv = gemv;
     ps.key.swap(key);
@@ -769,6 +770,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   AttendArgs aa{};
   aa.data = c->data;
   aa.recon_delta = recon_delta;
+  aa.run_cap = ps.run_cap;
   aa.prog = ps.plan_d;
   aa.q = q;
   aa.tail_k = tail_k;

@@ -31,6 +31,7 @@ struct PlanState {
   int64_t recon_blocks_off = 0, recon_tasks_off = 0;  // byte offsets in the plan
   int64_t recon_elems = 0;                            // reconstruction buffer (bf16 elements)
   bool gemv = false;                                  // latent projection as a wavefront GEMV
+  int run_cap = kRunCap;                              // run buffer entries of the plan
   int64_t tail_region = -1;                           // a prefill chunk's packed shared tail (or -1)
   int tail_T_pad = 0;                                 // its planned rows
 };

@@ -103,10 +103,14 @@ __host__ __device__ inline int64_t i8_scale_bytes(int T_pad) { return (int64_t)(
 // Most 256-token tiles in one block item (parts of larger blocks are split),
 // most KV heads one 64-column tile may span, and so the most fragment runs
 // one item gives a wave (plus an end marker): the R^K and R^V runs of every
-// head, per tile the P^K run, the scale unit (INT8) and the P^V run.
+// head, per tile the P^K run, the scale unit (INT8) and the P^V run.  A plan
+// sizes its run buffers for its own items (run_cap_for; kRunCap at most).
 constexpr int kMaxPartTiles = 8;
 constexpr int kMaxTileHeads = 4;
 constexpr int kRunCap = 2 * kMaxTileHeads + 3 * kMaxPartTiles + 2;
+__host__ __device__ inline int run_cap_for(int max_heads, int max_tiles, bool i8) {
+  return 2 * max_heads + (i8 ? 3 : 2) * max_tiles + 2;
+}
 constexpr int kRunBufs = 4;  // run buffers per wave in the attention kernel
 // A run (x, n) names n units of one kind, encoded in bits 28-29 of n:
 //   kRunBf16   bf16 fragments x .. x+n-1 (1 KiB each)
@@ -483,6 +487,7 @@ struct AttendArgs {
   int ring_offset;           // byte offset of the per-wave fragment rings in the work area
   int N_g;                   // query columns per KV head, n_q * G
   int recon_delta;           // fragments from `data` to the reconstruction buffer (dense items)
+  int run_cap;               // entries of a run buffer (the plan's bound, <= kRunCap)
   TailLens tl;               // tail lengths of this call
 };
 

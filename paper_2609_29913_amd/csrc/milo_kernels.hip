@@ -389,7 +389,8 @@ struct FragRing {
   __bf16* ring;               // this wave's NSLOT slots
   uint32_t ring_lds;          // LDS byte address of slot 0 (wave-uniform)
   const int2* run;            // current entry of the run buffers (LDS)
-  int2* rbuf;                 // this wave's kRunBufs run buffers of kRunCap entries
+  int2* rbuf;                 // this wave's kRunBufs run buffers of run_cap entries
+  int run_cap;
   int rb;                     // buffer the stream reads
   int64_t off;                // byte offset of the next unit
   int left;                   // units left in the current run
@@ -403,7 +404,7 @@ struct FragRing {
     int2 v = prog_read_b64(run);
     if (__builtin_amdgcn_readfirstlane(v.y) == 0) {  // end of a buffer: the next one
       rb = (rb + 1) % kRunBufs;
-      run = rbuf + rb * kRunCap;
+      run = rbuf + rb * run_cap;
       v = prog_read_b64(run);
     }
     const int x = __builtin_amdgcn_readfirstlane(v.x), n = __builtin_amdgcn_readfirstlane(v.y);
@@ -512,7 +513,8 @@ struct RunDeriver {
   int n_items;
   int gk;                      // next item to look at
   int gb;                      // buffer the next derivation fills
-  int2* rbuf;                  // all waves' run buffers: [wave][kRunBufs][kRunCap]
+  int2* rbuf;                  // all waves' run buffers: [wave][kRunBufs][run_cap]
+  int run_cap;
   int recon_delta;             // fragments from the factor buffer to the reconstruction buffer
 
   __device__ void derive(int lane) {
@@ -527,7 +529,7 @@ struct RunDeriver {
       }
     }
     if (lane < kWaves) {
-      int2* out = rbuf + ((size_t)lane * kRunBufs + gb) * kRunCap;
+      int2* out = rbuf + ((size_t)lane * kRunBufs + gb) * run_cap;
       int n = 0;
       auto put = [&](int x, int cnt) {
         lds_store_b64(out + n, make_int2(x, cnt));
@@ -1126,12 +1128,14 @@ __global__ __launch_bounds__(kThreads, 1) void attend_kernel(AttendArgs a) {
   rd.gb = 0;
   rd.rbuf = reinterpret_cast<int2*>(smem + (size_t)p.n_items * sizeof(WorkItem));
   rd.recon_delta = a.recon_delta;
+  rd.run_cap = a.run_cap;
+  fr.run_cap = a.run_cap;
   if (wave == 0) {
     rd.derive(threadIdx.x & 63);
     rd.derive(threadIdx.x & 63);
   }
   lds_barrier();
-  fr.rbuf = rd.rbuf + (size_t)wave * kRunBufs * kRunCap;
+  fr.rbuf = rd.rbuf + (size_t)wave * kRunBufs * a.run_cap;
   fr.start();
   for (int k = 0; k < p.n_items; ++k) {
     const WorkItem it = lds_item(smem + (size_t)k * sizeof(WorkItem));

@@ -289,7 +289,13 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
   // the rest for the program (fewer launches would cost the ring); when even a
   // short program leaves no room for that (ranks above 512), the weight tile
   // in two 128-token halves and a 4-slot ring; failing that, no ring
-  const size_t run_bytes = (size_t)kWaves * kRunBufs * kRunCap * sizeof(int2);
+  // run buffers sized for this plan's items: the most KV heads of a tile and
+  // the most tiles of a part
+  int max_nh = 1, max_pt = 1;
+  for (int k = 0; k < n_ct; ++k) max_nh = std::max(max_nh, til.nh[k]);
+  for (const Part& pt : parts) max_pt = std::max(max_pt, pt.ntile);
+  out->run_cap = run_cap_for(max_nh, max_pt, c.p_int8);
+  const size_t run_bytes = (size_t)kWaves * kRunBufs * out->run_cap * sizeof(int2);
   const size_t short_prog = 16 * sizeof(WorkItem) + run_bytes;
   auto room_for = [&](bool half_w) {
     const size_t b = attend_lds_base_bytes(c.d, out->rk_pad_max, out->rv_pad_max, half_w);

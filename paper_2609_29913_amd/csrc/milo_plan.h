@@ -45,6 +45,7 @@ struct Schedule {
   int gang = 1;           // workgroups per gang
   bool half_w = false;    // the weight tile in 128-token halves (LDS is short)
   int64_t count_off = 0;  // byte offset of the int32 [n_ct] slot counts in `bytes`
+  int run_cap = kRunCap;  // entries of each wave's run buffers (run_cap_for of this plan's items)
 };
 
 int max_owned(const BlockMeta& m);

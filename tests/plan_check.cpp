@@ -7,7 +7,7 @@
 //    exactly once;
 //  - block items carry their tile's first column, KV heads and column count,
 //    their block's rank-group split, at most kMaxPartTiles tiles, and derive
-//    at most kRunCap - 1 fragment runs per wave;
+//    fewer fragment runs per wave than the plan's run buffers hold;
 //  - partial slots: consecutive block items of one workgroup and column tile
 //    form a group (first item flagged first, last flagged flush) that owns one
 //    slot; slots of a tile are numbered densely from 0 and the plan's slot count
@@ -147,7 +147,8 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
     for (int k = 0; k < til.n_ct; ++k) cover[{b, k}].assign(meta[b].T_pad / kTile, 0);
   std::vector<int> tail_seen((size_t)n_q * n_kv * n_chunks, 0);
   std::vector<std::set<int>> slots_of_tile(til.n_ct);
-  const size_t run_bytes = (size_t)kWaves * kRunBufs * kRunCap * sizeof(int2);
+  const size_t run_bytes = (size_t)kWaves * kRunBufs * sch.run_cap * sizeof(int2);
+  CHECK(sch.run_cap >= 1 && sch.run_cap <= kRunCap, "run buffer of %d entries", sch.run_cap);
   for (int e = 0; e < sch.n_launch * kCUs; ++e) {
     const WgProgram& p = entries[e];
     if (p.n_items == 0) continue;
@@ -220,7 +221,7 @@ static void run_case(int case_no, int n_kv, int d, int G, int n_q, int n_chunks,
                      const int64_t unit = kind == kRunI8 ? kFragElems / 2 : kFragElems;  // elements per unit index
                      if ((int64_t)x * unit < lo || ((int64_t)x + cnt) * unit > hi) outside = true;
                    }, dense, kDelta);
-        CHECK(runs <= kRunCap - 1, "%d runs exceed the run buffer", runs);
+        CHECK(runs <= sch.run_cap - 1, "%d runs exceed the plan's run buffer of %d", runs, sch.run_cap);
         CHECK(!outside, "%s item: wave %d reads outside its block", dense ? "dense" : "latent", wave);
       }
       // slot groups

@@ -192,12 +192,12 @@ def test_plan_changes_between_calls():
 
 def test_work_split_over_several_launches(monkeypatch):
     """When the workgroup programs do not fit in LDS the step runs as several
-    attention launches.  A cap of 8960 program bytes holds the run buffers
-    (8 waves x 4 buffers x 34 runs x 8 bytes = 8704) and at most three 80-byte
-    items per workgroup; 1200 one-tile blocks on one KV head give some workgroup
-    at least five items in a single launch, so the plan needs two or more
-    launches."""
-    monkeypatch.setenv("MILO_MAX_PROGRAM_BYTES", "8960")
+    attention launches.  A cap of 1792 program bytes holds this plan's run
+    buffers (8 waves x 4 buffers x 6 runs x 8 bytes = 1536: one KV head per
+    tile, one tile per part) and at most three 80-byte items per workgroup;
+    1200 one-tile blocks on one KV head give some workgroup at least five items
+    in a single launch, so the plan needs two or more launches."""
+    monkeypatch.setenv("MILO_MAX_PROGRAM_BYTES", "1792")
     n = 1200
     inp = synth.make_problem(31, [32] * n, [16] * n, rank_v=[8] * n, n_kv_heads=1, head_dim=64, n_q=2,
                              n_q_heads=2, tail_cap=40, tail_len=[40, 3])

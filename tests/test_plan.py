@@ -89,7 +89,7 @@ def test_plan_split_over_launches(checker):
     """A program cap small enough to need several launches (1200 one-tile
     blocks on one KV head), and tail chunks with leftover solo workgroups."""
     n = 1200
-    cases = [_case(1, 64, 2, 2, 1, [32] * n, [16] * n, [8] * n, cap=8960),
+    cases = [_case(1, 64, 2, 2, 1, [32] * n, [16] * n, [8] * n, cap=1792),
              _case(8, 128, 5, 16, 8, [1024] * 30, [320] * 30, cap=12000)]
     out = _run(checker, cases)
     assert "launches 1 " not in out.splitlines()[0]
