@@ -206,6 +206,66 @@ def run_prefill(args, cfg, dev):
     print(json.dumps(result), flush=True)
 
 
+def run_svd(args, cfg, dev):
+    """Time the encoder's per-block truncated SVD (milo_block_svd, then
+    milo_block_factors at the entropy-allocated ranks) on one layer's key
+    blocks of the workload's block sizes (synthetic power-law spectra)."""
+    import torch
+    from paper_2609_29913_amd import milo
+    import oracle
+    T = synth.draw_block_tokens(cfg)
+    D = cfg.n_kv_heads * cfg.head_dim
+    blocks = [synth.gen_kv_block(b, int(t), D, 0.9) for b, t in enumerate(T)]
+    dev_blocks = [torch.from_numpy(x.view(np.int16)).to(dev) for x in blocks]
+    n_sv = [min(int(t), D) for t in T]
+    budget = sum(n_sv) // 2
+
+    def encode():
+        sigma, vt = milo.milo_block_svd(dev_blocks)
+        ranks = milo.milo_allocate_ranks(sigma, n_sv, budget, 32, D)
+        milo.milo_block_factors(dev_blocks, vt, ranks)
+        return ranks
+
+    for _ in range(args.warmup):
+        encode()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ranks = encode()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    sweeps = milo.milo_block_svd_sweeps()
+    # the Jacobi dominates: per sweep D - 1 rounds of D / 2 rotations, each
+    # updating two rows and two columns of G and two columns of V (3 flops per
+    # element): 9 D^3 flops per sweep; the Gram matrix 2 T D^2, the factors 2 T D r
+    nb = len(T)
+    jac = 9.0 * D ** 3 * sweeps * nb
+    flops = jac + sum(2.0 * int(t) * D * D for t in T) + sum(2.0 * int(t) * D * int(r) for t, r in zip(T, ranks))
+    tfs = flops / (ms * 1e-3) / 1e12
+    cpu = None
+    if not args.no_cpu_baseline:
+        t1 = time.perf_counter()
+        oracle.block_svd(synth.bf16_to_f64(blocks[0]))
+        t_one = time.perf_counter() - t1
+        cpu = {"value": 1.0 / (t_one * nb), "unit": "layers/s", "cores": 1, "kind": "oracle",
+               "sample": f"one {int(T[0])} x {D} block through the fp64 one-sided Jacobi SVD ({t_one:.1f} s), "
+                         f"extrapolated x{nb} blocks", "extrapolated": True}
+    result = {
+        "metric": "encoder layers per second (per-block truncated SVD + rank allocation + factors, 1 GPU)",
+        "value": 1e3 / ms, "unit": "layers/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic key blocks with power-law spectra (seeded), the workload's block sizes",
+        "config": {"workload": f"{cfg.name}_svd", "blocks": nb, "d_model": D, "tokens": int(np.sum(T)),
+                   "jacobi_sweeps_max": sweeps, "rank_budget": budget},
+        "roofline": {"bound": "alu", "achieved": tfs, "peak": 157.3, "unit": "TFLOP/s", "frac": tfs / 157.3,
+                     "traffic": None, "kernel": "jacobi_kernel (with gram_kernel, factor_kernel)",
+                     "flops_per_step": flops,
+                     "note": "fp32 VALU work of the whole encode (Jacobi at the largest sweep count) over its wall time; "
+                             "the Jacobi is a chain of D - 1 dependent rounds per sweep per block, latency-bound"},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def run_alloc(args, cfg, dev):
     """Time the encoder's entropy rank allocation (milo_allocate_ranks) on one
     layer's synthetic key spectra of the workload's block structure."""
@@ -384,6 +444,9 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true", help="only run a 1 GiB device copy (counter scaling)")
     ap.add_argument("--prefill", type=int, default=0, metavar="N",
                     help="time the causal prefill of an N-token chunk of one request instead (first layer)")
+    ap.add_argument("--svd", action="store_true",
+                    help="time the encoder's per-block truncated SVD (Gram matrix, Jacobi, factors) on one layer's "
+                         "key blocks of the workload instead (default workload then: the 7B-shaped layer)")
     ap.add_argument("--alloc", action="store_true",
                     help="time the encoder's entropy rank allocation on the workload's block structure instead")
     args = ap.parse_args()
@@ -405,11 +468,16 @@ def main():
     from paper_2609_29913_amd import milo
     milo.lib()
 
+    if args.svd and args.config == ap.get_default("config"):
+        args.config = "q7b_1l"
     cfg = synth.CONFIGS[args.config]
     if args.steps is None:
-        args.steps = 200 if args.alloc else 500 if cfg.n_layers == 1 else 10
+        args.steps = 3 if args.svd else 200 if args.alloc else 500 if cfg.n_layers == 1 else 10
     if args.warmup is None:
-        args.warmup = 20 if args.alloc else 200 if cfg.n_layers == 1 else 2
+        args.warmup = 1 if args.svd else 20 if args.alloc else 200 if cfg.n_layers == 1 else 2
+    if args.svd:
+        run_svd(args, cfg, dev)
+        return
     if args.prefill > 0:
         run_prefill(args, cfg, dev)
         return
