@@ -248,9 +248,10 @@ int milo_allocate_ranks(const float* sigma, int64_t ld, int32_t n_blocks, const 
 /* Encoder, per-block truncated SVD (Sec. 4.2 Eq. 3, Alg. 1 encoding stage).
  * milo_block_svd: for every block's keys (or values) K_b, the singular values and
  * right singular vectors, K_b = U diag(sigma) V^T: the Gram matrix K_b^T K_b in
- * fp32, its eigenvectors by cyclic Jacobi (rotations until every off-diagonal
- * entry is below 1e-6 of its diagonal geometric mean or 1e-10 of the trace, at
- * most 30 sweeps), the eigenvalues sorted in descending order,
+ * fp32, its eigenvectors by block Jacobi (blocks of 32 indices; rotations until
+ * every off-diagonal entry is below 1e-6 of its diagonal geometric mean or
+ * 1e-10 of the trace, at most 30 sweeps), the eigenvalues sorted in descending
+ * order,
  * sigma = sqrt(max(lambda, 0)).  The Gram matrix squares the condition number:
  * in fp32 the eigenvalues carry an absolute error of about 1e-7 .. 1e-6
  * lambda_max, so singular values far below 1e-3 sigma_max are correspondingly
@@ -262,7 +263,8 @@ int milo_allocate_ranks(const float* sigma, int64_t ld, int32_t n_blocks, const 
  *   sigma    device fp32 [n_blocks][D], out: non-increasing (values past
  *            min(T_b, D) are ~0); feed to milo_allocate_ranks (n_sv = min(T_b, D))
  *   vt       device fp32 [n_blocks][D][D], out: row j = right singular vector of sigma_j
- * Synchronous (allocates and frees a 2 n_blocks D^2 float workspace).
+ * Synchronous (allocates and frees a workspace of at most ~2 GiB: blocks are
+ * processed in groups that fit it, at least one at a time).
  * milo_block_factors: the truncated factors of rank r_b with the singular values
  * folded into P (Eq. 3 with Sigma in the left factor): P_b = K_b V_r = U_r Sigma_r
  * and R_b = V_r^T, in bf16 (fp32 accumulation), the inputs of milo_cache_create.
@@ -272,13 +274,18 @@ int milo_allocate_ranks(const float* sigma, int64_t ld, int32_t n_blocks, const 
  * Synchronous.  Errors (both): INVALID_ARG (NULL pointer, bad count or rank),
  * UNSUPPORTED (d_model), OUT_OF_MEMORY, HIP_ERROR.
  * milo_block_svd_sweeps: the largest number of Jacobi sweeps a block of the
- * last milo_block_svd call needed (30 means some block stopped at the cap). */
+ * last milo_block_svd call needed (30 means some block stopped at the cap).
+ * milo_block_svd_flops: the fp32 flops that call executed in its Gram products
+ * (2 T_b D^2 per block) and in the 64 x 64 x 64 products of its block rotations
+ * (counted on the device as they run); the scalar rotations inside the 64 x 64
+ * subproblems are not counted.  Both: INVALID_ARG for NULL. */
 int milo_block_svd(const uint16_t* const* k, const int32_t* tokens, int32_t n_blocks, int32_t d_model,
                    float* sigma, float* vt, void* hip_stream);
 int milo_block_factors(const uint16_t* const* k, const int32_t* tokens, int32_t n_blocks,
                        int32_t d_model, const float* vt, const int32_t* ranks,
                        uint16_t* const* p_out, uint16_t* const* r_out, void* hip_stream);
 int milo_block_svd_sweeps(int32_t* sweeps);
+int milo_block_svd_flops(double* flops);
 
 /* Release the cache and its device memory (synchronises the device first).
  * NULL is accepted and ignored. */

@@ -4,12 +4,15 @@
 // R = V_r^T that milo_cache_create stores.  (The ranks r_b in between come
 // from the entropy rank allocation, milo_allocate_ranks.)
 //
-//  gram_kernel     G_b = K_b^T K_b (fp32, D_pad x D_pad, zero-padded to an even size)
-//  jacobi_kernel   one workgroup per block: the symmetric eigenproblem of G_b by
-//                  parallel cyclic Jacobi (circle ordering: D_pad / 2 disjoint
-//                  rotations per round, D_pad - 1 rounds per sweep), rotations
-//                  accumulated into V; eigenvalues sorted (bitonic, LDS), sigma =
-//                  sqrt(max(lambda, 0)), V^T written row by row
+//  gram_kernel     G_b = K_b^T K_b (fp32, D_pad x D_pad, zero-padded to a multiple of 64)
+//  bj_*_kernel     the symmetric eigenproblem of G_b by block Jacobi: blocks of 32
+//                  indices paired by the circle ordering; per round one launch
+//                  sweeps every pair's 64 x 64 subproblem in LDS (scalar
+//                  cyclic Jacobi), the next rotates the rest of G and V by the
+//                  pair rotations (64 x 64 products in LDS); once per sweep the
+//                  host learns whether any block still rotated.  Then the
+//                  eigenvalues are sorted (bitonic, LDS), sigma = sqrt(max(lambda,
+//                  0)), V^T written row by row
 //  factor_kernel   P = K_b V_r (fp32 accumulation, bf16 out), R = V_r^T (bf16)
 //
 // Precision: the Gram matrix squares the condition number, so in fp32 the
@@ -30,8 +33,8 @@ namespace milo {
 namespace {
 
 constexpr int kMaxModel = 1024;      // largest D (= H_kv * d) the encoder handles
-constexpr int kJacobiThreads = 1024;
-constexpr int kMaxEncodeBlocks = 65535;  // blocks per call (one grid z-slice or workgroup each)
+constexpr size_t kEncodeWorkspace = size_t(2) << 30;  // G, V and rotations of the blocks in flight
+constexpr int kMaxEncodeBlocks = 65535;  // blocks per call (one grid z-slice or y-row each)
 constexpr int kGramTile = 64;        // G tile per workgroup (256 threads, 4 x 4 outputs each)
 constexpr int kGramK = 32;           // tokens per LDS stage
 
@@ -81,113 +84,376 @@ __device__ __forceinline__ void circle_pair(int n, int round, int t, int* p, int
   *q = x < y ? y : x;
 }
 
-// One workgroup per block: cyclic Jacobi on G_b (in place, global memory),
-// V_b accumulating the rotations, until a whole sweep finds no pair with
-// |G_pq| > tol sqrt(|G_pp G_qq|) and |G_pq| > 1e-10 trace(G) (or max_sweeps);
-// then sigma and V^T.  As in Rutishauser's formulation, a rotated pair's
-// off-diagonal entry is set to zero and its diagonal entries are updated as
-// G_pp - t G_pq and G_qq + t G_pq (t = tan of the angle) rather than taken from
-// the rotated rows: this keeps the eigenvalues at the accuracy of the Gram
-// matrix and lets rank-deficient blocks (T_b < D) converge.
-__global__ __launch_bounds__(kJacobiThreads) void jacobi_kernel(float* G_all, float* V_all, int D, int Dp, float tol,
-                                                                int max_sweeps, float* sigma, float* vt,
-                                                                int* sweeps_used) {
-  __shared__ float cs[kMaxModel / 2], sn[kMaxModel / 2], tn[kMaxModel / 2];
-  __shared__ float dp[kMaxModel / 2], dq[kMaxModel / 2], od[kMaxModel / 2];
-  __shared__ int pp[kMaxModel / 2], qq[kMaxModel / 2];
-  __shared__ float floor_abs;
-  __shared__ float key[kMaxModel];
-  __shared__ int idx[kMaxModel];
-  __shared__ int any_rot;
-  const int b = blockIdx.x, tid = threadIdx.x;
-  float* G = G_all + (size_t)b * Dp * Dp;
-  float* V = V_all + (size_t)b * Dp * Dp;
-  const int half = Dp / 2;
-  for (int x = tid; x < Dp * Dp; x += kJacobiThreads) V[x] = (x / Dp == x % Dp) ? 1.f : 0.f;
-  if (tid == 0) {
-    float tr = 0.f;
-    for (int i = 0; i < Dp; ++i) tr += G[(size_t)i * Dp + i];
-    floor_abs = 1e-10f * tr;
-  }
+// Block Jacobi.  The D_pad indices form n_blk = D_pad / 32 blocks of 32; a
+// sweep is n_blk - 1 rounds of the circle ordering over blocks, each round
+// n_blk / 2 disjoint block pairs.  Pair (u, w)'s subproblem is the 64 x 64
+// principal submatrix of G on blocks u and w: bj_solve_kernel rotates it by one
+// cyclic Jacobi sweep in LDS (same threshold as the whole problem) and stores
+// its rotation J; bj_apply_kernel then rotates the rest of G (G_pq <- J_p^T
+// G_pq J_q between pairs) and V (V[:, pair p] <- V[:, pair p] J_p).  A sweep in
+// which no subproblem needed a rotation leaves every off-diagonal entry of G
+// below the threshold.
+struct BJArgs {
+  float* G;           // [n][D_pad][D_pad] row-major, symmetric
+  float* V;           // [n][D_pad][D_pad], V[i][j] = component i of eigenvector j
+  float* J;           // [n][n_pair][64][64] the round's pair rotations
+  int* rot_pair;      // [n][n_pair] 1 if pair p's J is not the identity this round
+  int* rot_mat;       // [n] 1 if any pair of the matrix rotated this sweep
+  int* active;        // [n] 0 once a whole sweep found nothing to rotate
+  float* floor_abs;   // [n] 1e-10 trace(G_b)
+  unsigned* gemms;    // [n] 64^3 products executed (solves' re-orthogonalisation and applies)
+  int Dp, n_blk, round;
+  float tol;
+};
+constexpr int kBJ = 64;       // subproblem order (two blocks of 32)
+constexpr int kBJS = kBJ + 1;  // LDS row stride
+constexpr int kBJThreads = 256;
+constexpr int kMaxSweeps = 30;
+
+// V_b = I, floor_abs[b] = 1e-10 trace(G_b), the per-matrix flags cleared; grid: n.
+__global__ __launch_bounds__(kBJThreads) void bj_init_kernel(BJArgs a, int* sweeps_used) {
+  __shared__ float part[kBJThreads];
+  const int b = blockIdx.x, tid = threadIdx.x, Dp = a.Dp;
+  const float* G = a.G + (size_t)b * Dp * Dp;
+  float* V = a.V + (size_t)b * Dp * Dp;
+  for (int x = tid; x < Dp * Dp; x += kBJThreads) V[x] = (x / Dp == x % Dp) ? 1.f : 0.f;
+  float tr = 0.f;
+  for (int i = tid; i < Dp; i += kBJThreads) tr += G[(size_t)i * Dp + i];
+  part[tid] = tr;
   __syncthreads();
-  int sweep = 0;
-  for (; sweep < max_sweeps; ++sweep) {
-    if (tid == 0) any_rot = 0;
+  for (int w = kBJThreads / 2; w > 0; w /= 2) {
+    if (tid < w) part[tid] += part[tid + w];
     __syncthreads();
-    for (int round = 0; round < Dp - 1; ++round) {
-      // rotation of each pair (classical Jacobi: annihilates G_pq)
-      for (int t = tid; t < half; t += kJacobiThreads) {
-        int p, q;
-        circle_pair(Dp, round, t, &p, &q);
-        const float gpp = G[(size_t)p * Dp + p], gqq = G[(size_t)q * Dp + q], gpq = G[(size_t)p * Dp + q];
-        float c = 1.f, s = 0.f, tt = 0.f;
-        if (gpq != 0.f && fabsf(gpq) > tol * sqrtf(fabsf(gpp) * fabsf(gqq)) && fabsf(gpq) > floor_abs) {
-          const float theta = (gqq - gpp) / (2.f * gpq);
-          // t = sign(theta) / (|theta| + sqrt(1 + theta^2)); 1 / (2 theta) where theta^2 would overflow
-          tt = fabsf(theta) > 1e18f ? 0.5f / theta
-                                    : copysignf(1.f, theta) / (fabsf(theta) + sqrtf(1.f + theta * theta));
-          c = 1.f / sqrtf(1.f + tt * tt);
-          s = tt * c;
-          any_rot = 1;  // benign race: every writer stores 1
-        }
-        pp[t] = p;
-        qq[t] = q;
-        cs[t] = c;
-        sn[t] = s;
-        tn[t] = tt;
-        dp[t] = gpp;
-        dq[t] = gqq;
-        od[t] = gpq;
+  }
+  if (tid == 0) {
+    a.floor_abs[b] = 1e-10f * part[0];
+    a.active[b] = 1;
+    a.rot_mat[b] = 0;
+    a.gemms[b] = 0;
+    sweeps_used[b] = 0;
+  }
+}
+
+// 64 x 64 products in LDS, 256 threads, each the 4 x 4 outputs (ty + 16 u, tx + 16 v).
+// out = X^T Y (transpose_x) or X Y.
+template <bool TRANSPOSE_X>
+__device__ __forceinline__ void bj_product(const float (*X)[kBJS], const float (*Y)[kBJS], float acc[4][4]) {
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[u][v] = 0.f;
+  for (int k = 0; k < kBJ; ++k) {
+    float x[4], y[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) x[u] = TRANSPOSE_X ? X[k][ty + 16 * u] : X[ty + 16 * u][k];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) y[v] = Y[k][tx + 16 * v];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(x[u], y[v], acc[u][v]);
+  }
+}
+
+// Round rr of the circle ordering of the 64 subproblem indices, pair t (no division).
+__device__ __forceinline__ void circle_pair64(int rr, int t, int* p, int* q) {
+  auto at = [&](int i) {
+    int x = i - 1 + rr;
+    x = x >= kBJ - 1 ? x - (kBJ - 1) : x;
+    return i == 0 ? 0 : 1 + x;
+  };
+  const int x = at(t), y = at(kBJ - 1 - t);
+  *p = x < y ? x : y;
+  *q = x < y ? y : x;
+}
+
+// One workgroup per (pair, matrix): one cyclic Jacobi sweep (63 rounds of 32
+// disjoint rotations) over the pair's 64 x 64 subproblem in LDS.  (Solving the
+// subproblem to convergence on every visit costs several sweeps per visit and
+// saves at most one outer sweep, so each visit does one.)  As in Rutishauser's
+// formulation, a rotated index pair's off-diagonal entry is set to zero and its
+// diagonal entries become G_pp - t G_pq and G_qq + t G_pq (t = tan of the
+// angle): this keeps the eigenvalues at the accuracy of the Gram matrix and lets
+// rank-deficient blocks (T_b < D) converge.  The rotated subproblem goes back
+// into G; J, made orthogonal to rounding by one Newton-Schulz step
+// J (3 I - J^T J) / 2, goes to the rotation buffer for bj_apply_kernel.
+// grid: (n_blk / 2, n).
+__global__ __launch_bounds__(kBJThreads) void bj_solve_kernel(BJArgs a) {
+  __shared__ float S[kBJ][kBJS], Jm[kBJ][kBJS], M[kBJ][kBJS];
+  __shared__ float2 rot[kBJ / 2];  // (c, s) of index pair k this round
+  __shared__ int pq[kBJ / 2];      // p | q << 8
+  __shared__ float2 diag[kBJ / 2];  // (G_pp - t G_pq, G_qq + t G_pq) of a rotated pair
+  __shared__ int any_rot;
+  const int b = blockIdx.y, pair = blockIdx.x, tid = threadIdx.x, Dp = a.Dp;
+  const int n_pair = a.n_blk / 2;
+  if (!a.active[b]) return;
+  int u, w;
+  circle_pair(a.n_blk, a.round, pair, &u, &w);
+  auto gi = [&](int i) { return i < 32 ? u * 32 + i : w * 32 + (i - 32); };
+  float* G = a.G + (size_t)b * Dp * Dp;
+  for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+    const int i = x / kBJ, j = x % kBJ;
+    S[i][j] = G[(size_t)gi(i) * Dp + gi(j)];
+    Jm[i][j] = i == j ? 1.f : 0.f;
+  }
+  if (tid == 0) any_rot = 0;
+  const float tol = a.tol, flo = a.floor_abs[b];
+  // the 2 x 2 blocks (index pair k's rows, pair l's columns) with k <= l: 528 of
+  // them, enumerated as 16 row pairs (k, 31 - k) of 33 blocks each
+  constexpr int kHalf = kBJ / 2, kUpper = kHalf * (kHalf + 1) / 2;
+  __syncthreads();
+  for (int rr = 0; rr < kBJ - 1; ++rr) {
+    if (tid < kHalf) {
+      int p, q;
+      circle_pair64(rr, tid, &p, &q);
+      const float gpp = S[p][p], gqq = S[q][q], gpq = S[p][q];
+      float c = 1.f, s = 0.f, tt = 0.f;
+      if (gpq != 0.f && fabsf(gpq) > tol * sqrtf(fabsf(gpp) * fabsf(gqq)) && fabsf(gpq) > flo) {
+        const float theta = (gqq - gpp) / (2.f * gpq);
+        // t = sign(theta) / (|theta| + sqrt(1 + theta^2)); 1 / (2 theta) where theta^2 would overflow
+        tt = fabsf(theta) > 1e18f ? 0.5f / theta
+                                  : copysignf(1.f, theta) / (fabsf(theta) + sqrtf(1.f + theta * theta));
+        c = 1.f / sqrtf(1.f + tt * tt);
+        s = tt * c;
+        any_rot = 1;  // benign race: every writer stores 1
       }
-      __syncthreads();
-      // rows p, q: G <- J^T G
-      for (int x = tid; x < half * Dp; x += kJacobiThreads) {
-        const int t = x / Dp, j = x % Dp;
-        const float c = cs[t], s = sn[t];
+      rot[tid] = make_float2(c, s);
+      pq[tid] = p | q << 8;
+      diag[tid] = make_float2(gpp - tt * gpq, gqq + tt * gpq);
+    }
+    __syncthreads();
+    // S <- R^T S R, one 2 x 2 block per item, the mirror block written as its transpose
+#pragma unroll
+    for (int m = 0; m < (kUpper + kBJThreads - 1) / kBJThreads; ++m) {
+      const int x = tid + m * kBJThreads;
+      if (x >= kUpper) break;
+      const int r = x / (kHalf + 1), c0 = x % (kHalf + 1);
+      const bool first = c0 < kHalf - r;
+      const int k = first ? r : kHalf - 1 - r;
+      const int l = first ? r + c0 : k + (c0 - (kHalf - r));
+      const float2 rk = rot[k], rl = rot[l];
+      const float sk = rk.y, sl = rl.y;
+      if (sk == 0.f && sl == 0.f) continue;
+      const int pqk = pq[k];
+      const int pk = pqk & 255, qk = pqk >> 8;
+      if (k == l) {
+        const float2 dg = diag[k];
+        S[pk][qk] = 0.f;
+        S[qk][pk] = 0.f;
+        S[pk][pk] = dg.x;
+        S[qk][qk] = dg.y;
+        continue;
+      }
+      const int pql = pq[l];
+      const int pl = pql & 255, ql = pql >> 8;
+      const float ck = rk.x, cl = rl.x;
+      const float e00 = S[pk][pl], e01 = S[pk][ql], e10 = S[qk][pl], e11 = S[qk][ql];
+      // rows: r_p <- c r_p - s r_q, r_q <- s r_p + c r_q; then the same on columns
+      const float f00 = ck * e00 - sk * e10, f01 = ck * e01 - sk * e11;
+      const float f10 = sk * e00 + ck * e10, f11 = sk * e01 + ck * e11;
+      const float g00 = cl * f00 - sl * f01, g01 = sl * f00 + cl * f01;
+      const float g10 = cl * f10 - sl * f11, g11 = sl * f10 + cl * f11;
+      S[pk][pl] = g00;
+      S[pk][ql] = g01;
+      S[qk][pl] = g10;
+      S[qk][ql] = g11;
+      S[pl][pk] = g00;
+      S[ql][pk] = g01;
+      S[pl][qk] = g10;
+      S[ql][qk] = g11;
+    }
+    // J <- J R (columns p, q of every row): lane i of wave v takes row i and the
+    // index pairs v, v + 4, ...; the pairs' parameters are read before any update
+    {
+      const int i = tid % kBJ, v0 = tid / kBJ;
+      constexpr int kPer = kHalf / (kBJThreads / kBJ);
+      float2 rk[kPer];
+      int pqk[kPer];
+#pragma unroll
+      for (int m = 0; m < kPer; ++m) {
+        rk[m] = rot[v0 + m * (kBJThreads / kBJ)];
+        pqk[m] = pq[v0 + m * (kBJThreads / kBJ)];
+      }
+#pragma unroll
+      for (int m = 0; m < kPer; ++m) {
+        const float c = rk[m].x, s = rk[m].y;
         if (s == 0.f) continue;
-        float* rp = G + (size_t)pp[t] * Dp + j;
-        float* rq = G + (size_t)qq[t] * Dp + j;
-        const float gp = *rp, gq = *rq;
-        *rp = c * gp - s * gq;
-        *rq = s * gp + c * gq;
+        const int p = pqk[m] & 255, q = pqk[m] >> 8;
+        const float jp = Jm[i][p], jq = Jm[i][q];
+        Jm[i][p] = c * jp - s * jq;
+        Jm[i][q] = s * jp + c * jq;
       }
+    }
+    __syncthreads();
+  }
+  const bool rotated = any_rot != 0;
+  if (tid == 0) a.rot_pair[(size_t)b * n_pair + pair] = rotated ? 1 : 0;
+  if (!rotated) return;
+  for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+    const int i = x / kBJ, j = x % kBJ;
+    G[(size_t)gi(i) * Dp + gi(j)] = S[i][j];
+  }
+  // Newton-Schulz: M = J^T J, then J (3 I - M) / 2 = 1.5 J - 0.5 J M
+  float acc[4][4];
+  bj_product<true>(Jm, Jm, acc);
+  const int tx = tid % 16, ty = tid / 16;
+#pragma unroll
+  for (int uu = 0; uu < 4; ++uu)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) M[ty + 16 * uu][tx + 16 * v] = acc[uu][v];
+  __syncthreads();
+  bj_product<false>(Jm, M, acc);
+  float* Jout = a.J + ((size_t)b * n_pair + pair) * kBJ * kBJ;
+#pragma unroll
+  for (int uu = 0; uu < 4; ++uu)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = ty + 16 * uu, j = tx + 16 * v;
+      Jout[i * kBJ + j] = 1.5f * Jm[i][j] - 0.5f * acc[uu][v];
+    }
+  if (tid == 0) {
+    a.rot_mat[b] = 1;
+    atomicAdd(&a.gemms[b], 2u);
+  }
+}
+
+// Tasks of one matrix in a round: the n_pair (n_pair - 1) / 2 off-diagonal pair
+// blocks of G (p < q), then V's pair columns in groups of kVChunks 64-row
+// chunks (n_pair of them per group).
+constexpr int kVChunks = 1;  // 64-row chunks of V per workgroup (one load of J_p for all)
+__host__ __device__ inline int bj_v_groups(int Dp) { return (Dp / kBJ + kVChunks - 1) / kVChunks; }
+__host__ __device__ inline int bj_tasks(int n_blk, int Dp) {
+  const int n_pair = n_blk / 2;
+  return n_pair * (n_pair - 1) / 2 + bj_v_groups(Dp) * n_pair;
+}
+
+// One workgroup per (task, matrix): G_pq <- J_p^T G_pq J_q (and G_qp its
+// transpose), or V[chunk rows][pair p columns] <- that slice J_p.  An identity
+// J (a pair with no rotation) is skipped.  grid: (bj_tasks, n).
+__global__ __launch_bounds__(kBJThreads) void bj_apply_kernel(BJArgs a) {
+  __shared__ float A[kBJ][kBJS], Jp[kBJ][kBJS], Jq[kBJ][kBJS];
+  const int b = blockIdx.y, tid = threadIdx.x, Dp = a.Dp, n_pair = a.n_blk / 2;
+  if (!a.active[b]) return;
+  const int n_g = n_pair * (n_pair - 1) / 2;
+  int task = blockIdx.x;
+  const int* rot = a.rot_pair + (size_t)b * n_pair;
+  const float* Jb = a.J + (size_t)b * n_pair * kBJ * kBJ;
+  const int tx = tid % 16, ty = tid / 16;
+  float acc[4][4];
+  if (task < n_g) {
+    int p = 0;
+    while (task >= n_pair - 1 - p) {
+      task -= n_pair - 1 - p;
+      ++p;
+    }
+    const int q = p + 1 + task;
+    const bool rp = rot[p] != 0, rq = rot[q] != 0;
+    if (!rp && !rq) return;
+    int up, wp, uq, wq;
+    circle_pair(a.n_blk, a.round, p, &up, &wp);
+    circle_pair(a.n_blk, a.round, q, &uq, &wq);
+    auto gp = [&](int i) { return i < 32 ? up * 32 + i : wp * 32 + (i - 32); };
+    auto gq = [&](int i) { return i < 32 ? uq * 32 + i : wq * 32 + (i - 32); };
+    float* G = a.G + (size_t)b * Dp * Dp;
+    for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+      const int i = x / kBJ, j = x % kBJ;
+      A[i][j] = G[(size_t)gp(i) * Dp + gq(j)];
+      if (rp) Jp[i][j] = Jb[((size_t)p * kBJ + i) * kBJ + j];
+      if (rq) Jq[i][j] = Jb[((size_t)q * kBJ + i) * kBJ + j];
+    }
+    __syncthreads();
+    if (rp) {
+      bj_product<true>(Jp, A, acc);
       __syncthreads();
-      // columns p, q: G <- G J, V <- V J
-      for (int x = tid; x < Dp * half; x += kJacobiThreads) {
-        const int i = x / half, t = x % half;
-        const float c = cs[t], s = sn[t];
-        if (s == 0.f) continue;
-        const int p = pp[t], q = qq[t];
-        float* g = G + (size_t)i * Dp;
-        const float gp = g[p], gq = g[q];
-        g[p] = c * gp - s * gq;
-        g[q] = s * gp + c * gq;
-        float* v = V + (size_t)i * Dp;
-        const float vp = v[p], vq = v[q];
-        v[p] = c * vp - s * vq;
-        v[q] = s * vp + c * vq;
-      }
-      __syncthreads();
-      // the rotated 2 x 2 blocks, exactly diagonal
-      for (int t = tid; t < half; t += kJacobiThreads) {
-        if (sn[t] == 0.f) continue;
-        const int p = pp[t], q = qq[t];
-        G[(size_t)p * Dp + q] = 0.f;
-        G[(size_t)q * Dp + p] = 0.f;
-        G[(size_t)p * Dp + p] = dp[t] - tn[t] * od[t];
-        G[(size_t)q * Dp + q] = dq[t] + tn[t] * od[t];
-      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) A[ty + 16 * u][tx + 16 * v] = acc[u][v];
       __syncthreads();
     }
-    const bool done = any_rot == 0;
-    __syncthreads();
-    if (done) break;
+    if (rq) {
+      bj_product<false>(A, Jq, acc);
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) A[ty + 16 * u][tx + 16 * v] = acc[u][v];
+      __syncthreads();
+    }
+    for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+      const int i = x / kBJ, j = x % kBJ;
+      G[(size_t)gp(i) * Dp + gq(j)] = A[i][j];
+      G[(size_t)gq(i) * Dp + gp(j)] = A[j][i];
+    }
+    if (tid == 0) atomicAdd(&a.gemms[b], (rp ? 1u : 0u) + (rq ? 1u : 0u));
+    return;
   }
-  // eigenvalues in descending order (bitonic sort of (lambda, index) over a
-  // power of two of entries; padding entries sort last)
+  task -= n_g;
+  const int p = task % n_pair, group = task / n_pair;
+  if (!rot[p]) return;
+  int up, wp;
+  circle_pair(a.n_blk, a.round, p, &up, &wp);
+  auto gp = [&](int i) { return i < 32 ? up * 32 + i : wp * 32 + (i - 32); };
+  for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+    const int i = x / kBJ, j = x % kBJ;
+    Jp[i][j] = Jb[((size_t)p * kBJ + i) * kBJ + j];
+  }
+  const int c0 = group * kVChunks, c1 = min(c0 + kVChunks, Dp / kBJ);
+  for (int chunk = c0; chunk < c1; ++chunk) {
+    float* V = a.V + (size_t)b * Dp * Dp + (size_t)chunk * kBJ * Dp;
+    for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+      const int i = x / kBJ, j = x % kBJ;
+      A[i][j] = V[(size_t)i * Dp + gp(j)];
+    }
+    __syncthreads();
+    bj_product<false>(A, Jp, acc);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) V[(size_t)(ty + 16 * u) * Dp + gp(tx + 16 * v)] = acc[u][v];
+    __syncthreads();  // A is reloaded by the next chunk
+  }
+  if (tid == 0) atomicAdd(&a.gemms[b], (unsigned)(c1 - c0));
+}
+
+// End of a sweep: a matrix with no rotation in it is done; the others count the
+// sweep.  *remaining = matrices still active.  grid: 1.
+__global__ __launch_bounds__(1024) void bj_sweep_end_kernel(BJArgs a, int n, int sweep, int* sweeps_used,
+                                                            int* remaining) {
+  __shared__ int count;
+  if (threadIdx.x == 0) count = 0;
+  __syncthreads();
+  int mine = 0;
+  for (int b = threadIdx.x; b < n; b += 1024) {
+    if (a.active[b]) {
+      if (a.rot_mat[b]) {
+        sweeps_used[b] = sweep + 1;
+        ++mine;
+      } else {
+        a.active[b] = 0;
+      }
+    }
+    a.rot_mat[b] = 0;
+  }
+  if (mine) atomicAdd(&count, mine);
+  __syncthreads();
+  if (threadIdx.x == 0) *remaining = count;
+}
+
+// Eigenvalues in descending order (bitonic sort of (lambda, index) over a power
+// of two of entries; padding entries sort last), sigma = sqrt(max(lambda, 0)),
+// and V^T row by row; grid: n.
+__global__ __launch_bounds__(1024) void bj_finish_kernel(const float* G_all, const float* V_all, int D, int Dp,
+                                                         float* sigma, float* vt) {
+  __shared__ float key[kMaxModel];
+  __shared__ int idx[kMaxModel];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const float* G = G_all + (size_t)b * Dp * Dp;
+  const float* V = V_all + (size_t)b * Dp * Dp;
   int n2 = 1;
   while (n2 < Dp) n2 *= 2;
-  for (int x = tid; x < n2; x += kJacobiThreads) {
+  for (int x = tid; x < n2; x += 1024) {
     const float g = x < D ? G[(size_t)x * Dp + x] : -INFINITY;
     key[x] = g == g ? g : -INFINITY;  // NaN (non-finite input) ranks with the padding, after every index < D
     idx[x] = x;
@@ -195,7 +461,7 @@ __global__ __launch_bounds__(kJacobiThreads) void jacobi_kernel(float* G_all, fl
   __syncthreads();
   for (int size = 2; size <= n2; size *= 2)
     for (int stride = size / 2; stride > 0; stride /= 2) {
-      for (int x = tid; x < n2; x += kJacobiThreads) {
+      for (int x = tid; x < n2; x += 1024) {
         const int y = x ^ stride;
         if (y > x) {
           const bool desc = (x & size) == 0;
@@ -212,13 +478,12 @@ __global__ __launch_bounds__(kJacobiThreads) void jacobi_kernel(float* G_all, fl
       }
       __syncthreads();
     }
-  for (int j = tid; j < D; j += kJacobiThreads) sigma[(size_t)b * D + j] = sqrtf(fmaxf(key[j], 0.f));
-  for (int x = tid; x < D * D; x += kJacobiThreads) {
+  for (int j = tid; j < D; j += 1024) sigma[(size_t)b * D + j] = sqrtf(fmaxf(key[j], 0.f));
+  for (int x = tid; x < D * D; x += 1024) {
     const int j = x / D, col = x % D;
     const int src = idx[j] < D ? idx[j] : 0;  // always true: ties break by index, padding sorts after
     vt[((size_t)b * D + j) * D + col] = V[(size_t)col * Dp + src];
   }
-  if (tid == 0) sweeps_used[b] = sweep;
 }
 
 // P_b = K_b V_r (T_b x r_b, bf16) and R_b = V_r^T (r_b x D, bf16); grid: one
@@ -289,6 +554,7 @@ hipError_t upload(const T* host, size_t n, T** dev, hipStream_t s) {
 
 struct Encoding {
   int last_sweeps_max = 0;
+  double last_flops = 0;
 };
 Encoding g_enc;
 
@@ -310,18 +576,23 @@ extern "C" int milo_block_svd(const uint16_t* const* k, const int32_t* tokens, i
     if (tokens[b] < 1) return enc_fail(MILO_ERR_INVALID_ARG, "block %lld: T_b must be >= 1 (got %lld)", b, tokens[b]);
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
-  const int D = d_model, Dp = D + (D & 1);
+  const int D = d_model, Dp = (D + kBJ - 1) / kBJ * kBJ;  // blocks of 32, an even number of them
+  const int n_blk = Dp / 32, n_pair = n_blk / 2;
+  // blocks in flight: their G, V and pair rotations within the workspace bound
+  const size_t per_block = ((size_t)2 * Dp * Dp + (size_t)n_pair * kBJ * kBJ) * sizeof(float);
+  const int chunk = (int)std::max<size_t>(1, std::min<size_t>(n_blocks, kEncodeWorkspace / per_block));
   const uint16_t** k_d = nullptr;
   int32_t* t_d = nullptr;
-  float *G = nullptr, *V = nullptr;
-  int* sw_d = nullptr;
+  float *G = nullptr, *V = nullptr, *J = nullptr;
+  int* flags = nullptr;
   auto cleanup = [&]() {
     (void)hipStreamSynchronize(s);
     (void)hipFree(k_d);
     (void)hipFree(t_d);
     (void)hipFree(G);
     (void)hipFree(V);
-    (void)hipFree(sw_d);
+    (void)hipFree(J);
+    (void)hipFree(flags);
   };
   auto hfail = [&](hipError_t e, const char* what) {
     cleanup();
@@ -332,21 +603,67 @@ extern "C" int milo_block_svd(const uint16_t* const* k, const int32_t* tokens, i
   hipError_t e;
   if ((e = upload(k, n_blocks, const_cast<const uint16_t***>(&k_d), s)) != hipSuccess) return hfail(e, "key table");
   if ((e = upload(tokens, n_blocks, &t_d, s)) != hipSuccess) return hfail(e, "token counts");
-  const size_t mat = (size_t)n_blocks * Dp * Dp;
+  const size_t mat = (size_t)chunk * Dp * Dp;
   if ((e = hipMalloc(&G, mat * sizeof(float))) != hipSuccess) return hfail(e, "Gram workspace");
   if ((e = hipMalloc(&V, mat * sizeof(float))) != hipSuccess) return hfail(e, "eigenvector workspace");
-  if ((e = hipMalloc(&sw_d, n_blocks * sizeof(int))) != hipSuccess) return hfail(e, "sweep counts");
-  const int tiles = (Dp + kGramTile - 1) / kGramTile;
-  hipLaunchKernelGGL(gram_kernel, dim3(tiles * tiles, 1, n_blocks), dim3(256), 0, s, k_d, t_d, D, Dp, G);
-  if ((e = hipGetLastError()) != hipSuccess) return hfail(e, "gram kernel");
-  hipLaunchKernelGGL(jacobi_kernel, dim3(n_blocks), dim3(kJacobiThreads), 0, s, G, V, D, Dp, 1e-6f, 30, sigma, vt,
-                     sw_d);
-  if ((e = hipGetLastError()) != hipSuccess) return hfail(e, "jacobi kernel");
-  std::vector<int> sw(n_blocks);
-  if ((e = hipMemcpyAsync(sw.data(), sw_d, n_blocks * sizeof(int), hipMemcpyDeviceToHost, s)) != hipSuccess)
-    return hfail(e, "sweep counts");
-  if ((e = hipStreamSynchronize(s)) != hipSuccess) return hfail(e, "hipStreamSynchronize");
-  g_enc.last_sweeps_max = *std::max_element(sw.begin(), sw.end());
+  if ((e = hipMalloc(&J, (size_t)chunk * n_pair * kBJ * kBJ * sizeof(float))) != hipSuccess)
+    return hfail(e, "rotation workspace");
+  // per block: rot_pair [n_pair], rot_mat, active, floor_abs, gemms, sweeps_used; then `remaining`
+  const size_t n_flags = (size_t)chunk * (n_pair + 5) + 1;
+  if ((e = hipMalloc(&flags, n_flags * sizeof(int))) != hipSuccess) return hfail(e, "sweep flags");
+  BJArgs a{};
+  a.G = G;
+  a.V = V;
+  a.J = J;
+  a.rot_pair = flags;
+  a.rot_mat = a.rot_pair + (size_t)chunk * n_pair;
+  a.active = a.rot_mat + chunk;
+  a.floor_abs = reinterpret_cast<float*>(a.active + chunk);
+  a.gemms = reinterpret_cast<unsigned*>(a.floor_abs + chunk);
+  int* sweeps_d = reinterpret_cast<int*>(a.gemms + chunk);
+  int* remaining_d = sweeps_d + chunk;
+  a.Dp = Dp;
+  a.n_blk = n_blk;
+  a.tol = 1e-6f;
+  const int tiles = Dp / kGramTile;
+  int sweeps_max = 0;
+  double flops = 0;
+  std::vector<int> sw(chunk);
+  std::vector<unsigned> gm(chunk);
+  for (int b0 = 0; b0 < n_blocks; b0 += chunk) {
+    const int nb = std::min(chunk, n_blocks - b0);
+    hipLaunchKernelGGL(gram_kernel, dim3(tiles * tiles, 1, nb), dim3(256), 0, s, k_d + b0, t_d + b0, D, Dp, G);
+    if ((e = hipGetLastError()) != hipSuccess) return hfail(e, "gram kernel");
+    hipLaunchKernelGGL(bj_init_kernel, dim3(nb), dim3(kBJThreads), 0, s, a, sweeps_d);
+    if ((e = hipGetLastError()) != hipSuccess) return hfail(e, "jacobi init kernel");
+    for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
+      for (int round = 0; round < n_blk - 1; ++round) {
+        a.round = round;
+        hipLaunchKernelGGL(bj_solve_kernel, dim3(n_pair, nb), dim3(kBJThreads), 0, s, a);
+        hipLaunchKernelGGL(bj_apply_kernel, dim3(bj_tasks(n_blk, Dp), nb), dim3(kBJThreads), 0, s, a);
+      }
+      hipLaunchKernelGGL(bj_sweep_end_kernel, dim3(1), dim3(1024), 0, s, a, nb, sweep, sweeps_d, remaining_d);
+      if ((e = hipGetLastError()) != hipSuccess) return hfail(e, "jacobi kernels");
+      int remaining = 0;
+      if ((e = hipMemcpyAsync(&remaining, remaining_d, sizeof(int), hipMemcpyDeviceToHost, s)) != hipSuccess)
+        return hfail(e, "active block count");
+      if ((e = hipStreamSynchronize(s)) != hipSuccess) return hfail(e, "hipStreamSynchronize");
+      if (remaining == 0) break;
+    }
+    hipLaunchKernelGGL(bj_finish_kernel, dim3(nb), dim3(1024), 0, s, G, V, D, Dp, sigma + (size_t)b0 * D,
+                       vt + (size_t)b0 * D * D);
+    if ((e = hipGetLastError()) != hipSuccess) return hfail(e, "jacobi finish kernel");
+    if ((e = hipMemcpyAsync(sw.data(), sweeps_d, nb * sizeof(int), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipMemcpyAsync(gm.data(), a.gemms, nb * sizeof(unsigned), hipMemcpyDeviceToHost, s)) != hipSuccess)
+      return hfail(e, "sweep counts");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return hfail(e, "hipStreamSynchronize");
+    for (int i = 0; i < nb; ++i) {
+      sweeps_max = std::max(sweeps_max, sw[i]);
+      flops += 2.0 * kBJ * kBJ * kBJ * gm[i] + 2.0 * tokens[b0 + i] * (double)D * D;
+    }
+  }
+  g_enc.last_sweeps_max = sweeps_max;
+  g_enc.last_flops = flops;
   cleanup();
   return MILO_OK;
 }
@@ -355,6 +672,13 @@ extern "C" int milo_block_svd_sweeps(int32_t* sweeps) {
   clear_error();
   if (!sweeps) return enc_fail(MILO_ERR_INVALID_ARG, "NULL argument");
   *sweeps = g_enc.last_sweeps_max;
+  return MILO_OK;
+}
+
+extern "C" int milo_block_svd_flops(double* flops) {
+  clear_error();
+  if (!flops) return enc_fail(MILO_ERR_INVALID_ARG, "NULL argument");
+  *flops = g_enc.last_flops;
   return MILO_OK;
 }
 

@@ -90,6 +90,8 @@ def lib() -> ctypes.CDLL:
         L.milo_block_factors.restype = ctypes.c_int
         L.milo_block_svd_sweeps.argtypes = [_c_i32p]
         L.milo_block_svd_sweeps.restype = ctypes.c_int
+        L.milo_block_svd_flops.argtypes = [ctypes.POINTER(ctypes.c_double)]
+        L.milo_block_svd_flops.restype = ctypes.c_int
         L.milo_cache_read_int8.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, vp, vp]
         L.milo_cache_read_int8.restype = ctypes.c_int
         L.milo_cache_plan_builds.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
@@ -370,6 +372,12 @@ def milo_block_svd(blocks, stream=None):
 def milo_block_svd_sweeps() -> int:
     v = ctypes.c_int32()
     _check(lib().milo_block_svd_sweeps(ctypes.byref(v)))
+    return v.value
+
+
+def milo_block_svd_flops() -> float:
+    v = ctypes.c_double()
+    _check(lib().milo_block_svd_flops(ctypes.byref(v)))
     return v.value
 
 
