@@ -50,6 +50,7 @@ int hip_fail(hipError_t e, const char* what) {
   } while (0)
 
 constexpr int64_t kAlignElems = kFragElems;  // every packed factor starts on a whole fragment
+constexpr int64_t kPackStageElems = int64_t(64) << 20;  // staging of host factors (128 MiB of bf16)
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -210,7 +211,7 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
   c->rk.assign(desc->rank_k, desc->rank_k + c->n_blocks);
   c->rv.assign(desc->rank_v, desc->rank_v + c->n_blocks);
   c->meta.resize(c->n_blocks);
-  int64_t off = 0, max_src = 0, max_tpad = 0;
+  int64_t off = 0, max_src = 0, max_tpad = 0, total_src = 0;
   for (int b = 0; b < c->n_blocks; ++b) {
     BlockMeta& m = c->meta[b];
     m.T = c->T[b];
@@ -227,6 +228,7 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
       if (i8 && w == kPV) elems = i8_factor_bytes(m.T_pad, m.rv_pad) / 2 + i8_scale_bytes(m.T_pad) / 2;
       off = round_up(off + elems, kAlignElems);
       max_src = std::max<int64_t>(max_src, (int64_t)f.rows * f.cols);
+      total_src += round_up((int64_t)f.rows * f.cols, 8);
     }
     max_tpad = std::max<int64_t>(max_tpad, m.T_pad);
   }
@@ -235,7 +237,13 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     delete c;
     return fail(MILO_ERR_UNSUPPORTED, "cache of %lld elements exceeds the 2^31-fragment index range", (long long)off);
   }
-  const int64_t need = off * 2 + (src_on_device ? 0 : max_src * 2);
+  // host sources go through a staging buffer: one factor at a time for INT8
+  // (whose scales need a kernel per factor), else as many as kPackStageElems hold
+  const int64_t stage_elems =
+      src_on_device ? 0
+      : i8          ? max_src
+                    : std::max<int64_t>(round_up(max_src, 8), std::min<int64_t>(total_src, kPackStageElems));
+  const int64_t need = off * 2 + stage_elems * 2;
   const int64_t cap = env_byte_cap();
   if (cap >= 0 && need > cap) {
     delete c;
@@ -256,7 +264,7 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
   if (e != hipSuccess) { c->device = -1; return cleanup_fail(hip_fail(e, "hipGetDevice")); }
   if ((e = hipMalloc(&c->data, (size_t)c->data_elems * 2)) != hipSuccess)
     return cleanup_fail(hip_fail(e, "hipMalloc(packed factors)"));
-  if (!src_on_device && (e = hipMalloc(&staging, (size_t)max_src * 2)) != hipSuccess)
+  if (!src_on_device && (e = hipMalloc(&staging, (size_t)stage_elems * 2)) != hipSuccess)
     return cleanup_fail(hip_fail(e, "hipMalloc(staging)"));
   float *ks = nullptr, *vs = nullptr;
   int* bad = nullptr;
@@ -269,7 +277,62 @@ int milo_cache_create(const milo_cache_desc* desc, const uint16_t* const* pk, co
     if ((e = hipMemsetAsync(bad, 0, sizeof(int), s)) != hipSuccess) return cleanup_fail(hip_fail(e, "hipMemsetAsync"));
   }
   const uint16_t* const* srcs[4] = {pk, rk, pv, rv};
-  for (int b = 0; b < c->n_blocks; ++b) {
+  if (!i8) {
+    // every factor one job of pack_batch_kernel, in (block, factor) order; with
+    // host sources a batch ends where the staging buffer is full
+    const int n_jobs = c->n_blocks * 4;
+    std::vector<PackArgs> jobs(n_jobs);
+    std::vector<int64_t> starts(n_jobs + 1, 0), stage_at(src_on_device ? 0 : n_jobs);
+    std::vector<int> batch_end;
+    int64_t fill = 0;
+    for (int j = 0; j < n_jobs; ++j) {
+      const int b = j / 4, w = j % 4;
+      const FactorGeom f = geom_of(*c, b, w);
+      const uint16_t* src = srcs[w][b];
+      if (!src_on_device) {
+        const int64_t elems = round_up((int64_t)f.rows * f.cols, 8);
+        if (fill > 0 && fill + elems > stage_elems) {
+          batch_end.push_back(j);
+          fill = 0;
+        }
+        stage_at[j] = fill;
+        src = staging + fill;
+        fill += elems;
+      }
+      jobs[j] = PackArgs{src, c->data + factor_offset(c->meta[b], w), f, frag_count(f), nullptr};
+      starts[j + 1] = starts[j] + frag_count(f);
+    }
+    batch_end.push_back(n_jobs);
+    PackArgs* jobs_d = nullptr;
+    const size_t job_bytes = sizeof(PackArgs) * n_jobs, start_bytes = sizeof(int64_t) * (n_jobs + 1);
+    if ((e = hipMalloc(&jobs_d, job_bytes + start_bytes)) != hipSuccess)
+      return cleanup_fail(hip_fail(e, "hipMalloc(pack jobs)"));
+    int64_t* starts_d = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(jobs_d) + job_bytes);
+    auto jobs_fail = [&](hipError_t err, const char* what) {
+      (void)hipStreamSynchronize(s);
+      (void)hipFree(jobs_d);
+      return cleanup_fail(hip_fail(err, what));
+    };
+    if ((e = hipMemcpyAsync(jobs_d, jobs.data(), job_bytes, hipMemcpyHostToDevice, s)) != hipSuccess ||
+        (e = hipMemcpyAsync(starts_d, starts.data(), start_bytes, hipMemcpyHostToDevice, s)) != hipSuccess)
+      return jobs_fail(e, "hipMemcpyAsync(pack jobs)");
+    int j0 = 0;
+    for (const int j1 : batch_end) {
+      if (!src_on_device)
+        for (int j = j0; j < j1; ++j) {
+          const FactorGeom& f = jobs[j].geom;
+          if ((e = hipMemcpyAsync(staging + stage_at[j], srcs[j % 4][j / 4], (size_t)f.rows * f.cols * 2,
+                                  hipMemcpyHostToDevice, s)) != hipSuccess)
+            return jobs_fail(e, "hipMemcpyAsync(factor)");
+        }
+      if ((e = launch_pack_batch(jobs_d + j0, starts_d + j0, j1 - j0, starts[j1] - starts[j0], s)) != hipSuccess)
+        return jobs_fail(e, "pack kernel");
+      j0 = j1;
+    }
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return jobs_fail(e, "hipStreamSynchronize");
+    (void)hipFree(jobs_d);
+  }
+  for (int b = 0; i8 && b < c->n_blocks; ++b) {
     const BlockMeta& m = c->meta[b];
     for (int w = 0; w < 4; ++w) {
       const FactorGeom f = geom_of(*c, b, w);

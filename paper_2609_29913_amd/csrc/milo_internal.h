@@ -517,6 +517,10 @@ int report_error(int code, const char* msg);  // stores msg, returns code
 bool timing_enabled();
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+// bf16 factors in one launch: jobs and starts (n_jobs + 1 running sums of the
+// jobs' fragment counts, n_frags = starts[n_jobs] - starts[0]) in device memory.
+hipError_t launch_pack_batch(const PackArgs* jobs, const int64_t* starts, int n_jobs, int64_t n_frags,
+                             hipStream_t s);
 // INT8 P factors: per-row scales of a row-major bf16 factor [rows][cols] into
 // scale[0 .. rows_pad) (rows past `rows` get 0); a row that is not finite sets *bad.
 hipError_t launch_row_scales(const uint16_t* src, int rows, int cols, int rows_pad, float* scale, int* bad,

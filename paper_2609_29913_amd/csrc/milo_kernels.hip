@@ -131,6 +131,23 @@ __device__ __forceinline__ void wait_vmcnt() {
 // ---------------------------------------------------------------------------
 // Packing
 // ---------------------------------------------------------------------------
+// bf16 factor: the 8 elements of lane `lane` of fragment `frag`, one 16-byte store
+__device__ __forceinline__ void pack_bf16_fragment(const PackArgs& a, int64_t frag, int lane) {
+  uint16_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    int row, col;
+    frag_source(a.geom, frag, lane, e, &row, &col);
+    v[e] = (row < a.geom.rows && col < a.geom.cols) ? a.src[(int64_t)row * a.geom.cols + col] : 0;
+  }
+  uint4 out;
+  out.x = v[0] | ((uint32_t)v[1] << 16);
+  out.y = v[2] | ((uint32_t)v[3] << 16);
+  out.z = v[4] | ((uint32_t)v[5] << 16);
+  out.w = v[6] | ((uint32_t)v[7] << 16);
+  *reinterpret_cast<uint4*>(a.dst + frag * kFragElems + lane * 8) = out;
+}
+
 __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t frag = gid >> 6;
@@ -159,19 +176,23 @@ __global__ __launch_bounds__(256) void pack_kernel(PackArgs a) {
         make_uint2(w[0], w[1]);
     return;
   }
-  uint16_t v[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    int row, col;
-    frag_source(a.geom, frag, lane, e, &row, &col);
-    v[e] = (row < a.geom.rows && col < a.geom.cols) ? a.src[(int64_t)row * a.geom.cols + col] : 0;
+  pack_bf16_fragment(a, frag, lane);
+}
+
+// Many bf16 factors in one launch: job j packs fragments
+// starts[j] .. starts[j + 1] - 1 of a flat fragment range that begins at
+// starts[0]; 4 fragments per workgroup, each lane finding its job by binary search.
+__global__ __launch_bounds__(256) void pack_batch_kernel(const PackArgs* jobs, const int64_t* starts, int n_jobs) {
+  const int64_t g = starts[0] + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = (int)(threadIdx.x & 63);
+  if (g >= starts[n_jobs]) return;
+  int lo = 0, hi = n_jobs - 1;  // the last job whose start is <= g
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (starts[mid] <= g) lo = mid;
+    else hi = mid - 1;
   }
-  uint4 out;
-  out.x = v[0] | ((uint32_t)v[1] << 16);
-  out.y = v[2] | ((uint32_t)v[3] << 16);
-  out.z = v[4] | ((uint32_t)v[5] << 16);
-  out.w = v[6] | ((uint32_t)v[7] << 16);
-  *reinterpret_cast<uint4*>(a.dst + frag * kFragElems + lane * 8) = out;
+  pack_bf16_fragment(jobs[lo], g - starts[lo], lane);
 }
 
 // INT8 P factors: per-row scale s = max |P[row][:]| / 127 (fp32, correctly
@@ -1240,6 +1261,15 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
+hipError_t launch_pack_batch(const PackArgs* jobs, const int64_t* starts, int n_jobs, int64_t n_frags,
+                             hipStream_t s) {
+  if (n_jobs == 0 || n_frags == 0) return hipSuccess;
+  const int64_t groups = (n_frags + 3) / 4;
+  if (groups > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pack_batch_kernel, dim3((unsigned)groups), dim3(256), 0, s, jobs, starts, n_jobs);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
   if (a.n_frags == 0) return hipSuccess;
   const int64_t threads = a.n_frags * 64;
