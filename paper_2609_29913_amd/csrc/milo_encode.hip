@@ -107,7 +107,8 @@ struct BJArgs {
 };
 constexpr int kBJ = 64;       // subproblem order (two blocks of 32)
 constexpr int kBJS = kBJ + 1;  // LDS row stride
-constexpr int kBJThreads = 256;
+constexpr int kBJThreads = 256;    // init and apply kernels (the 64 x 64 products: one 32 x 32 quadrant per wave)
+constexpr int kSolveThreads = 1024;  // subproblem sweep: one 2 x 2 block and two row pairs of J per thread per round
 constexpr int kMaxSweeps = 30;
 
 // V_b = I, floor_abs[b] = 1e-10 trace(G_b), the per-matrix flags cleared; grid: n.
@@ -134,27 +135,29 @@ __global__ __launch_bounds__(kBJThreads) void bj_init_kernel(BJArgs a, int* swee
   }
 }
 
-// 64 x 64 products in LDS, 256 threads, each the 4 x 4 outputs (ty + 16 u, tx + 16 v).
-// out = X^T Y (transpose_x) or X Y.
+// 64 x 64 x 64 products in LDS on four waves, by v_mfma_f32_32x32x2_f32: wave w
+// of the four computes the 32 x 32 quadrant (rows 32 (w >> 1), columns
+// 32 (w & 1)) of X^T Y (transpose_x) or X Y.  Operand lanes: A (row l % 32,
+// k l / 32), B (k l / 32, column l % 32); the result in the 32 x 32 MFMA layout,
+// lane l holding column l % 32 of rows 8 (i / 4) + 4 (l / 32) + i % 4, i = 0..15
+// (bj_row, bj_col give its place in the 64 x 64 result).
+typedef float f32x16e __attribute__((ext_vector_type(16)));
 template <bool TRANSPOSE_X>
-__device__ __forceinline__ void bj_product(const float (*X)[kBJS], const float (*Y)[kBJS], float acc[4][4]) {
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) acc[u][v] = 0.f;
-  for (int k = 0; k < kBJ; ++k) {
-    float x[4], y[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) x[u] = TRANSPOSE_X ? X[k][ty + 16 * u] : X[ty + 16 * u][k];
-#pragma unroll
-    for (int v = 0; v < 4; ++v) y[v] = Y[k][tx + 16 * v];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(x[u], y[v], acc[u][v]);
+__device__ __forceinline__ f32x16e bj_product(const float (*X)[kBJS], const float (*Y)[kBJS]) {
+  const int lane = threadIdx.x & 63, w = (threadIdx.x >> 6) & 3;
+  const int r0 = 32 * (w >> 1), c0 = 32 * (w & 1), m = lane & 31, kk = lane >> 5;
+  f32x16e acc = {};
+#pragma unroll 8
+  for (int k0 = 0; k0 < kBJ; k0 += 2) {
+    const float x = TRANSPOSE_X ? X[k0 + kk][r0 + m] : X[r0 + m][k0 + kk];
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x, Y[k0 + kk][c0 + m], acc, 0, 0, 0);
   }
+  return acc;
 }
+__device__ __forceinline__ int bj_row(int i) {
+  return 32 * (((threadIdx.x >> 6) & 3) >> 1) + 8 * (i >> 2) + 4 * ((threadIdx.x & 63) >> 5) + (i & 3);
+}
+__device__ __forceinline__ int bj_col() { return 32 * ((threadIdx.x >> 6) & 1) + (threadIdx.x & 31); }
 
 // Round rr of the circle ordering of the 64 subproblem indices, pair t (no division).
 __device__ __forceinline__ void circle_pair64(int rr, int t, int* p, int* q) {
@@ -179,7 +182,7 @@ __device__ __forceinline__ void circle_pair64(int rr, int t, int* p, int* q) {
 // into G; J, made orthogonal to rounding by one Newton-Schulz step
 // J (3 I - J^T J) / 2, goes to the rotation buffer for bj_apply_kernel.
 // grid: (n_blk / 2, n).
-__global__ __launch_bounds__(kBJThreads) void bj_solve_kernel(BJArgs a) {
+__global__ __launch_bounds__(kSolveThreads) void bj_solve_kernel(BJArgs a) {
   __shared__ float S[kBJ][kBJS], Jm[kBJ][kBJS], M[kBJ][kBJS];
   __shared__ float2 rot[kBJ / 2];  // (c, s) of index pair k this round
   __shared__ int pq[kBJ / 2];      // p | q << 8
@@ -192,7 +195,7 @@ __global__ __launch_bounds__(kBJThreads) void bj_solve_kernel(BJArgs a) {
   circle_pair(a.n_blk, a.round, pair, &u, &w);
   auto gi = [&](int i) { return i < 32 ? u * 32 + i : w * 32 + (i - 32); };
   float* G = a.G + (size_t)b * Dp * Dp;
-  for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+  for (int x = tid; x < kBJ * kBJ; x += kSolveThreads) {
     const int i = x / kBJ, j = x % kBJ;
     S[i][j] = G[(size_t)gi(i) * Dp + gi(j)];
     Jm[i][j] = i == j ? 1.f : 0.f;
@@ -225,8 +228,8 @@ __global__ __launch_bounds__(kBJThreads) void bj_solve_kernel(BJArgs a) {
     __syncthreads();
     // S <- R^T S R, one 2 x 2 block per item, the mirror block written as its transpose
 #pragma unroll
-    for (int m = 0; m < (kUpper + kBJThreads - 1) / kBJThreads; ++m) {
-      const int x = tid + m * kBJThreads;
+    for (int m = 0; m < (kUpper + kSolveThreads - 1) / kSolveThreads; ++m) {
+      const int x = tid + m * kSolveThreads;
       if (x >= kUpper) break;
       const int r = x / (kHalf + 1), c0 = x % (kHalf + 1);
       const bool first = c0 < kHalf - r;
@@ -264,16 +267,16 @@ __global__ __launch_bounds__(kBJThreads) void bj_solve_kernel(BJArgs a) {
       S[ql][qk] = g11;
     }
     // J <- J R (columns p, q of every row): lane i of wave v takes row i and the
-    // index pairs v, v + 4, ...; the pairs' parameters are read before any update
+    // index pairs v, v + 16; the pairs' parameters are read before any update
     {
       const int i = tid % kBJ, v0 = tid / kBJ;
-      constexpr int kPer = kHalf / (kBJThreads / kBJ);
+      constexpr int kPer = kHalf / (kSolveThreads / kBJ);
       float2 rk[kPer];
       int pqk[kPer];
 #pragma unroll
       for (int m = 0; m < kPer; ++m) {
-        rk[m] = rot[v0 + m * (kBJThreads / kBJ)];
-        pqk[m] = pq[v0 + m * (kBJThreads / kBJ)];
+        rk[m] = rot[v0 + m * (kSolveThreads / kBJ)];
+        pqk[m] = pq[v0 + m * (kSolveThreads / kBJ)];
       }
 #pragma unroll
       for (int m = 0; m < kPer; ++m) {
@@ -290,28 +293,24 @@ __global__ __launch_bounds__(kBJThreads) void bj_solve_kernel(BJArgs a) {
   const bool rotated = any_rot != 0;
   if (tid == 0) a.rot_pair[(size_t)b * n_pair + pair] = rotated ? 1 : 0;
   if (!rotated) return;
-  for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
+  for (int x = tid; x < kBJ * kBJ; x += kSolveThreads) {
     const int i = x / kBJ, j = x % kBJ;
     G[(size_t)gi(i) * Dp + gi(j)] = S[i][j];
   }
-  // Newton-Schulz: M = J^T J, then J (3 I - M) / 2 = 1.5 J - 0.5 J M
-  float acc[4][4];
-  bj_product<true>(Jm, Jm, acc);
-  const int tx = tid % 16, ty = tid / 16;
+  // Newton-Schulz: M = J^T J, then J (3 I - M) / 2 = 1.5 J - 0.5 J M (the
+  // products on the first four waves)
+  if (tid < kBJThreads) {
+    const f32x16e t = bj_product<true>(Jm, Jm);
 #pragma unroll
-  for (int uu = 0; uu < 4; ++uu)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) M[ty + 16 * uu][tx + 16 * v] = acc[uu][v];
+    for (int i = 0; i < 16; ++i) M[bj_row(i)][bj_col()] = t[i];
+  }
   __syncthreads();
-  bj_product<false>(Jm, M, acc);
-  float* Jout = a.J + ((size_t)b * n_pair + pair) * kBJ * kBJ;
+  if (tid < kBJThreads) {
+    const f32x16e t = bj_product<false>(Jm, M);
+    float* Jout = a.J + ((size_t)b * n_pair + pair) * kBJ * kBJ;
 #pragma unroll
-  for (int uu = 0; uu < 4; ++uu)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int i = ty + 16 * uu, j = tx + 16 * v;
-      Jout[i * kBJ + j] = 1.5f * Jm[i][j] - 0.5f * acc[uu][v];
-    }
+    for (int i = 0; i < 16; ++i) Jout[bj_row(i) * kBJ + bj_col()] = 1.5f * Jm[bj_row(i)][bj_col()] - 0.5f * t[i];
+  }
   if (tid == 0) {
     a.rot_mat[b] = 1;
     atomicAdd(&a.gemms[b], 2u);
@@ -339,8 +338,6 @@ __global__ __launch_bounds__(kBJThreads) void bj_apply_kernel(BJArgs a) {
   int task = blockIdx.x;
   const int* rot = a.rot_pair + (size_t)b * n_pair;
   const float* Jb = a.J + (size_t)b * n_pair * kBJ * kBJ;
-  const int tx = tid % 16, ty = tid / 16;
-  float acc[4][4];
   if (task < n_g) {
     int p = 0;
     while (task >= n_pair - 1 - p) {
@@ -364,21 +361,17 @@ __global__ __launch_bounds__(kBJThreads) void bj_apply_kernel(BJArgs a) {
     }
     __syncthreads();
     if (rp) {
-      bj_product<true>(Jp, A, acc);
+      const f32x16e t = bj_product<true>(Jp, A);
       __syncthreads();
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) A[ty + 16 * u][tx + 16 * v] = acc[u][v];
+      for (int i = 0; i < 16; ++i) A[bj_row(i)][bj_col()] = t[i];
       __syncthreads();
     }
     if (rq) {
-      bj_product<false>(A, Jq, acc);
+      const f32x16e t = bj_product<false>(A, Jq);
       __syncthreads();
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) A[ty + 16 * u][tx + 16 * v] = acc[u][v];
+      for (int i = 0; i < 16; ++i) A[bj_row(i)][bj_col()] = t[i];
       __syncthreads();
     }
     for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
@@ -407,11 +400,9 @@ __global__ __launch_bounds__(kBJThreads) void bj_apply_kernel(BJArgs a) {
       A[i][j] = V[(size_t)i * Dp + gp(j)];
     }
     __syncthreads();
-    bj_product<false>(A, Jp, acc);
+    const f32x16e t = bj_product<false>(A, Jp);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) V[(size_t)(ty + 16 * u) * Dp + gp(tx + 16 * v)] = acc[u][v];
+    for (int i = 0; i < 16; ++i) V[(size_t)bj_row(i) * Dp + gp(bj_col())] = t[i];
     __syncthreads();  // A is reloaded by the next chunk
   }
   if (tid == 0) atomicAdd(&a.gemms[b], (unsigned)(c1 - c0));
@@ -639,7 +630,7 @@ extern "C" int milo_block_svd(const uint16_t* const* k, const int32_t* tokens, i
     for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
       for (int round = 0; round < n_blk - 1; ++round) {
         a.round = round;
-        hipLaunchKernelGGL(bj_solve_kernel, dim3(n_pair, nb), dim3(kBJThreads), 0, s, a);
+        hipLaunchKernelGGL(bj_solve_kernel, dim3(n_pair, nb), dim3(kSolveThreads), 0, s, a);
         hipLaunchKernelGGL(bj_apply_kernel, dim3(bj_tasks(n_blk, Dp), nb), dim3(kBJThreads), 0, s, a);
       }
       hipLaunchKernelGGL(bj_sweep_end_kernel, dim3(1), dim3(1024), 0, s, a, nb, sweep, sweeps_d, remaining_d);
