@@ -157,6 +157,12 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
   std::vector<int> grp_nh(n_cg, 1);  // most KV heads of a tile in the group
   for (int k = 0; k < n_ct; ++k) grp_nh[k / C] = std::max(grp_nh[k / C], til.nh[k]);
   out->gang = C;
+  // a workgroup folds consecutive block items of one column tile into one
+  // partial where the kernel keeps that partial in registers (at most two
+  // latent rank tiles per wave)
+  int max_own_all = 0;
+  for (int j = 0; j < n_sel; ++j) max_own_all = std::max(max_own_all, max_owned(item_meta(table[j])));
+  const bool fold = max_own_all <= 2;
   double total_blk = 0.0;
   for (int j = 0; j < n_sel; ++j) {
     const BlockMeta m = item_meta(table[j]);
@@ -250,9 +256,16 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
       lists[lo].push_back(ki);
       load[lo] += jobs[ki].cost;
     }
-    for (auto& l : lists)  // tail jobs first, then the longest block jobs
+    // tail jobs first, then the longest block jobs.  Where items fold, the
+    // block jobs go by column group first: consecutive items of one column
+    // tile share one partial slot, so a gang writes (and the merge reads) one
+    // partial per column group instead of one per block.  Where they do not,
+    // the order stays by length alone, which keeps the column groups of one
+    // block close in time on different gangs (its P is read while cached).
+    for (auto& l : lists)
       std::stable_sort(l.begin(), l.end(), [&](int x, int y) {
         if ((jobs[x].part < 0) != (jobs[y].part < 0)) return jobs[x].part < 0;
+        if (fold && jobs[x].cg != jobs[y].cg) return jobs[x].cg < jobs[y].cg;
         return jobs[x].cost > jobs[y].cost;
       });
     return *std::max_element(load.begin(), load.end());
@@ -281,10 +294,6 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
     out->max_own = std::max(out->max_own, max_owned(m));
   }
 
-  // a workgroup folds consecutive block items of one column tile into one
-  // partial where the kernel keeps that partial in registers (at most two
-  // latent rank tiles per wave)
-  const bool fold = out->max_own <= 2;
   // LDS plan: the projected query, weight tile and a 6-slot fragment ring,
   // the rest for the program (fewer launches would cost the ring); when even a
   // short program leaves no room for that (ranks above 512), the weight tile

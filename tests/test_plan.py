@@ -110,6 +110,21 @@ def test_column_tiling_choices(checker):
     assert "tiles 40 (mode 1) gang 8" in lines[3]
 
 
+def test_folded_slots_per_column_group(checker):
+    """The 14B-shaped batch has five column groups per gang.  With every block
+    rebuilt (dense items, foldable) each gang's items go by column group and fold
+    into one slot per gang and tile: 32 slots per column tile instead of one per
+    block.  The latent plan (ranks to 768, three rank tiles per wave: the kernel
+    does not fold) keeps one slot per block and its order by length."""
+    cfg = synth.CONFIGS["q14b_48l"]
+    T = synth.draw_block_tokens(cfg)
+    r = synth.draw_ranks(cfg, 0, len(T))
+    args = (cfg.n_kv_heads, cfg.head_dim, cfg.group, cfg.n_q, _chunks(cfg.tail, cfg.tail), T, r)
+    lines = _run(checker, [_case(*args, recon=1), _case(*args, recon=0)]).splitlines()
+    assert "gang 8" in lines[0] and "slots 32 " in lines[0], lines[0]
+    assert "slots 256 " in lines[1], lines[1]
+
+
 def test_plans_with_reconstructed_blocks(checker):
     """Reconstruct-then-attend plans: every block or every other block rebuilt,
     on the workloads and on random shapes (few and many columns per KV head):
