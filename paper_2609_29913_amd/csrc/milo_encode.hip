@@ -4,7 +4,8 @@
 // R = V_r^T that milo_cache_create stores.  (The ranks r_b in between come
 // from the entropy rank allocation, milo_allocate_ranks.)
 //
-//  gram_kernel     G_b = K_b^T K_b (fp32, D_pad x D_pad, zero-padded to a multiple of 64)
+//  gram_kernel     G_b = K_b^T K_b (bf16 MFMA, fp32 accumulation; D_pad x D_pad,
+//                  zero-padded to a multiple of 64)
 //  bj_*_kernel     the symmetric eigenproblem of G_b by block Jacobi: blocks of 32
 //                  indices paired by the circle ordering; per round one launch
 //                  sweeps every pair's 64 x 64 subproblem in LDS (scalar
@@ -35,45 +36,54 @@ namespace {
 constexpr int kMaxModel = 1024;      // largest D (= H_kv * d) the encoder handles
 constexpr size_t kEncodeWorkspace = size_t(2) << 30;  // G, V and rotations of the blocks in flight
 constexpr int kMaxEncodeBlocks = 65535;  // blocks per call (one grid z-slice or y-row each)
-constexpr int kGramTile = 64;        // G tile per workgroup (256 threads, 4 x 4 outputs each)
+constexpr int kGramTile = 64;        // G tile per workgroup (four waves, a 32 x 32 quadrant each)
 constexpr int kGramK = 32;           // tokens per LDS stage
 
 __device__ __forceinline__ float bf(uint16_t u) { return __uint_as_float(static_cast<uint32_t>(u) << 16); }
 
-// G_b[i][j] = sum_t K_b[t][i] K_b[t][j] over i, j < D (tokens in order); rows and
-// columns D .. D_pad - 1 are zero.  grid: (D_pad / 64 rounded up)^2 x n_blocks.
+// G_b[i][j] = sum_t K_b[t][i] K_b[t][j] over i, j < D; rows and columns
+// D .. D_pad - 1 are zero.  One workgroup (four waves) per 64 x 64 tile of G:
+// 32 tokens at a time go to LDS transposed ([dim][token], bf16) and each wave
+// accumulates its 32 x 32 quadrant with v_mfma_f32_32x32x16_bf16 (products of
+// bf16 values are exact in fp32; only the fp32 accumulation rounds).
+// grid: (D_pad / 64)^2 x n_blocks.
+typedef __bf16 bf16x8g __attribute__((ext_vector_type(8)));
+typedef float f32x16g __attribute__((ext_vector_type(16)));
+constexpr int kGramStride = kGramK + 8;  // bf16 row stride of a staged [dim][token] slice
 __global__ __launch_bounds__(256) void gram_kernel(const uint16_t* const* k, const int32_t* tokens, int D, int Dp,
                                                    float* G_all) {
-  __shared__ float a[kGramK][kGramTile + 1], c[kGramK][kGramTile + 1];
+  __shared__ __align__(16) uint16_t a[kGramTile][kGramStride], c[kGramTile][kGramStride];
   const int b = blockIdx.z;
   const int T = tokens[b];
   const uint16_t* K = k[b];
   float* G = G_all + (size_t)b * Dp * Dp;
-  const int tiles = (Dp + kGramTile - 1) / kGramTile;
+  const int tiles = Dp / kGramTile;
   const int i0 = (blockIdx.x % tiles) * kGramTile, j0 = (blockIdx.x / tiles) * kGramTile;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  float acc[4][4] = {};
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r0 = 32 * (w >> 1), c0 = 32 * (w & 1), m = lane & 31, hi = lane >> 5;
+  f32x16g acc = {};
   for (int t0 = 0; t0 < T; t0 += kGramK) {
-    for (int x = threadIdx.x; x < kGramK * kGramTile; x += 256) {
-      const int tt = x / kGramTile, col = x % kGramTile, t = t0 + tt;
-      a[tt][col] = (t < T && i0 + col < D) ? bf(K[(int64_t)t * D + i0 + col]) : 0.f;
-      c[tt][col] = (t < T && j0 + col < D) ? bf(K[(int64_t)t * D + j0 + col]) : 0.f;
+    // thread: token t0 + tid / 8, dims 8 (tid % 8) .. +7 of both tiles
+    const int tt = tid >> 3, d8 = 8 * (tid & 7), t = t0 + tt;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int di = i0 + d8 + e, dj = j0 + d8 + e;
+      a[d8 + e][tt] = (t < T && di < D) ? K[(int64_t)t * D + di] : (uint16_t)0;
+      c[d8 + e][tt] = (t < T && dj < D) ? K[(int64_t)t * D + dj] : (uint16_t)0;
     }
     __syncthreads();
-    for (int tt = 0; tt < kGramK; ++tt)
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(a[tt][ty + 16 * u], c[tt][tx + 16 * v], acc[u][v]);
+    for (int kk = 0; kk < kGramK / 16; ++kk) {
+      // A: G rows (dims of the i tile) x 16 tokens; B: 16 tokens x dims of the j tile
+      const bf16x8g x = *reinterpret_cast<const bf16x8g*>(&a[r0 + m][16 * kk + 8 * hi]);
+      const bf16x8g y = *reinterpret_cast<const bf16x8g*>(&c[c0 + m][16 * kk + 8 * hi]);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, acc, 0, 0, 0);
+    }
     __syncthreads();
   }
+  // lane (hi, m) holds column c0 + m of rows r0 + 8 (i / 4) + 4 hi + i % 4
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int i = i0 + ty + 16 * u, j = j0 + tx + 16 * v;
-      if (i < Dp && j < Dp) G[(size_t)i * Dp + j] = acc[u][v];
-    }
+  for (int i = 0; i < 16; ++i) G[(size_t)(i0 + r0 + 8 * (i >> 2) + 4 * hi + (i & 3)) * Dp + j0 + c0 + m] = acc[i];
 }
 
 // Round `round` of the circle ordering of n (even) indices: pair t's members.
