@@ -99,7 +99,7 @@ __device__ __forceinline__ void circle_pair(int n, int round, int t, int* p, int
 // n_blk / 2 disjoint block pairs.  Pair (u, w)'s subproblem is the 64 x 64
 // principal submatrix of G on blocks u and w: bj_solve_kernel rotates it by one
 // cyclic Jacobi sweep in LDS (same threshold as the whole problem) and stores
-// its rotation J; bj_apply_kernel then rotates the rest of G (G_pq <- J_p^T
+// its rotation J; bj_apply_*_kernel then rotate the rest of G (G_pq <- J_p^T
 // G_pq J_q between pairs) and V (V[:, pair p] <- V[:, pair p] J_p).  A sweep in
 // which no subproblem needed a rotation leaves every off-diagonal entry of G
 // below the threshold.
@@ -190,7 +190,7 @@ __device__ __forceinline__ void circle_pair64(int rr, int t, int* p, int* q) {
 // angle): this keeps the eigenvalues at the accuracy of the Gram matrix and lets
 // rank-deficient blocks (T_b < D) converge.  The rotated subproblem goes back
 // into G; J, made orthogonal to rounding by one Newton-Schulz step
-// J (3 I - J^T J) / 2, goes to the rotation buffer for bj_apply_kernel.
+// J (3 I - J^T J) / 2, goes to the rotation buffer for the apply kernels.
 // grid: (n_blk / 2, n).
 __global__ __launch_bounds__(kSolveThreads) void bj_solve_kernel(BJArgs a) {
   __shared__ float S[kBJ][kBJS], Jm[kBJ][kBJS], M[kBJ][kBJS];
@@ -327,95 +327,93 @@ __global__ __launch_bounds__(kSolveThreads) void bj_solve_kernel(BJArgs a) {
   }
 }
 
-// Tasks of one matrix in a round: the n_pair (n_pair - 1) / 2 off-diagonal pair
-// blocks of G (p < q), then V's pair columns in groups of kVChunks 64-row
-// chunks (n_pair of them per group).
-constexpr int kVChunks = 1;  // 64-row chunks of V per workgroup (one load of J_p for all)
-__host__ __device__ inline int bj_v_groups(int Dp) { return (Dp / kBJ + kVChunks - 1) / kVChunks; }
-__host__ __device__ inline int bj_tasks(int n_blk, int Dp) {
-  const int n_pair = n_blk / 2;
-  return n_pair * (n_pair - 1) / 2 + bj_v_groups(Dp) * n_pair;
-}
-
-// One workgroup per (task, matrix): G_pq <- J_p^T G_pq J_q (and G_qp its
-// transpose), or V[chunk rows][pair p columns] <- that slice J_p.  An identity
-// J (a pair with no rotation) is skipped.  grid: (bj_tasks, n).
-__global__ __launch_bounds__(kBJThreads) void bj_apply_kernel(BJArgs a) {
+// The rest of a round, in two launches.  bj_apply_g_kernel: one workgroup per
+// (off-diagonal pair block p < q of G, matrix): G_pq <- J_p^T G_pq J_q and G_qp
+// its transpose.  bj_apply_v_kernel: one workgroup per (pair p, 64-row chunk
+// of V, matrix): V[chunk rows][pair p columns] <- that slice J_p (two LDS
+// tiles, so four workgroups fit per CU).  An identity J (a pair with no
+// rotation) is skipped.  Rows of a pair's index set are two runs of 32, so
+// 4-float groups are contiguous and 16-byte aligned in G, V and J.
+__global__ __launch_bounds__(kBJThreads) void bj_apply_g_kernel(BJArgs a) {
   __shared__ float A[kBJ][kBJS], Jp[kBJ][kBJS], Jq[kBJ][kBJS];
   const int b = blockIdx.y, tid = threadIdx.x, Dp = a.Dp, n_pair = a.n_blk / 2;
   if (!a.active[b]) return;
-  const int n_g = n_pair * (n_pair - 1) / 2;
   int task = blockIdx.x;
   const int* rot = a.rot_pair + (size_t)b * n_pair;
   const float* Jb = a.J + (size_t)b * n_pair * kBJ * kBJ;
-  if (task < n_g) {
-    int p = 0;
-    while (task >= n_pair - 1 - p) {
-      task -= n_pair - 1 - p;
-      ++p;
-    }
-    const int q = p + 1 + task;
-    const bool rp = rot[p] != 0, rq = rot[q] != 0;
-    if (!rp && !rq) return;
-    int up, wp, uq, wq;
-    circle_pair(a.n_blk, a.round, p, &up, &wp);
-    circle_pair(a.n_blk, a.round, q, &uq, &wq);
-    auto gp = [&](int i) { return i < 32 ? up * 32 + i : wp * 32 + (i - 32); };
-    auto gq = [&](int i) { return i < 32 ? uq * 32 + i : wq * 32 + (i - 32); };
-    float* G = a.G + (size_t)b * Dp * Dp;
-    for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
-      const int i = x / kBJ, j = x % kBJ;
-      A[i][j] = G[(size_t)gp(i) * Dp + gq(j)];
-      if (rp) Jp[i][j] = Jb[((size_t)p * kBJ + i) * kBJ + j];
-      if (rq) Jq[i][j] = Jb[((size_t)q * kBJ + i) * kBJ + j];
-    }
-    __syncthreads();
+  int p = 0;
+  while (task >= n_pair - 1 - p) {
+    task -= n_pair - 1 - p;
+    ++p;
+  }
+  const int q = p + 1 + task;
+  const bool rp = rot[p] != 0, rq = rot[q] != 0;
+  if (!rp && !rq) return;
+  int up, wp, uq, wq;
+  circle_pair(a.n_blk, a.round, p, &up, &wp);
+  circle_pair(a.n_blk, a.round, q, &uq, &wq);
+  auto gp = [&](int i) { return i < 32 ? up * 32 + i : wp * 32 + (i - 32); };
+  auto gq = [&](int i) { return i < 32 ? uq * 32 + i : wq * 32 + (i - 32); };
+  float* G = a.G + (size_t)b * Dp * Dp;
+  for (int x = tid; x < kBJ * kBJ / 4; x += kBJThreads) {
+    const int i = x / (kBJ / 4), j = 4 * (x % (kBJ / 4));
+    const float4 g = *reinterpret_cast<const float4*>(G + (size_t)gp(i) * Dp + gq(j));
+    A[i][j] = g.x, A[i][j + 1] = g.y, A[i][j + 2] = g.z, A[i][j + 3] = g.w;
     if (rp) {
-      const f32x16e t = bj_product<true>(Jp, A);
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < 16; ++i) A[bj_row(i)][bj_col()] = t[i];
-      __syncthreads();
+      const float4 v = *reinterpret_cast<const float4*>(Jb + ((size_t)p * kBJ + i) * kBJ + j);
+      Jp[i][j] = v.x, Jp[i][j + 1] = v.y, Jp[i][j + 2] = v.z, Jp[i][j + 3] = v.w;
     }
     if (rq) {
-      const f32x16e t = bj_product<false>(A, Jq);
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < 16; ++i) A[bj_row(i)][bj_col()] = t[i];
-      __syncthreads();
+      const float4 v = *reinterpret_cast<const float4*>(Jb + ((size_t)q * kBJ + i) * kBJ + j);
+      Jq[i][j] = v.x, Jq[i][j + 1] = v.y, Jq[i][j + 2] = v.z, Jq[i][j + 3] = v.w;
     }
-    for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
-      const int i = x / kBJ, j = x % kBJ;
-      G[(size_t)gp(i) * Dp + gq(j)] = A[i][j];
-      G[(size_t)gq(i) * Dp + gp(j)] = A[j][i];
-    }
-    if (tid == 0) atomicAdd(&a.gemms[b], (rp ? 1u : 0u) + (rq ? 1u : 0u));
-    return;
   }
-  task -= n_g;
-  const int p = task % n_pair, group = task / n_pair;
-  if (!rot[p]) return;
+  __syncthreads();
+  if (rp) {
+    const f32x16e t = bj_product<true>(Jp, A);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 16; ++i) A[bj_row(i)][bj_col()] = t[i];
+    __syncthreads();
+  }
+  if (rq) {
+    const f32x16e t = bj_product<false>(A, Jq);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 16; ++i) A[bj_row(i)][bj_col()] = t[i];
+    __syncthreads();
+  }
+  for (int x = tid; x < kBJ * kBJ / 4; x += kBJThreads) {
+    const int i = x / (kBJ / 4), j = 4 * (x % (kBJ / 4));
+    *reinterpret_cast<float4*>(G + (size_t)gp(i) * Dp + gq(j)) = make_float4(A[i][j], A[i][j + 1], A[i][j + 2], A[i][j + 3]);
+    *reinterpret_cast<float4*>(G + (size_t)gq(i) * Dp + gp(j)) = make_float4(A[j][i], A[j + 1][i], A[j + 2][i], A[j + 3][i]);
+  }
+  if (tid == 0) atomicAdd(&a.gemms[b], (rp ? 1u : 0u) + (rq ? 1u : 0u));
+}
+
+__global__ __launch_bounds__(kBJThreads) void bj_apply_v_kernel(BJArgs a) {
+  __shared__ float A[kBJ][kBJS], Jp[kBJ][kBJS];
+  const int b = blockIdx.y, tid = threadIdx.x, Dp = a.Dp, n_pair = a.n_blk / 2;
+  if (!a.active[b]) return;
+  const int p = blockIdx.x % n_pair, chunk = blockIdx.x / n_pair;
+  if (!a.rot_pair[(size_t)b * n_pair + p]) return;
   int up, wp;
   circle_pair(a.n_blk, a.round, p, &up, &wp);
   auto gp = [&](int i) { return i < 32 ? up * 32 + i : wp * 32 + (i - 32); };
-  for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
-    const int i = x / kBJ, j = x % kBJ;
-    Jp[i][j] = Jb[((size_t)p * kBJ + i) * kBJ + j];
+  const float* J = a.J + ((size_t)b * n_pair + p) * kBJ * kBJ;
+  float* V = a.V + (size_t)b * Dp * Dp + (size_t)chunk * kBJ * Dp;
+  for (int x = tid; x < kBJ * kBJ / 4; x += kBJThreads) {
+    const int i = x / (kBJ / 4), j = 4 * (x % (kBJ / 4));
+    const float4 v = *reinterpret_cast<const float4*>(V + (size_t)i * Dp + gp(j));
+    A[i][j] = v.x, A[i][j + 1] = v.y, A[i][j + 2] = v.z, A[i][j + 3] = v.w;
+    const float4 r = *reinterpret_cast<const float4*>(J + (size_t)i * kBJ + j);
+    Jp[i][j] = r.x, Jp[i][j + 1] = r.y, Jp[i][j + 2] = r.z, Jp[i][j + 3] = r.w;
   }
-  const int c0 = group * kVChunks, c1 = min(c0 + kVChunks, Dp / kBJ);
-  for (int chunk = c0; chunk < c1; ++chunk) {
-    float* V = a.V + (size_t)b * Dp * Dp + (size_t)chunk * kBJ * Dp;
-    for (int x = tid; x < kBJ * kBJ; x += kBJThreads) {
-      const int i = x / kBJ, j = x % kBJ;
-      A[i][j] = V[(size_t)i * Dp + gp(j)];
-    }
-    __syncthreads();
-    const f32x16e t = bj_product<false>(A, Jp);
+  __syncthreads();
+  const f32x16e t = bj_product<false>(A, Jp);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) V[(size_t)bj_row(i) * Dp + gp(bj_col())] = t[i];
-    __syncthreads();  // A is reloaded by the next chunk
-  }
-  if (tid == 0) atomicAdd(&a.gemms[b], (unsigned)(c1 - c0));
+  for (int i = 0; i < 16; ++i) V[(size_t)bj_row(i) * Dp + gp(bj_col())] = t[i];
+  if (tid == 0) atomicAdd(&a.gemms[b], 1u);
 }
 
 // End of a sweep: a matrix with no rotation in it is done; the others count the
@@ -641,7 +639,9 @@ extern "C" int milo_block_svd(const uint16_t* const* k, const int32_t* tokens, i
       for (int round = 0; round < n_blk - 1; ++round) {
         a.round = round;
         hipLaunchKernelGGL(bj_solve_kernel, dim3(n_pair, nb), dim3(kSolveThreads), 0, s, a);
-        hipLaunchKernelGGL(bj_apply_kernel, dim3(bj_tasks(n_blk, Dp), nb), dim3(kBJThreads), 0, s, a);
+        if (n_pair > 1)
+          hipLaunchKernelGGL(bj_apply_g_kernel, dim3(n_pair * (n_pair - 1) / 2, nb), dim3(kBJThreads), 0, s, a);
+        hipLaunchKernelGGL(bj_apply_v_kernel, dim3(n_pair * (Dp / kBJ), nb), dim3(kBJThreads), 0, s, a);
       }
       hipLaunchKernelGGL(bj_sweep_end_kernel, dim3(1), dim3(1024), 0, s, a, nb, sweep, sweeps_d, remaining_d);
       if ((e = hipGetLastError()) != hipSuccess) return hfail(e, "jacobi kernels");
