@@ -31,6 +31,13 @@ that maximise the retained spectral information (Eq. 5) under a total rank
 budget and per-block bounds (Eq. 6), found by the greedy over marginal gains
 (Eq. 7) that the paper describes.
 
+`rope` is the rotary position embedding of the Qwen2 models the paper
+measures (Sec. 3 studies, and Sec. 4.2 factorises, the keys before it is
+applied); `attend_dense` and `attend_prefill` apply it to the keys that the
+factors define when they are given the blocks' positions, which is what
+attending such a cache by reconstruction means (Sec. 4.5, Alg. 1 full-rank
+reconstruction: the rank space cannot carry the rotation).
+
 `attend_latent` reaches the same numbers by exact reassociation,
 q.(P R)_t = P_t.(R q) and sum_t w_t (P R)_t = (sum_t w_t P_t) R, which is the
 order the GPU path follows: project the query per block, score against P^K
@@ -46,7 +53,7 @@ import math
 import numpy as np
 
 __all__ = ["allocate_ranks", "attend_dense", "attend_latent", "attend_prefill", "block_factors", "block_svd",
-           "dequantize_rows_int8", "quantize_rows_int8", "reconstruct", "spectral_information"]
+           "dequantize_rows_int8", "quantize_rows_int8", "reconstruct", "rope", "spectral_information"]
 
 
 def _mm(a: np.ndarray, b: np.ndarray, ordered: bool) -> np.ndarray:
@@ -85,6 +92,40 @@ def reconstruct(p: np.ndarray, r: np.ndarray, ordered: bool = False) -> np.ndarr
     return _mm(p, r, ordered)
 
 
+def rope(x, positions, theta: float) -> np.ndarray:
+    """Rotary position embedding (RoFormer, Su et al.) in the rotate-half
+    arrangement of the Qwen2 models the paper measures.  Along the last axis
+    (length d, even), element j < d/2 pairs with element j + d/2; the pair (u, v)
+    of a row at position p turns by the angle p * theta^(-2j/d):
+        (u, v) -> (u cos - v sin,  v cos + u sin).
+    positions holds one integer per index of the first axis; the angles are
+    formed in float64 from the integer position.  Returns a new float64 array."""
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    if d % 2:
+        raise ValueError("the rotated axis must have even length")
+    pos = np.asarray(positions, dtype=np.int64)
+    if pos.shape != x.shape[:1]:
+        raise ValueError("one position per row of the first axis")
+    freq = float(theta) ** (-2.0 * np.arange(d // 2, dtype=np.float64) / d)
+    ang = pos.astype(np.float64)[:, None] * freq[None, :]       # [rows, d/2]
+    ang = ang.reshape(ang.shape[:1] + (1,) * (x.ndim - 2) + ang.shape[1:])
+    c, s = np.cos(ang), np.sin(ang)
+    u, v = x[..., : d // 2], x[..., d // 2:]
+    return np.concatenate([u * c - v * s, v * c + u * s], axis=-1)
+
+
+def _block_keys(pk, rk, b, d, key_pos, rope_theta, ordered):
+    """The keys block b's factors define (Eq. 3), rotated to the block's
+    positions key_pos[b] + t when key_pos is given (pre-RoPE keys)."""
+    k = reconstruct(pk[b], rk[b], ordered)
+    if key_pos is None:
+        return k
+    T = k.shape[0]
+    kh = k.reshape(T, -1, d)                               # [T, H_kv, d]
+    return rope(kh, int(key_pos[b]) + np.arange(T), rope_theta).reshape(T, -1)
+
+
 def _shapes(q, rk_list, tail_k):
     n_q, n_q_heads, d = q.shape
     n_kv = tail_k.shape[2]
@@ -96,7 +137,8 @@ def _shapes(q, rk_list, tail_k):
     return n_q, n_q_heads, d, n_kv, n_q_heads // n_kv
 
 
-def attend_dense(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale, ordered=False):
+def attend_dense(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale, ordered=False, key_pos=None,
+                 rope_theta=None):
     """Definition: Eq. 1 over the keys/values that the factors of the selected
     blocks define (Eq. 3), in table order, followed by request i's first
     tail_len[i] uncompressed tail tokens:
@@ -109,10 +151,14 @@ def attend_dense(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale, orde
         P^K_b [T_b, rk_b], R^K_b [rk_b, H_kv*d], P^V_b [T_b, rv_b], R^V_b [rv_b, H_kv*d]
     table: selected block ids, in order
     q: [n_q, H_q, d]; tail_k, tail_v: [n_q, tail_cap, H_kv, d]; tail_len: [n_q]
+    key_pos, rope_theta: optional (pre-RoPE keys): key_pos indexed by block id
+        gives the position of the block's first token; the key of token t is
+        then rope(K_b[t], key_pos[b] + t, rope_theta), per KV head.  The
+        queries and the tail keys are taken as already rotated.
     returns o: [n_q, H_q, d] float64
     """
     n_q, n_q_heads, d, n_kv, G = _shapes(q, [rk[b] for b in table], tail_k)
-    keys = [reconstruct(pk[b], rk[b], ordered) for b in table]
+    keys = [_block_keys(pk, rk, b, d, key_pos, rope_theta, ordered) for b in table]
     vals = [reconstruct(pv[b], rv[b], ordered) for b in table]
     out = np.empty((n_q, n_q_heads, d))
     for i in range(n_q):
@@ -212,20 +258,21 @@ def attend_latent(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_len, scale,
     return (out, weights) if return_weights else out
 
 
-def attend_prefill(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_base, scale):
+def attend_prefill(pk, rk, pv, rv, table, q, tail_k, tail_v, tail_base, scale, key_pos=None, rope_theta=None):
     """Causal prefill of one request (Alg. 1 inference stage with a multi-token
     input query Q, Eq. 1 with the causal mask of an autoregressive model over
     Q's own tokens): token j of the chunk q [n_tok, H_q, d] attends to the
     selected blocks and to the first tail_base + j + 1 rows of the one tail
     tail_k / tail_v [tail_cap, H_kv, d] (the rows before the chunk, then the
-    chunk's own tokens up to and including j).  Returns [n_tok, H_q, d]."""
+    chunk's own tokens up to and including j).  key_pos / rope_theta as for
+    attend_dense.  Returns [n_tok, H_q, d]."""
     n_tok = q.shape[0]
     if tail_base + n_tok > tail_k.shape[0]:
         raise ValueError("the tail must hold tail_base + n_tok rows")
     tk = np.broadcast_to(tail_k, (n_tok,) + tail_k.shape)
     tv = np.broadcast_to(tail_v, (n_tok,) + tail_v.shape)
     tail_len = tail_base + 1 + np.arange(n_tok)
-    return attend_dense(pk, rk, pv, rv, table, q, tk, tv, tail_len, scale)
+    return attend_dense(pk, rk, pv, rv, table, q, tk, tv, tail_len, scale, key_pos=key_pos, rope_theta=rope_theta)
 
 
 # --------------------------------------------------------------------------
