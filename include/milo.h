@@ -213,6 +213,35 @@ int milo_attend_prefill(milo_cache* cache, const int32_t* block_table, int32_t n
 int milo_cache_set_path(milo_cache* cache, int32_t path);
 int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n);
 
+/* Pre-RoPE keys.  The paper factorises keys before the rotary position
+ * embedding is applied (Sec. 3 studies the low rank of pre-RoPE keys); such a
+ * cache cannot be attended in rank space (the rotation does not commute with
+ * R^K), so after this call every selected block is reconstructed (Sec. 4.5,
+ * Alg. 1 full-rank reconstruction) and its keys are rotated before attention,
+ * whatever milo_cache_set_path says: token t of block b sits at position
+ * block_pos[b] + t and its key, per KV head, becomes
+ *        (u, v) -> (u cos a - v sin a,  v cos a + u sin a),  a = p theta^(-2j/d)
+ * for each pair u = k[j], v = k[j + d/2], j < d/2 (the rotate-half arrangement
+ * of the Qwen2 models the paper evaluates).  The rotation is applied to the
+ * fp32 reconstruction, before its bf16 rounding; its cosines and sines come
+ * from a table of fp32 values of angles formed in fp64, composed as
+ * p = 256 h + l with the angle-sum formulas (error ~1e-7 per element).  The
+ * queries and the dense tail's keys are taken as already rotated (at the
+ * query's own position), as a serving stack stores them.
+ *   theta      rotary base (Qwen2.5: 1e6), finite and > 1; 0 turns the
+ *              rotation off again (keys attended as stored).
+ *   block_pos  host [n_blocks] first-token positions, 0 <= block_pos[b] and
+ *              block_pos[b] + T_b rounded up to 256 <= 2^24; NULL places the
+ *              blocks one after another in id order from position 0.  Blocks
+ *              may overlap or leave gaps (a retriever's reordering).
+ * Builds the table (16 KiB per 256 positions at d = 128) on the device and
+ * waits for the device before freeing the previous one; later calls rebuild
+ * their plan.  INT8 caches (attended latent only) return UNSUPPORTED, and so
+ * does milo_attend_decode_noalloc on such a cache when a block is selected.
+ * Errors: INVALID_ARG (NULL cache, theta, positions), UNSUPPORTED,
+ * OUT_OF_MEMORY, HIP_ERROR. */
+int milo_cache_set_rope(milo_cache* cache, double theta, const int64_t* block_pos);
+
 /* Entropy-based rank allocation of the encoder (Sec. 4.3): the per-block ranks
  * r_b that maximise the retained spectral information sum_b H_b(r_b), with
  * H_b(r) = sum_{j<=r} log(1 + sigma_{b,j}^2 / eps^2) (Eq. 5), subject to

@@ -106,6 +106,12 @@ struct milo_cache {
   uint16_t* recon_d = nullptr;           // its start, a whole number of fragments from `data`
   int64_t recon_cap = 0;                 // capacity in bf16 elements
   PlanState plan;                        // the plan of the previous call
+  // pre-RoPE keys (milo_cache_set_rope): first-token position per block, and
+  // the rotation table the reconstruction kernel reads
+  std::vector<int32_t> rope_pos;         // empty: keys are attended as stored
+  float* rope_d = nullptr;
+  int32_t rope_hi_rows = 0;
+  int32_t rope_gen = 0;                  // changes with every setting (plan keys)
 };
 
 namespace {
@@ -147,6 +153,7 @@ void destroy(milo_cache* c) {
     (void)hipFree(c->plan_d);
     (void)hipFree(c->tail_len_d);
     (void)hipFree(c->recon_raw);
+    (void)hipFree(c->rope_d);
     (void)hipHostFree(c->plan_pinned);
     if (c->plan_evt) (void)hipEventDestroy(c->plan_evt);
     if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
@@ -419,6 +426,69 @@ int milo_cache_set_path(milo_cache* cache, int32_t path) {
   return MILO_OK;
 }
 
+int milo_cache_set_rope(milo_cache* cache, double theta, const int64_t* block_pos) {
+  g_err.clear();
+  if (!cache) return fail(MILO_ERR_INVALID_ARG, "cache is NULL");
+  milo_cache* c = cache;
+  if (theta == 0.0) {
+    if (!c->rope_pos.empty()) {
+      c->rope_pos.clear();
+      ++c->rope_gen;
+    }
+    return MILO_OK;
+  }
+  if (!std::isfinite(theta) || theta <= 1.0) return fail(MILO_ERR_INVALID_ARG, "theta must be finite and > 1");
+  if (c->p_int8) return fail(MILO_ERR_UNSUPPORTED, "caches with INT8 P factors attend latent only");
+  // positions: the caller's, or the blocks one after another in id order
+  std::vector<int32_t> pos(c->n_blocks);
+  int64_t next = 0, max_end = 0;
+  for (int b = 0; b < c->n_blocks; ++b) {
+    const int64_t p = block_pos ? block_pos[b] : next;
+    const int64_t end = p + c->meta[b].T_pad;  // the padded rows are rotated too (they are zero)
+    if (p < 0 || end > kRopeMaxPos)
+      return fail(MILO_ERR_INVALID_ARG, "block %d at position %lld: its %d rows (padded to %d) must lie in [0, %lld)",
+                  b, (long long)p, c->T[b], c->meta[b].T_pad, (long long)kRopeMaxPos);
+    pos[b] = (int32_t)p;
+    next = p + c->T[b];
+    max_end = std::max(max_end, end);
+  }
+  // the table: angle l w_j (rows l < 256) and 256 h w_j (rows 256 + h), formed
+  // in fp64, w_j = theta^(-2j/d)
+  const int d = c->d, half = d / 2;
+  const int hi_rows = (int)((max_end - 1) / kRopeLowRows) + 1;
+  const int rows = kRopeLowRows + hi_rows;
+  std::vector<float> tab((size_t)rows * d);
+  for (int j = 0; j < half; ++j) {
+    const double w = std::pow(theta, -2.0 * j / d);
+    for (int r = 0; r < rows; ++r) {
+      const double ang = (r < kRopeLowRows ? (double)r : (double)kRopeLowRows * (r - kRopeLowRows)) * w;
+      tab[(size_t)r * d + j] = (float)std::cos(ang);
+      tab[(size_t)r * d + half + j] = (float)std::sin(ang);
+    }
+  }
+  int dev = -1;
+  MILO_HIP(hipGetDevice(&dev));
+  if (dev != c->device) return fail(MILO_ERR_INVALID_ARG, "cache lives on device %d, current device is %d", c->device, dev);
+  float* t_d = nullptr;
+  if (hipMalloc(&t_d, tab.size() * sizeof(float)) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(MILO_ERR_OUT_OF_MEMORY, "rotation table of %lld bytes", (long long)(tab.size() * sizeof(float)));
+  }
+  if (const hipError_t e = hipMemcpy(t_d, tab.data(), tab.size() * sizeof(float), hipMemcpyHostToDevice);
+      e != hipSuccess) {
+    (void)hipFree(t_d);
+    return hip_fail(e, "rotation table upload");
+  }
+  // earlier calls may still read the old table
+  MILO_HIP(hipDeviceSynchronize());
+  (void)hipFree(c->rope_d);
+  c->rope_d = t_d;
+  c->rope_hi_rows = hi_rows;
+  c->rope_pos = std::move(pos);
+  ++c->rope_gen;
+  return MILO_OK;
+}
+
 int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n) {
   g_err.clear();
   if (!cache || !n) return fail(MILO_ERR_INVALID_ARG, "NULL argument");
@@ -623,8 +693,10 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   if (dev != c->device) return fail(MILO_ERR_INVALID_ARG, "cache lives on device %d, current device is %d", c->device, dev);
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
 
-  // ---- which blocks are reconstructed (milo_cache_set_path) ----
-  if (c->path == MILO_PATH_RECONSTRUCT && !ws.can_recon())
+  // ---- which blocks are reconstructed (milo_cache_set_path; every block of a
+  // cache with pre-RoPE keys, milo_cache_set_rope) ----
+  const bool rope = !c->rope_pos.empty();
+  if ((c->path == MILO_PATH_RECONSTRUCT || (rope && n_sel > 0)) && !ws.can_recon())
     return fail(MILO_ERR_UNSUPPORTED, "this entry point attends latent only (reconstruction needs a workspace)");
   std::vector<char> recon((size_t)std::max(n_sel, 1), 0);
   int n_recon = 0;
@@ -635,7 +707,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     if (must && !ws.can_recon())
       return fail(MILO_ERR_UNSUPPORTED, "block %d has rank above %d and needs reconstruction, which this entry point "
                   "does not do", b, kMaxRank);
-    if (must) recon[j] = 1;
+    if (must || rope) recon[j] = 1;
     else if (c->path != MILO_PATH_LATENT && ws.can_recon())
       recon[j] = c->path == MILO_PATH_RECONSTRUCT ||
                  recon_pays(c->T[b], c->rk[b], c->rv[b], (int64_t)n_q * n_q_heads, c->n_kv * c->d, c->d);
@@ -700,6 +772,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
   key.push_back(n_recon);
   key.push_back(gemv ? 1 : 0);
   key.push_back(tail_tiles);
+  key.push_back(rope ? c->rope_gen : -1);
   key.insert(key.end(), block_table, block_table + n_sel);
   const int n_cols = n_q * n_q_heads;
   if (key != ps.key) {
@@ -716,7 +789,8 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     int64_t tail_region = -1;
     if (n_recon > 0 || shared_tail) {
       region.assign(c->n_blocks + 1, -1);
-      build_recon_plan(c->meta.data(), block_table, n_sel, recon.data(), c->n_kv, c->d, &region, &rp);
+      build_recon_plan(c->meta.data(), block_table, n_sel, recon.data(), c->n_kv, c->d, &region, &rp,
+                       rope ? c->rope_pos.data() : nullptr);
     }
     if (shared_tail) {
       meta_x = c->meta;
@@ -908,6 +982,8 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ra.recon = rbuf;
     ra.blocks = reinterpret_cast<const ReconBlock*>(ps.plan_d + ps.recon_blocks_off);
     ra.tasks = reinterpret_cast<const int2*>(ps.plan_d + ps.recon_tasks_off);
+    ra.rope = c->rope_d;
+    ra.rope_hi_rows = c->rope_hi_rows;
     e = launch_recon(ra, c->d, ps.n_recon_tasks, s, ev[4], ev[5]);
     if (e != hipSuccess) return launch_fail(e, "reconstruction kernel launch");
   }

@@ -321,15 +321,28 @@ __host__ __device__ inline int rk_frag_split(int rk0, int nrt, int nk, int g, in
 struct ReconBlock {
   BlockMeta src;    // the block's factors in the cache buffer
   int64_t dst;      // element offset of its region in the reconstruction buffer
-  int32_t pad[2];
+  int32_t pos0;     // pre-RoPE keys: position of the block's first token; -1: keys as stored
+  int32_t pad;
 };
 static_assert(sizeof(ReconBlock) == 64, "reconstruction block layout");
 // task: x = reconstruction block (-1: none), y = tile << 8 | g << 1 | side (0: K, 1: V)
+// Rotary embedding of pre-RoPE keys (Sec. 3: the factorised keys are taken
+// before the rotation, which does not commute with R^K, so such blocks are
+// reconstructed and rotated before attention).  Rotate-half arrangement: dim
+// j < d/2 pairs with j + d/2 and the pair at position p turns by p w_j,
+// w_j = theta^(-2j/d).  The angle is split as p = 256 h + l: table rows
+// [0, 256) hold cos / sin of l w_j, rows 256 + h those of 256 h w_j (each row d
+// floats: d/2 cosines, then d/2 sines; fp32 values of angles formed in fp64),
+// combined by the angle-sum formulas.
+constexpr int kRopeLowRows = 256;
+constexpr int64_t kRopeMaxPos = 1LL << 24;  // positions below this (table of at most 65536 high rows)
 struct ReconArgs {
   const uint16_t* data;       // packed factors
   uint16_t* recon;            // reconstruction buffer
   const ReconBlock* blocks;   // [n_recon]
   const int2* tasks;          // [grid]
+  const float* rope;          // rotation table of pre-RoPE keys (NULL: none)
+  int32_t rope_hi_rows;       // rows after the kRopeLowRows low rows
 };
 // the BlockMeta of head g of a reconstructed block whose region starts at
 // element `region` (offsets relative to the reconstruction buffer)

@@ -429,7 +429,7 @@ bool build_schedule(const PlanInput& c, const int32_t* table, int n_sel, int n_q
 }
 
 void build_recon_plan(const BlockMeta* meta, const int32_t* table, int n_sel, const char* recon, int n_kv, int d,
-                      std::vector<int64_t>* region, ReconPlan* out) {
+                      std::vector<int64_t>* region, ReconPlan* out, const int32_t* rope_pos) {
   out->blocks.clear();
   out->tasks.clear();
   out->elems = 0;
@@ -443,6 +443,7 @@ void build_recon_plan(const BlockMeta* meta, const int32_t* table, int n_sel, co
     ReconBlock rb{};
     rb.src = m;
     rb.dst = out->elems;
+    rb.pos0 = rope_pos ? rope_pos[b] : -1;
     (*region)[b] = out->elems;
     out->elems += 2 * (int64_t)m.T_pad * D;
     const int i = (int)out->blocks.size();

@@ -62,9 +62,10 @@ struct ReconPlan {
   int64_t elems = 0;  // reconstruction buffer size (bf16 elements)
 };
 // Regions of the blocks table[0 .. n_sel) chosen by recon[j] != 0, laid out
-// consecutively; fills region[block id] (others -1) and the tasks.
+// consecutively; fills region[block id] (others -1) and the tasks.  rope_pos
+// (indexed by block id, or NULL): first-token positions of pre-RoPE keys.
 void build_recon_plan(const BlockMeta* meta, const int32_t* table, int n_sel, const char* recon, int n_kv, int d,
-                      std::vector<int64_t>* region, ReconPlan* out);
+                      std::vector<int64_t>* region, ReconPlan* out, const int32_t* rope_pos = nullptr);
 
 // Build the plan for the selected blocks table[0 .. n_sel), n_q requests with
 // n_chunks planned tail chunks each, over the column tiles `til`.  program_cap

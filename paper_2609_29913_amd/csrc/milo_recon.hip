@@ -11,12 +11,17 @@
 // cache stores P^K and R^V rank-contiguous already; P^V (token-contiguous, for
 // the latent value pass) and R^K (dim-contiguous, for the query projection)
 // are transposed on their way into LDS.  The next step's slices are loaded
-// into registers while the current step's MFMAs run (two LDS buffers).  Wave w
-// computes tokens 64 (w % 4) .. +63 times dims (d / 2)(w / 4) .. +d/2; for K
-// it forms K^T = R^T P^T, so a lane's accumulators hold consecutive dims of
-// one token and the tile goes to LDS as [token][dim], for V it forms P R,
-// giving consecutive tokens of one dim and an LDS tile [dim][token]; the
-// packed fragments are then stored with one 16-byte store per lane.
+// into registers while the current step's MFMAs run (two LDS buffers).  Every
+// wave computes a 32-row-block x 32-column-block share of the tile: for V,
+// tokens 64 (w % 4) .. +63 times dims (d / 2)(w / 4) .. +d/2; for K, the dim
+// blocks b0 and b0 + d/64 (dims x and x + d/2, the pairs a rotary embedding
+// turns together) of tokens 64 (w % 4) .. +63 with b0 = w / 4 at d = 128, of
+// tokens 32 w .. +31 with b0 = 0 at d = 64.  For K it forms K^T = R^T P^T, so
+// a lane's accumulators hold consecutive dims of one token and the tile goes
+// to LDS as [token][dim] (pre-RoPE keys are rotated in fp32 on the way), for V
+// it forms P R, giving consecutive tokens of one dim and an LDS tile
+// [dim][token]; the packed fragments are then stored with one 16-byte store
+// per lane.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -48,8 +53,10 @@ constexpr size_t recon_lds_bytes(int D) {
 template <int D, int SIDE>
 __device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock& rb, int g, int t,
                                            unsigned char* smem) {
-  constexpr int NJ = D / 64;  // 32-column blocks of a wave's d / 2 dims
   constexpr int side = SIDE;
+  // the wave's share: TI token blocks x TJ dim blocks of 32 (see above)
+  constexpr int TI = (side == 0 && D == 64) ? 1 : 2;
+  constexpr int TJ = side == 0 ? 2 : D / 64;
   const BlockMeta& bm = rb.src;
   const int nrt = (side ? bm.rv_pad : bm.rk_pad) >> 5;  // 32-rank steps
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -135,12 +142,15 @@ __device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock&
     }
   };
 
-  const int wt = wave & 3, wd = wave >> 2;
-  f32x16r acc[2][NJ];
+  auto tok_block = [&](int i) { return TI == 2 ? 2 * (wave & 3) + i : wave; };
+  auto dim_block = [&](int j) {
+    return side == 0 ? (D == 128 ? (wave >> 2) : 0) + (D / 64) * j : (D / 64) * (wave >> 2) + j;
+  };
+  f32x16r acc[TI][TJ];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16r{};
+    for (int j = 0; j < TJ; ++j) acc[i][j] = f32x16r{};
   load(0);
   stage(0);
   __syncthreads();
@@ -151,43 +161,76 @@ __device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock&
     const __bf16* B = sB + buf * D * kStageStride;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      bf16x8r af[2], bfr[NJ];
+      bf16x8r af[TI], bfr[TJ];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8r*>(A + (32 * (2 * wt + i) + lrow) * kStageStride + 16 * kk + 8 * lhi);
+      for (int i = 0; i < TI; ++i)
+        af[i] = *reinterpret_cast<const bf16x8r*>(A + (32 * tok_block(i) + lrow) * kStageStride + 16 * kk + 8 * lhi);
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8r*>(B + ((D / 2) * wd + 32 * j + lrow) * kStageStride + 16 * kk +
-                                                   8 * lhi);
+      for (int j = 0; j < TJ; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8r*>(B + (32 * dim_block(j) + lrow) * kStageStride + 16 * kk + 8 * lhi);
       if (side == 0) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < TI; ++i)
 #pragma unroll
-          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32r(bfr[j], af[i], acc[i][j]);  // K^T: [dim][token]
+          for (int j = 0; j < TJ; ++j) acc[i][j] = mfma32r(bfr[j], af[i], acc[i][j]);  // K^T: [dim][token]
       } else {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < TI; ++i)
 #pragma unroll
-          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32r(af[i], bfr[j], acc[i][j]);  // V: [token][dim]
+          for (int j = 0; j < TJ; ++j) acc[i][j] = mfma32r(af[i], bfr[j], acc[i][j]);  // V: [token][dim]
       }
     }
     if (kc + 1 < nrt) stage(buf ^ 1);  // the other buffer: its last readers passed the previous barrier
     __syncthreads();
   }
 
+  // pre-RoPE keys: lane (lhi, lrow) holds dims x = 32 b0 + 8 jj + 4 lhi + u and
+  // x + d/2 of token 32 tok_block(i) + lrow of tile t, at position
+  // pos0 + 256 t + that token; the pair turns by the angle p w_x, its cosine and
+  // sine composed from the table's low (p mod 256) and high (p / 256) rows
+  if constexpr (side == 0) {
+    if (rb.pos0 >= 0) {
+      const float* hi_tab = a.rope + kRopeLowRows * D;
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int p = rb.pos0 + kTile * t + 32 * tok_block(i) + lrow;
+        const float* lo = a.rope + (p & (kRopeLowRows - 1)) * D;
+        const float* hi = hi_tab + (int64_t)min(p / kRopeLowRows, a.rope_hi_rows - 1) * D;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int x = 32 * dim_block(0) + 8 * jj + 4 * lhi;  // < d / 2
+          const float4 cl = *reinterpret_cast<const float4*>(lo + x);
+          const float4 sl = *reinterpret_cast<const float4*>(lo + D / 2 + x);
+          const float4 ch = *reinterpret_cast<const float4*>(hi + x);
+          const float4 sh = *reinterpret_cast<const float4*>(hi + D / 2 + x);
+          const float c_l[4] = {cl.x, cl.y, cl.z, cl.w}, s_l[4] = {sl.x, sl.y, sl.z, sl.w};
+          const float c_h[4] = {ch.x, ch.y, ch.z, ch.w}, s_h[4] = {sh.x, sh.y, sh.z, sh.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float c = c_h[u] * c_l[u] - s_h[u] * s_l[u];
+            const float sn = s_h[u] * c_l[u] + c_h[u] * s_l[u];
+            const float k0 = acc[i][0][4 * jj + u], k1 = acc[i][1][4 * jj + u];
+            acc[i][0][4 * jj + u] = k0 * c - k1 * sn;
+            acc[i][1][4 * jj + u] = k1 * c + k0 * sn;
+          }
+        }
+      }
+    }
+  }
+
   // the tile as bf16 in LDS (all staging reads are done: the loop ended on a barrier)
   __bf16* O = reinterpret_cast<__bf16*>(smem);
   constexpr int kOK = D + 8, kOV = kTile + 8;  // row strides: K [token][dim], V [dim][token]
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < NJ; ++j)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
         bf16x4r v;
 #pragma unroll
         for (int u = 0; u < 4; ++u) v[u] = (__bf16)acc[i][j][4 * jj + u];
-        const int tok_blk = 32 * (2 * wt + i), dim_blk = (D / 2) * wd + 32 * j;
+        const int tok_blk = 32 * tok_block(i), dim_blk = 32 * dim_block(j);
         if (side == 0)  // rows: dims 8 jj + 4 lhi + u of the block, column: token lrow
           *reinterpret_cast<bf16x4r*>(O + (tok_blk + lrow) * kOK + dim_blk + 8 * jj + 4 * lhi) = v;
         else  // rows: tokens 8 jj + 4 lhi + u, column: dim lrow

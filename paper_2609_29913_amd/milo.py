@@ -109,6 +109,8 @@ def lib() -> ctypes.CDLL:
         L.milo_cache_set_path.restype = ctypes.c_int
         L.milo_cache_recon_blocks.argtypes = [vp, _c_i32p]
         L.milo_cache_recon_blocks.restype = ctypes.c_int
+        L.milo_cache_set_rope.argtypes = [vp, ctypes.c_double, ctypes.POINTER(ctypes.c_int64)]
+        L.milo_cache_set_rope.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -426,6 +428,19 @@ def milo_cache_read_int8(cache: int, block: int, which: int, shape):
 def milo_cache_set_path(cache: int, path: int) -> None:
     """MILO_PATH_LATENT, MILO_PATH_RECONSTRUCT or MILO_PATH_AUTO (Sec. 4.5 inference path)."""
     _check(lib().milo_cache_set_path(ctypes.c_void_p(cache), int(path)))
+
+
+def milo_cache_set_rope(cache: int, theta: float, block_pos: Sequence[int] | None = None) -> None:
+    """Pre-RoPE keys (Sec. 3): block b's token t sits at block_pos[b] + t (None: the
+    blocks one after another in id order); theta = 0 turns the rotation off."""
+    pos = None
+    if block_pos is not None:
+        arr = np.ascontiguousarray(np.asarray(block_pos, dtype=np.int64))
+        shape = _CACHES.get(cache)
+        if arr.ndim != 1 or (shape is not None and arr.shape[0] != shape[0]):
+            raise ValueError(f"block_pos must hold one position per block (got shape {arr.shape})")
+        pos = arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+    _check(lib().milo_cache_set_rope(ctypes.c_void_p(cache), float(theta), pos))
 
 
 def milo_cache_recon_blocks(cache: int) -> int:
