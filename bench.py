@@ -63,7 +63,9 @@ def counter_summary(workload: str) -> str:
 def workload_name(cfg, args) -> str:
     """The workload as the JSON line and the profile summaries name it."""
     path = getattr(args, "path", "latent")
-    return cfg.name + ("_int8" if getattr(args, "int8", False) else "") + ("" if path == "latent" else f"_{path}")
+    rope = getattr(args, "rope", 0.0) > 0
+    return (cfg.name + ("_int8" if getattr(args, "int8", False) else "") +
+            ("_rope" if rope else "" if path == "latent" else f"_{path}"))
 
 
 PATHS = {"latent": 0, "reconstruct": 1, "auto": 2}  # MILO_PATH_* of milo_cache_set_path
@@ -94,13 +96,15 @@ class Layer:
     """One layer's device state: its cache, queries, tails and output (the host
     copies of the factors are not kept)."""
 
-    def __init__(self, inp: synth.LayerInputs, dev, p_int8: bool = False, path: str = "latent"):
+    def __init__(self, inp: synth.LayerInputs, dev, p_int8: bool = False, path: str = "latent", rope: float = 0.0):
         import torch
         from paper_2609_29913_amd import milo
         self.cache = milo.milo_cache_create(inp.block_tokens, inp.rank_k, inp.rank_v, inp.n_kv_heads,
                                             inp.head_dim, inp.pk, inp.rk, inp.pv, inp.rv, p_int8=p_int8)
         if path != "latent":
             milo.milo_cache_set_path(self.cache, PATHS[path])
+        if rope > 0:
+            milo.milo_cache_set_rope(self.cache, rope)  # blocks one after another from position 0
         self.q = to_device(inp.q, dev)
         self.tk = to_device(inp.tail_k, dev)
         self.tv = to_device(inp.tail_v, dev)
@@ -433,6 +437,9 @@ def main():
     ap.add_argument("--path", choices=sorted(PATHS), default="latent",
                     help="how blocks are attended: latent (rank space), reconstruct (full-rank K/V rebuilt "
                          "per step, Sec. 4.5) or auto (per block, by the library's cost model)")
+    ap.add_argument("--rope", type=float, default=0.0, metavar="THETA",
+                    help="keys stored before the rotary embedding (base THETA, e.g. 1e6): every block is "
+                         "reconstructed and its keys rotated to their positions (milo_cache_set_rope)")
     ap.add_argument("--grow-tails", action="store_true",
                     help="decode loop: every request's tail grows by one token per step (warm-up and timed "
                          "steps), ending at the workload's tail length")
@@ -502,7 +509,7 @@ def main():
         out_bytes += 4 * x.n_q * x.n_q_heads * x.head_dim
         mean_ranks.append(float(x.rank_k.mean()))
         t1 = time.perf_counter()
-        groups[0].append(Layer(x, dev, args.int8, args.path))
+        groups[0].append(Layer(x, dev, args.int8, args.path, args.rope))
         t_make += time.perf_counter() - t1
         if cfg.n_layers > 1:
             print(f"bench: layer {l + 1}/{cfg.n_layers} ready ({time.perf_counter() - t_gen:.0f} s, "
@@ -511,7 +518,8 @@ def main():
             x0 = x
     copies = max(1, int(np.ceil(args.rotate_bytes / per_step)))
     for _ in range(1, copies):
-        groups.append([Layer(synth.gen_layer(cfg, l), dev, args.int8, args.path) for l in range(cfg.n_layers)])
+        groups.append([Layer(synth.gen_layer(cfg, l), dev, args.int8, args.path, args.rope)
+                       for l in range(cfg.n_layers)])
     stream = torch.cuda.current_stream()
     if args.grow_tails:
         for grp in groups:
@@ -661,19 +669,19 @@ def main():
         },
         "cpu_baseline": None,
     }
-    if args.path != "latent":
+    if args.path != "latent" or args.rope > 0:
         # the route's own work: rebuilt blocks do 2 T D (rk + rv) flops of
         # reconstruction and 4 N T d of dense attention instead of the latent
         # 2 N (rk + rv)(T + d); the roofline above prices the latent work
         recon_avg_s = recon_ms / n_calls * 1e-3
         result["route"] = {
-            "path": args.path,
+            "path": "reconstruct, pre-RoPE keys rotated" if args.rope > 0 else args.path,
             "reconstructed_blocks_per_step": recon_blocks,
             "blocks_per_step": x0.n_blocks * cfg.n_layers,
             "recon_kernel_avg_us": recon_avg_s * 1e6,
             "attend_plus_recon_us": (att_avg_s + recon_avg_s) * 1e6,
         }
-        if args.path == "reconstruct":
+        if args.path == "reconstruct" or args.rope > 0:
             rflops = recon_flops_step / cfg.n_layers
             result["route"]["route_flops_per_layer"] = rflops
             result["route"]["route_tflops"] = rflops / (att_avg_s + recon_avg_s) / 1e12
@@ -682,7 +690,7 @@ def main():
         for layer in grp:
             milo.milo_cache_free(layer.cache)
     result["env"] = device_env(dev)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.rope == 0:  # the oracle baseline times the unrotated latent order
         result["cpu_baseline"] = cpu_baseline(x0, cfg.n_layers, args.cpu_budget)
     print(json.dumps(result), flush=True)
 

@@ -223,20 +223,19 @@ int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n);
  *        (u, v) -> (u cos a - v sin a,  v cos a + u sin a),  a = p theta^(-2j/d)
  * for each pair u = k[j], v = k[j + d/2], j < d/2 (the rotate-half arrangement
  * of the Qwen2 models the paper evaluates).  The rotation is applied to the
- * fp32 reconstruction, before its bf16 rounding; its cosines and sines come
- * from a table of fp32 values of angles formed in fp64, composed as
- * p = 256 h + l with the angle-sum formulas (error ~1e-7 per element).  The
- * queries and the dense tail's keys are taken as already rotated (at the
+ * fp32 reconstruction, before its bf16 rounding: the angle is formed in turns,
+ * p theta^(-2j/d) / (2 pi), in fp64, reduced to [0, 1) and its sine and
+ * cosine taken in fp32 (angle error below ~1e-6 rad at any int32 position).
+ * The queries and the dense tail's keys are taken as already rotated (at the
  * query's own position), as a serving stack stores them.
  *   theta      rotary base (Qwen2.5: 1e6), finite and > 1; 0 turns the
  *              rotation off again (keys attended as stored).
  *   block_pos  host [n_blocks] first-token positions, 0 <= block_pos[b] and
- *              block_pos[b] + T_b rounded up to 256 <= 2^24; NULL places the
- *              blocks one after another in id order from position 0.  Blocks
- *              may overlap or leave gaps (a retriever's reordering).
- * Builds the table (16 KiB per 256 positions at d = 128) on the device and
- * waits for the device before freeing the previous one; later calls rebuild
- * their plan.  INT8 caches (attended latent only) return UNSUPPORTED, and so
+ *              block_pos[b] + T_b rounded up to 256 <= 2^31 - 1; NULL places
+ *              the blocks one after another in id order from position 0.
+ *              Blocks may overlap or leave gaps (a retriever's reordering).
+ * Uploads d/2 frequencies (fp64) and waits for the device before freeing the
+ * previous ones; later calls rebuild their plan.  INT8 caches (attended latent only) return UNSUPPORTED, and so
  * does milo_attend_decode_noalloc on such a cache when a block is selected.
  * Errors: INVALID_ARG (NULL cache, theta, positions), UNSUPPORTED,
  * OUT_OF_MEMORY, HIP_ERROR. */

@@ -109,8 +109,7 @@ struct milo_cache {
   // pre-RoPE keys (milo_cache_set_rope): first-token position per block, and
   // the rotation table the reconstruction kernel reads
   std::vector<int32_t> rope_pos;         // empty: keys are attended as stored
-  float* rope_d = nullptr;
-  int32_t rope_hi_rows = 0;
+  double* rope_d = nullptr;              // [d/2] w_j / (2 pi)
   int32_t rope_gen = 0;                  // changes with every setting (plan keys)
 };
 
@@ -441,49 +440,37 @@ int milo_cache_set_rope(milo_cache* cache, double theta, const int64_t* block_po
   if (c->p_int8) return fail(MILO_ERR_UNSUPPORTED, "caches with INT8 P factors attend latent only");
   // positions: the caller's, or the blocks one after another in id order
   std::vector<int32_t> pos(c->n_blocks);
-  int64_t next = 0, max_end = 0;
+  int64_t next = 0;
   for (int b = 0; b < c->n_blocks; ++b) {
     const int64_t p = block_pos ? block_pos[b] : next;
-    const int64_t end = p + c->meta[b].T_pad;  // the padded rows are rotated too (they are zero)
-    if (p < 0 || end > kRopeMaxPos)
+    // the padded rows are rotated too (they are zero)
+    if (p < 0 || p + c->meta[b].T_pad > kRopeMaxEnd)
       return fail(MILO_ERR_INVALID_ARG, "block %d at position %lld: its %d rows (padded to %d) must lie in [0, %lld)",
-                  b, (long long)p, c->T[b], c->meta[b].T_pad, (long long)kRopeMaxPos);
+                  b, (long long)p, c->T[b], c->meta[b].T_pad, (long long)kRopeMaxEnd);
     pos[b] = (int32_t)p;
     next = p + c->T[b];
-    max_end = std::max(max_end, end);
   }
-  // the table: angle l w_j (rows l < 256) and 256 h w_j (rows 256 + h), formed
-  // in fp64, w_j = theta^(-2j/d)
-  const int d = c->d, half = d / 2;
-  const int hi_rows = (int)((max_end - 1) / kRopeLowRows) + 1;
-  const int rows = kRopeLowRows + hi_rows;
-  std::vector<float> tab((size_t)rows * d);
-  for (int j = 0; j < half; ++j) {
-    const double w = std::pow(theta, -2.0 * j / d);
-    for (int r = 0; r < rows; ++r) {
-      const double ang = (r < kRopeLowRows ? (double)r : (double)kRopeLowRows * (r - kRopeLowRows)) * w;
-      tab[(size_t)r * d + j] = (float)std::cos(ang);
-      tab[(size_t)r * d + half + j] = (float)std::sin(ang);
-    }
-  }
+  // the frequencies in turns per position, w_j / (2 pi), w_j = theta^(-2j/d)
+  const int half = c->d / 2;
+  std::vector<double> turns(half);
+  for (int j = 0; j < half; ++j) turns[j] = std::pow(theta, -2.0 * j / c->d) / (2.0 * M_PI);
   int dev = -1;
   MILO_HIP(hipGetDevice(&dev));
   if (dev != c->device) return fail(MILO_ERR_INVALID_ARG, "cache lives on device %d, current device is %d", c->device, dev);
-  float* t_d = nullptr;
-  if (hipMalloc(&t_d, tab.size() * sizeof(float)) != hipSuccess) {
+  double* t_d = nullptr;
+  if (hipMalloc(&t_d, turns.size() * sizeof(double)) != hipSuccess) {
     (void)hipGetLastError();
-    return fail(MILO_ERR_OUT_OF_MEMORY, "rotation table of %lld bytes", (long long)(tab.size() * sizeof(float)));
+    return fail(MILO_ERR_OUT_OF_MEMORY, "rotation frequencies");
   }
-  if (const hipError_t e = hipMemcpy(t_d, tab.data(), tab.size() * sizeof(float), hipMemcpyHostToDevice);
+  if (const hipError_t e = hipMemcpy(t_d, turns.data(), turns.size() * sizeof(double), hipMemcpyHostToDevice);
       e != hipSuccess) {
     (void)hipFree(t_d);
-    return hip_fail(e, "rotation table upload");
+    return hip_fail(e, "rotation frequency upload");
   }
-  // earlier calls may still read the old table
+  // earlier calls may still read the old frequencies
   MILO_HIP(hipDeviceSynchronize());
   (void)hipFree(c->rope_d);
   c->rope_d = t_d;
-  c->rope_hi_rows = hi_rows;
   c->rope_pos = std::move(pos);
   ++c->rope_gen;
   return MILO_OK;
@@ -982,8 +969,7 @@ int attend_call(milo_cache* c, PlanState& ps, Workspace& ws, const int32_t* bloc
     ra.recon = rbuf;
     ra.blocks = reinterpret_cast<const ReconBlock*>(ps.plan_d + ps.recon_blocks_off);
     ra.tasks = reinterpret_cast<const int2*>(ps.plan_d + ps.recon_tasks_off);
-    ra.rope = c->rope_d;
-    ra.rope_hi_rows = c->rope_hi_rows;
+    ra.rope_turns = c->rope_d;
     e = launch_recon(ra, c->d, ps.n_recon_tasks, s, ev[4], ev[5]);
     if (e != hipSuccess) return launch_fail(e, "reconstruction kernel launch");
   }

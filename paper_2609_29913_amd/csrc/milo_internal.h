@@ -330,19 +330,16 @@ static_assert(sizeof(ReconBlock) == 64, "reconstruction block layout");
 // before the rotation, which does not commute with R^K, so such blocks are
 // reconstructed and rotated before attention).  Rotate-half arrangement: dim
 // j < d/2 pairs with j + d/2 and the pair at position p turns by p w_j,
-// w_j = theta^(-2j/d).  The angle is split as p = 256 h + l: table rows
-// [0, 256) hold cos / sin of l w_j, rows 256 + h those of 256 h w_j (each row d
-// floats: d/2 cosines, then d/2 sines; fp32 values of angles formed in fp64),
-// combined by the angle-sum formulas.
-constexpr int kRopeLowRows = 256;
-constexpr int64_t kRopeMaxPos = 1LL << 24;  // positions below this (table of at most 65536 high rows)
+// w_j = theta^(-2j/d).  The kernel forms the angle in turns, p w_j / (2 pi),
+// in fp64 from the table of w_j / (2 pi), keeps its fractional part and takes
+// sine and cosine in fp32 (sincospi); positions are int32.
+constexpr int64_t kRopeMaxEnd = 2147483647;  // every padded row's position below this
 struct ReconArgs {
   const uint16_t* data;       // packed factors
   uint16_t* recon;            // reconstruction buffer
   const ReconBlock* blocks;   // [n_recon]
   const int2* tasks;          // [grid]
-  const float* rope;          // rotation table of pre-RoPE keys (NULL: none)
-  int32_t rope_hi_rows;       // rows after the kRopeLowRows low rows
+  const double* rope_turns;   // [d/2] w_j / (2 pi) of pre-RoPE keys (NULL: none)
 };
 // the BlockMeta of head g of a reconstructed block whose region starts at
 // element `region` (offsets relative to the reconstruction buffer)

@@ -186,29 +186,26 @@ __device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock&
 
   // pre-RoPE keys: lane (lhi, lrow) holds dims x = 32 b0 + 8 jj + 4 lhi + u and
   // x + d/2 of token 32 tok_block(i) + lrow of tile t, at position
-  // pos0 + 256 t + that token; the pair turns by the angle p w_x, its cosine and
-  // sine composed from the table's low (p mod 256) and high (p / 256) rows
+  // p = pos0 + 256 t + that token; the pair turns by the angle p w_x, formed in
+  // turns in fp64 (exact to ~1e-9 turns for int32 positions), reduced to [0, 1)
+  // and evaluated by sincospi in fp32
   if constexpr (side == 0) {
     if (rb.pos0 >= 0) {
-      const float* hi_tab = a.rope + kRopeLowRows * D;
 #pragma unroll
-      for (int i = 0; i < TI; ++i) {
-        const int p = rb.pos0 + kTile * t + 32 * tok_block(i) + lrow;
-        const float* lo = a.rope + (p & (kRopeLowRows - 1)) * D;
-        const float* hi = hi_tab + (int64_t)min(p / kRopeLowRows, a.rope_hi_rows - 1) * D;
+      for (int jj = 0; jj < 4; ++jj) {
+        const int x = 32 * dim_block(0) + 8 * jj + 4 * lhi;  // < d / 2
+        const double2 w01 = *reinterpret_cast<const double2*>(a.rope_turns + x);
+        const double2 w23 = *reinterpret_cast<const double2*>(a.rope_turns + x + 2);
+        const double w[4] = {w01.x, w01.y, w23.x, w23.y};
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          const int x = 32 * dim_block(0) + 8 * jj + 4 * lhi;  // < d / 2
-          const float4 cl = *reinterpret_cast<const float4*>(lo + x);
-          const float4 sl = *reinterpret_cast<const float4*>(lo + D / 2 + x);
-          const float4 ch = *reinterpret_cast<const float4*>(hi + x);
-          const float4 sh = *reinterpret_cast<const float4*>(hi + D / 2 + x);
-          const float c_l[4] = {cl.x, cl.y, cl.z, cl.w}, s_l[4] = {sl.x, sl.y, sl.z, sl.w};
-          const float c_h[4] = {ch.x, ch.y, ch.z, ch.w}, s_h[4] = {sh.x, sh.y, sh.z, sh.w};
+        for (int i = 0; i < TI; ++i) {
+          const double p = (double)(rb.pos0 + kTile * t + 32 * tok_block(i) + lrow);
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float c = c_h[u] * c_l[u] - s_h[u] * s_l[u];
-            const float sn = s_h[u] * c_l[u] + c_h[u] * s_l[u];
+            const double turns = p * w[u];
+            const float r = (float)(turns - floor(turns));
+            float sn, c;
+            sincospif(2.f * r, &sn, &c);
             const float k0 = acc[i][0][4 * jj + u], k1 = acc[i][1][4 * jj + u];
             acc[i][0][4 * jj + u] = k0 * c - k1 * sn;
             acc[i][1][4 * jj + u] = k1 * c + k0 * sn;

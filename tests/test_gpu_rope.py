@@ -6,7 +6,7 @@ rebuilt and its keys rotated to their positions before attention.
 
 Covered: head dims 64 and 128 (the two key-tile arrangements of the
 reconstruction kernel), ragged blocks, positions given per block (overlapping,
-out of order, up to the 2^24 limit, so the table's high rows are exercised) or
+out of order, up to the int32 limit, where the fp64 angle reduction matters) or
 by default one after another, block subsets, positions changed on one cache,
 rotation switched off again, prefill, a 7B-shaped layer, and the refusals
 (INT8 caches, the no-allocation entry point, bad arguments).  Each case also
@@ -25,6 +25,7 @@ from test_gpu_parity import SHAPES
 pytestmark = pytest.mark.gpu
 
 THETA = 1e6
+LIMIT = (1 << 31) - 1  # padded rows' positions stay below this
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -50,9 +51,9 @@ def _check(got, inp, key_pos, table=None, tail_len=None, label=""):
 
 
 def _positions(inp, seed):
-    """Random first-token positions with each block's padded rows below 2^24."""
+    """Random first-token positions with each block's padded rows below 2^31 - 1."""
     rng = np.random.default_rng(seed)
-    return [int(rng.integers(0, (1 << 24) - 256 * -(-int(t) // 256) + 1)) for t in inp.block_tokens]
+    return [int(rng.integers(0, LIMIT - 256 * -(-int(t) // 256) + 1)) for t in inp.block_tokens]
 
 
 @pytest.mark.parametrize("name", ["ragged_d128_g4", "d64_g7_two_col_tiles", "g16", "q7b_shape_5_blocks"])
@@ -88,7 +89,7 @@ def test_rope_default_positions_subsets_and_changes():
         table = [3, 1]
         _check(gl.attend(table=table).cpu().numpy(), inp, default_pos, table=table, label="subset [3, 1]")
         assert milo.milo_cache_recon_blocks(gl.cache) == 2
-        new_pos = [5_000_000, 0, 77, 1_000_003]
+        new_pos = [2_000_000_000, 0, 77, 1_000_003]
         milo.milo_cache_set_rope(gl.cache, THETA, new_pos)
         _check(gl.attend(table=table).cpu().numpy(), inp, new_pos, table=table, label="new positions")
         milo.milo_cache_set_rope(gl.cache, 0.0)
@@ -152,17 +153,17 @@ def test_rope_refusals():
         for theta in (1.0, -5.0, float("inf"), float("nan")):
             with pytest.raises(milo.MiloError, match="theta"):
                 milo.milo_cache_set_rope(gl.cache, theta)
-        for pos in ([-1, 0], [0, (1 << 24) - 255], [(1 << 24) - 255, 0]):
+        for pos in ([-1, 0], [0, LIMIT - 255], [LIMIT - 255, 0]):
             with pytest.raises(milo.MiloError, match="must lie in"):
                 milo.milo_cache_set_rope(gl.cache, THETA, pos)
         with pytest.raises(ValueError):
             milo.milo_cache_set_rope(gl.cache, THETA, [0])
         # the last valid position of a 100-token block padded to 256 rows
-        milo.milo_cache_set_rope(gl.cache, THETA, [0, (1 << 24) - 256])
+        milo.milo_cache_set_rope(gl.cache, THETA, [0, LIMIT - 256])
         out = torch.zeros(inp.q.shape, dtype=torch.float32, device="cuda")
         with pytest.raises(milo.MiloError, match="latent only"):
             milo.milo_attend_decode_noalloc(gl.cache, [0, 1], gl.q, gl.tk, gl.tv, inp.tail_len, inp.scale, out)
-        _check(gl.attend().cpu().numpy(), inp, [0, (1 << 24) - 256], label="positions at the limit")
+        _check(gl.attend().cpu().numpy(), inp, [0, LIMIT - 256], label="positions at the limit")
     finally:
         gl.free()
     g8 = GpuLayer(inp, p_int8=True)
