@@ -674,6 +674,10 @@ def main():
         # reconstruction and 4 N T d of dense attention instead of the latent
         # 2 N (rk + rv)(T + d); the roofline above prices the latent work
         recon_avg_s = recon_ms / n_calls * 1e-3
+        result["roofline"]["note"] = ("latent accounting: the latent route's bytes and flops over the attention "
+                                      "kernel alone; with reconstructed blocks that is not the work done (the "
+                                      "route object gives the reconstruction time and, for every block rebuilt, "
+                                      "the route's own flops)")
         result["route"] = {
             "path": "reconstruct, pre-RoPE keys rotated" if args.rope > 0 else args.path,
             "reconstructed_blocks_per_step": recon_blocks,
