@@ -225,7 +225,8 @@ int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n);
  * of the Qwen2 models the paper evaluates).  The rotation is applied to the
  * fp32 reconstruction, before its bf16 rounding: the angle is formed in turns,
  * p theta^(-2j/d) / (2 pi), in fp64, reduced to [0, 1) and its sine and
- * cosine taken in fp32 (angle error below ~1e-6 rad at any int32 position).
+ * cosine taken in fp32 by the hardware's turn-based instructions (error below
+ * ~1e-6 at any int32 position).
  * The queries and the dense tail's keys are taken as already rotated (at the
  * query's own position), as a serving stack stores them.
  *   theta      rotary base (Qwen2.5: 1e6), finite and > 1; 0 turns the

@@ -332,7 +332,7 @@ static_assert(sizeof(ReconBlock) == 64, "reconstruction block layout");
 // j < d/2 pairs with j + d/2 and the pair at position p turns by p w_j,
 // w_j = theta^(-2j/d).  The kernel forms the angle in turns, p w_j / (2 pi),
 // in fp64 from the table of w_j / (2 pi), keeps its fractional part and takes
-// sine and cosine in fp32 (sincospi); positions are int32.
+// sine and cosine in fp32; positions are int32.
 constexpr int64_t kRopeMaxEnd = 2147483647;  // every padded row's position below this
 struct ReconArgs {
   const uint16_t* data;       // packed factors

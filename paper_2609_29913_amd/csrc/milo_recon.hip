@@ -188,7 +188,8 @@ __device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock&
   // x + d/2 of token 32 tok_block(i) + lrow of tile t, at position
   // p = pos0 + 256 t + that token; the pair turns by the angle p w_x, formed in
   // turns in fp64 (exact to ~1e-9 turns for int32 positions), reduced to [0, 1)
-  // and evaluated by sincospi in fp32
+  // and evaluated by the hardware's sine and cosine of an angle in turns (fp32;
+  // error below 1.3e-7 over [0, 1), measured on gfx950)
   if constexpr (side == 0) {
     if (rb.pos0 >= 0) {
 #pragma unroll
@@ -204,8 +205,7 @@ __device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock&
           for (int u = 0; u < 4; ++u) {
             const double turns = p * w[u];
             const float r = (float)(turns - floor(turns));
-            float sn, c;
-            sincospif(2.f * r, &sn, &c);
+            const float sn = __builtin_amdgcn_sinf(r), c = __builtin_amdgcn_cosf(r);
             const float k0 = acc[i][0][4 * jj + u], k1 = acc[i][1][4 * jj + u];
             acc[i][0][4 * jj + u] = k0 * c - k1 * sn;
             acc[i][1][4 * jj + u] = k1 * c + k0 * sn;
