@@ -98,6 +98,9 @@ def test_attend_null_cache_and_free_null():
     v = ctypes.c_int64()
     assert milo.lib().milo_cache_device_bytes(None, ctypes.byref(v)) == milo.MILO_ERR_INVALID_ARG
     assert milo.lib().milo_cache_read_factor(None, 0, 0, None) == milo.MILO_ERR_INVALID_ARG
+    assert milo.lib().milo_cache_set_path(None, 0) == milo.MILO_ERR_INVALID_ARG
+    assert milo.lib().milo_cache_set_rope(None, 1e6, None) == milo.MILO_ERR_INVALID_ARG
+    assert "cache is NULL" in milo.milo_last_error()
 
 
 def test_timing_read_without_calls():
