@@ -92,6 +92,11 @@ def test_rope_default_positions_subsets_and_changes():
         new_pos = [2_000_000_000, 0, 77, 1_000_003]
         milo.milo_cache_set_rope(gl.cache, THETA, new_pos)
         _check(gl.attend(table=table).cpu().numpy(), inp, new_pos, table=table, label="new positions")
+        # AUTO would keep these low-rank blocks latent; pre-RoPE keys are rebuilt all the same
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_AUTO)
+        _check(gl.attend().cpu().numpy(), inp, new_pos, label="new positions, AUTO path")
+        assert milo.milo_cache_recon_blocks(gl.cache) == inp.n_blocks
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_LATENT)
         milo.milo_cache_set_rope(gl.cache, 0.0)
         again = gl.attend().cpu().numpy()
         assert milo.milo_cache_recon_blocks(gl.cache) == 0
