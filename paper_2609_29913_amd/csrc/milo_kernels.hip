@@ -687,14 +687,18 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 
   // ---- projection: Qt[rank][col] (stored [col][rank]), once per KV head of
   // the tile; each column stores its own head's result.  Dense items: Qt is
-  // the scaled query itself ----
+  // the query itself times the sign of the scale, exact in bf16, and the
+  // scale's magnitude goes onto the fp32 scores (sscale below).  A scaled
+  // query rounded to bf16 would put a relative error of 2^-9 on every score,
+  // which a peaked softmax turns into an output error near 1e-2 ----
   if (dense) {
+    const float sgn = a.qscale > 0.f ? 1.f : a.qscale < 0.f ? -1.f : 0.f;
     for (int x = tid; x < kCols * kRowChunks; x += kThreads) {
       const int cl = x / kRowChunks, j = x % kRowChunks;
       const bf16x8 v = ld_bf16x8(qimg + cl * D + 8 * (j ^ (cl % kRowChunks)));
       bf16x8 o;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (__bf16)((float)v[e] * a.qscale);
+      for (int e = 0; e < 8; ++e) o[e] = (__bf16)((float)v[e] * sgn);
       *reinterpret_cast<bf16x8*>(qt + cl * qsd + 8 * j) = o;
     }
   } else if (GV && own_k > 0) {
@@ -777,6 +781,10 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   for (int r = 0; r < MAX_RT; ++r) oacc[r][0] = oacc[r][1] = f32x16{};
   float m_run[2] = {-INFINITY, -INFINITY};
   float l_run[2] = {0.f, 0.f};
+  // factor (> 0) from the MFMA's raw scores to scores in log2 units: the
+  // magnitude of the scale for dense items, 1 otherwise (the projection
+  // carries it); applied in the column maximum and the weights' exponent
+  const float sscale = dense && a.qscale != 0.f ? fabsf(a.qscale) : 1.f;
   const __bf16* qr0 = qt + lrow * qsd + 8 * lhi;
   const __bf16* qr1 = qt + (32 + lrow) * qsd + 8 * lhi;
   // weight operand rows of the wave's segment (relative step st at 16 st)
@@ -845,7 +853,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       for (int v = 0; v < 16; ++v) mx[ch] = fmaxf(mx[ch], sc[ch][v]);
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
-      mx[ch] = fmaxf(mx[ch], __shfl_xor(mx[ch], 32));
+      mx[ch] = fmaxf(mx[ch], __shfl_xor(mx[ch], 32)) * sscale;
       red[wave * kCols + 32 * ch + lrow] = mx[ch];  // both lane halves hold the same value
     }
     lds_barrier();
@@ -871,7 +879,7 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const float w = fast_exp2(sc[ch][4 * j + u] - mref);
+          const float w = fast_exp2(fmaf(sc[ch][4 * j + u], sscale, -mref));
           lsum += w;
           if constexpr (I8) wv[ch][j][u] = (__bf16)(w * vsc[4 * j + u]);
           else wv[ch][j][u] = (__bf16)w;

@@ -258,3 +258,31 @@ def test_full_rank_identity_factors_give_dense_attention():
     got, n_rec = _run(inp, milo.MILO_PATH_AUTO, label="P = K, R = I at rank 1024")
     assert n_rec == 2
     assert max_rel_l2(got, oracle.attend_dense(**oracle_args(inp))) <= TOL_REL_L2
+
+
+@pytest.mark.parametrize("scale", [-0.09, 0.0])
+def test_nonpositive_scales_on_both_routes(scale):
+    """A negative or zero softmax temperature (any finite scale is accepted):
+    dense items score with the query times the sign of the scale and put its
+    magnitude on the fp32 scores, so both routes must still match the oracle;
+    at scale 0 the weights are uniform."""
+    import torch
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(61, [700, 300], [96, 64], n_kv_heads=2, head_dim=128, n_q=3, n_q_heads=14,
+                             tail_cap=40, tail_len=[40, 0, 17])
+    a = oracle_args(inp)
+    a["scale"] = scale
+    ref = oracle.attend_latent(**a)
+    gl = GpuLayer(inp)
+    try:
+        for path in (milo.MILO_PATH_LATENT, milo.MILO_PATH_RECONSTRUCT):
+            milo.milo_cache_set_path(gl.cache, path)
+            out = torch.full(inp.q.shape, float("nan"), dtype=torch.float32, device="cuda")
+            milo.milo_attend_decode(gl.cache, list(range(inp.n_blocks)), gl.q, gl.tk, gl.tv, inp.tail_len, scale,
+                                    out)
+            torch.cuda.synchronize()
+            err = max_rel_l2(out.cpu().numpy(), ref)
+            print(f"[recon] scale {scale}, path {path}: max rel-L2 = {err:.3e}", flush=True)
+            assert err <= TOL_REL_L2
+    finally:
+        gl.free()
