@@ -186,8 +186,9 @@ int milo_attend_prefill(milo_cache* cache, const int32_t* block_table, int32_t n
  *                          the result is lifted through R^V.
  *   MILO_PATH_RECONSTRUCT  every selected block is first rebuilt at full rank,
  *                          K_b = P^K_b R^K_b and V_b = P^V_b R^V_b (Alg. 1
- *                          full-rank reconstruction; bf16 with fp32
- *                          accumulation), into a per-call buffer of the cache
+ *                          full-rank reconstruction; fp32 accumulation, keys
+ *                          stored as fp16 (saturated at +-65504), values as
+ *                          bf16), into a per-call buffer of the cache
  *                          (4 T_pad H_kv d bytes per selected block, kept and
  *                          grown like the rest of the workspace), and then
  *                          attended as uncompressed keys and values.

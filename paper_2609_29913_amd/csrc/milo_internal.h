@@ -307,12 +307,14 @@ __host__ __device__ inline int rk_frag_split(int rk0, int nrt, int nk, int g, in
 // ---------------------------------------------------------------------------
 // Reconstruct-then-attend (Sec. 4.5 inference path, Alg. 1 full-rank
 // reconstruction): a selected block may instead be rebuilt as its full-rank keys
-// and values, K_b = P^K R^K and V_b = P^V R^V (bf16, fp32 accumulation), into a
+// and values, K_b = P^K R^K and V_b = P^V R^V (fp32 accumulation; keys stored as
+// fp16, values as bf16), into a
 // per-call buffer, and then attended like an uncompressed block.  For KV head g
 // the buffer holds K_{b,g} (T_pad x d) in the P^K fragment layout and V_{b,g}
 // in the P^V fragment layout, both with "rank" d, so the attention kernel reads
 // them with its latent loops unchanged: the scores of a column are K_{b,g} q
-// (the query itself, scaled, takes the place of the projected query) and the
+// (the query itself, as fp16, takes the place of the projected query; fp16
+// score MFMAs, the scale on the fp32 scores) and the
 // value pass yields the output directly (no up-projection).  Such "dense"
 // block items need one KV head per column tile.
 //   region of reconstructed block i: 2 T_pad D elements; head g at 2 g T_pad d,

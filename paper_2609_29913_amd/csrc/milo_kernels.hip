@@ -52,6 +52,13 @@ __device__ __forceinline__ bf16x8 i8_to_bf16x8(uint2 raw) {
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+// the same product on operands that hold fp16 bit patterns (rebuilt keys and
+// the query of dense items)
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ f32x16 mfma32_f16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                0, 0);
+}
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
@@ -687,19 +694,21 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
 
   // ---- projection: Qt[rank][col] (stored [col][rank]), once per KV head of
   // the tile; each column stores its own head's result.  Dense items: Qt is
-  // the query itself times the sign of the scale, exact in bf16, and the
-  // scale's magnitude goes onto the fp32 scores (sscale below).  A scaled
-  // query rounded to bf16 would put a relative error of 2^-9 on every score,
-  // which a peaked softmax turns into an output error near 1e-2 ----
+  // the query itself times the sign of the scale, as fp16 (exact for the
+  // bf16 query in fp16's normal range; saturated at +-65504) to meet the
+  // rebuilt keys, which are fp16 too, in the fp16 score MFMA; the scale's
+  // magnitude goes onto the fp32 scores (sscale below).  A scaled query
+  // rounded to 16 bits would put a relative rounding error on every score,
+  // which a peaked softmax magnifies ----
   if (dense) {
     const float sgn = a.qscale > 0.f ? 1.f : a.qscale < 0.f ? -1.f : 0.f;
     for (int x = tid; x < kCols * kRowChunks; x += kThreads) {
       const int cl = x / kRowChunks, j = x % kRowChunks;
       const bf16x8 v = ld_bf16x8(qimg + cl * D + 8 * (j ^ (cl % kRowChunks)));
-      bf16x8 o;
+      f16x8 o;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (__bf16)((float)v[e] * sgn);
-      *reinterpret_cast<bf16x8*>(qt + cl * qsd + 8 * j) = o;
+      for (int e = 0; e < 8; ++e) o[e] = (_Float16)fminf(fmaxf((float)v[e] * sgn, -65504.f), 65504.f);
+      *reinterpret_cast<f16x8*>(qt + cl * qsd + 8 * j) = o;
     }
   } else if (GV && own_k > 0) {
     // small batches (a tile of at most kGemvCols columns): the projection as a
@@ -794,25 +803,32 @@ __device__ __forceinline__ void block_item(const AttendArgs& a, const WorkItem& 
   for (int tt = 0; tt < ntiles; ++tt) {
     const int tw = (tile0 + tt) * kTile + wave * kTokWave;
     f32x16 s0 = {}, s1 = {};
-    {
-      // operands of rank step k: ak (P^K sub-tile), b0/b1 (Qt column tiles);
-      // nks is even (ranks are padded to 32), so the loop runs over step pairs
+    // operands of rank step k: ak (P^K sub-tile, or rebuilt keys), b0/b1 (Qt
+    // column tiles); nks is even (ranks are padded to 32), so the loop runs over
+    // step pairs; dense items multiply fp16 operands
+    auto scores = [&](auto mma) {
       bf16x8 ak = take_p();
       bf16x8 b0 = ld_bf16x8(qr0), b1 = ld_bf16x8(qr1);
       for (int k = 0; k < nks; k += 2) {
         const bf16x8 ck = take_p();
         const bf16x8 d0 = ld_bf16x8(qr0 + 16 * (k + 1));
         const bf16x8 d1 = ld_bf16x8(qr1 + 16 * (k + 1));
-        s0 = mfma32(ak, b0, s0);
-        s1 = mfma32(ak, b1, s1);
+        s0 = mma(ak, b0, s0);
+        s1 = mma(ak, b1, s1);
         if (k + 2 < nks) {
           ak = take_p();
           b0 = ld_bf16x8(qr0 + 16 * (k + 2));
           b1 = ld_bf16x8(qr1 + 16 * (k + 2));
         }
-        s0 = mfma32(ck, d0, s0);
-        s1 = mfma32(ck, d1, s1);
+        s0 = mma(ck, d0, s0);
+        s1 = mma(ck, d1, s1);
       }
+    };
+    if constexpr (I8) {
+      scores(mfma32);
+    } else {
+      if (dense) scores(mfma32_f16);
+      else scores(mfma32);
     }
     f32x16 sc[2] = {s0, s1};
     // INT8 P factors: the scores of int8 codes times each token's K scale; the

@@ -1,7 +1,8 @@
 // Full-rank reconstruction of selected blocks (Sec. 4.5 inference path, Alg. 1
 // full-rank reconstruction): K_b = P^K_b R^K_b and V_b = P^V_b R^V_b, one KV
-// head's d columns and one 256-token tile per workgroup, written as bf16 into
-// the reconstruction buffer in the fragment layouts the attention kernel reads
+// head's d columns and one 256-token tile per workgroup, written (keys as fp16,
+// values as bf16) into the reconstruction buffer in the fragment layouts the
+// attention kernel reads
 // (P^K layout for K_{b,g}, P^V layout for V_{b,g}, both with rank d).
 //
 // A workgroup (8 waves) accumulates its 256 x d output tile over the block's
@@ -33,6 +34,7 @@ namespace {
 typedef __bf16 bf16x8r __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4r __attribute__((ext_vector_type(4)));
 typedef float f32x16r __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x4r __attribute__((ext_vector_type(4)));
 
 constexpr int kReconThreads = 512;
 constexpr int kStageStride = 40;  // bf16 row stride of a staged 32-rank slice (+8: conflict-free reads)
@@ -224,14 +226,21 @@ __device__ __forceinline__ void recon_task(const ReconArgs& a, const ReconBlock&
     for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        bf16x4r v;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = (__bf16)acc[i][j][4 * jj + u];
         const int tok_blk = 32 * tok_block(i), dim_blk = 32 * dim_block(j);
-        if (side == 0)  // rows: dims 8 jj + 4 lhi + u of the block, column: token lrow
-          *reinterpret_cast<bf16x4r*>(O + (tok_blk + lrow) * kOK + dim_blk + 8 * jj + 4 * lhi) = v;
-        else  // rows: tokens 8 jj + 4 lhi + u, column: dim lrow
+        if (side == 0) {
+          // keys as fp16 (saturated at +-65504): 8x finer than bf16 where the
+          // score of a peaked softmax needs it; rows: dims 8 jj + 4 lhi + u of
+          // the block, column: token lrow
+          f16x4r v;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] = (_Float16)fminf(fmaxf(acc[i][j][4 * jj + u], -65504.f), 65504.f);
+          *reinterpret_cast<f16x4r*>(O + (tok_blk + lrow) * kOK + dim_blk + 8 * jj + 4 * lhi) = v;
+        } else {  // values as bf16; rows: tokens 8 jj + 4 lhi + u, column: dim lrow
+          bf16x4r v;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] = (__bf16)acc[i][j][4 * jj + u];
           *reinterpret_cast<bf16x4r*>(O + (dim_blk + lrow) * kOV + tok_blk + 8 * jj + 4 * lhi) = v;
+        }
       }
   __syncthreads();
 
@@ -295,8 +304,16 @@ __global__ __launch_bounds__(256) void pack_tail_kernel(TailPackArgs a) {
     const int tiles = a.T_pad / kTile;
     const int kap = (int)(fr % nks), t = (int)((fr / nks) % tiles), w = (int)(fr / ((int64_t)nks * tiles));
     const int row = 32 * (kWaves * t + w) + m;
-    if (row < a.rows) v = *reinterpret_cast<const uint4*>(a.tail_k + row * rs + (int64_t)g * D + 16 * kap + 8 * c);
-    else v = make_uint4(0, 0, 0, 0);
+    if (row < a.rows) {
+      // keys as fp16, as the reconstruction kernel stores them (saturated at +-65504)
+      const uint4 kb = *reinterpret_cast<const uint4*>(a.tail_k + row * rs + (int64_t)g * D + 16 * kap + 8 * c);
+      const __bf16* kv = reinterpret_cast<const __bf16*>(&kb);
+      _Float16* hv = reinterpret_cast<_Float16*>(&v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) hv[e] = (_Float16)fminf(fmaxf((float)kv[e], -65504.f), 65504.f);
+    } else {
+      v = make_uint4(0, 0, 0, 0);
+    }
   } else {
     // fragment rho T_pad / 16 + sig of the P^V layout at rank d: tokens 16 sig + 8 c .. +7 of dim 32 rho + m
     const int T16 = a.T_pad / 16;

@@ -286,3 +286,34 @@ def test_nonpositive_scales_on_both_routes(scale):
             assert err <= TOL_REL_L2
     finally:
         gl.free()
+
+
+def test_sharp_attention_on_the_reconstruct_route():
+    """Attention three times sharper than the workloads' (scores spanning ~40
+    log2 units): rebuilt keys are stored as fp16 and meet the query exactly
+    in the fp16 score MFMA, so the reconstruct route, with and without rotated
+    keys, stays at the bar (rebuilt bf16 keys would reach ~1.3e-2 here)."""
+    import torch
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(23, [700, 1024, 100, 513], [64, 288, 32, 128], [96, 256, 16, 128], n_kv_heads=4,
+                             head_dim=128, n_q=3, n_q_heads=28, tail_cap=90, tail_len=[90, 0, 45])
+    scale = 3 * inp.scale
+    a = oracle_args(inp)
+    a["scale"] = scale
+    key_pos = [0, 5000, 123, 77777]
+    refs = {False: oracle.attend_latent(**a), True: oracle.attend_dense(**a, key_pos=key_pos, rope_theta=1e6)}
+    gl = GpuLayer(inp)
+    try:
+        milo.milo_cache_set_path(gl.cache, milo.MILO_PATH_RECONSTRUCT)
+        for rope in (False, True):
+            if rope:
+                milo.milo_cache_set_rope(gl.cache, 1e6, key_pos)
+            out = torch.full(inp.q.shape, float("nan"), dtype=torch.float32, device="cuda")
+            milo.milo_attend_decode(gl.cache, list(range(inp.n_blocks)), gl.q, gl.tk, gl.tv, inp.tail_len, scale,
+                                    out)
+            torch.cuda.synchronize()
+            err = max_rel_l2(out.cpu().numpy(), refs[rope])
+            print(f"[recon] 3x sharper attention, rotated keys {rope}: max rel-L2 = {err:.3e}", flush=True)
+            assert err <= TOL_REL_L2
+    finally:
+        gl.free()
