@@ -621,7 +621,7 @@ class CacheWorkspace : public Workspace {
 // D = H_kv d:
 //   latent        4.24e-9 N (rk + rv)(T + d)        (latent block items)
 //   reconstruct   4.17e-9 T D (rk + rv)             (reconstruction GEMMs)
-//               + 1.99e-6 T D                       (writing, then reading, the bf16 K and V)
+//               + 1.99e-6 T D                       (writing, then reading, the 16-bit K and V)
 //               + 7.06e-9 N T d                     (dense block items)
 // and reconstruction is chosen below 0.85 of the latent time (mixed plans
 // measured slower than the sum of their parts near the tie).
