@@ -121,3 +121,32 @@ def test_int8_parity_random_shapes(seed):
     from test_gpu_parity import _random_case
     inp, table = _random_case(seed)
     _check(inp, f"random seed {seed}", table=table)
+
+
+@pytest.mark.parametrize("n_tok,tail_base", [(20, 250), (160, 100)])
+def test_int8_prefill(n_tok, tail_base):
+    """Causal prefill of one request's chunk over an INT8 cache: INT8 caches
+    attend the shared tail with tail items per token (chunks of 128 tokens
+    and more do not pack it, which needs reconstruction buffers), against the
+    oracle's prefill on the dequantised factors."""
+    import torch
+    from helpers import to_device
+    from paper_2609_29913_amd import milo
+    inp = synth.make_problem(71 + n_tok, [1024, 300], [288, 64], n_kv_heads=4, head_dim=128, n_q=n_tok,
+                             n_q_heads=28, tail_cap=tail_base + n_tok)
+    table = [0, 1]
+    gl = GpuLayer(inp, p_int8=True)
+    try:
+        tk, tv = to_device(inp.tail_k[0]), to_device(inp.tail_v[0])
+        out = torch.full(inp.q.shape, float("nan"), dtype=torch.float32, device="cuda")
+        milo.milo_attend_prefill(gl.cache, table, gl.q, tk, tv, tail_base, inp.scale, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+    finally:
+        gl.free()
+    a = oracle_args_int8(inp, table)
+    ref = oracle.attend_prefill(a["pk"], a["rk"], a["pv"], a["rv"], table, a["q"], a["tail_k"][0], a["tail_v"][0],
+                                tail_base, inp.scale)
+    err = max_rel_l2(got, ref)
+    print(f"[int8] prefill {n_tok} tokens after {tail_base}: max rel-L2 = {err:.3e}", flush=True)
+    assert err <= TOL_REL_L2
