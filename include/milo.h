@@ -224,7 +224,7 @@ int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n);
  *        (u, v) -> (u cos a - v sin a,  v cos a + u sin a),  a = p theta^(-2j/d)
  * for each pair u = k[j], v = k[j + d/2], j < d/2 (the rotate-half arrangement
  * of the Qwen2 models the paper evaluates).  The rotation is applied to the
- * fp32 reconstruction, before its bf16 rounding: the angle is formed in turns,
+ * fp32 reconstruction, before its rounding to fp16: the angle is formed in turns,
  * p theta^(-2j/d) / (2 pi), in fp64, reduced to [0, 1) and its sine and
  * cosine taken in fp32 by the hardware's turn-based instructions (error below
  * ~1e-6 at any int32 position).
@@ -237,8 +237,9 @@ int milo_cache_recon_blocks(const milo_cache* cache, int32_t* n);
  *              the blocks one after another in id order from position 0.
  *              Blocks may overlap or leave gaps (a retriever's reordering).
  * Uploads d/2 frequencies (fp64) and waits for the device before freeing the
- * previous ones; later calls rebuild their plan.  INT8 caches (attended latent only) return UNSUPPORTED, and so
- * does milo_attend_decode_noalloc on such a cache when a block is selected.
+ * previous ones; later calls rebuild their plan.  INT8 caches (attended latent
+ * only) return UNSUPPORTED, and so does milo_attend_decode_noalloc on such a
+ * cache when a block is selected.
  * Errors: INVALID_ARG (NULL cache, theta, positions), UNSUPPORTED,
  * OUT_OF_MEMORY, HIP_ERROR. */
 int milo_cache_set_rope(milo_cache* cache, double theta, const int64_t* block_pos);
